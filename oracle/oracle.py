@@ -1,0 +1,266 @@
+"""ctypes front end of the CPU oracle (qcnn_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by __graft_entry__.smoke() and by
+the cpu_baseline leg of bench.py, never by the product package.  Everything
+here is marshalling (numpy arrays in, float64 arrays out) plus the layer-by-
+layer composition of a whole network from the oracle's own layer functions.
+
+Paper: Wu et al., "Quantized Convolutional Neural Networks for Mobile Devices",
+CVPR 2016 -- Sec. 3.1 Eq. (5) (fully-connected layer) and Sec. 3.2 Eq. (7)
+(convolutional layer), each computed through the table of sub-codeword inner
+products and, independently, as a dense layer on the rebuilt weights.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "qcnn_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+ERRORS = {-1: "bad argument", -2: "bad shape", -3: "K out of range", -4: "code >= K", -5: "out of memory"}
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain C, -O2, no fast-math, OpenMP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _signatures():
+    P, I = ctypes.c_void_p, ctypes.c_int
+    return {
+        "qo_lut": [P, I, I, I, I, P, I, I, I, P, P],
+        "qo_conv_lut": [P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P],
+        "qo_conv_direct": [P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P],
+        "qo_conv_points": [P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, I, P, P],
+        "qo_fc_lut": [P, I, I, P, I, I, I, P, I, P, I, P, P],
+        "qo_fc_direct": [P, I, I, P, I, I, I, P, I, P, I, P],
+        "qo_fc_points": [P, I, I, P, I, I, I, P, I, P, I, P, I, P, P],
+        "qo_maxpool": [P, I, I, I, I, I, I, P],
+        "qo_threads": [],
+    }
+
+
+def load(path: str):
+    """Load an oracle shared library (the default build, or another build of
+    the same source, e.g. a deliberately broken copy in a pin test)."""
+    cdll = ctypes.CDLL(path)
+    for name, args in _signatures().items():
+        f = getattr(cdll, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    return cdll
+
+
+_lib = None
+_override = None
+
+
+def use(cdll) -> None:
+    """Route the functions below to ``cdll`` (None restores the default)."""
+    global _override
+    _override = cdll
+
+
+def lib():
+    global _lib
+    if _override is not None:
+        return _override
+    if _lib is None:
+        _lib = load(build())
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _chk(rc: int) -> None:
+    if rc != 0:
+        raise OracleError(ERRORS.get(rc, "error %d" % rc))
+
+
+def _f32(a):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return a, a.ctypes.data
+
+
+def _u8(a):
+    a = np.ascontiguousarray(a, dtype=np.uint8)
+    return a, a.ctypes.data
+
+
+def _opt_f32(a):
+    if a is None:
+        return None, None
+    return _f32(a)
+
+
+def threads() -> int:
+    return lib().qo_threads()
+
+
+def out_size(n: int, k: int, s: int, p: int) -> int:
+    span = n + 2 * p - k
+    return span // s + 1 if span >= 0 else 0
+
+
+def lut(x, D, with_bound=False):
+    """Table of Sec. 3.1/3.2: [N][M][K][H][W] float64 (and the |term| sums)."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    N, Cs, H, W = x.shape
+    M, K, Csp = D.shape
+    out = np.empty((N, M, K, H, W), np.float64)
+    ab = np.empty_like(out) if with_bound else None
+    _chk(lib().qo_lut(xp, N, Cs, H, W, Dp, M, K, Csp, out.ctypes.data,
+                      ab.ctypes.data if ab is not None else None))
+    return (out, ab) if with_bound else out
+
+
+def conv_lut(x, D, codes, stride=1, pad=0, bias=None, relu=False, with_bound=False):
+    """Conv layer through the table, Eq. (7): [N][C_t][H_o][W_o] float64."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    codes, cp = _u8(codes)
+    bias, bp = _opt_f32(bias)
+    N, Cs, H, W = x.shape
+    M, K, Csp = D.shape
+    Ct, dk, dk2, M2 = codes.shape
+    assert dk == dk2 and M2 == M
+    Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
+    y = np.empty((N, Ct, max(Ho, 0), max(Wo, 0)), np.float64)
+    ab = np.empty_like(y) if with_bound else None
+    _chk(lib().qo_conv_lut(xp, N, Cs, H, W, Dp, M, K, Csp, cp, Ct, dk, stride, pad, bp,
+                           int(bool(relu)), y.ctypes.data,
+                           ab.ctypes.data if ab is not None else None))
+    return (y, ab) if with_bound else y
+
+
+def conv_direct(x, D, codes, stride=1, pad=0, bias=None, relu=False):
+    """Conv layer as a dense cross-correlation on the rebuilt kernel, Eq. (1)/(7)."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    codes, cp = _u8(codes)
+    bias, bp = _opt_f32(bias)
+    N, Cs, H, W = x.shape
+    M, K, Csp = D.shape
+    Ct, dk, _, _ = codes.shape
+    Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
+    y = np.empty((N, Ct, max(Ho, 0), max(Wo, 0)), np.float64)
+    _chk(lib().qo_conv_direct(xp, N, Cs, H, W, Dp, M, K, Csp, cp, Ct, dk, stride, pad, bp,
+                              int(bool(relu)), y.ctypes.data))
+    return y
+
+
+def conv_points(x, D, codes, pts, stride=1, pad=0, bias=None, relu=False):
+    """Selected responses (n, c_t, yo, xo) of the conv layer: (values, bounds)."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    codes, cp = _u8(codes)
+    bias, bp = _opt_f32(bias)
+    pts = np.ascontiguousarray(pts, dtype=np.int32).reshape(-1, 4)
+    N, Cs, H, W = x.shape
+    M, K, Csp = D.shape
+    Ct, dk, _, _ = codes.shape
+    y = np.empty(len(pts), np.float64)
+    ab = np.empty(len(pts), np.float64)
+    _chk(lib().qo_conv_points(xp, N, Cs, H, W, Dp, M, K, Csp, cp, Ct, dk, stride, pad, bp,
+                              int(bool(relu)), pts.ctypes.data, len(pts), y.ctypes.data,
+                              ab.ctypes.data))
+    return y, ab
+
+
+def fc_lut(x, D, codes, bias=None, relu=False, with_bound=False):
+    """FC layer through the table, Eq. (5): [N][C_t] float64."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    codes, cp = _u8(codes)
+    bias, bp = _opt_f32(bias)
+    N, Cs = x.shape
+    M, K, Csp = D.shape
+    Ct, M2 = codes.shape
+    assert M2 == M
+    y = np.empty((N, Ct), np.float64)
+    ab = np.empty_like(y) if with_bound else None
+    _chk(lib().qo_fc_lut(xp, N, Cs, Dp, M, K, Csp, cp, Ct, bp, int(bool(relu)), y.ctypes.data,
+                         ab.ctypes.data if ab is not None else None))
+    return (y, ab) if with_bound else y
+
+
+def fc_direct(x, D, codes, bias=None, relu=False):
+    """FC layer as a dense product with the rebuilt weights, Eq. (2)/(5)."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    codes, cp = _u8(codes)
+    bias, bp = _opt_f32(bias)
+    N, Cs = x.shape
+    M, K, Csp = D.shape
+    Ct, _ = codes.shape
+    y = np.empty((N, Ct), np.float64)
+    _chk(lib().qo_fc_direct(xp, N, Cs, Dp, M, K, Csp, cp, Ct, bp, int(bool(relu)), y.ctypes.data))
+    return y
+
+
+def fc_points(x, D, codes, pts, bias=None, relu=False):
+    """Selected responses (n, c_t) of the FC layer: (values, bounds)."""
+    x, xp = _f32(x)
+    D, Dp = _f32(D)
+    codes, cp = _u8(codes)
+    bias, bp = _opt_f32(bias)
+    pts = np.ascontiguousarray(pts, dtype=np.int32).reshape(-1, 2)
+    N, Cs = x.shape
+    M, K, Csp = D.shape
+    Ct, _ = codes.shape
+    y = np.empty(len(pts), np.float64)
+    ab = np.empty(len(pts), np.float64)
+    _chk(lib().qo_fc_points(xp, N, Cs, Dp, M, K, Csp, cp, Ct, bp, int(bool(relu)),
+                            pts.ctypes.data, len(pts), y.ctypes.data, ab.ctypes.data))
+    return y, ab
+
+
+def maxpool(x, k=3, s=2):
+    """k x k / stride s max pooling, no padding (network glue)."""
+    x, xp = _f32(x)
+    N, C, H, W = x.shape
+    y = np.empty((N, C, out_size(H, k, s, 0), out_size(W, k, s, 0)), np.float64)
+    _chk(lib().qo_maxpool(xp, N, C, H, W, k, s, y.ctypes.data))
+    return y
+
+
+def network(x, layers, absolute=False, layer_inputs=None):
+    """Run a stack of PQ layers and pools through the oracle.
+
+    ``layers`` is a list of dicts from the workload generator: kind 'conv'
+    (D, codes, stride, pad, relu), 'fc' (D, codes, relu) or 'pool' (k, s).
+    Each layer takes the fp32 rounding of the previous layer's float64 output,
+    as the GPU path would receive it.  With ``absolute`` every value is
+    replaced by its magnitude and ReLU is dropped (|x|, |D|, no ReLU): that
+    network's output bounds the sum of |terms| that reach each final output.
+    If ``layer_inputs`` is a list, the fp32 input of every layer is appended.
+    Returns the float64 output of the last layer.
+    """
+    h = np.abs(x) if absolute else x
+    for L in layers:
+        h32 = np.ascontiguousarray(h, dtype=np.float32)
+        if layer_inputs is not None:
+            layer_inputs.append(h32)
+        if L["kind"] == "pool":
+            h = maxpool(h32, L["k"], L["s"])
+            continue
+        D = np.abs(L["D"]) if absolute else L["D"]
+        relu = bool(L["relu"]) and not absolute
+        if L["kind"] == "conv":
+            h = conv_lut(h32, D, L["codes"], L["stride"], L["pad"], None, relu)
+        else:
+            h = fc_lut(h32.reshape(h32.shape[0], -1), D, L["codes"], None, relu)
+    return h

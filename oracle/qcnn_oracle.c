@@ -1,0 +1,426 @@
+/*
+ * qcnn_oracle.c -- TEST INFRASTRUCTURE ONLY.  Not part of the product path.
+ *
+ * Only tests/, the smoke check (__graft_entry__.smoke) and the benchmark's
+ * cpu_baseline leg may load or call this file.  It shares no code, header,
+ * table or constant with the HIP library under paper_1512_06473_amd/csrc.
+ *
+ * A plain, slow, obviously correct CPU implementation of the test-phase
+ * forward of a product-quantized (PQ) layer, from
+ *   J. Wu, C. Leng, Y. Wang, Q. Hu, J. Cheng, "Quantized Convolutional Neural
+ *   Networks for Mobile Devices", CVPR 2016 (arXiv 1512.06473).
+ *
+ * What it computes (paper notation):
+ *   - Sec. 2, Eq. (3): an inner product split over M subspaces; each sub-vector
+ *     of the weights is replaced by a sub-codeword c^(m)_{k_m}.
+ *   - Sec. 3.1, Eq. (5) and the test-phase paragraph after it: for a
+ *     fully-connected layer, the input S is split into M sub-vectors S^(m);
+ *     the inner products of S^(m) with every sub-codeword of D^(m) go into a
+ *     look-up table; each response T(c_t) is then the sum over m of the table
+ *     entry selected by k_m(c_t).
+ *   - Sec. 3.2, Eq. (7): for a convolutional layer the split is along input
+ *     channels, one sub-codebook D^(m) is shared by all kernel offsets p_k,
+ *     the table is pre-computed at every input position p_s, and T_{p_t}(c_t)
+ *     sums the table entry selected by k_m(c_t, p_k) over the receptive-field
+ *     pairs (p_k, p_s) and over m.
+ *
+ * Every floating-point sum is taken in double precision from the fp32 inputs.
+ *
+ * Readings of points the paper leaves open (each is stated where it is used):
+ *   R1 layouts: x [N][C_s][H][W]; codebooks D [M][K][C'_s] (row k of D[m] is
+ *      the sub-codeword D^(m)_k); conv codes [C_t][d_k][d_k][M] holding
+ *      k_m(c_t, p_k) for p_k = (ky, kx); FC codes [C_t][M] holding k_m(c_t).
+ *   R2 the (p_k, p_s) pairing of Eq. (1) is cross-correlation with stride s
+ *      and zero padding p: p_s = p_t * s - p + p_k, no kernel flip.
+ *   R3 positions in the zero padding hold S = 0, so <D_k, 0> = 0: they add
+ *      nothing and are skipped.
+ *   R4 subspace m covers input channels [m C'_s, (m+1) C'_s) (the "even split"
+ *      of Sec. 3.1), so C_s = M C'_s.
+ *   R5 optional per-output-channel bias and ReLU are applied after the sum;
+ *      neither is part of Eq. (5) or Eq. (7), a NULL bias and relu = 0 give
+ *      exactly those equations.
+ *
+ * Return value of every entry point: 0 on success, otherwise one of the
+ * negative QO_E* codes below; on error nothing is written.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+#define QO_EARG   (-1) /* null pointer or non-positive size */
+#define QO_ESHAPE (-2) /* C_s != M C'_s, or an empty output */
+#define QO_EK     (-3) /* K outside [1, 256] */
+#define QO_ECODE  (-4) /* a code >= K */
+#define QO_ENOMEM (-5)
+
+static int out_size(int in, int k, int s, int p) {
+  int span = in + 2 * p - k;
+  if (span < 0) return 0;
+  return span / s + 1;
+}
+
+static int check_pq(int N, int Cs, int M, int K, int Csp) {
+  if (N < 1 || Cs < 1 || M < 1 || Csp < 1) return QO_EARG;
+  if (K < 1 || K > 256) return QO_EK;
+  if (Cs != M * Csp) return QO_ESHAPE;
+  return 0;
+}
+
+static int check_codes(const uint8_t* codes, size_t n, int K) {
+  for (size_t i = 0; i < n; ++i)
+    if ((int)codes[i] >= K) return QO_ECODE;
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Look-up table (Sec. 3.1 test phase; Sec. 3.2 last paragraph):
+ *   lut[n][m][k][y][x] = < D^(m)_k , S^(m)_{(y,x)} >
+ *                      = sum_{j < C'_s} D[m][k][j] * x[n][m C'_s + j][y][x]
+ * over the real (unpadded) input positions only (R3).
+ * absb, if non-NULL, receives sum_j |D[m][k][j] * x[...]| (the sum of the
+ * absolute values of the terms, used for the rounding-error bound).        */
+int qo_lut(const float* x, int N, int Cs, int H, int W,
+           const float* D, int M, int K, int Csp,
+           double* lut, double* absb) {
+  int e;
+  if (!x || !D || !lut) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (H < 1 || W < 1) return QO_EARG;
+  const size_t HW = (size_t)H * W;
+#pragma omp parallel for schedule(static)
+  for (int n = 0; n < N; ++n)
+    for (int m = 0; m < M; ++m)
+      for (int k = 0; k < K; ++k)
+        for (size_t p = 0; p < HW; ++p) {
+          double s = 0.0, a = 0.0;
+          for (int j = 0; j < Csp; ++j) {
+            double term = (double)D[((size_t)m * K + k) * Csp + j] *
+                          (double)x[((size_t)n * Cs + (size_t)m * Csp + j) * HW + p];
+            s += term;
+            a += fabs(term);
+          }
+          size_t o = (((size_t)n * M + m) * K + k) * HW + p;
+          lut[o] = s;
+          if (absb) absb[o] = a;
+        }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Convolutional layer through the table, Eq. (7) third line:
+ *   T_{p_t}(c_t) = sum_{(p_k, p_s)} sum_m lut[m][ k_m(c_t, p_k) ][p_s]
+ * with p_t = (yo, xo), p_k = (ky, kx), p_s = (yo s - p + ky, xo s - p + kx)
+ * (R2); pairs whose p_s falls in the padding contribute 0 and are skipped
+ * (R3).  Then + bias[c_t] and ReLU if requested (R5).
+ * y: [N][C_t][H_o][W_o].  absb (nullable): the bound sum over every product
+ * |D * x| that enters the response, plus |bias|.                            */
+int qo_conv_lut(const float* x, int N, int Cs, int H, int W,
+                const float* D, int M, int K, int Csp,
+                const uint8_t* codes, int Ct, int dk, int stride, int pad,
+                const float* bias, int relu, double* y, double* absb) {
+  int e;
+  if (!x || !D || !codes || !y) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (H < 1 || W < 1 || Ct < 1 || dk < 1 || stride < 1 || pad < 0) return QO_EARG;
+  const int Ho = out_size(H, dk, stride, pad), Wo = out_size(W, dk, stride, pad);
+  if (Ho < 1 || Wo < 1) return QO_ESHAPE;
+  if ((e = check_codes(codes, (size_t)Ct * dk * dk * M, K))) return e;
+  const size_t HW = (size_t)H * W;
+  const size_t per_img = (size_t)M * K * HW;
+  int failed = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int n = 0; n < N; ++n) {
+    /* Table for one image: step 1. */
+    double* lut = (double*)malloc(per_img * sizeof(double));
+    double* alut = absb ? (double*)malloc(per_img * sizeof(double)) : NULL;
+    if (!lut || (absb && !alut)) { free(lut); free(alut); failed = 1; continue; }
+    qo_lut(x + (size_t)n * Cs * HW, 1, Cs, H, W, D, M, K, Csp, lut, alut);
+    /* Step 2: sum of selected entries. */
+    for (int t = 0; t < Ct; ++t)
+      for (int yo = 0; yo < Ho; ++yo)
+        for (int xo = 0; xo < Wo; ++xo) {
+          double s = 0.0, a = 0.0;
+          for (int ky = 0; ky < dk; ++ky) {
+            int yi = yo * stride - pad + ky;
+            if (yi < 0 || yi >= H) continue;
+            for (int kx = 0; kx < dk; ++kx) {
+              int xi = xo * stride - pad + kx;
+              if (xi < 0 || xi >= W) continue;
+              for (int m = 0; m < M; ++m) {
+                int k = codes[(((size_t)t * dk + ky) * dk + kx) * M + m];
+                size_t o = ((size_t)m * K + k) * HW + (size_t)yi * W + xi;
+                s += lut[o];
+                if (alut) a += alut[o];
+              }
+            }
+          }
+          if (bias) { s += (double)bias[t]; a += fabs((double)bias[t]); }
+          if (relu && s < 0.0) s = 0.0;
+          size_t oi = (((size_t)n * Ct + t) * Ho + yo) * Wo + xo;
+          y[oi] = s;
+          if (absb) absb[oi] = a;
+        }
+    free(lut);
+    free(alut);
+  }
+  return failed ? QO_ENOMEM : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Independent route for the same layer, Eq. (7) second line read with
+ * D^(m) B^(m)_{c_t,p_k} = D^(m)_{k_m(c_t,p_k)}: rebuild the dense kernel
+ *   What[c_t][m C'_s + j][ky][kx] = D[m][ k_m(c_t,(ky,kx)) ][j]
+ * and evaluate Eq. (1), the plain receptive-field sum of <W_{c_t,p_k}, S_{p_s}>,
+ * with no table.  Shares nothing with qo_conv_lut but the layouts.          */
+int qo_conv_direct(const float* x, int N, int Cs, int H, int W,
+                   const float* D, int M, int K, int Csp,
+                   const uint8_t* codes, int Ct, int dk, int stride, int pad,
+                   const float* bias, int relu, double* y) {
+  int e;
+  if (!x || !D || !codes || !y) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (H < 1 || W < 1 || Ct < 1 || dk < 1 || stride < 1 || pad < 0) return QO_EARG;
+  const int Ho = out_size(H, dk, stride, pad), Wo = out_size(W, dk, stride, pad);
+  if (Ho < 1 || Wo < 1) return QO_ESHAPE;
+  if ((e = check_codes(codes, (size_t)Ct * dk * dk * M, K))) return e;
+  const size_t wsz = (size_t)Ct * Cs * dk * dk;
+  double* What = (double*)malloc(wsz * sizeof(double));
+  if (!What) return QO_ENOMEM;
+  for (int t = 0; t < Ct; ++t)
+    for (int ky = 0; ky < dk; ++ky)
+      for (int kx = 0; kx < dk; ++kx)
+        for (int m = 0; m < M; ++m) {
+          int k = codes[(((size_t)t * dk + ky) * dk + kx) * M + m];
+          for (int j = 0; j < Csp; ++j)
+            What[(((size_t)t * Cs + (size_t)m * Csp + j) * dk + ky) * dk + kx] =
+                (double)D[((size_t)m * K + k) * Csp + j];
+        }
+  const size_t HW = (size_t)H * W;
+#pragma omp parallel for schedule(static)
+  for (int n = 0; n < N; ++n)
+    for (int t = 0; t < Ct; ++t)
+      for (int yo = 0; yo < Ho; ++yo)
+        for (int xo = 0; xo < Wo; ++xo) {
+          double s = 0.0;
+          for (int c = 0; c < Cs; ++c)
+            for (int ky = 0; ky < dk; ++ky) {
+              int yi = yo * stride - pad + ky;
+              if (yi < 0 || yi >= H) continue;
+              for (int kx = 0; kx < dk; ++kx) {
+                int xi = xo * stride - pad + kx;
+                if (xi < 0 || xi >= W) continue;
+                s += What[(((size_t)t * Cs + c) * dk + ky) * dk + kx] *
+                     (double)x[((size_t)n * Cs + c) * HW + (size_t)yi * W + xi];
+              }
+            }
+          if (bias) s += (double)bias[t];
+          if (relu && s < 0.0) s = 0.0;
+          y[(((size_t)n * Ct + t) * Ho + yo) * Wo + xo] = s;
+        }
+  free(What);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Single responses of the conv layer, for spot checks at sizes where a whole
+ * table would be too slow: pts is [P][4] = (n, c_t, yo, xo).  Each response
+ * is Eq. (7) with every table entry it selects evaluated from its definition
+ * (the C'_s-term inner product) on the spot.                                */
+int qo_conv_points(const float* x, int N, int Cs, int H, int W,
+                   const float* D, int M, int K, int Csp,
+                   const uint8_t* codes, int Ct, int dk, int stride, int pad,
+                   const float* bias, int relu,
+                   const int32_t* pts, int P, double* y, double* absb) {
+  int e;
+  if (!x || !D || !codes || !pts || !y || P < 0) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (H < 1 || W < 1 || Ct < 1 || dk < 1 || stride < 1 || pad < 0) return QO_EARG;
+  const int Ho = out_size(H, dk, stride, pad), Wo = out_size(W, dk, stride, pad);
+  if (Ho < 1 || Wo < 1) return QO_ESHAPE;
+  for (int i = 0; i < P; ++i) {
+    const int32_t* q = pts + 4 * (size_t)i;
+    if (q[0] < 0 || q[0] >= N || q[1] < 0 || q[1] >= Ct || q[2] < 0 || q[2] >= Ho ||
+        q[3] < 0 || q[3] >= Wo) return QO_EARG;
+  }
+  const size_t HW = (size_t)H * W;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int i = 0; i < P; ++i) {
+    const int n = pts[4 * (size_t)i], t = pts[4 * (size_t)i + 1];
+    const int yo = pts[4 * (size_t)i + 2], xo = pts[4 * (size_t)i + 3];
+    double s = 0.0, a = 0.0;
+    for (int ky = 0; ky < dk; ++ky) {
+      int yi = yo * stride - pad + ky;
+      if (yi < 0 || yi >= H) continue;
+      for (int kx = 0; kx < dk; ++kx) {
+        int xi = xo * stride - pad + kx;
+        if (xi < 0 || xi >= W) continue;
+        for (int m = 0; m < M; ++m) {
+          int k = codes[(((size_t)t * dk + ky) * dk + kx) * M + m];
+          for (int j = 0; j < Csp; ++j) {
+            double term = (double)D[((size_t)m * K + k) * Csp + j] *
+                          (double)x[((size_t)n * Cs + (size_t)m * Csp + j) * HW +
+                                    (size_t)yi * W + xi];
+            s += term;
+            a += fabs(term);
+          }
+        }
+      }
+    }
+    if (bias) { s += (double)bias[t]; a += fabs((double)bias[t]); }
+    if (relu && s < 0.0) s = 0.0;
+    y[i] = s;
+    if (absb) absb[i] = a;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Fully-connected layer through the table, Eq. (5) last line and the
+ * test-phase paragraph of Sec. 3.1:
+ *   lut[m][k] = < D^(m)_k , S^(m) > = sum_j D[m][k][j] * x[n][m C'_s + j]
+ *   T(c_t)    = sum_m lut[m][ k_m(c_t) ]
+ * x: [N][C_s], codes: [C_t][M], y: [N][C_t].  absb as for the conv layer.  */
+int qo_fc_lut(const float* x, int N, int Cs,
+              const float* D, int M, int K, int Csp,
+              const uint8_t* codes, int Ct,
+              const float* bias, int relu, double* y, double* absb) {
+  int e;
+  if (!x || !D || !codes || !y) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (Ct < 1) return QO_EARG;
+  if ((e = check_codes(codes, (size_t)Ct * M, K))) return e;
+  int failed = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int n = 0; n < N; ++n) {
+    double* lut = (double*)malloc((size_t)M * K * sizeof(double));
+    double* alut = (double*)malloc((size_t)M * K * sizeof(double));
+    if (!lut || !alut) { free(lut); free(alut); failed = 1; continue; }
+    for (int m = 0; m < M; ++m)
+      for (int k = 0; k < K; ++k) {
+        double s = 0.0, a = 0.0;
+        for (int j = 0; j < Csp; ++j) {
+          double term = (double)D[((size_t)m * K + k) * Csp + j] *
+                        (double)x[(size_t)n * Cs + (size_t)m * Csp + j];
+          s += term;
+          a += fabs(term);
+        }
+        lut[(size_t)m * K + k] = s;
+        alut[(size_t)m * K + k] = a;
+      }
+    for (int t = 0; t < Ct; ++t) {
+      double s = 0.0, a = 0.0;
+      for (int m = 0; m < M; ++m) {
+        int k = codes[(size_t)t * M + m];
+        s += lut[(size_t)m * K + k];
+        a += alut[(size_t)m * K + k];
+      }
+      if (bias) { s += (double)bias[t]; a += fabs((double)bias[t]); }
+      if (relu && s < 0.0) s = 0.0;
+      y[(size_t)n * Ct + t] = s;
+      if (absb) absb[(size_t)n * Ct + t] = a;
+    }
+    free(lut);
+    free(alut);
+  }
+  return failed ? QO_ENOMEM : 0;
+}
+
+/* Independent route, Eq. (5) first line with W^(m)_{c_t} replaced by its
+ * sub-codeword (Eq. (4): D^(m) B^(m)): What[c_t][m C'_s + j] =
+ * D[m][k_m(c_t)][j], then Eq. (2), T(c_t) = <What_{c_t}, S>.               */
+int qo_fc_direct(const float* x, int N, int Cs,
+                 const float* D, int M, int K, int Csp,
+                 const uint8_t* codes, int Ct,
+                 const float* bias, int relu, double* y) {
+  int e;
+  if (!x || !D || !codes || !y) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (Ct < 1) return QO_EARG;
+  if ((e = check_codes(codes, (size_t)Ct * M, K))) return e;
+  double* What = (double*)malloc((size_t)Ct * Cs * sizeof(double));
+  if (!What) return QO_ENOMEM;
+  for (int t = 0; t < Ct; ++t)
+    for (int m = 0; m < M; ++m) {
+      int k = codes[(size_t)t * M + m];
+      for (int j = 0; j < Csp; ++j)
+        What[(size_t)t * Cs + (size_t)m * Csp + j] = (double)D[((size_t)m * K + k) * Csp + j];
+    }
+#pragma omp parallel for schedule(static)
+  for (int n = 0; n < N; ++n)
+    for (int t = 0; t < Ct; ++t) {
+      double s = 0.0;
+      for (int c = 0; c < Cs; ++c) s += What[(size_t)t * Cs + c] * (double)x[(size_t)n * Cs + c];
+      if (bias) s += (double)bias[t];
+      if (relu && s < 0.0) s = 0.0;
+      y[(size_t)n * Ct + t] = s;
+    }
+  free(What);
+  return 0;
+}
+
+/* Single FC responses: pts is [P][2] = (n, c_t); each is Eq. (5) with the
+ * selected entries evaluated from their definition on the spot.            */
+int qo_fc_points(const float* x, int N, int Cs,
+                 const float* D, int M, int K, int Csp,
+                 const uint8_t* codes, int Ct,
+                 const float* bias, int relu,
+                 const int32_t* pts, int P, double* y, double* absb) {
+  int e;
+  if (!x || !D || !codes || !pts || !y || P < 0) return QO_EARG;
+  if ((e = check_pq(N, Cs, M, K, Csp))) return e;
+  if (Ct < 1) return QO_EARG;
+  for (int i = 0; i < P; ++i)
+    if (pts[2 * (size_t)i] < 0 || pts[2 * (size_t)i] >= N || pts[2 * (size_t)i + 1] < 0 ||
+        pts[2 * (size_t)i + 1] >= Ct) return QO_EARG;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int i = 0; i < P; ++i) {
+    const int n = pts[2 * (size_t)i], t = pts[2 * (size_t)i + 1];
+    double s = 0.0, a = 0.0;
+    for (int m = 0; m < M; ++m) {
+      int k = codes[(size_t)t * M + m];
+      for (int j = 0; j < Csp; ++j) {
+        double term = (double)D[((size_t)m * K + k) * Csp + j] *
+                      (double)x[(size_t)n * Cs + (size_t)m * Csp + j];
+        s += term;
+        a += fabs(term);
+      }
+    }
+    if (bias) { s += (double)bias[t]; a += fabs((double)bias[t]); }
+    if (relu && s < 0.0) s = 0.0;
+    y[i] = s;
+    if (absb) absb[i] = a;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Network glue, not part of the paper's method: max pooling over k x k
+ * windows with stride s and no padding (out = floor((in - k) / s) + 1).
+ * x: [N][C][H][W] fp32, y: [N][C][Ho][Wo] (the max is exact).              */
+int qo_maxpool(const float* x, int N, int C, int H, int W, int k, int s, double* y) {
+  if (!x || !y || N < 1 || C < 1 || H < 1 || W < 1 || k < 1 || s < 1) return QO_EARG;
+  const int Ho = out_size(H, k, s, 0), Wo = out_size(W, k, s, 0);
+  if (Ho < 1 || Wo < 1) return QO_ESHAPE;
+  for (int n = 0; n < N; ++n)
+    for (int c = 0; c < C; ++c)
+      for (int yo = 0; yo < Ho; ++yo)
+        for (int xo = 0; xo < Wo; ++xo) {
+          double best = -INFINITY;
+          for (int dy = 0; dy < k; ++dy)
+            for (int dx = 0; dx < k; ++dx) {
+              double v = x[(((size_t)n * C + c) * H + yo * s + dy) * W + xo * s + dx];
+              if (v > best) best = v;
+            }
+          y[(((size_t)n * C + c) * Ho + yo) * Wo + xo] = best;
+        }
+  return 0;
+}
+
+/* Threads the OpenMP runtime will use (1 when built without OpenMP). */
+#ifdef _OPENMP
+#include <omp.h>
+int qo_threads(void) { return omp_get_max_threads(); }
+#else
+int qo_threads(void) { return 1; }
+#endif

@@ -1,0 +1,123 @@
+"""A compact battery of oracle pins that needs only numpy, run in a child
+process against a given build of the oracle (see test_oracle_mutants.py).
+
+Every reference here is independent of the oracle's code: hand-worked values,
+a numpy dense convolution / matrix product on kernels rebuilt from the codes
+(Eq. (4), (6)), and numpy einsum for the table (Sec. 3.1 test phase).
+"""
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from oracle import oracle as O  # noqa: E402
+from paper_1512_06473_amd import workloads as wl  # noqa: E402
+
+
+def dense_conv(x, Wt, stride, pad, bias=None):
+    """Plain numpy cross-correlation (float64), one kernel offset at a time."""
+    N, Cs, H, W = x.shape
+    Ct, _, dk, _ = Wt.shape
+    Ho, Wo = (H + 2 * pad - dk) // stride + 1, (W + 2 * pad - dk) // stride + 1
+    xp = np.zeros((N, Cs, H + 2 * pad, W + 2 * pad))
+    xp[:, :, pad:pad + H, pad:pad + W] = x
+    y = np.zeros((N, Ct, Ho, Wo))
+    for ky in range(dk):
+        for kx in range(dk):
+            win = xp[:, :, ky:ky + stride * (Ho - 1) + 1:stride, kx:kx + stride * (Wo - 1) + 1:stride]
+            y += np.einsum("tc,nchw->nthw", Wt[:, :, ky, kx], win)
+    if bias is not None:
+        y += bias[None, :, None, None]
+    return y
+
+
+def rebuilt_conv(D, codes):
+    M, K, Csp = D.shape
+    Ct, dk, _, _ = codes.shape
+    sub = D[np.arange(M)[None, None, None, :], codes.astype(np.int64)]
+    return sub.transpose(0, 3, 4, 1, 2).reshape(Ct, M * Csp, dk, dk).astype(np.float64)
+
+
+def rebuilt_fc(D, codes):
+    M = D.shape[0]
+    sub = D[np.arange(M)[None, :], codes.astype(np.int64)]
+    return sub.reshape(codes.shape[0], -1).astype(np.float64)
+
+
+def checks():
+    out = []
+    # hand-worked (see test_oracle.py for the arithmetic)
+    x = np.array([[[[1, 2, 0], [0, 1, 3], [2, 0, 1]], [[0, 1, 1], [2, 0, 0], [1, 1, 2]]]], np.float32)
+    D = np.array([[[2], [-1]], [[1], [3]]], np.float32)
+    c = np.zeros((1, 2, 2, 2), np.uint8)
+    c[0, 0, 0], c[0, 0, 1], c[0, 1, 0], c[0, 1, 1] = [0, 1], [1, 0], [1, 1], [0, 0]
+    out.append(("hand conv", np.array_equal(O.conv_lut(x, D, c, 1, 0), [[[[9, 13], [7, 6]]]])))
+    x = np.arange(1, 10, dtype=np.float32).reshape(1, 1, 3, 3)
+    c = np.zeros((1, 3, 3, 1), np.uint8)
+    c[0, 1, 1, 0] = 1
+    b = np.array([-4], np.float32)
+    out.append(("hand conv s2p1", np.array_equal(
+        O.conv_lut(x, np.array([[[1], [-2]]], np.float32), c, 2, 1, bias=b, relu=True),
+        [[[[5, 3], [0, 0]]]])))
+    out.append(("hand fc", np.array_equal(
+        O.fc_lut(np.array([[1, 2, 3, 4]], np.float32),
+                 np.array([[[1, 0], [0, 1]], [[1, 1], [2, -1]]], np.float32),
+                 np.array([[0, 1], [1, 0]], np.uint8)), [[3, 9]])))
+    rng = np.random.Generator(np.random.PCG64(1234))
+    for shape in [(2, 8, 7, 6, 5, 3, 1, 1, 4, 16), (1, 6, 9, 7, 3, 3, 2, 1, 3, 8),
+                  (1, 3, 15, 15, 2, 7, 4, 0, 3, 16), (1, 8, 6, 6, 3, 5, 1, 2, 4, 32)]:
+        N, Cs, H, W, Ct, dk, s, p, Csp, K = shape
+        x, D, codes = wl.random_conv(rng, N, Cs, H, W, Ct, dk, s, p, Csp, K)
+        bias = rng.standard_normal(Ct).astype(np.float32)
+        ref = dense_conv(x.astype(np.float64), rebuilt_conv(D, codes), s, p, bias.astype(np.float64))
+        y, A = O.conv_lut(x, D, codes, s, p, bias=bias, with_bound=True)
+        out.append(("conv lut %s" % (shape,), y.shape == ref.shape and np.allclose(y, ref, rtol=1e-11, atol=1e-11)))
+        out.append(("conv direct %s" % (shape,),
+                    np.allclose(O.conv_direct(x, D, codes, s, p, bias=bias), ref, rtol=1e-11, atol=1e-11)))
+        Aref = dense_conv(np.abs(x).astype(np.float64), np.abs(rebuilt_conv(D, codes)), s, p,
+                          np.abs(bias).astype(np.float64))
+        out.append(("conv bound %s" % (shape,), np.allclose(A, Aref, rtol=1e-11, atol=1e-11)))
+        pts = np.array([[0, Ct - 1, y.shape[2] - 1, 0], [N - 1, 0, 0, y.shape[3] - 1]], np.int32)
+        v, a = O.conv_points(x, D, codes, pts, s, p, bias=bias)
+        out.append(("conv points %s" % (shape,), np.allclose(v, ref[tuple(pts.T)], rtol=1e-11, atol=1e-11)
+                    and np.allclose(a, Aref[tuple(pts.T)], rtol=1e-11, atol=1e-11)))
+    x, D, _ = wl.random_conv(rng, 2, 12, 4, 5, 1, 1, 1, 0, 3, 7)
+    L = O.lut(x, D)
+    want = np.einsum("mkj,nmjhw->nmkhw", D.astype(np.float64), x.astype(np.float64).reshape(2, 4, 3, 4, 5))
+    out.append(("lut einsum", np.allclose(L, want, rtol=1e-12, atol=1e-12)))
+    for (N, Cs, Ct, Csp, K) in [(3, 12, 7, 4, 8), (2, 9, 5, 3, 32)]:
+        x, D, codes = wl.random_fc(rng, N, Cs, Ct, Csp, K)
+        bias = rng.standard_normal(Ct).astype(np.float32)
+        ref = x.astype(np.float64) @ rebuilt_fc(D, codes).T + bias
+        y, A = O.fc_lut(x, D, codes, bias=bias, with_bound=True)
+        out.append(("fc lut", np.allclose(y, ref, rtol=1e-11, atol=1e-11)))
+        out.append(("fc direct", np.allclose(O.fc_direct(x, D, codes, bias=bias), ref, rtol=1e-11, atol=1e-11)))
+        Aref = np.abs(x).astype(np.float64) @ np.abs(rebuilt_fc(D, codes)).T + np.abs(bias)
+        out.append(("fc bound", np.allclose(A, Aref, rtol=1e-11, atol=1e-11)))
+        pts = np.array([[N - 1, Ct - 1], [0, 1]], np.int32)
+        v, a = O.fc_points(x, D, codes, pts, bias=bias)
+        out.append(("fc points", np.allclose(v, ref[tuple(pts.T)], rtol=1e-11, atol=1e-11)))
+    xm = rng.standard_normal((1, 2, 7, 9)).astype(np.float32)
+    ym = O.maxpool(xm, 3, 2)
+    ref = np.array([[[[xm[0, ch, 2 * i:2 * i + 3, 2 * j:2 * j + 3].max() for j in range(4)] for i in range(3)]
+                     for ch in range(2)]])
+    out.append(("maxpool", np.array_equal(ym, ref)))
+    return out
+
+
+def run(libpath=None):
+    if libpath:
+        O.use(O.load(libpath))
+    res = checks()
+    bad = [name for name, ok in res if not ok]
+    for name in bad:
+        print("FAILED:", name)
+    return 1 if bad else 0
+
+
+if __name__ == "__main__":
+    sys.exit(run(sys.argv[1] if len(sys.argv) > 1 else None))

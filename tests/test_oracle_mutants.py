@@ -1,0 +1,80 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case below plants one mistake in a copy of the oracle's C source (a
+dropped term, a wrong sign, a swapped or transposed index, an off-by-one),
+builds it, and runs tests/pin_battery.py against that build in a child
+process: the battery must report a failure.  The unmodified source must pass.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "qcnn_oracle.c")
+
+# (function, text to replace, replacement, what the mistake is)
+MUTANTS = [
+    ("qo_conv_lut", "codes[(((size_t)t * dk + ky) * dk + kx) * M + m]",
+     "codes[(((size_t)t * dk + kx) * dk + ky) * M + m]", "kernel offsets ky/kx swapped in the code index"),
+    ("qo_conv_lut", "int xi = xo * stride - pad + kx;", "int xi = xo * stride + pad + kx;", "padding sign"),
+    ("qo_conv_lut", "int yi = yo * stride - pad + ky;", "int yi = yo - pad + ky;", "stride dropped on rows"),
+    ("qo_conv_lut", "if (xi < 0 || xi >= W) continue;", "if (xi < 1 || xi >= W) continue;",
+     "off-by-one at the left border"),
+    ("qo_conv_lut", "for (int m = 0; m < M; ++m) {", "for (int m = 1; m < M; ++m) {", "first subspace dropped"),
+    ("qo_conv_lut",
+     "if (bias) { s += (double)bias[t]; a += fabs((double)bias[t]); }\n          if (relu && s < 0.0) s = 0.0;",
+     "if (relu && s < 0.0) s = 0.0;\n          if (bias) { s += (double)bias[t]; a += fabs((double)bias[t]); }",
+     "ReLU applied before the bias"),
+    ("qo_conv_lut", "if (alut) a += alut[o];", "if (alut) a += lut[o];", "bound sums signed terms"),
+    ("qo_lut", "for (int j = 0; j < Csp; ++j) {", "for (int j = 1; j < Csp; ++j) {", "dropped term of the inner product"),
+    ("qo_lut", "(double)x[((size_t)n * Cs + (size_t)m * Csp + j) * HW + p]",
+     "(double)x[((size_t)n * Cs + (size_t)m + j) * HW + p]", "wrong subspace channel offset"),
+    ("qo_lut", "(double)D[((size_t)m * K + k) * Csp + j]", "(double)D[((size_t)m * Csp + j) * K + k]",
+     "codebook transposed"),
+    ("qo_lut", "s += term;", "s -= term;", "sign of the table entry"),
+    ("qo_fc_lut", "int k = codes[(size_t)t * M + m];", "int k = codes[(size_t)m * Ct + t];", "FC codes transposed"),
+    ("qo_fc_lut", "(double)x[(size_t)n * Cs + (size_t)m * Csp + j]", "(double)x[(size_t)m * Csp + j]",
+     "FC image index dropped"),
+    ("qo_conv_direct", "What[(((size_t)t * Cs + (size_t)m * Csp + j) * dk + ky) * dk + kx]",
+     "What[(((size_t)t * Cs + (size_t)m * Csp + j) * dk + kx) * dk + ky]", "rebuilt kernel transposed"),
+    ("qo_conv_points", "int xi = xo * stride - pad + kx;", "int xi = xo * stride - pad + ky;", "point: kx read as ky"),
+    ("qo_fc_direct", "for (int c = 0; c < Cs; ++c) s +=", "for (int c = 0; c < Cs - 1; ++c) s +=", "FC last input dropped"),
+    ("qo_maxpool", "if (v > best) best = v;", "if (v < best || best == -INFINITY) best = v;", "min instead of max"),
+]
+
+
+def _mutate(src: str, func: str, old: str, new: str) -> str:
+    start = src.index("int %s(" % func)
+    end = src.index("\n}\n", start)
+    body = src[start:end]
+    assert old in body, (func, old)
+    return src[:start] + body.replace(old, new, 1) + src[end:]
+
+
+def _battery(lib: str) -> subprocess.CompletedProcess:
+    return subprocess.run([sys.executable, os.path.join(ROOT, "tests", "pin_battery.py"), lib],
+                          capture_output=True, text=True, timeout=300)
+
+
+def _build(src_text: str, tmp_path, name: str) -> str:
+    c = tmp_path / (name + ".c")
+    so = tmp_path / (name + ".so")
+    c.write_text(src_text)
+    subprocess.check_call(["gcc", "-O1", "-std=c99", "-fPIC", "-shared", "-o", str(so), str(c), "-lm"])
+    return str(so)
+
+
+def test_unmodified_oracle_passes(tmp_path):
+    lib = _build(open(SRC).read(), tmp_path, "orig")
+    r = _battery(lib)
+    assert r.returncode == 0, r.stdout + r.stderr
+
+
+@pytest.mark.parametrize("mut", MUTANTS, ids=[m[3] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, mut):
+    func, old, new, what = mut
+    lib = _build(_mutate(open(SRC).read(), func, old, new), tmp_path, "mut")
+    r = _battery(lib)
+    assert r.returncode == 1 and "FAILED" in r.stdout, "mutant survived: %s\n%s%s" % (what, r.stdout, r.stderr)
