@@ -1,0 +1,188 @@
+"""Benchmark of the PQ layer forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--configs cfg1,cfg3,...]
+
+Headline workload: the AlexNet-conv3-shaped PQ conv layer (32 x 256 x 13 x 13
+-> 384 channels, 3x3, pad 1, C'_s = 4, K = 128), synthetic seeded inputs
+resident in HBM before timing.  One step = one qcnn_conv_forward call, i.e.
+the whole hot path of a PQ conv layer: table build, gather-accumulate and
+epilogue, all in the library's HIP kernel.  Prints ONE JSON line.
+
+Timing: W untimed warm-up steps, then K steps between two HIP events on the
+stream the kernels run on, with a device synchronize on both sides.  Because
+the fused kernel is the only launch of a step, the event time / K is also
+the kernel's average duration used for the roofline figure.
+
+The other four workloads (the small conv, the fc6-shaped FC layer, the
+VGG-conv3-shaped conv and the AlexNet-shaped forward) are timed the same way
+and reported under "per_config".
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--configs", default="cfg1,cfg3,cfg4,cfg5",
+                    help="extra workloads to time besides the headline (comma list, or 'none')")
+    ap.add_argument("--only", default=None, help="time only this workload and exit (profiling runs)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the PQ forward shards over images with no exchange, and this "
+              "build runs on a single MI355X; --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1512_06473_amd import api, workloads, workmodel
+    from paper_1512_06473_amd.network import Network
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+
+    def T(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    def make_step(cfg):
+        d = workloads.generate(cfg)
+        wl = d["spec"]
+        if cfg == "cfg5":
+            net = Network(d["layers"], dev)
+            x = T(d["x"])
+            return (lambda: net.forward(x)), wl, d
+        L = d["layers"][0]
+        x, D, c = T(d["x"]), T(L["D"]), T(L["codes"])
+        if L["kind"] == "conv":
+            y = torch.empty((wl.N, L["spec"].Ct, api.out_size(wl.in_shape[1], L["spec"].dk, L["stride"], L["pad"]),
+                             api.out_size(wl.in_shape[2], L["spec"].dk, L["stride"], L["pad"])),
+                            dtype=torch.float32, device=dev)
+            return (lambda: api.conv_forward(x, D, c, L["stride"], L["pad"], out=y)), wl, d
+        y = torch.empty((wl.N, L["spec"].Ct), dtype=torch.float32, device=dev)
+        return (lambda: api.fc_forward(x, D, c, out=y)), wl, d
+
+    def time_steps(step, steps, warmup):
+        stream = torch.cuda.current_stream(dev)
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize(dev)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        wall = time.perf_counter() - t0
+        return e0.elapsed_time(e1) / steps, wall * 1e3 / steps
+
+    def work_of(wl):
+        per_layer = workmodel.workload_work(wl)
+        tot = dict(dense_flops=0, gathers=0, lut=0, lds=0, hbm=0)
+        for _, w in per_layer:
+            tot["dense_flops"] += w.dense_flops
+            tot["gathers"] += w.gathers
+            tot["lut"] += w.lut_entries
+            tot["lds"] += w.lds_bytes
+            tot["hbm"] += w.hbm_bytes
+        return tot
+
+    if args.only:
+        step, wl, _ = make_step(args.only)
+        ms, _ = time_steps(step, args.steps, args.warmup)
+        print(json.dumps({"only": args.only, "ms_per_step": ms}))
+        return
+
+    # ---------------------------------------------------------------- headline
+    step, wl, data = make_step("cfg2")
+    ms, wall_ms = time_steps(step, args.steps, args.warmup)
+    w = work_of(wl)
+    sec = ms * 1e-3
+    images_s = wl.N / sec
+    lds_achieved = w["lds"] / sec
+    line = {
+        "metric": "images/s (AlexNet-conv3-shaped PQ conv layer; also effective dense GFLOP/s and LDS roofline %)",
+        "value": images_s,
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded |N(0,1)| activations, N(0,0.05^2) codebooks, uniform uint8 codes)",
+        "config": {"workload": "cfg2: PQ conv 32x256x13x13 -> 384, 3x3 s1 p1, C's=4 (M=64), K=128",
+                   "global_batch": wl.N, "parallelism": "none (1 GPU)"},
+        "effective_dense_gflops": w["dense_flops"] / sec / 1e9,
+        "roofline": {
+            "bound": "lds",
+            "achieved": lds_achieved / 1e9,
+            "peak": workmodel.LDS_PEAK_BPS / 1e9,
+            "unit": "GB/s",
+            "frac": lds_achieved / workmodel.LDS_PEAK_BPS,
+            "traffic": None,
+            "kernel": "conv_pq (fused table build + gather)",
+            "algorithmic_bytes_per_launch": w["lds"],
+            "hbm_frac": w["hbm"] / sec / workmodel.HBM_PEAK_BPS,
+        },
+        "wall_ms_per_step": wall_ms,
+    }
+
+    # ------------------------------------------------------------ other configs
+    per = {}
+    extra = [] if args.configs == "none" else [c for c in args.configs.split(",") if c]
+    for cfg in extra:
+        st, wlc, _ = make_step(cfg)
+        steps = max(5, args.steps // (10 if cfg in ("cfg4", "cfg5") else 1))
+        m, _ = time_steps(st, steps, max(2, args.warmup // 2))
+        wc = work_of(wlc)
+        s = m * 1e-3
+        per[cfg] = {"ms_per_step": m, "images_s": wlc.N / s, "effective_dense_gflops": wc["dense_flops"] / s / 1e9,
+                    "lds_frac": wc["lds"] / s / workmodel.LDS_PEAK_BPS,
+                    "hbm_frac": wc["hbm"] / s / workmodel.HBM_PEAK_BPS, "steps": steps}
+        del st
+    line["per_config"] = per
+
+    # ------------------------------------------------------------ CPU baseline
+    if not args.no_cpu:
+        from oracle import oracle
+        L = data["layers"][0]
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            oracle.conv_lut(data["x"], L["D"], L["codes"], L["stride"], L["pad"])
+            reps += 1
+            if time.perf_counter() - t0 >= 10.0:
+                break
+        el = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": reps * wl.N / el, "unit": "images/s", "cores": oracle.threads(),
+                                "kind": "oracle",
+                                "sample": "%d full passes of the 32-image batch through the oracle's table path "
+                                          "(float64, OpenMP over images), %.1f s" % (reps, el)}
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

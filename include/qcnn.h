@@ -1,0 +1,128 @@
+/*
+ * qcnn.h -- C ABI of the product-quantized (PQ) layer forward on AMD MI355X
+ * (gfx950).
+ *
+ * Method: J. Wu, C. Leng, Y. Wang, Q. Hu, J. Cheng, "Quantized Convolutional
+ * Neural Networks for Mobile Devices", CVPR 2016 (arXiv 1512.06473).
+ *
+ * Notation (Sec. 2 and 3 of the paper): a layer has C_s input and C_t output
+ * channels.  The C_s-dimensional input space is split evenly into M subspaces
+ * of C'_s = C_s / M consecutive channels (Sec. 3.1; Sec. 3.2 splits a conv
+ * kernel along its input channels).  Subspace m has a sub-codebook D^(m) of K
+ * sub-codewords of length C'_s, and every weight sub-vector is stored as the
+ * index of one sub-codeword: k_m(c_t) for a fully-connected layer (Eq. (5)),
+ * k_m(c_t, p_k) for a conv kernel at offset p_k (Eq. (7)).
+ *
+ * Test phase (Sec. 3.1, the paragraph after Eq. (5); Sec. 3.2 after Eq. (7)):
+ *   1. table:  L[m][k][p_s] = < D^(m)_k , S^(m)_{p_s} >  at each input position;
+ *   2. gather: each response is the sum of M (conv: M d_k^2) table entries
+ *      selected by the codes.
+ *
+ * Conventions shared by every entry point
+ *   - All pointers are DEVICE pointers on the current HIP device (torch CUDA
+ *     tensors on ROCm qualify), C-contiguous, fp32 unless noted.  The caller
+ *     owns every buffer; the library never frees, retains or caches a caller
+ *     pointer beyond the call.
+ *   - Layouts: feature maps NCHW [N][C][H][W]; codebooks [M][K][C'_s] (row k
+ *     of subspace m is D^(m)_k); conv codes uint8 [C_t][d_k][d_k][M] with
+ *     codes[t][ky][kx][m] = k_m(c_t, (ky, kx)); FC codes uint8 [C_t][M] with
+ *     codes[t][m] = k_m(c_t).
+ *   - The conv pairing of input and kernel positions (Eq. (1)) is
+ *     cross-correlation: input row  yo * stride - pad + ky, column
+ *     xo * stride - pad + kx; positions in the zero padding contribute 0.
+ *     H_o = floor((H + 2 pad - d_k) / stride) + 1, likewise W_o.
+ *   - Optional bias [C_t] (NULL for none) is added after the sum, then ReLU if
+ *     relu != 0.  Neither is part of Eq. (5)/(7); NULL/0 give exactly those.
+ *   - Limits: 1 <= K <= 256 (codes are uint8), 1 <= C'_s <= 16, C_s = M C'_s.
+ *     Every code must be < K: this is a precondition that the release path
+ *     does not report; the kernels clamp a code to K - 1, so a bad code gives
+ *     a wrong value but never an access outside the layer's table.  Setting
+ *     the environment variable QCNN_CHECK_CODES=1 makes every call verify the
+ *     codes first (one extra kernel and a host sync) and return
+ *     QCNN_ERR_CODE_RANGE on violation.
+ *   - The code array must start at a 4-byte aligned address (any fresh
+ *     device allocation does); otherwise QCNN_ERR_UNSUPPORTED.
+ *   - Inputs and outputs must not overlap.
+ *   - Errors: every argument is validated on the host BEFORE any HIP call;
+ *     on a validation error nothing is launched and no output is touched.
+ *     Launch or runtime failures return QCNN_ERR_HIP.  No call aborts and no
+ *     C++ exception crosses the ABI.
+ *   - Execution is asynchronous on `stream` (a hipStream_t; NULL = the legacy
+ *     default stream): a call returns once its kernels are enqueued.  Calls
+ *     are reentrant; work that needs temporary device memory allocates it
+ *     stream-ordered on `stream` (hipMallocAsync / hipFreeAsync), so
+ *     concurrent calls on different streams never share it.
+ */
+#ifndef QCNN_H
+#define QCNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum qcnn_status {
+  QCNN_OK = 0,
+  QCNN_ERR_NULL = 1,        /* a required pointer is NULL */
+  QCNN_ERR_SHAPE = 2,       /* a size < 1 (pad < 0), C_s != M C'_s, empty output, overflow */
+  QCNN_ERR_K_RANGE = 3,     /* K < 1 or K > 256 */
+  QCNN_ERR_CODE_RANGE = 4,  /* a code >= K (only with QCNN_CHECK_CODES=1) */
+  QCNN_ERR_HIP = 5,         /* a HIP runtime call or kernel launch failed */
+  QCNN_ERR_UNSUPPORTED = 6, /* C'_s > 16, codes not 4-byte aligned, grid or LDS limits */
+  QCNN_ERR_ALIAS = 7        /* an output overlaps an input */
+} qcnn_status;
+
+/* Build the table of sub-codeword inner products (Sec. 3.1 test phase;
+ * Sec. 3.2, table over input positions; Table 1 term d_s^2 C_s K):
+ *   lut[n][m][k][y][x] = sum_{j < C'_s} codebooks[m][k][j] * x[n][m C'_s + j][y][x]
+ * x: [N][C_s][H][W]; codebooks: [M][K][C'_s]; lut (output): [N][M][K][H][W].
+ * A fully-connected input is H = W = 1.  The fused forwards below do not need
+ * this table in memory; this entry point exports it. */
+qcnn_status qcnn_lut_build(const float* x, int N, int C_s, int H, int W,
+                           const float* codebooks, int M, int K, int Csp,
+                           float* lut, void* stream);
+
+/* Forward of a PQ convolutional layer, Eq. (7):
+ *   y[n][t][yo][xo] = sum_{ky,kx inside} sum_m L[n][m][ codes[t][ky][kx][m] ]
+ *                                            [yo stride - pad + ky][xo stride - pad + kx]
+ *                     (+ bias[t]) (ReLU)
+ * x: [N][C_s][H][W]; codebooks: [M][K][C'_s]; codes: uint8 [C_t][d_k][d_k][M];
+ * bias: [C_t] or NULL; y (output): [N][C_t][H_o][W_o].
+ * The table is built tile by tile in LDS and never written to memory. */
+qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W,
+                              const float* codebooks, int M, int K, int Csp,
+                              const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                              const float* bias, int relu, float* y, void* stream);
+
+/* Forward of a PQ fully-connected layer, Eq. (5):
+ *   y[n][t] = sum_m L[n][m][ codes[t][m] ]  (+ bias[t]) (ReLU),
+ *   L[n][m][k] = sum_j codebooks[m][k][j] * x[n][m C'_s + j]
+ * x: [N][C_s]; codebooks: [M][K][C'_s]; codes: uint8 [C_t][M]; bias: [C_t] or
+ * NULL; y (output): [N][C_t]. */
+qcnn_status qcnn_fc_forward(const float* x, int N, int C_s,
+                            const float* codebooks, int M, int K, int Csp,
+                            const uint8_t* codes, int C_t,
+                            const float* bias, int relu, float* y, void* stream);
+
+/* Network glue between PQ layers (not part of the paper's method): max
+ * pooling over k x k windows with stride s and no padding,
+ *   y[n][c][yo][xo] = max_{dy,dx < k} x[n][c][yo s + dy][xo s + dx],
+ * H_o = floor((H - k) / s) + 1.  x: [N][C][H][W]; y (output): [N][C][H_o][W_o]. */
+qcnn_status qcnn_maxpool2d(const float* x, int N, int C, int H, int W, int k, int s,
+                           float* y, void* stream);
+
+/* Output size of a conv / pool along one axis (0 if empty).  Host only. */
+int qcnn_out_size(int in, int k, int stride, int pad);
+
+/* Static description of a status code.  Host only; never NULL. */
+const char* qcnn_status_string(qcnn_status s);
+
+/* ABI version, currently 1. */
+int qcnn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QCNN_H */

@@ -1,0 +1,137 @@
+"""Python binding of the C ABI (include/qcnn.h): argument marshalling only.
+
+torch tensors supply device memory and the current HIP stream; every step of
+the computation runs in the library's HIP kernels.  Functions take and return
+torch tensors on a ROCm device; outputs are allocated with torch.empty when
+``out`` is not given.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+
+from ._lib import check, lib
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int, device=None) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if t.dim() != ndim:
+        raise ValueError("%s must have %d dims, got shape %s" % (name, ndim, tuple(t.shape)))
+    if not t.is_cuda:
+        raise ValueError("%s must be on a GPU device" % name)
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def out_size(n: int, k: int, stride: int = 1, pad: int = 0) -> int:
+    return lib().qcnn_out_size(n, k, stride, pad)
+
+
+def lut_build(x: torch.Tensor, codebooks: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Table of sub-codeword inner products [N][M][K][H][W] (qcnn_lut_build).
+
+    x: [N][C_s][H][W] (or [N][C_s] for an FC input) fp32; codebooks [M][K][C'_s] fp32.
+    """
+    x4 = x if x.dim() == 4 else x.reshape(x.shape[0], x.shape[1], 1, 1)
+    _need(x4, "x", torch.float32, 4)
+    _need(codebooks, "codebooks", torch.float32, 3, x.device)
+    N, Cs, H, W = x4.shape
+    M, K, Csp = codebooks.shape
+    if out is None:
+        out = torch.empty((N, M, K, H, W), dtype=torch.float32, device=x.device)
+    _need(out, "out", torch.float32, 5, x.device)
+    if tuple(out.shape) != (N, M, K, H, W):
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, M, K, H, W)))
+    check(lib().qcnn_lut_build(x4.data_ptr(), N, Cs, H, W, codebooks.data_ptr(), M, K, Csp,
+                               out.data_ptr(), _stream(x)), "qcnn_lut_build")
+    return out
+
+
+def conv_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, stride: int = 1, pad: int = 0,
+                 bias: Optional[torch.Tensor] = None, relu: bool = False,
+                 out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """PQ conv layer forward, Eq. (7) (qcnn_conv_forward).
+
+    x [N][C_s][H][W] fp32, codebooks [M][K][C'_s] fp32, codes uint8 [C_t][d_k][d_k][M],
+    bias [C_t] fp32 or None.  Returns y [N][C_t][H_o][W_o].
+    """
+    _need(x, "x", torch.float32, 4)
+    _need(codebooks, "codebooks", torch.float32, 3, x.device)
+    _need(codes, "codes", torch.uint8, 4, x.device)
+    N, Cs, H, W = x.shape
+    M, K, Csp = codebooks.shape
+    Ct, dk, dk2, M2 = codes.shape
+    if dk != dk2 or M2 != M:
+        raise ValueError("codes shape %s does not match [C_t][d_k][d_k][M=%d]" % (tuple(codes.shape), M))
+    Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
+    bp = 0
+    if bias is not None:
+        _need(bias, "bias", torch.float32, 1, x.device)
+        if bias.shape[0] != Ct:
+            raise ValueError("bias must have C_t=%d entries" % Ct)
+        bp = bias.data_ptr()
+    if out is None:
+        out = torch.empty((N, Ct, max(Ho, 0), max(Wo, 0)), dtype=torch.float32, device=x.device)
+    _need(out, "out", torch.float32, 4, x.device)
+    if tuple(out.shape) != (N, Ct, Ho, Wo):
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, Ct, Ho, Wo)))
+    check(lib().qcnn_conv_forward(x.data_ptr(), N, Cs, H, W, codebooks.data_ptr(), M, K, Csp,
+                                  codes.data_ptr(), Ct, dk, stride, pad, bp or None, int(bool(relu)),
+                                  out.data_ptr(), _stream(x)), "qcnn_conv_forward")
+    return out
+
+
+def fc_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor,
+               bias: Optional[torch.Tensor] = None, relu: bool = False,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """PQ fully-connected layer forward, Eq. (5) (qcnn_fc_forward).
+
+    x [N][C_s] fp32 (any trailing shape is flattened), codebooks [M][K][C'_s],
+    codes uint8 [C_t][M], bias [C_t] or None.  Returns y [N][C_t].
+    """
+    if x.dim() != 2:
+        x = x.reshape(x.shape[0], -1)
+    _need(x, "x", torch.float32, 2)
+    _need(codebooks, "codebooks", torch.float32, 3, x.device)
+    _need(codes, "codes", torch.uint8, 2, x.device)
+    N, Cs = x.shape
+    M, K, Csp = codebooks.shape
+    Ct, M2 = codes.shape
+    if M2 != M:
+        raise ValueError("codes shape %s does not match [C_t][M=%d]" % (tuple(codes.shape), M))
+    bp = 0
+    if bias is not None:
+        _need(bias, "bias", torch.float32, 1, x.device)
+        if bias.shape[0] != Ct:
+            raise ValueError("bias must have C_t=%d entries" % Ct)
+        bp = bias.data_ptr()
+    if out is None:
+        out = torch.empty((N, Ct), dtype=torch.float32, device=x.device)
+    _need(out, "out", torch.float32, 2, x.device)
+    if tuple(out.shape) != (N, Ct):
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, Ct)))
+    check(lib().qcnn_fc_forward(x.data_ptr(), N, Cs, codebooks.data_ptr(), M, K, Csp, codes.data_ptr(), Ct,
+                                bp or None, int(bool(relu)), out.data_ptr(), _stream(x)), "qcnn_fc_forward")
+    return out
+
+
+def maxpool2d(x: torch.Tensor, k: int = 3, s: int = 2, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """k x k / stride s max pooling, no padding (qcnn_maxpool2d): network glue."""
+    _need(x, "x", torch.float32, 4)
+    N, C, H, W = x.shape
+    Ho, Wo = out_size(H, k, s, 0), out_size(W, k, s, 0)
+    if out is None:
+        out = torch.empty((N, C, max(Ho, 0), max(Wo, 0)), dtype=torch.float32, device=x.device)
+    _need(out, "out", torch.float32, 4, x.device)
+    check(lib().qcnn_maxpool2d(x.data_ptr(), N, C, H, W, k, s, out.data_ptr(), _stream(x)), "qcnn_maxpool2d")
+    return out

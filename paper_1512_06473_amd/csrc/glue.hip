@@ -1,0 +1,49 @@
+// Network glue that is not part of the paper's method, and a debug check.
+//
+// Max pooling joins the PQ layers of the AlexNet-shaped forward (k x k
+// windows, stride s, no padding).  It moves 4 bytes per input element once
+// and is bound by HBM; one thread computes one output.
+#include "qcnn_internal.h"
+
+namespace qcnn {
+namespace {
+
+__global__ __launch_bounds__(256) void maxpool_kernel(const float* __restrict__ x, int H, int W, int k, int s,
+                                                      int Ho, int Wo, size_t total, float* __restrict__ y) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int xo = (int)(i % Wo);
+  const int yo = (int)((i / Wo) % Ho);
+  const size_t plane = i / ((size_t)Wo * Ho);
+  const float* src = x + plane * H * W + (size_t)(yo * s) * W + xo * s;
+  float best = src[0];
+  for (int dy = 0; dy < k; ++dy)
+    for (int dx = 0; dx < k; ++dx) best = fmaxf(best, src[dy * W + dx]);
+  y[i] = best;
+}
+
+__global__ __launch_bounds__(256) void code_check_kernel(const uint8_t* __restrict__ codes, size_t n, int K,
+                                                         int* __restrict__ bad) {
+  int mine = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    mine += codes[i] >= K;
+  if (mine) atomicAdd(bad, mine);
+}
+
+}  // namespace
+
+hipError_t launch_maxpool(const float* x, int N, int C, int H, int W, int k, int s, int Ho, int Wo, float* y,
+                          hipStream_t stream) {
+  const size_t total = (size_t)N * C * Ho * Wo;
+  hipLaunchKernelGGL(maxpool_kernel, dim3((unsigned)ceil_div_z(total, 256)), dim3(256), 0, stream, x, H, W, k, s,
+                     Ho, Wo, total, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_code_check(const uint8_t* codes, size_t n, int K, int* bad, hipStream_t stream) {
+  const unsigned blocks = (unsigned)std::min<size_t>(1024, std::max<size_t>(1, ceil_div_z(n, 256)));
+  hipLaunchKernelGGL(code_check_kernel, dim3(blocks), dim3(256), 0, stream, codes, n, K, bad);
+  return hipGetLastError();
+}
+
+}  // namespace qcnn

@@ -1,0 +1,167 @@
+// C ABI of libqcnn: host-side validation, then kernel launches on the
+// caller's stream.  Every check runs before the first HIP call, so a rejected
+// call launches nothing and leaves every output untouched.
+#include <stdlib.h>
+#include <string.h>
+
+#include <initializer_list>
+
+#include "qcnn_internal.h"
+
+namespace {
+
+using qcnn::ConvShape;
+
+constexpr int kMaxGridYZ = 65535;
+constexpr size_t kMaxElems = (size_t)1 << 40;
+
+bool env_flag(const char* name) {
+  const char* v = getenv(name);
+  return v && *v && strcmp(v, "0") != 0;
+}
+
+// [a, a + na) and [b, b + nb) (bytes) overlap?
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+bool mul_ok(size_t* acc, size_t v) {
+  if (v != 0 && *acc > kMaxElems / v) return false;
+  *acc *= v;
+  return true;
+}
+
+// Elements of a product of positive ints, or 0 on overflow past kMaxElems.
+size_t elems(std::initializer_list<int> dims) {
+  size_t n = 1;
+  for (int d : dims)
+    if (!mul_ok(&n, (size_t)d)) return 0;
+  return n;
+}
+
+qcnn_status check_pq(int N, int Cs, int M, int K, int Csp) {
+  if (N < 1 || Cs < 1 || M < 1 || Csp < 1) return QCNN_ERR_SHAPE;
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  if ((long long)M * Csp != Cs) return QCNN_ERR_SHAPE;
+  if (Csp > 16) return QCNN_ERR_UNSUPPORTED;
+  if (N > kMaxGridYZ || M > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
+  return QCNN_OK;
+}
+
+qcnn_status hip_status(hipError_t e) { return e == hipSuccess ? QCNN_OK : QCNN_ERR_HIP; }
+
+// QCNN_CHECK_CODES=1: count codes >= K on the device and wait for the answer.
+qcnn_status check_codes(const uint8_t* codes, size_t n, int K, hipStream_t st) {
+  static const bool enabled = env_flag("QCNN_CHECK_CODES");
+  if (!enabled || K >= 256) return QCNN_OK;  // uint8 codes are always < 256
+  int* bad = nullptr;
+  int host = 0;
+  hipError_t e = hipMallocAsync((void**)&bad, sizeof(int), st);
+  if (e != hipSuccess) return QCNN_ERR_HIP;
+  e = hipMemsetAsync(bad, 0, sizeof(int), st);
+  if (e == hipSuccess) e = qcnn::launch_code_check(codes, n, K, bad, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(&host, bad, sizeof(int), hipMemcpyDeviceToHost, st);
+  hipError_t e2 = hipFreeAsync(bad, st);
+  if (e == hipSuccess) e = e2;
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return QCNN_ERR_HIP;
+  return host ? QCNN_ERR_CODE_RANGE : QCNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qcnn_version(void) { return 1; }
+
+int qcnn_out_size(int in, int k, int stride, int pad) {
+  if (in < 1 || k < 1 || stride < 1 || pad < 0) return 0;
+  const long long span = (long long)in + 2LL * pad - k;
+  if (span < 0) return 0;
+  return (int)(span / stride + 1);
+}
+
+const char* qcnn_status_string(qcnn_status s) {
+  switch (s) {
+    case QCNN_OK: return "ok";
+    case QCNN_ERR_NULL: return "a required pointer is NULL";
+    case QCNN_ERR_SHAPE: return "invalid shape (size < 1, C_s != M*C's, empty output or overflow)";
+    case QCNN_ERR_K_RANGE: return "K must be in [1, 256]";
+    case QCNN_ERR_CODE_RANGE: return "a code is >= K";
+    case QCNN_ERR_HIP: return "HIP runtime error";
+    case QCNN_ERR_UNSUPPORTED: return "layer not supported by the kernels (C's > 16, grid or LDS limits)";
+    case QCNN_ERR_ALIAS: return "an output overlaps an input";
+  }
+  return "unknown status";
+}
+
+qcnn_status qcnn_lut_build(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
+                           int Csp, float* lut, void* stream) {
+  if (!x || !codebooks || !lut) return QCNN_ERR_NULL;
+  if (H < 1 || W < 1) return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(N, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  const size_t nx = elems({N, C_s, H, W}), nd = elems({M, K, Csp});
+  const size_t nl = elems({N, M, K, H, W});
+  if (!nx || !nd || !nl) return QCNN_ERR_SHAPE;
+  if (overlap(lut, nl * 4, x, nx * 4) || overlap(lut, nl * 4, codebooks, nd * 4)) return QCNN_ERR_ALIAS;
+  return hip_status(qcnn::launch_lut_build(x, N, C_s, H, W, codebooks, M, K, Csp, lut, (hipStream_t)stream));
+}
+
+qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
+                              int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                              const float* bias, int relu, float* y, void* stream) {
+  if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
+  if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0) return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(N, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  const int Ho = qcnn_out_size(H, d_k, stride, pad), Wo = qcnn_out_size(W, d_k, stride, pad);
+  if (Ho < 1 || Wo < 1) return QCNN_ERR_SHAPE;
+  const size_t nx = elems({N, C_s, H, W}), nd = elems({M, K, Csp}), nc = elems({C_t, d_k, d_k, M});
+  const size_t ny = elems({N, C_t, Ho, Wo});
+  if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
+  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, nc) ||
+      overlap(y, ny * 4, bias, (size_t)C_t * 4))
+    return QCNN_ERR_ALIAS;
+  if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
+  ConvShape sh{N, C_s, H, W, M, K, Csp, C_t, d_k, stride, pad, Ho, Wo};
+  if (!qcnn::conv_supported(sh)) return QCNN_ERR_UNSUPPORTED;
+  if (qcnn::ceil_div(C_t, 32) > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
+  hipStream_t st = (hipStream_t)stream;
+  s = check_codes(codes, nc, K, st);
+  if (s != QCNN_OK) return s;
+  return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, codes, bias, relu ? 1 : 0, y, st));
+}
+
+qcnn_status qcnn_fc_forward(const float* x, int N, int C_s, const float* codebooks, int M, int K, int Csp,
+                            const uint8_t* codes, int C_t, const float* bias, int relu, float* y, void* stream) {
+  if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
+  if (C_t < 1) return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(N, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  const size_t nx = elems({N, C_s}), nd = elems({M, K, Csp}), nc = elems({C_t, M}), ny = elems({N, C_t});
+  if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
+  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, nc) ||
+      overlap(y, ny * 4, bias, (size_t)C_t * 4))
+    return QCNN_ERR_ALIAS;
+  if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
+  hipStream_t st = (hipStream_t)stream;
+  s = check_codes(codes, nc, K, st);
+  if (s != QCNN_OK) return s;
+  return hip_status(qcnn::launch_fc_forward(N, C_s, M, K, Csp, C_t, x, codebooks, codes, bias, relu ? 1 : 0, y, st));
+}
+
+qcnn_status qcnn_maxpool2d(const float* x, int N, int C, int H, int W, int k, int s, float* y, void* stream) {
+  if (!x || !y) return QCNN_ERR_NULL;
+  if (N < 1 || C < 1 || H < 1 || W < 1 || k < 1 || s < 1) return QCNN_ERR_SHAPE;
+  const int Ho = qcnn_out_size(H, k, s, 0), Wo = qcnn_out_size(W, k, s, 0);
+  if (Ho < 1 || Wo < 1) return QCNN_ERR_SHAPE;
+  const size_t nx = elems({N, C, H, W}), ny = elems({N, C, Ho, Wo});
+  if (!nx || !ny) return QCNN_ERR_SHAPE;
+  if (overlap(y, ny * 4, x, nx * 4)) return QCNN_ERR_ALIAS;
+  return hip_status(qcnn::launch_maxpool(x, N, C, H, W, k, s, Ho, Wo, y, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,54 @@
+// Internal declarations shared by the HIP sources of libqcnn (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "qcnn.h"
+
+namespace qcnn {
+
+constexpr int kWave = 64;  // CDNA wavefront width
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+inline size_t ceil_div_z(size_t a, size_t b) { return (a + b - 1) / b; }
+
+// Read byte `idx` of a code array whose base is 4-byte aligned (the C ABI
+// checks this).  The dword holding the byte is loaded instead of the byte, so
+// a wave-uniform index becomes one scalar load; an aligned dword never
+// straddles a page, so the bytes next to the last code cannot fault.
+__device__ __forceinline__ uint32_t code_at(const uint8_t* __restrict__ codes, size_t idx) {
+  const uint32_t word = reinterpret_cast<const uint32_t*>(codes)[idx >> 2];
+  return (word >> ((uint32_t)(idx & 3) * 8u)) & 0xffu;
+}
+
+// ---------------------------------------------------------------- launchers
+// Each returns a hipError_t from the launch (hipGetLastError after it).
+
+struct ConvShape {
+  int N, Cs, H, W, M, K, Csp, Ct, dk, stride, pad, Ho, Wo;
+};
+
+hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const float* D, int M, int K,
+                            int Csp, float* lut, hipStream_t stream);
+
+// Returns hipErrorInvalidConfiguration when no tiling fits the device.
+hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
+                               const float* bias, int relu, float* y, hipStream_t stream);
+
+hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
+                             const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream);
+
+hipError_t launch_maxpool(const float* x, int N, int C, int H, int W, int k, int s, int Ho, int Wo, float* y,
+                          hipStream_t stream);
+
+// Counts codes >= K into *bad (device int, zeroed by the caller).
+hipError_t launch_code_check(const uint8_t* codes, size_t n, int K, int* bad, hipStream_t stream);
+
+// True when the conv kernels can tile this layer (host-side, no HIP call).
+bool conv_supported(const ConvShape& s);
+
+}  // namespace qcnn

@@ -1,0 +1,137 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry point
+include/qcnn.h declares, and rejects bad arguments on the host before any HIP
+call (fake device pointers are safe here because validation fails first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1512_06473_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qcnn.h")
+
+FAKE = 0x10000      # never dereferenced: validation rejects the call first
+FAKE2 = 0x800000
+
+
+@pytest.fixture(scope="module")
+def L():
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qcnn_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    decl = declared_functions()
+    assert decl == sorted(_lib.SIGNATURES), (decl, sorted(_lib.SIGNATURES))
+
+
+def test_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_exported_dynamic_symbols():
+    # Plain C names (no C++ mangling) in the dynamic symbol table.
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
+    names = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    for name in declared_functions():
+        assert name in names, name
+
+
+def test_version_status_outsize(L):
+    assert L.qcnn_version() == 1
+    for code, name in _lib.STATUS.items():
+        s = L.qcnn_status_string(code)
+        assert isinstance(s, bytes) and len(s) > 0
+    assert L.qcnn_status_string(99) == b"unknown status"
+    assert L.qcnn_out_size(13, 3, 1, 1) == 13
+    assert L.qcnn_out_size(227, 11, 4, 0) == 55
+    assert L.qcnn_out_size(27, 5, 1, 2) == 27
+    assert L.qcnn_out_size(55, 3, 2, 0) == 27
+    assert L.qcnn_out_size(2, 3, 1, 0) == 0
+    assert L.qcnn_out_size(0, 1, 1, 0) == 0
+
+
+def conv(L, **kw):
+    a = dict(x=FAKE, N=2, Cs=8, H=5, W=5, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, Ct=4, dk=3, s=1, p=1,
+             bias=None, relu=0, y=FAKE2, stream=None)
+    a.update(kw)
+    return L.qcnn_conv_forward(a["x"], a["N"], a["Cs"], a["H"], a["W"], a["D"], a["M"], a["K"], a["Csp"],
+                               a["codes"], a["Ct"], a["dk"], a["s"], a["p"], a["bias"], a["relu"], a["y"],
+                               a["stream"])
+
+
+def fc(L, **kw):
+    a = dict(x=FAKE, N=2, Cs=8, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, Ct=4, bias=None, relu=0, y=FAKE2,
+             stream=None)
+    a.update(kw)
+    return L.qcnn_fc_forward(a["x"], a["N"], a["Cs"], a["D"], a["M"], a["K"], a["Csp"], a["codes"], a["Ct"],
+                             a["bias"], a["relu"], a["y"], a["stream"])
+
+
+NULL, SHAPE, KR, UNSUP, ALIAS = 1, 2, 3, 6, 7
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(x=None), NULL), (dict(D=None), NULL), (dict(codes=None), NULL), (dict(y=None), NULL),
+    (dict(N=0), SHAPE), (dict(Cs=0), SHAPE), (dict(H=0), SHAPE), (dict(W=-1), SHAPE), (dict(Ct=0), SHAPE),
+    (dict(dk=0), SHAPE), (dict(s=0), SHAPE), (dict(p=-1), SHAPE), (dict(M=3), SHAPE), (dict(Csp=3), SHAPE),
+    (dict(K=0), KR), (dict(K=257), KR), (dict(K=-5), KR),
+    (dict(H=1, W=1, p=0), SHAPE),                 # 3x3 kernel on 1x1 input: empty output
+    (dict(Cs=34, M=2, Csp=17), UNSUP),           # C's > 16
+    (dict(codes=FAKE + 1), UNSUP),                # codes not 4-byte aligned
+    (dict(N=70000), UNSUP),                       # grid limit
+    (dict(y=FAKE), ALIAS),                        # output == input
+    (dict(y=FAKE + 64), ALIAS),                   # output starts inside the input
+    (dict(bias=FAKE2 + 16), ALIAS),               # bias inside the output
+    (dict(N=60000, Cs=1 << 14, M=1 << 12, H=1 << 12, W=1 << 12, p=0), SHAPE),  # element count overflow
+])
+def test_conv_rejects(L, kw, want):
+    assert conv(L, **kw) == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(x=None), NULL), (dict(codes=None), NULL), (dict(y=None), NULL),
+    (dict(N=0), SHAPE), (dict(Ct=0), SHAPE), (dict(M=3), SHAPE), (dict(K=300), KR),
+    (dict(codes=FAKE + 2), UNSUP), (dict(y=FAKE), ALIAS),
+])
+def test_fc_rejects(L, kw, want):
+    assert fc(L, **kw) == want
+
+
+def test_lut_and_pool_reject(L):
+    assert L.qcnn_lut_build(None, 1, 8, 4, 4, FAKE, 2, 16, 4, FAKE2, None) == NULL
+    assert L.qcnn_lut_build(FAKE, 1, 8, 4, 4, FAKE, 2, 0, 4, FAKE2, None) == KR
+    assert L.qcnn_lut_build(FAKE, 1, 8, 0, 4, FAKE, 2, 16, 4, FAKE2, None) == SHAPE
+    assert L.qcnn_lut_build(FAKE, 1, 8, 4, 4, FAKE, 2, 16, 4, FAKE, None) == ALIAS
+    assert L.qcnn_maxpool2d(None, 1, 1, 5, 5, 3, 2, FAKE2, None) == NULL
+    assert L.qcnn_maxpool2d(FAKE, 1, 1, 2, 2, 3, 2, FAKE2, None) == SHAPE
+    assert L.qcnn_maxpool2d(FAKE, 1, 1, 5, 5, 3, 0, FAKE2, None) == SHAPE
+    assert L.qcnn_maxpool2d(FAKE, 1, 1, 5, 5, 3, 2, FAKE, None) == ALIAS
+
+
+def test_python_binding_rejects_host_tensors():
+    import torch
+    from paper_1512_06473_amd import api
+    x = torch.zeros(1, 8, 5, 5)
+    D = torch.zeros(2, 16, 4)
+    codes = torch.zeros(4, 3, 3, 2, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="GPU"):
+        api.conv_forward(x, D, codes, 1, 1)
+    with pytest.raises(TypeError):
+        api.conv_forward(x.double(), D, codes, 1, 1)
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "nope.so"))
+    with pytest.raises(ImportError, match="not built"):
+        _lib.lib()

@@ -1,0 +1,276 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bar (fp32 outputs): |gpu - oracle| <= 1e-5 * sum|terms| + 1e-6 per element,
+where sum|terms| is the oracle's sum of the magnitudes of every product that
+enters the output.  Integer-valued inputs (x in 0..7, D in -8..8) keep every
+partial sum exact in fp32, so there the comparison is bit-exact: that checks
+all code, subspace, offset, stride and padding indexing.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1512_06473_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+RTOL, ATOL = 1e-5, 1e-6
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_1512_06473_amd import api as a
+    return a
+
+
+def T(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def assert_bound(gpu, ref, A, what):
+    gpu = np.asarray(gpu, np.float64)
+    assert gpu.shape == ref.shape, (what, gpu.shape, ref.shape)
+    assert np.all(np.isfinite(gpu)), what + ": non-finite output"
+    err = np.abs(gpu - ref)
+    lim = RTOL * A + ATOL
+    bad = err > lim
+    assert not bad.any(), "%s: %d of %d outside the bound; worst err/limit %.3g" % (
+        what, int(bad.sum()), bad.size, float((err / lim).max()))
+
+
+def assert_exact(gpu, ref, what):
+    gpu = np.asarray(gpu)
+    assert gpu.shape == ref.shape, (what, gpu.shape, ref.shape)
+    diff = gpu.astype(np.float64) != ref
+    assert not diff.any(), "%s: %d of %d differ (integer data must be bit-exact)" % (what, int(diff.sum()), diff.size)
+
+
+def run_conv(api, dev, x, D, codes, s, p, bias=None, relu=False):
+    y = api.conv_forward(T(x, dev), T(D, dev), T(codes, dev), s, p,
+                         None if bias is None else T(bias, dev), relu)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def run_fc(api, dev, x, D, codes, bias=None, relu=False):
+    y = api.fc_forward(T(x, dev), T(D, dev), T(codes, dev), None if bias is None else T(bias, dev), relu)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def sample_points(rng, N, Ct, Ho, Wo, count):
+    """Random (n, t, yo, xo) plus every corner and edge midpoint of a few maps."""
+    pts = [np.stack([rng.integers(0, N, count), rng.integers(0, Ct, count),
+                     rng.integers(0, Ho, count), rng.integers(0, Wo, count)], 1)]
+    edge = []
+    for n in (0, N - 1):
+        for t in (0, Ct - 1, Ct // 2):
+            for yo in (0, Ho // 2, Ho - 1):
+                for xo in (0, Wo // 2, Wo - 1):
+                    edge.append((n, t, yo, xo))
+    pts.append(np.array(edge))
+    return np.concatenate(pts).astype(np.int32)
+
+
+# ------------------------------------------------------------ headline configs
+
+@pytest.mark.parametrize("integer", [False, True])
+@pytest.mark.parametrize("cfg", ["cfg1", "cfg2"])
+def test_conv_config_full(api, dev, oracle, cfg, integer):
+    d = wl.generate(cfg, integer=integer)
+    L = d["layers"][0]
+    y = run_conv(api, dev, d["x"], L["D"], L["codes"], L["stride"], L["pad"])
+    ref, A = oracle.conv_lut(d["x"], L["D"], L["codes"], L["stride"], L["pad"], with_bound=True)
+    if integer:
+        assert_exact(y, ref, cfg + " integer")
+    else:
+        assert_bound(y, ref, A, cfg)
+
+
+@pytest.mark.parametrize("integer", [False, True])
+def test_fc_config_full(api, dev, oracle, integer):
+    d = wl.generate("cfg3", integer=integer)
+    L = d["layers"][0]
+    y = run_fc(api, dev, d["x"], L["D"], L["codes"])
+    ref, A = oracle.fc_lut(d["x"], L["D"], L["codes"], with_bound=True)
+    if integer:
+        assert_exact(y, ref, "cfg3 integer")
+    else:
+        assert_bound(y, ref, A, "cfg3")
+
+
+@pytest.mark.parametrize("integer", [False, True])
+def test_cfg4_sampled(api, dev, oracle, integer):
+    # Full-size VGG-conv3-shaped layer, checked on sampled outputs (the oracle
+    # evaluates each one from its definition).
+    d = wl.generate("cfg4", integer=integer)
+    L = d["layers"][0]
+    y = run_conv(api, dev, d["x"], L["D"], L["codes"], L["stride"], L["pad"])
+    rng = np.random.Generator(np.random.PCG64(41))
+    pts = sample_points(rng, *y.shape, 6000)
+    ref, A = oracle.conv_points(d["x"], L["D"], L["codes"], pts, L["stride"], L["pad"])
+    got = y[tuple(pts.T)]
+    if integer:
+        assert_exact(got, ref, "cfg4 integer (sampled)")
+    else:
+        assert_bound(got, ref, A, "cfg4 (sampled)")
+
+
+def test_cfg4_two_images_full(api, dev, oracle):
+    d = wl.generate("cfg4", N=2)
+    L = d["layers"][0]
+    y = run_conv(api, dev, d["x"], L["D"], L["codes"], 1, 1)
+    ref, A = oracle.conv_lut(d["x"], L["D"], L["codes"], 1, 1, with_bound=True)
+    assert_bound(y, ref, A, "cfg4 N=2")
+
+
+def test_cfg5_per_layer_and_end_to_end(api, dev, oracle):
+    from paper_1512_06473_amd.network import Network
+    d = wl.generate("cfg5")
+    net = Network(d["layers"], dev)
+    keep = []
+    out = net.forward(T(d["x"], dev), keep)
+    torch.cuda.synchronize()
+    acts = [d["x"]] + [k.cpu().numpy() for k in keep]
+    rng = np.random.Generator(np.random.PCG64(55))
+    # Per layer: the oracle gets the GPU's own fp32 input of that layer.
+    for i, spec in enumerate(d["layers"]):
+        hin, hout = acts[i], acts[i + 1]
+        what = "cfg5 layer %d (%s)" % (i, spec["kind"])
+        if spec["kind"] == "pool":
+            assert_exact(hout, oracle.maxpool(hin, spec["k"], spec["s"]), what)
+        elif spec["kind"] == "conv":
+            pts = sample_points(rng, *hout.shape, 3000)
+            ref, A = oracle.conv_points(hin, spec["D"], spec["codes"], pts, spec["stride"], spec["pad"],
+                                        relu=spec["relu"])
+            assert_bound(hout[tuple(pts.T)], ref, A, what)
+        else:
+            x2 = hin.reshape(hin.shape[0], -1)
+            pts = np.stack([rng.integers(0, hout.shape[0], 3000), rng.integers(0, hout.shape[1], 3000)],
+                           1).astype(np.int32)
+            ref, A = oracle.fc_points(x2, spec["D"], spec["codes"], pts, relu=spec["relu"])
+            assert_bound(hout[tuple(pts.T)], ref, A, what)
+    # End to end on two images: the oracle network in float64 from the same
+    # input, bounded by the absolute network (|x|, |D|, no ReLU).
+    xs = d["x"][:2]
+    ref = oracle.network(xs, d["layers"])
+    A = oracle.network(xs, d["layers"], absolute=True)
+    assert_bound(out.cpu().numpy()[:2], ref, A, "cfg5 end to end")
+
+
+# ----------------------------------------------------------------- table export
+
+@pytest.mark.parametrize("shape", [(1, 16, 14, 14, 4, 16), (32, 256, 13, 13, 4, 128), (128, 9216, 1, 1, 4, 32),
+                                   (3, 6, 5, 7, 3, 64), (2, 40, 9, 9, 8, 256), (2, 5, 3, 4, 5, 1)])
+def test_lut_build(api, dev, oracle, shape):
+    N, Cs, H, W, Csp, K = shape
+    rng = np.random.Generator(np.random.PCG64(sum(shape)))
+    x, D, _ = wl.random_conv(rng, N, Cs, H, W, 1, 1, 1, 0, Csp, K)
+    L = api.lut_build(T(x, dev), T(D, dev))
+    torch.cuda.synchronize()
+    ref, A = oracle.lut(x, D, with_bound=True)
+    assert_bound(L.cpu().numpy(), ref, A, "lut %s" % (shape,))
+    xi, Di, _ = wl.random_conv(rng, N, Cs, H, W, 1, 1, 1, 0, Csp, K, integer=True)
+    Li = api.lut_build(T(xi, dev), T(Di, dev))
+    torch.cuda.synchronize()
+    assert_exact(Li.cpu().numpy(), oracle.lut(xi, Di), "lut integer %s" % (shape,))
+
+
+# ----------------------------------------------------------------- edge shapes
+
+CONV_EDGE = [
+    # N, Cs, H, W, Ct, dk, stride, pad, Csp, K
+    (1, 16, 14, 14, 32, 3, 1, 1, 4, 16),
+    (3, 12, 11, 9, 33, 3, 1, 1, 4, 32),      # C_t not a multiple of the channel block, odd map
+    (2, 3, 47, 47, 20, 11, 4, 0, 3, 64),     # conv1-like, stride 4, 11x11
+    (2, 24, 15, 15, 17, 5, 1, 2, 4, 128),    # conv2-like 5x5 pad 2
+    (1, 40, 9, 70, 5, 3, 1, 1, 8, 256),      # wide map (several column tiles), K = 256
+    (2, 10, 8, 8, 7, 1, 1, 0, 5, 9),         # 1x1 kernel, C's = 5 (runtime-length path)
+    (1, 32, 6, 6, 3, 3, 2, 3, 16, 8),        # pad > d_k/2, C's = 16
+    (4, 2, 5, 5, 65, 2, 3, 1, 1, 2),         # even kernel, stride 3, C's = 1
+    (1, 8, 1, 1, 4, 3, 1, 1, 4, 1),          # 1x1 input, only the centre tap is inside; K = 1
+    (2, 6, 30, 1, 3, 3, 2, 1, 2, 4),         # one-column map
+    (1, 64, 57, 57, 9, 3, 1, 1, 8, 128),     # positions far beyond one tile
+]
+
+
+@pytest.mark.parametrize("shape", CONV_EDGE)
+def test_conv_edge(api, dev, oracle, shape):
+    N, Cs, H, W, Ct, dk, s, p, Csp, K = shape
+    rng = np.random.Generator(np.random.PCG64(sum(shape) + 7))
+    x, D, codes = wl.random_conv(rng, N, Cs, H, W, Ct, dk, s, p, Csp, K)
+    b = rng.standard_normal(Ct).astype(np.float32)
+    for bias, relu in [(None, False), (b, True)]:
+        y = run_conv(api, dev, x, D, codes, s, p, bias, relu)
+        ref, A = oracle.conv_lut(x, D, codes, s, p, bias=bias, relu=relu, with_bound=True)
+        assert_bound(y, ref, A, "conv %s bias=%s relu=%s" % (shape, bias is not None, relu))
+    xi, Di, ci = wl.random_conv(rng, N, Cs, H, W, Ct, dk, s, p, Csp, K, integer=True)
+    assert_exact(run_conv(api, dev, xi, Di, ci, s, p), oracle.conv_lut(xi, Di, ci, s, p), "conv int %s" % (shape,))
+
+
+FC_EDGE = [
+    # N, Cs, Ct, Csp, K
+    (1, 64, 10, 4, 32),
+    (65, 96, 257, 4, 32),     # one image past a wave, C_t past a block
+    (130, 300, 1000, 3, 16),
+    (64, 4096, 1000, 4, 32),  # fc8-shaped, one wave of images
+    (7, 48, 33, 1, 16),       # C's = 1, K = 16 (the paper's fc8 setting)
+    (5, 80, 70, 8, 256),
+    (3, 10, 5, 5, 1),         # K = 1, runtime-length C's
+]
+
+
+@pytest.mark.parametrize("shape", FC_EDGE)
+def test_fc_edge(api, dev, oracle, shape):
+    N, Cs, Ct, Csp, K = shape
+    rng = np.random.Generator(np.random.PCG64(sum(shape) + 3))
+    x, D, codes = wl.random_fc(rng, N, Cs, Ct, Csp, K)
+    b = rng.standard_normal(Ct).astype(np.float32)
+    for bias, relu in [(None, False), (b, True)]:
+        y = run_fc(api, dev, x, D, codes, bias, relu)
+        ref, A = oracle.fc_lut(x, D, codes, bias=bias, relu=relu, with_bound=True)
+        assert_bound(y, ref, A, "fc %s bias=%s relu=%s" % (shape, bias is not None, relu))
+    xi, Di, ci = wl.random_fc(rng, N, Cs, Ct, Csp, K, integer=True)
+    assert_exact(run_fc(api, dev, xi, Di, ci), oracle.fc_lut(xi, Di, ci), "fc int %s" % (shape,))
+
+
+@pytest.mark.parametrize("shape", [(64, 96, 55, 55, 3, 2), (2, 5, 13, 13, 3, 2), (1, 2, 7, 9, 2, 3), (1, 1, 3, 3, 3, 1)])
+def test_maxpool(api, dev, oracle, shape):
+    N, C, H, W, k, s = shape
+    x = np.random.Generator(np.random.PCG64(1)).standard_normal((N, C, H, W)).astype(np.float32)
+    y = api.maxpool2d(T(x, dev), k, s)
+    torch.cuda.synchronize()
+    assert_exact(y.cpu().numpy(), oracle.maxpool(x, k, s), "maxpool %s" % (shape,))
+
+
+# ------------------------------------------------------------------ semantics
+
+def test_side_stream_and_determinism(api, dev, oracle):
+    d = wl.generate("cfg3", N=64)
+    L = d["layers"][0]
+    x, D, c = T(d["x"], dev), T(L["D"], dev), T(L["codes"], dev)
+    s = torch.cuda.Stream(dev)
+    with torch.cuda.stream(s):
+        y1 = api.fc_forward(x, D, c)
+        y2 = api.fc_forward(x, D, c)
+    s.synchronize()
+    assert torch.equal(y1, y2), "repeated calls must be bitwise identical"
+    ref, A = oracle.fc_lut(d["x"], L["D"], L["codes"], with_bound=True)
+    assert_bound(y1.cpu().numpy(), ref, A, "fc on a side stream")
+
+
+def test_out_of_range_codes_are_clamped(api, dev, oracle):
+    # Precondition violation: codes >= K.  The kernels clamp them to K - 1.
+    rng = np.random.Generator(np.random.PCG64(77))
+    x, D, codes = wl.random_conv(rng, 1, 8, 6, 6, 4, 3, 1, 1, 4, 16, integer=True)
+    bad = codes.copy()
+    bad[::2] = 200
+    y = run_conv(api, dev, x, D, bad, 1, 1)
+    assert_exact(y, oracle.conv_lut(x, D, np.minimum(bad, 15), 1, 1), "clamped codes")
