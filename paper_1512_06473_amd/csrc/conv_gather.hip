@@ -200,11 +200,12 @@ hipError_t launch_csp(const ConvPtrs& a, const ConvParams& p, int G, dim3 grid, 
 
 bool conv_supported(const ConvShape& s) {
   Tiling t;
-  return choose_tiling(s, &t);
+  return conv_flat_supported(s) || choose_tiling(s, &t);
 }
 
 hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
                                const float* bias, int relu, float* y, hipStream_t stream) {
+  if (conv_flat_supported(s)) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream);
   Tiling t;
   if (!choose_tiling(s, &t)) return hipErrorInvalidConfiguration;
   const ConvPtrs a{x, D, codes, bias, y};

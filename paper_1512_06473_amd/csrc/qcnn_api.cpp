@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <initializer_list>
+#include <mutex>
 
 #include "qcnn_internal.h"
 
@@ -51,6 +52,22 @@ qcnn_status check_pq(int N, int Cs, int M, int K, int Csp) {
 }
 
 qcnn_status hip_status(hipError_t e) { return e == hipSuccess ? QCNN_OK : QCNN_ERR_HIP; }
+
+// Once per device: keep memory freed by hipFreeAsync in the default pool, so
+// the per-call workspaces are recycled instead of remapped.
+bool prepare_device() {
+  static std::mutex mu;
+  static bool done[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return false;
+  if (dev >= 64) return true;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!done[dev]) {
+    if (qcnn::retain_pool_memory() != hipSuccess) return false;
+    done[dev] = true;
+  }
+  return true;
+}
 
 // QCNN_CHECK_CODES=1: count codes >= K on the device and wait for the answer.
 qcnn_status check_codes(const uint8_t* codes, size_t n, int K, hipStream_t st) {
@@ -130,6 +147,7 @@ qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, cons
   if (!qcnn::conv_supported(sh)) return QCNN_ERR_UNSUPPORTED;
   if (qcnn::ceil_div(C_t, 32) > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
   hipStream_t st = (hipStream_t)stream;
+  if (!prepare_device()) return QCNN_ERR_HIP;
   s = check_codes(codes, nc, K, st);
   if (s != QCNN_OK) return s;
   return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, codes, bias, relu ? 1 : 0, y, st));
@@ -148,6 +166,7 @@ qcnn_status qcnn_fc_forward(const float* x, int N, int C_s, const float* codeboo
     return QCNN_ERR_ALIAS;
   if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
   hipStream_t st = (hipStream_t)stream;
+  if (!prepare_device()) return QCNN_ERR_HIP;
   s = check_codes(codes, nc, K, st);
   if (s != QCNN_OK) return s;
   return hip_status(qcnn::launch_fc_forward(N, C_s, M, K, Csp, C_t, x, codebooks, codes, bias, relu ? 1 : 0, y, st));

@@ -51,4 +51,13 @@ hipError_t launch_code_check(const uint8_t* codes, size_t n, int K, int* bad, hi
 // True when the conv kernels can tile this layer (host-side, no HIP call).
 bool conv_supported(const ConvShape& s);
 
+// Stride-1 kernel on the flattened padded grid (conv_flat.hip).
+bool conv_flat_supported(const ConvShape& s);
+hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
+                            const float* bias, int relu, float* y, hipStream_t stream);
+
+// Keep freed stream-ordered allocations in the device's default pool
+// (called once per device before the first hipMallocAsync).
+hipError_t retain_pool_memory();
+
 }  // namespace qcnn

@@ -198,6 +198,17 @@ CONV_EDGE = [
     (1, 8, 1, 1, 4, 3, 1, 1, 4, 1),          # 1x1 input, only the centre tap is inside; K = 1
     (2, 6, 30, 1, 3, 3, 2, 1, 2, 4),         # one-column map
     (1, 64, 57, 57, 9, 3, 1, 1, 8, 128),     # positions far beyond one tile
+    # stride-1 shapes for the flattened-grid kernel: grid widths of every
+    # residue mod 4, pad 0..2, K not a multiple of 16, C's of 1..8, ragged
+    # channel blocks and tiles, long subspace ranges (split over blocks)
+    (3, 12, 13, 13, 200, 3, 1, 1, 4, 9),
+    (2, 20, 10, 11, 7, 3, 1, 0, 5, 32),
+    (1, 18, 9, 14, 33, 3, 1, 2, 6, 1),
+    (5, 16, 7, 12, 13, 3, 1, 1, 8, 64),
+    (2, 6, 16, 5, 3, 3, 1, 1, 3, 100),
+    (2, 512, 6, 6, 16, 3, 1, 1, 2, 16),
+    (4, 32, 8, 8, 40, 1, 1, 0, 4, 128),
+    (1, 7, 3, 3, 5, 3, 1, 1, 1, 7),
 ]
 
 
