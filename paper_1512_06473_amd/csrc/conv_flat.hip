@@ -48,7 +48,7 @@ struct FlatParams {
   int npb;               // 16-position blocks per table tile
   int tc, tblocks, splits, m_per_split;
   int work, per_xcd;
-  int ct_pad, tb;        // layout of the relaid codes: [M][ct_pad][tb] uint8
+  int ct_pad;            // layout of the relaid codes: [M][ct_pad][taps] uint8
   int relu;
 };
 
@@ -89,8 +89,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   extern __shared__ float4 lut4[];
   float* lut = reinterpret_cast<float*>(lut4);
   constexpr int TAPS = DK * DK;
-  constexpr int TB = (TAPS + 3) & ~3;  // code bytes per (subspace, channel), dword aligned
-  constexpr int CW = TW * TB / 4;      // code dwords per wave and subspace
+  constexpr int NQ = TW * TAPS;        // table reads per wave and subspace
+  constexpr int CW = (NQ + 3) / 4;     // code dwords per wave and subspace
+  constexpr int PD = 8;                // table reads kept in flight
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
 
@@ -182,13 +183,16 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         bb[kb][c] = kb < kblocks ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, doff[kb][c], 0, 0)) : 0.f;
   };
   load_operands(m0, av, bv);
+  // This wave's codes for subspace m: TW x TAPS consecutive bytes, in SGPRs.
+  auto load_codes = [&](int mm, uint32_t (&w)[CW]) {
+    const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)mm * p.ct_pad + t0) * TAPS);
+#pragma unroll
+    for (int k = 0; k < CW; ++k) w[k] = ow[k];
+  };
+  uint32_t cw[CW];
+  load_codes(m0, cw);
 
   for (int m = m0; m < m1; ++m) {
-    // ---- this wave's codes for subspace m, into SGPRs (used after the build)
-    const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)m * p.ct_pad + t0) * TB);
-    uint32_t cw[CW];
-#pragma unroll
-    for (int k = 0; k < CW; ++k) cw[k] = ow[k];
     __syncthreads();  // every wave is done reading the previous table
     // ---- table build: lut[k][pos] = sum_j D[m][k][j] x[pos][m C's + j]
 #pragma unroll
@@ -207,26 +211,29 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     }
     if (m + 1 < m1) load_operands(m + 1, av, bv);  // registers are free again after the build
     __syncthreads();
-    // ---- gather-accumulate, Eq. (7)
+    // ---- gather-accumulate, Eq. (7).  The (channel, tap) pairs of this wave
+    // form one stream of NQ table reads; PD of them are kept in flight.
+    auto tap_addr = [&](int k) -> uint32_t {
+      const uint32_t code = (cw[k >> 2] >> (8 * (k & 3))) & 0xffu;
+      return ((code * row_q) << 4) + tapbase[k % TAPS];
+    };
+    const char* lbase = reinterpret_cast<const char*>(lut4);
+    f4v qb[PD];
 #pragma unroll
-    for (int i = 0; i < TW; ++i) {
-      f4v q[TAPS];
+    for (int k = 0; k < PD && k < NQ; ++k) qb[k] = *reinterpret_cast<const f4v*>(lbase + tap_addr(k));
 #pragma unroll
-      for (int tap = 0; tap < TAPS; ++tap) {
-        const int byte = i * TB + tap;
-        const uint32_t code = (cw[byte >> 2] >> (8 * (byte & 3))) & 0xffu;
-        q[tap] = *reinterpret_cast<const f4v*>(reinterpret_cast<const char*>(lut4) + (((code * row_q) << 4) + tapbase[tap]));
-      }
-#pragma unroll
-      for (int tap = 0; tap < TAPS; ++tap) {
-        switch ((((tap / DK) * WG4) + (tap % DK)) & 3) {
-          case 0: tap_add<0>(acc[i], q[tap]); break;
-          case 1: tap_add<1>(acc[i], q[tap]); break;
-          case 2: tap_add<2>(acc[i], q[tap]); break;
-          default: tap_add<3>(acc[i], q[tap]); break;
-        }
+    for (int k = 0; k < NQ; ++k) {
+      const f4v q = qb[k % PD];
+      if (k + PD < NQ) qb[k % PD] = *reinterpret_cast<const f4v*>(lbase + tap_addr(k + PD));
+      const int i = k / TAPS, tap = k % TAPS;
+      switch ((((tap / DK) * WG4) + (tap % DK)) & 3) {
+        case 0: tap_add<0>(acc[i], q); break;
+        case 1: tap_add<1>(acc[i], q); break;
+        case 2: tap_add<2>(acc[i], q); break;
+        default: tap_add<3>(acc[i], q); break;
       }
     }
+    if (m + 1 < m1) load_codes(m + 1, cw);  // latency hidden by the next table build
   }
 
   // ---- epilogue
@@ -253,36 +260,29 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   }
 }
 
-// codes8[m][t][tap] = min(code, K-1), the codes of one (subspace, channel)
-// padded to a whole number of dwords; padding entries 0.  A block owns 8
-// output channels: their codes are 8 taps M contiguous bytes, read coalesced
-// into LDS, then written out as 8 tb-byte groups per subspace.
-constexpr int kCodeT = 8;
+// codes8[m][t][tap] = min(code, K-1); channels past C_t are 0.  One thread
+// writes one dword (4 consecutive bytes of the [m][t][tap] order); the bytes
+// it reads are scattered, but the whole code array is small and L2-resident.
 __global__ __launch_bounds__(256) void flat_codes_kernel(const uint8_t* __restrict__ codes, int Ct, int taps, int M,
-                                                         int K, int ct_pad, int tb, int mchunk,
-                                                         uint8_t* __restrict__ codes8) {
-  extern __shared__ uint8_t stage[];  // [kCodeT][taps][mchunk]
-  const int t0 = blockIdx.x * kCodeT;
-  for (int m0 = 0; m0 < M; m0 += mchunk) {
-    const int mc = min(mchunk, M - m0);
-    __syncthreads();
-    for (int i = threadIdx.x; i < kCodeT * taps * mc; i += blockDim.x) {
-      const int mm = i % mc, row = i / mc;  // row = tl * taps + tap
-      const int t = t0 + row / taps;
+                                                         int K, int ct_pad, uint32_t* __restrict__ codes8) {
+  const int nwords = (M * ct_pad * taps + 3) / 4;  // the plan keeps M ct_pad taps below 2^31
+  const int per_m = ct_pad * taps;
+  for (int wi = blockIdx.x * blockDim.x + threadIdx.x; wi < nwords; wi += gridDim.x * blockDim.x) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int o = wi * 4 + b;
+      const int m = o / per_m;
+      const int r = o - m * per_m;
+      const int t = r / taps, tap = r - t * taps;
       uint32_t v = 0;
-      if (t < Ct) {
-        v = codes[((size_t)t0 * taps + row) * M + m0 + mm];
+      if (m < M && t < Ct) {
+        v = codes[((size_t)t * taps + tap) * M + m];
         v = v < (uint32_t)(K - 1) ? v : (uint32_t)(K - 1);
       }
-      stage[i] = (uint8_t)v;
+      word |= v << (8 * b);
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < mc * kCodeT * tb; i += blockDim.x) {
-      const int tap = i % tb, rest = i / tb;
-      const int tl = rest % kCodeT, mm = rest / kCodeT;
-      const uint8_t v = tap < taps ? stage[(tl * taps + tap) * mc + mm] : (uint8_t)0;
-      codes8[((size_t)(m0 + mm) * ct_pad + t0 + tl) * tb + tap] = v;
-    }
+    codes8[wi] = word;
   }
 }
 
@@ -348,7 +348,6 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
   const size_t lds = (size_t)((s.K + 15) / 16 * 16) * p.PR * sizeof(float);
   (void)kMaxKB;
   if (lds > kLdsMax) return false;
-  p.tb = (s.dk * s.dk + 3) & ~3;
   bool found = false;
   double best = 0;
   for (int TW : {12}) {
@@ -366,6 +365,7 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
       q.work = (int)work;
       q.per_xcd = ceil_div(q.work, 8);
       q.ct_pad = tblocks * tc;
+      if ((long long)s.M * q.ct_pad * s.dk * s.dk + 4 > (1LL << 31)) continue;
       const double c = plan_cost(q, TW);
       if (!found || c < best) {
         found = true;
@@ -429,19 +429,18 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
     fprintf(stderr, "qcnn conv_flat: tiles=%d tc=%d tblocks=%d splits=%d work=%d PR=%d npb=%d lds=%zu\n",
             pl.p.tiles, pl.p.tc, pl.p.tblocks, pl.p.splits, pl.p.work, pl.p.PR, pl.p.npb, pl.lds);
   const FlatParams& p = pl.p;
-  const size_t n_codes = (size_t)p.M * p.ct_pad * p.tb;
+  const size_t n_codes = (size_t)p.M * p.ct_pad * p.dk * p.dk;
   const size_t out_elems = (size_t)p.N * p.Ct * p.Ho * p.Wo;
-  const size_t code_bytes = (n_codes + 255) & ~(size_t)255;
+  const size_t code_bytes = (n_codes + 4 + 255) & ~(size_t)255;  // + the tail of the last dword load
   const size_t ws = code_bytes + (p.splits > 1 ? (size_t)p.splits * out_elems * sizeof(float) : 0);
   char* base = nullptr;
   hipError_t e = hipMallocAsync((void**)&base, ws, stream);
   if (e != hipSuccess) return e;
   uint8_t* codes8 = reinterpret_cast<uint8_t*>(base);
   float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
-  const int mchunk = std::min(p.M, 4096 / (kCodeT * p.dk * p.dk));
-  hipLaunchKernelGGL(flat_codes_kernel, dim3(ceil_div(p.ct_pad, kCodeT)), dim3(256),
-                     (size_t)kCodeT * p.dk * p.dk * mchunk, stream, codes, p.Ct, p.dk * p.dk, p.M, p.K, p.ct_pad,
-                     p.tb, mchunk, codes8);
+  const size_t nwords = (n_codes + 3) / 4;
+  hipLaunchKernelGGL(flat_codes_kernel, dim3((unsigned)std::min<size_t>(2048, ceil_div_z(nwords, 256))), dim3(256), 0,
+                     stream, codes, p.Ct, p.dk * p.dk, p.M, p.K, p.ct_pad, reinterpret_cast<uint32_t*>(codes8));
   e = hipGetLastError();
   if (e == hipSuccess) {
     switch (p.dk) {
