@@ -9,9 +9,13 @@ the whole hot path of a PQ conv layer: table build, gather-accumulate and
 epilogue, all in the library's HIP kernel.  Prints ONE JSON line.
 
 Timing: W untimed warm-up steps, then K steps between two HIP events on the
-stream the kernels run on, with a device synchronize on both sides.  Because
-the fused kernel is the only launch of a step, the event time / K is also
-the kernel's average duration used for the roofline figure.
+stream the kernels run on, with a device synchronize on both sides; that
+gives `value` and `ms_per_step`.  A second pass of K steps switches on the
+library's kernel timing (HIP events recorded by the library on the same
+stream around the main gather kernel of each call) and gives the kernel's
+average duration, from which the roofline's `achieved` is computed.  A step
+also runs a code re-layout kernel and, when the subspaces are split over
+workgroups, a split-sum kernel; those are outside the kernel timing.
 
 The other four workloads (the small conv, the fc6-shaped FC layer, the
 VGG-conv3-shaped conv and the AlexNet-shaped forward) are timed the same way
@@ -40,6 +44,28 @@ def parse():
                     help="extra workloads to time besides the headline (comma list, or 'none')")
     ap.add_argument("--only", default=None, help="time only this workload and exit (profiling runs)")
     return ap.parse_args()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary, or None when there is none or when the kernel's
+    source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "%s_%s_traffic.txt" % (kernel, workload))
+    src = os.path.join(ROOT, "paper_1512_06473_amd", "csrc", "%s.hip" % kernel)
+    if not (os.path.exists(path) and os.path.exists(src)):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def main():
@@ -107,19 +133,46 @@ def main():
             tot["hbm"] += w.hbm_bytes
         return tot
 
+    def kernel_ms(step, steps):
+        """Average duration of the main kernel of a step, from the library's
+        own HIP events on the launch stream (a second pass of `steps` steps)."""
+        api.timing_read()  # drop anything recorded earlier
+        api.timing_enable(True)
+        try:
+            for _ in range(steps):
+                step()
+        finally:
+            api.timing_enable(False)
+        total, n = api.timing_read()
+        return total / n, n
+
+    if args.only == "copy":
+        # Plain device-to-device copy of a known size: the calibration run for
+        # the FETCH_SIZE / WRITE_SIZE counters.
+        nbytes = 256 << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        ms, _ = time_steps(lambda: dst.copy_(src), args.steps, args.warmup)
+        print(json.dumps({"only": "copy", "bytes_read": nbytes, "bytes_written": nbytes, "ms_per_step": ms,
+                          "GB_s": 2 * nbytes / ms / 1e6}))
+        return
     if args.only:
         step, wl, _ = make_step(args.only)
         ms, _ = time_steps(step, args.steps, args.warmup)
-        print(json.dumps({"only": args.only, "ms_per_step": ms}))
+        kms, kn = kernel_ms(step, args.steps)
+        print(json.dumps({"only": args.only, "ms_per_step": ms, "main_kernel_us": kms * 1e3,
+                          "main_kernel_launches": kn}))
         return
 
     # ---------------------------------------------------------------- headline
     step, wl, data = make_step("cfg2")
     ms, wall_ms = time_steps(step, args.steps, args.warmup)
+    kms, klaunches = kernel_ms(step, args.steps)
     w = work_of(wl)
     sec = ms * 1e-3
     images_s = wl.N / sec
-    lds_achieved = w["lds"] / sec
+    lds_achieved = w["lds"] / (kms * 1e-3)
+    traffic = measured_traffic("conv_flat", "cfg2")
     line = {
         "metric": "images/s (AlexNet-conv3-shaped PQ conv layer; also effective dense GFLOP/s and LDS roofline %)",
         "value": images_s,
@@ -142,10 +195,12 @@ def main():
             "peak": workmodel.LDS_PEAK_BPS / 1e9,
             "unit": "GB/s",
             "frac": lds_achieved / workmodel.LDS_PEAK_BPS,
-            "traffic": None,
-            "kernel": "conv_pq (fused table build + gather)",
+            "traffic": traffic,
+            "kernel": "conv_flat_kernel (fused table build + gather-accumulate)",
+            "kernel_us": kms * 1e3,
+            "kernel_launches_timed": klaunches,
             "algorithmic_bytes_per_launch": w["lds"],
-            "hbm_frac": w["hbm"] / sec / workmodel.HBM_PEAK_BPS,
+            "hbm_frac": w["hbm"] / (kms * 1e-3) / workmodel.HBM_PEAK_BPS,
         },
         "wall_ms_per_step": wall_ms,
     }
@@ -157,11 +212,13 @@ def main():
         st, wlc, _ = make_step(cfg)
         steps = max(5, args.steps // (10 if cfg in ("cfg4", "cfg5") else 1))
         m, _ = time_steps(st, steps, max(2, args.warmup // 2))
+        km, kn = kernel_ms(st, steps)
         wc = work_of(wlc)
         s = m * 1e-3
         per[cfg] = {"ms_per_step": m, "images_s": wlc.N / s, "effective_dense_gflops": wc["dense_flops"] / s / 1e9,
                     "lds_frac": wc["lds"] / s / workmodel.LDS_PEAK_BPS,
-                    "hbm_frac": wc["hbm"] / s / workmodel.HBM_PEAK_BPS, "steps": steps}
+                    "hbm_frac": wc["hbm"] / s / workmodel.HBM_PEAK_BPS, "steps": steps,
+                    "main_kernels_ms_per_step": km * kn / steps, "main_kernel_launches_per_step": kn // steps}
         del st
     line["per_config"] = per
 

@@ -121,6 +121,21 @@ const char* qcnn_status_string(qcnn_status s);
 /* ABI version, currently 1. */
 int qcnn_version(void);
 
+/* Kernel timing, for benchmarks and profiling.  While enabled, every
+ * compute call above records a pair of HIP events on its stream around its
+ * main kernel (the gather kernel of qcnn_conv_forward and qcnn_fc_forward,
+ * the table kernel of qcnn_lut_build); code re-layout and split-sum kernels
+ * are outside the pair.  Off by default; when off the calls create no events.
+ * Enabling and disabling are process-wide and take effect for later calls. */
+qcnn_status qcnn_timing_enable(int enable);
+
+/* Waits for every pair recorded since the last read, returns their summed
+ * elapsed milliseconds in *total_ms and their number in *launches, then
+ * destroys them.  QCNN_ERR_NULL if an argument is NULL; QCNN_ERR_HIP if an
+ * event could not be created, recorded or read (the sums then cover the
+ * readable pairs only). */
+qcnn_status qcnn_timing_read(double* total_ms, long long* launches);
+
 #ifdef __cplusplus
 }
 #endif

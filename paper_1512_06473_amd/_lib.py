@@ -22,6 +22,8 @@ SIGNATURES = {
     "qcnn_out_size": ([I, I, I, I], I),
     "qcnn_status_string": ([I], ctypes.c_char_p),
     "qcnn_version": ([], I),
+    "qcnn_timing_enable": ([I], I),
+    "qcnn_timing_read": ([ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong)], I),
 }
 
 STATUS = {0: "QCNN_OK", 1: "QCNN_ERR_NULL", 2: "QCNN_ERR_SHAPE", 3: "QCNN_ERR_K_RANGE",

@@ -7,7 +7,8 @@ torch tensors on a ROCm device; outputs are allocated with torch.empty when
 """
 from __future__ import annotations
 
-from typing import Optional
+import ctypes
+from typing import Optional, Tuple
 
 import torch
 
@@ -135,3 +136,16 @@ def maxpool2d(x: torch.Tensor, k: int = 3, s: int = 2, out: Optional[torch.Tenso
     _need(out, "out", torch.float32, 4, x.device)
     check(lib().qcnn_maxpool2d(x.data_ptr(), N, C, H, W, k, s, out.data_ptr(), _stream(x)), "qcnn_maxpool2d")
     return out
+
+
+def timing_enable(enable: bool = True) -> None:
+    """Switch the library's kernel timing on or off (events around each call's main kernel)."""
+    check(lib().qcnn_timing_enable(1 if enable else 0), "qcnn_timing_enable")
+
+
+def timing_read() -> Tuple[float, int]:
+    """(summed milliseconds, launches) of the main kernels timed since the last read."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_longlong(0)
+    check(lib().qcnn_timing_read(ctypes.byref(ms), ctypes.byref(n)), "qcnn_timing_read")
+    return ms.value, n.value

@@ -124,7 +124,10 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
 #pragma unroll
   for (int tap = 0; tap < TAPS; ++tap)
     tapbase[tap] = (uint32_t)(lane + (((tap / DK) * p.Wg + (tap % DK)) >> 2)) * 16u;
-  const uint32_t row_q = (uint32_t)p.PR / 4u;  // table row stride in 16-byte quads
+  // Table row stride in bytes, held in a VGPR so that code * stride + tap
+  // base is one v_mad_u32_u24 (codes < 256, strides < 2^16).
+  uint32_t row_bytes = (uint32_t)p.PR * 4u;
+  asm volatile("" : "+v"(row_bytes));
   // Input element (n, m C's + j, yy, xx) sits at byte ((n Cs + j) HW + yy W + xx) * 4
   // + m C's HW * 4; the subspace part goes into the scalar offset.  Only
   // the per-lane (vector) offset is range checked, so every lane whose value
@@ -215,7 +218,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     // form one stream of NQ table reads; PD of them are kept in flight.
     auto tap_addr = [&](int k) -> uint32_t {
       const uint32_t code = (cw[k >> 2] >> (8 * (k & 3))) & 0xffu;
-      return ((code * row_q) << 4) + tapbase[k % TAPS];
+      return __umul24(code, row_bytes) + tapbase[k % TAPS];
     };
     const char* lbase = reinterpret_cast<const char*>(lut4);
     f4v qb[PD];
@@ -403,8 +406,8 @@ hipError_t launch_nc(const FlatPlan& pl, const float* x, const float* D, const u
 template <int DK>
 hipError_t launch_wg(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
                      float* y, float* partial, hipStream_t stream) {
-  if (DK == 1) return launch_nc<DK, 0>(pl, x, D, codes8, bias, y, partial, stream);  // one tap: no shift
-  switch (pl.p.Wg & 3) {
+  if constexpr (DK == 1) return launch_nc<DK, 0>(pl, x, D, codes8, bias, y, partial, stream);  // one tap: no shift
+  else switch (pl.p.Wg & 3) {
     case 0: return launch_nc<DK, 0>(pl, x, D, codes8, bias, y, partial, stream);
     case 1: return launch_nc<DK, 1>(pl, x, D, codes8, bias, y, partial, stream);
     case 2: return launch_nc<DK, 2>(pl, x, D, codes8, bias, y, partial, stream);
@@ -443,6 +446,7 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
                      stream, codes, p.Ct, p.dk * p.dk, p.M, p.K, p.ct_pad, reinterpret_cast<uint32_t*>(codes8));
   e = hipGetLastError();
   if (e == hipSuccess) {
+    KernelTimer timer(stream);
     switch (p.dk) {
       case 1: e = launch_wg<1>(pl, x, D, codes8, bias, y, partial, stream); break;
       case 3: e = launch_wg<3>(pl, x, D, codes8, bias, y, partial, stream); break;

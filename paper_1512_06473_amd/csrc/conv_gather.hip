@@ -182,6 +182,7 @@ hipError_t launch_g(const ConvPtrs& a, const ConvParams& p, dim3 grid, size_t ld
   auto k = conv_pq_generic<CSP, G, kTW>;
   hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
+  KernelTimer timer(stream);
   hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, stream, a.x, a.D, a.codes, a.bias, a.y, p);
   return hipGetLastError();
 }

@@ -162,6 +162,7 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
   }
   e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e == hipSuccess) {
+    KernelTimer timer(stream);
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, x, D, codes, bias, y, partial, p);
     e = hipGetLastError();
   }

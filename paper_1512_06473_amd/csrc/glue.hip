@@ -22,6 +22,8 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const float* __restrict__ 
   y[i] = best;
 }
 
+__global__ void zero_int_kernel(int* __restrict__ v) { *v = 0; }
+
 __global__ __launch_bounds__(256) void code_check_kernel(const uint8_t* __restrict__ codes, size_t n, int K,
                                                          int* __restrict__ bad) {
   int mine = 0;
@@ -42,6 +44,7 @@ hipError_t launch_maxpool(const float* x, int N, int C, int H, int W, int k, int
 
 hipError_t launch_code_check(const uint8_t* codes, size_t n, int K, int* bad, hipStream_t stream) {
   const unsigned blocks = (unsigned)std::min<size_t>(1024, std::max<size_t>(1, ceil_div_z(n, 256)));
+  hipLaunchKernelGGL(zero_int_kernel, dim3(1), dim3(1), 0, stream, bad);  // a kernel, not a memset node
   hipLaunchKernelGGL(code_check_kernel, dim3(blocks), dim3(256), 0, stream, codes, n, K, bad);
   return hipGetLastError();
 }

@@ -54,6 +54,7 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
   const int ky = 256 / px;
   dim3 block(px, ky);
   dim3 grid(ceil_div(HW, px), M, N);
+  KernelTimer timer(stream);
   switch (Csp) {
 #define QCNN_LUT_CASE(C) \
   case C: hipLaunchKernelGGL(lut_build_kernel<C>, grid, block, 0, stream, x, D, lut, Cs, HW, M, K, Csp); break;

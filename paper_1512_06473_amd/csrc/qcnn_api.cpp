@@ -4,8 +4,11 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <initializer_list>
 #include <mutex>
+#include <utility>
+#include <vector>
 
 #include "qcnn_internal.h"
 
@@ -77,8 +80,7 @@ qcnn_status check_codes(const uint8_t* codes, size_t n, int K, hipStream_t st) {
   int host = 0;
   hipError_t e = hipMallocAsync((void**)&bad, sizeof(int), st);
   if (e != hipSuccess) return QCNN_ERR_HIP;
-  e = hipMemsetAsync(bad, 0, sizeof(int), st);
-  if (e == hipSuccess) e = qcnn::launch_code_check(codes, n, K, bad, st);
+  e = qcnn::launch_code_check(codes, n, K, bad, st);
   if (e == hipSuccess) e = hipMemcpyAsync(&host, bad, sizeof(int), hipMemcpyDeviceToHost, st);
   hipError_t e2 = hipFreeAsync(bad, st);
   if (e == hipSuccess) e = e2;
@@ -87,9 +89,82 @@ qcnn_status check_codes(const uint8_t* codes, size_t n, int K, hipStream_t st) {
   return host ? QCNN_ERR_CODE_RANGE : QCNN_OK;
 }
 
+// Kernel timing state: event pairs recorded by KernelTimer, read back and
+// destroyed by qcnn_timing_read.
+struct TimingState {
+  std::mutex mu;
+  std::atomic<bool> on{false};
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pairs;
+  bool failed = false;
+};
+
+TimingState& timing() {
+  static TimingState t;
+  return t;
+}
+
 }  // namespace
 
+namespace qcnn {
+
+KernelTimer::KernelTimer(hipStream_t stream) : stream_(stream) {
+  if (!timing().on.load(std::memory_order_relaxed)) return;
+  if (hipEventCreate(&start_) != hipSuccess) {
+    start_ = nullptr;
+  } else if (hipEventRecord(start_, stream_) != hipSuccess) {
+    (void)hipEventDestroy(start_);
+    start_ = nullptr;
+  }
+  if (!start_) {
+    std::lock_guard<std::mutex> lock(timing().mu);
+    timing().failed = true;
+  }
+}
+
+KernelTimer::~KernelTimer() {
+  if (!start_) return;
+  hipEvent_t stop = nullptr;
+  TimingState& t = timing();
+  if (hipEventCreate(&stop) != hipSuccess || hipEventRecord(stop, stream_) != hipSuccess) {
+    if (stop) (void)hipEventDestroy(stop);
+    (void)hipEventDestroy(start_);
+    std::lock_guard<std::mutex> lock(t.mu);
+    t.failed = true;
+    return;
+  }
+  std::lock_guard<std::mutex> lock(t.mu);
+  t.pairs.emplace_back(start_, stop);
+}
+
+}  // namespace qcnn
+
 extern "C" {
+
+qcnn_status qcnn_timing_enable(int enable) {
+  timing().on.store(enable != 0);
+  return QCNN_OK;
+}
+
+qcnn_status qcnn_timing_read(double* total_ms, long long* launches) {
+  if (!total_ms || !launches) return QCNN_ERR_NULL;
+  TimingState& t = timing();
+  std::lock_guard<std::mutex> lock(t.mu);
+  double sum = 0.0;
+  bool ok = !t.failed;
+  for (auto& pr : t.pairs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(pr.second) != hipSuccess || hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
+      ok = false;
+    sum += ms;
+    (void)hipEventDestroy(pr.first);
+    (void)hipEventDestroy(pr.second);
+  }
+  *total_ms = sum;
+  *launches = (long long)t.pairs.size();
+  t.pairs.clear();
+  t.failed = false;
+  return ok ? QCNN_OK : QCNN_ERR_HIP;
+}
 
 int qcnn_version(void) { return 1; }
 

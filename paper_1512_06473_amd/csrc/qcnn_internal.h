@@ -45,7 +45,7 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
 hipError_t launch_maxpool(const float* x, int N, int C, int H, int W, int k, int s, int Ho, int Wo, float* y,
                           hipStream_t stream);
 
-// Counts codes >= K into *bad (device int, zeroed by the caller).
+// Zeroes *bad (a device int), then counts the codes >= K into it.
 hipError_t launch_code_check(const uint8_t* codes, size_t n, int K, int* bad, hipStream_t stream);
 
 // True when the conv kernels can tile this layer (host-side, no HIP call).
@@ -55,6 +55,21 @@ bool conv_supported(const ConvShape& s);
 bool conv_flat_supported(const ConvShape& s);
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
                             const float* bias, int relu, float* y, hipStream_t stream);
+
+// Brackets the main kernel of a call with a pair of HIP events on its
+// stream while kernel timing is switched on (qcnn_timing_enable); does
+// nothing otherwise.  The pairs are read back by qcnn_timing_read.
+class KernelTimer {
+ public:
+  explicit KernelTimer(hipStream_t stream);
+  ~KernelTimer();
+  KernelTimer(const KernelTimer&) = delete;
+  KernelTimer& operator=(const KernelTimer&) = delete;
+
+ private:
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+};
 
 // Keep freed stream-ordered allocations in the device's default pool
 // (called once per device before the first hipMallocAsync).

@@ -135,3 +135,14 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "nope.so"))
     with pytest.raises(ImportError, match="not built"):
         _lib.lib()
+
+
+def test_timing_calls_without_gpu(L):
+    # Nothing recorded yet: reading returns zero launches without touching HIP.
+    ms = ctypes.c_double(-1.0)
+    n = ctypes.c_longlong(-1)
+    assert L.qcnn_timing_read(None, ctypes.byref(n)) == NULL
+    assert L.qcnn_timing_read(ctypes.byref(ms), None) == NULL
+    assert L.qcnn_timing_enable(0) == 0
+    assert L.qcnn_timing_read(ctypes.byref(ms), ctypes.byref(n)) == 0
+    assert ms.value == 0.0 and n.value == 0
