@@ -1,36 +1,53 @@
-// Stride-1 PQ convolution on a flattened, zero-padded image grid.
+// PQ convolution on a flattened image grid, with the table in LDS.
 //
 // Paper: Sec. 3.2, Eq. (7): each response sums, over the receptive-field
 // pairs (p_k, p_s) and the subspaces m, the table entry <D^(m)_k, S^(m)_{p_s}>
 // selected by the code k = k_m(c_t, p_k); the table is pre-computed over the
 // input positions (paragraph after Eq. (7); Table 1 term d_s^2 C_s K).
 //
-// Layout.  All N images are stacked into one flat grid of width Wg = W + pad
-// whose rows are the padded image rows; the right padding of a row is the
-// left padding of the next one and the bottom padding of an image is the top
-// padding of the next, so every halo cell is a zero shared by its neighbours.
-// Output (n, yo, xo) is grid slot s = (n (H + pad) + yo) Wg + xo, and kernel
-// tap (ky, kx) reads grid position s + ky Wg + kx: one uniform shift per tap.
-// Slots with yo >= H_o or xo >= W_o are computed and discarded.
+// Layout.  The output maps are stacked into one flat grid of width Wg; grid
+// slot s = ((n S + strip) Hg + yo) Wg + xl holds output (n, yo, strip sw + xl)
+// (S column strips of sw outputs per image; S = 1 for maps that fit).
+//
+// Virtual subspaces.  The sum of Eq. (7) is split into pieces that are each
+// a stride-1 correlation with a small ROWS x COLS tap grid on that layout:
+//   * stride s: a kernel tap (ky, kx) = (s u + a, s v + b) reads input
+//     (s (yo + u) + a - pad, s (xo + v) + b - pad), so for a fixed phase
+//     (a, b) the tap is a shift (u, v) of the output slot over a table built
+//     at the phase's input positions;
+//   * large kernels: the kernel rows are cut into G groups of ROWS rows, and
+//     group g's table is built at input rows shifted by s g ROWS.
+// A virtual subspace v = (m, a, b, g) has its own table (subspace m's
+// codewords against the inputs it samples); its taps are the ROWS x COLS
+// grid (u', v') with kernel tap ky = s (g ROWS + u') + a, kx = s v' + b, and
+// grid entries past the kernel read a row of zeros.  Tap (u', v') of slot s
+// reads table position s + u' Wg + v': one uniform shift per tap.
+// For stride 1 with ROWS <= the rows the halo absorbs, neighbouring images
+// share their zero halo (Wg = W + pad, Hg = H + pad: the right padding of a
+// row is the left padding of the next one); otherwise each image keeps its
+// own margin (Hg = H_o + ROWS - 1, Wg = sw + COLS - 1) and every table value
+// comes from its own coordinates.
 //
 // Work split.  A tile is 252 consecutive slots: lane l of every wave owns
 // the quad of slots 4l .. 4l+3 (lane 63 only supplies neighbour values; the
-// next tile recomputes its slots).  For one subspace m the workgroup builds,
-// in LDS, the table rows of every grid position the tile can touch,
+// next tile recomputes its slots).  For one virtual subspace the workgroup
+// builds, in LDS, the table rows of every position the tile can touch,
 // lut[k][0 .. P_T), with MFMA (v_mfma_f32_16x16x4_f32: 16 positions x 16
 // codewords x 4 input channels per instruction).  Each wave then owns TW
 // output channels; per (channel, tap) the code is a wave-uniform scalar, the
 // lane reads the aligned 16-byte quad of its row at the tap's quad offset,
 // and the 0..3 elements that fall past the quad come from lane l+1 through a
-// DPP wave shift.  So a tap costs one ds_read_b128, one address add and four
-// fp32 adds per lane, all reads are aligned and bank-conflict free.
+// DPP wave shift.  So a tap costs one ds_read_b128, one address
+// multiply-add and four fp32 adds per lane, all reads are aligned and
+// bank-conflict free.
 //
-// Codes are re-laid out once per call to codes8[m][t][tap] (clamped to K-1),
-// so that one wave's codes for a subspace are a few contiguous dwords that
-// scalar loads bring into SGPRs before the table build; the gather then needs
-// one scalar extract and multiply per code.  The subspaces may be
-// split over workgroups (partial sums reduced in a fixed order by a second
-// kernel); blocks are mapped so that the workgroups of one tile share an XCD
+// Codes are re-laid out once per call to codes8[v][t][tap] (clamped to K-1,
+// the zero row for grid taps past the kernel), so that one wave's codes for
+// a virtual subspace are a few contiguous dwords that scalar loads bring into
+// SGPRs during the table build.  The virtual subspaces may be split over
+// workgroups: each then stores its partial sums tile by tile (whole cache
+// lines per store instruction) and a second kernel adds them in a fixed
+// order.  Blocks are mapped so that the workgroups of one tile share an XCD
 // (and its L2) for the input reads of the table build.
 #include <stdio.h>
 #include <stdlib.h>
@@ -40,15 +57,18 @@
 namespace qcnn {
 
 struct FlatParams {
-  int N, Cs, H, W, M, K, Csp, Ct, dk, pad, Ho, Wo;
-  int Wg, Hg;            // grid width W + pad, grid rows per image H + pad
-  int grid_pos;          // positions that hold input or halo: (N Hg + pad) Wg
-  int tiles;             // ceil(N Hg Wg / 252)
+  int N, Cs, H, W, M, K, Csp, Ct, dk, stride, pad, Ho, Wo;
+  int S, sw;             // column strips per image, output columns per strip (S = 1: sw = W_o)
+  int Wg, Hg;            // grid width, grid rows per image
+  int grid_pos;          // grid positions that may hold input (beyond: zero)
+  int tiles;             // ceil(N S Hg Wg / 252)
+  int G, V;              // kernel-row groups; virtual subspaces M s^2 G
+  int zrow;              // table row of zeros for grid taps past the kernel, or -1
   int PR;                // table row stride in floats (PR / 4 odd: conflict-free MFMA stores)
   int npb;               // 16-position blocks per table tile
-  int tc, tblocks, splits, m_per_split;
+  int tc, tblocks, splits, v_per_split;
   int work, per_xcd;
-  int ct_pad;            // layout of the relaid codes: [M][ct_pad][taps] uint8
+  int ct_pad;            // layout of the relaid codes: [V][ct_pad][taps] uint8
   int relu;
 };
 
@@ -79,7 +99,10 @@ __device__ __forceinline__ void tap_add(float (&a)[4], const f4v& q) {
   }
 }
 
-template <int DK, int WG4, int NC, int TW>
+// GEN = false: one virtual subspace per subspace (stride 1, one row group),
+// so the input offsets of the table build are fixed per lane.  GEN = true:
+// stride phases and/or row groups; the offsets move with the virtual subspace.
+template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
 __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __restrict__ x,
                                                                  const float* __restrict__ D,
                                                                  const uint8_t* __restrict__ codes8,
@@ -88,9 +111,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
                                                                  FlatParams p) {
   extern __shared__ float4 lut4[];
   float* lut = reinterpret_cast<float*>(lut4);
-  constexpr int TAPS = DK * DK;
-  constexpr int NQ = TW * TAPS;        // table reads per wave and subspace
-  constexpr int CW = (NQ + 3) / 4;     // code dwords per wave and subspace
+  constexpr int TAPS = ROWS * COLS;
+  constexpr int NQ = TW * TAPS;        // table reads per wave and virtual subspace
+  constexpr int CW = (NQ + 3) / 4;     // code dwords per wave and virtual subspace
   constexpr int PD = 8;                // table reads kept in flight
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -106,56 +129,73 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   const int split = rem - tb * p.splits;
   const int s0 = tile * kTileSlots;
   const int t0 = tb * p.tc + wave * TW;
-  const int m0 = split * p.m_per_split;
-  const int m1 = min(p.M, m0 + p.m_per_split);
+  const int v0 = split * p.v_per_split;
+  const int v1 = min(p.V, v0 + p.v_per_split);
   const int HW = p.H * p.W;
 
-  // ---- table-build operands that do not depend on m.  A operand: lane
-  // supplies row l % 16 (a position) and column l / 16 (an input channel of
-  // the subspace); B operand: row l / 16 (channel), column l % 16 (codeword).
-  // Both are read with raw buffer loads: an offset past the buffer's end
-  // returns 0, which is exactly the value of a halo position, of a channel
-  // beyond C'_s and of a codeword beyond K.
+  if (p.zrow >= 0)  // the zero row; the build never writes it, the first barrier publishes it
+    for (int i = threadIdx.x; i < p.PR; i += kThreads) lut[p.zrow * p.PR + i] = 0.f;
+
+  // ---- table-build operands.  A operand: lane supplies row l % 16 (a
+  // position) and column l / 16 (an input channel of the subspace); B
+  // operand: row l / 16 (channel), column l % 16 (codeword).  Both are read
+  // with raw buffer loads: an offset past the buffer's end returns 0, which
+  // is exactly the value of a halo position, of a channel beyond C'_s and of
+  // a codeword beyond K.
   constexpr uint32_t kOOB = 0x80000000u;
   const int arow = lane & 15, acol = lane >> 4;
-  // LDS byte address of this lane's quad for each tap, relative to a table row:
-  // the tap shifts the quad index by (ky Wg + kx) / 4.
+  // LDS byte address of this lane's quad for each tap, relative to a table
+  // row: tap (u', v') shifts the quad index by (u' Wg + v') / 4.
   uint32_t tapbase[TAPS];
 #pragma unroll
   for (int tap = 0; tap < TAPS; ++tap)
-    tapbase[tap] = (uint32_t)(lane + (((tap / DK) * p.Wg + (tap % DK)) >> 2)) * 16u;
+    tapbase[tap] = (uint32_t)(lane + (((tap / COLS) * p.Wg + (tap % COLS)) >> 2)) * 16u;
   // Table row stride in bytes, held in a VGPR so that code * stride + tap
   // base is one v_mad_u32_u24 (codes < 256, strides < 2^16).
   uint32_t row_bytes = (uint32_t)p.PR * 4u;
   asm volatile("" : "+v"(row_bytes));
   // Input element (n, m C's + j, yy, xx) sits at byte ((n Cs + j) HW + yy W + xx) * 4
-  // + m C's HW * 4; the subspace part goes into the scalar offset.  Only
-  // the per-lane (vector) offset is range checked, so every lane whose value
-  // must be 0 gets an offset past the end on its own.
-  uint32_t xoff[kMaxPB][NC];
+  // + m C's HW * 4; the subspace part goes into the scalar offset.  Only the
+  // per-lane (vector) offset is range checked, so every lane whose value must
+  // be 0 gets an offset past the end on its own.  Grid position f of this
+  // lane: input row s i - pad (+ the virtual subspace's row shift), column
+  // s (strip sw + c) - pad (+ its column shift).
+  uint32_t xoff[kMaxPB][NC];   // !GEN: final offsets
+  int ybase[kMaxPB], xbase[kMaxPB];  // GEN: input row / column before the shift (invalid: a large negative)
+  int xb[kMaxPB][NC];          // GEN: offset before the shift
 #pragma unroll
   for (int i = 0; i < kMaxPB; ++i) {
     const int pb = wave + kWaves * i;
     const int f = s0 + 16 * pb + arow;
     const int row = f / p.Wg, c = f - row * p.Wg;
-    const int n = row / p.Hg, yy = row - n * p.Hg - p.pad, xx = c - p.pad;
-    const bool ok = pb < p.npb && f < p.grid_pos && n < p.N && yy >= 0 && xx >= 0;
+    const int g = row / p.Hg, n = g / p.S, strip = g - n * p.S;
+    const int yy = p.stride * (row - g * p.Hg) - p.pad, xx = p.stride * (strip * p.sw + c) - p.pad;
+    const bool ok = pb < p.npb && f < p.grid_pos && n < p.N;
+    if constexpr (GEN) {
+      ybase[i] = ok ? yy : -(1 << 28);
+      xbase[i] = xx;
+    }
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) {
       const int j = 4 * cc + acol;
-      xoff[i][cc] = (ok && j < p.Csp) ? (uint32_t)((n * p.Cs + j) * HW + yy * p.W + xx) * 4u : kOOB;
+      if constexpr (GEN) {
+        xb[i][cc] = j < p.Csp ? (n * p.Cs + j) * HW + yy * p.W + xx : -(1 << 30);
+      } else {
+        const bool in = ok && j < p.Csp && yy >= 0 && yy < p.H && xx >= 0 && xx < p.W;
+        xoff[i][cc] = in ? (uint32_t)((n * p.Cs + j) * HW + yy * p.W + xx) * 4u : kOOB;
+      }
     }
   }
   // Codebook entry (k, j) of subspace m sits at byte (k C's + j) * 4 of that
-  // subspace's codebook; rows k >= K and channels j >= C's are past the end.
-  uint32_t doff[kMaxKB][NC];
+  // subspace's codebook.  Rows k >= K fall past the buffer's end by
+  // themselves; channels j >= C's get an offset past the end here.
+  uint32_t dlane[NC];
 #pragma unroll
-  for (int kb = 0; kb < kMaxKB; ++kb)
-#pragma unroll
-    for (int cc = 0; cc < NC; ++cc) {
-      const int k = kb * 16 + arow, j = 4 * cc + acol;
-      doff[kb][cc] = (k < p.K && j < p.Csp) ? (uint32_t)(k * p.Csp + j) * 4u : kOOB;
-    }
+  for (int cc = 0; cc < NC; ++cc) {
+    const int j = 4 * cc + acol;
+    dlane[cc] = j < p.Csp ? (uint32_t)(arow * p.Csp + j) * 4u : kOOB;
+  }
+  const uint32_t dstep = (uint32_t)(16 * p.Csp * 4);  // bytes from one 16-row block to the next
   const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(x), 0, (int)((size_t)p.N * p.Cs * HW * 4), 0x00020000);
 
@@ -168,35 +208,60 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   const int kblocks = (p.K + 15) >> 4;
   const f4v zero4 = {0.f, 0.f, 0.f, 0.f};
 
-  // Table-build operands, double-buffered: those of subspace m+1 are loaded
-  // while the waves gather from the table of subspace m.
+  // Table-build operands, double-buffered: those of virtual subspace v+1 are
+  // loaded while the waves gather from the table of v.
   float av[kMaxPB][NC], bv[kMaxKB][NC];
-  auto load_operands = [&](int mm, float (&a)[kMaxPB][NC], float (&bb)[kMaxKB][NC]) {
+  auto load_operands = [&](int vv, float (&a)[kMaxPB][NC], float (&bb)[kMaxKB][NC]) {
+    int m = vv, dy = 0, dx = 0;
+    if constexpr (GEN) {  // v = ((m s + a) s + b) G + g
+      const int g = vv % p.G;
+      int r = vv / p.G;
+      dx = r % p.stride;
+      r /= p.stride;
+      dy = r % p.stride + p.stride * g * ROWS;
+      m = r / p.stride;
+    }
     const __amdgpu_buffer_rsrc_t dres = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<float*>(D + (size_t)mm * p.K * p.Csp), 0, p.K * p.Csp * 4, 0x00020000);
+        const_cast<float*>(D + (size_t)m * p.K * p.Csp), 0, p.K * p.Csp * 4, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < kMaxPB; ++i)
+    for (int i = 0; i < kMaxPB; ++i) {
+      bool in = true;
+      if constexpr (GEN) {
+        const int yy = ybase[i] + dy, xx = xbase[i] + dx;
+        in = yy >= 0 && yy < p.H && xx >= 0 && xx < p.W;
+      }
 #pragma unroll
-      for (int c = 0; c < NC; ++c)
-        a[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, xoff[i][c], mm * p.Csp * HW * 4, 0));
+      for (int c = 0; c < NC; ++c) {
+        uint32_t off;
+        if constexpr (GEN)
+          off = (in && xb[i][c] >= -(1 << 29)) ? (uint32_t)((xb[i][c] + dy * p.W + dx) * 4) : kOOB;
+        else
+          off = xoff[i][c];
+        a[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, m * p.Csp * HW * 4, 0));
+      }
+    }
 #pragma unroll
     for (int kb = 0; kb < kMaxKB; ++kb)
 #pragma unroll
       for (int c = 0; c < NC; ++c)
-        bb[kb][c] = kb < kblocks ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, doff[kb][c], 0, 0)) : 0.f;
+        bb[kb][c] = kb < kblocks ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, dlane[c] + kb * dstep, 0, 0))
+                                 : 0.f;
   };
-  load_operands(m0, av, bv);
-  // This wave's codes for subspace m: TW x TAPS consecutive bytes, in SGPRs.
-  auto load_codes = [&](int mm, uint32_t (&w)[CW]) {
-    const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)mm * p.ct_pad + t0) * TAPS);
+  load_operands(v0, av, bv);
+  // This wave's codes for virtual subspace v: TW x TAPS consecutive bytes, in SGPRs.
+  auto load_codes = [&](int vv, uint32_t (&cwv)[CW]) {
+    const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)vv * p.ct_pad + t0) * TAPS);
 #pragma unroll
-    for (int k = 0; k < CW; ++k) w[k] = ow[k];
+    for (int k = 0; k < CW; ++k) cwv[k] = ow[k];
   };
   uint32_t cw[CW];
-  load_codes(m0, cw);
 
-  for (int m = m0; m < m1; ++m) {
+  for (int v = v0; v < v1; ++v) {
     __syncthreads();  // every wave is done reading the previous table
+    // The codes of v arrive during the build.  (A barrier waits for every
+    // outstanding scalar load, so issuing them before one would expose their
+    // latency.)
+    load_codes(v, cw);
     // ---- table build: lut[k][pos] = sum_j D[m][k][j] x[pos][m C's + j]
 #pragma unroll
     for (int kb = 0; kb < kMaxKB; ++kb) {
@@ -212,7 +277,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         }
       }
     }
-    if (m + 1 < m1) load_operands(m + 1, av, bv);  // registers are free again after the build
+    if (v + 1 < v1) load_operands(v + 1, av, bv);  // registers are free again after the build
     __syncthreads();
     // ---- gather-accumulate, Eq. (7).  The (channel, tap) pairs of this wave
     // form one stream of NQ table reads; PD of them are kept in flight.
@@ -229,78 +294,114 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
       const f4v q = qb[k % PD];
       if (k + PD < NQ) qb[k % PD] = *reinterpret_cast<const f4v*>(lbase + tap_addr(k + PD));
       const int i = k / TAPS, tap = k % TAPS;
-      switch ((((tap / DK) * WG4) + (tap % DK)) & 3) {
+      switch ((((tap / COLS) * WG4) + (tap % COLS)) & 3) {
         case 0: tap_add<0>(acc[i], q); break;
         case 1: tap_add<1>(acc[i], q); break;
         case 2: tap_add<2>(acc[i], q); break;
         default: tap_add<3>(acc[i], q); break;
       }
     }
-    if (m + 1 < m1) load_codes(m + 1, cw);  // latency hidden by the next table build
   }
 
   // ---- epilogue
   if (lane == kWave - 1) return;  // its slots belong to the next tile
+  if (partial) {
+    // partial[split][tile][t][j][lane] holds slot 4 lane + j of the tile:
+    // every store instruction writes 256 contiguous bytes.
+    float* dst = partial + (((size_t)split * p.tiles + tile) * p.ct_pad + t0) * 256 + lane;
+#pragma unroll
+    for (int i = 0; i < TW; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dst[(size_t)i * 256 + 64 * j] = acc[i][j];
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int s = s0 + 4 * lane + j;
-    const int row = s / p.Wg, xo = s - row * p.Wg;
-    const int n = row / p.Hg, yo = row - n * p.Hg;
-    if (n >= p.N || yo >= p.Ho || xo >= p.Wo) continue;
+    const int row = s / p.Wg, xl = s - row * p.Wg;
+    const int g = row / p.Hg, yo = row - g * p.Hg;
+    const int n = g / p.S, xo = (g - n * p.S) * p.sw + xl;
+    if (n >= p.N || yo >= p.Ho || xl >= p.sw || xo >= p.Wo) continue;
 #pragma unroll
     for (int i = 0; i < TW; ++i) {
       const int t = t0 + i;
       if (t >= p.Ct) break;
       const size_t o = (((size_t)n * p.Ct + t) * p.Ho + yo) * p.Wo + xo;
-      if (partial) {
-        partial[(size_t)split * p.N * p.Ct * p.Ho * p.Wo + o] = acc[i][j];
-      } else {
-        float v = acc[i][j] + (bias ? bias[t] : 0.f);
-        if (p.relu) v = fmaxf(v, 0.f);
-        y[o] = v;
-      }
+      float v = acc[i][j] + (bias ? bias[t] : 0.f);
+      if (p.relu) v = fmaxf(v, 0.f);
+      y[o] = v;
     }
   }
 }
 
-// codes8[m][t][tap] = min(code, K-1); channels past C_t are 0.  One thread
-// writes one dword (4 consecutive bytes of the [m][t][tap] order); the bytes
-// it reads are scattered, but the whole code array is small and L2-resident.
-__global__ __launch_bounds__(256) void flat_codes_kernel(const uint8_t* __restrict__ codes, int Ct, int taps, int M,
-                                                         int K, int ct_pad, uint32_t* __restrict__ codes8) {
-  const int nwords = (M * ct_pad * taps + 3) / 4;  // the plan keeps M ct_pad taps below 2^31
-  const int per_m = ct_pad * taps;
+// codes8[v][t][tap]: the code of kernel tap (ky, kx) = (s (g ROWS + u') + a,
+// s v' + b) of subspace m for virtual subspace v = ((m s + a) s + b) G + g
+// and grid tap (u', v') = (tap / COLS, tap % COLS), clamped to K-1; grid taps
+// past the kernel get the zero row; channels past C_t get 0.  One thread
+// writes one dword (4 consecutive bytes); the bytes it reads are scattered,
+// but the whole code array is small and L2-resident.
+struct CodeMap {
+  int Ct, dk, stride, M, G, rows, cols, K, ct_pad, zrow, V;
+};
+
+__global__ __launch_bounds__(256) void flat_codes_kernel(const uint8_t* __restrict__ codes, CodeMap q,
+                                                         uint32_t* __restrict__ codes8) {
+  const int taps = q.rows * q.cols;
+  const int per_v = q.ct_pad * taps;
+  const int nwords = (q.V * per_v + 3) / 4;  // the plan keeps V ct_pad taps below 2^31
   for (int wi = blockIdx.x * blockDim.x + threadIdx.x; wi < nwords; wi += gridDim.x * blockDim.x) {
     uint32_t word = 0;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int o = wi * 4 + b;
-      const int m = o / per_m;
-      const int r = o - m * per_m;
+    for (int bb = 0; bb < 4; ++bb) {
+      const int o = wi * 4 + bb;
+      const int v = o / per_v;
+      const int r = o - v * per_v;
       const int t = r / taps, tap = r - t * taps;
-      uint32_t v = 0;
-      if (m < M && t < Ct) {
-        v = codes[((size_t)t * taps + tap) * M + m];
-        v = v < (uint32_t)(K - 1) ? v : (uint32_t)(K - 1);
+      uint32_t val = 0;
+      if (v < q.V && t < q.Ct) {
+        const int g = v % q.G;
+        int rr = v / q.G;
+        const int pb = rr % q.stride;
+        rr /= q.stride;
+        const int pa = rr % q.stride, m = rr / q.stride;
+        const int ky = q.stride * (g * q.rows + tap / q.cols) + pa, kx = q.stride * (tap % q.cols) + pb;
+        if (ky < q.dk && kx < q.dk) {
+          val = codes[(((size_t)t * q.dk + ky) * q.dk + kx) * q.M + m];
+          val = val < (uint32_t)(q.K - 1) ? val : (uint32_t)(q.K - 1);
+        } else {
+          val = (uint32_t)q.zrow;
+        }
       }
-      word |= v << (8 * b);
+      word |= val << (8 * bb);
     }
     codes8[wi] = word;
   }
 }
 
-// y = sum over splits in order + bias, then ReLU (y is NCHW, bias per channel).
-__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ partial, int splits,
-                                                           size_t total, int plane, int Ct,
-                                                           const float* __restrict__ bias, int relu,
-                                                           float* __restrict__ y) {
+// y = sum over splits in order + bias, then ReLU.  One thread per stored
+// partial value, in the partials' own order [tile][t][j][lane] (so every
+// split's values are read with whole cache lines); the thread finds the
+// output element of its slot, if the slot is one, and writes it.
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ partial, FlatParams p,
+                                                           const float* __restrict__ bias, float* __restrict__ y) {
+  const size_t per_split = (size_t)p.tiles * p.ct_pad * 256;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= total) return;
+  if (i >= per_split) return;
+  const int lane = (int)(i & 63), j = (int)((i >> 6) & 3);
+  if (lane == kWave - 1) return;  // that lane's slots belong to the next tile (not stored)
+  const size_t r = i >> 8;
+  const int t = (int)(r % p.ct_pad);
+  const int tile = (int)(r / p.ct_pad);
+  const int slot = tile * kTileSlots + 4 * lane + j;
+  const int row = slot / p.Wg, xl = slot - row * p.Wg;
+  const int g = row / p.Hg, yo = row - g * p.Hg;
+  const int n = g / p.S, xo = (g - n * p.S) * p.sw + xl;
+  if (t >= p.Ct || n >= p.N || yo >= p.Ho || xl >= p.sw || xo >= p.Wo) return;
   float s = partial[i];
-  for (int k = 1; k < splits; ++k) s += partial[(size_t)k * total + i];
-  if (bias) s += bias[(i / plane) % Ct];
-  if (relu) s = fmaxf(s, 0.f);
-  y[i] = s;
+  for (int k = 1; k < p.splits; ++k) s += partial[(size_t)k * per_split + i];
+  if (bias) s += bias[t];
+  if (p.relu) s = fmaxf(s, 0.f);
+  y[(((size_t)n * p.Ct + t) * p.Ho + yo) * p.Wo + xo] = s;
 }
 
 constexpr size_t kLdsMax = 160 * 1024;
@@ -308,111 +409,181 @@ constexpr size_t kLdsMax = 160 * 1024;
 
 struct FlatPlan {
   FlatParams p;
+  int rows, cols;  // tap grid of a virtual subspace
+  bool gen;        // offsets move with the virtual subspace
   int TW;
   size_t lds;
 };
 
 // Estimated cost (arbitrary units ~ CU clocks) of a plan, for the choice of
-// channel block and subspace split.
-double plan_cost(const FlatParams& p, int TW) {
-  const double vals = 51.0;     // lookups per clock per CU (VALU bound, 1.25 ops / lookup)
+// layout, strips, channel block and subspace split.
+double plan_cost(const FlatParams& p, int taps, int TW) {
+  const double vals = 40.0;     // table values gathered per clock per CU
   const double mfma = 256.0;    // f32 MFMA flops per clock per CU
-  const int taps = p.dk * p.dk;
-  const double mper = (double)p.m_per_split;
+  const double vper = (double)p.v_per_split;
   const double gather = (double)kWaves * TW * taps * 256 / vals;
   const double build = (double)p.npb * 16 * 16 * ((p.K + 15) / 16) * 4 * ((p.Csp + 3) / 4) * 2 / mfma;
-  const double per_wg = mper * (gather + build + 400.0);
+  const double per_wg = vper * (gather + build + 1500.0);
   const double rounds = (double)((p.work + 255) / 256);
   double cost = rounds * per_wg;
-  if (p.splits > 1) cost += (double)p.splits * 2.0 * p.N * p.Ct * p.Ho * p.Wo * 4 / 3.0e3;  // ~3 kB/clk chip-wide
+  if (p.splits > 1)  // partial sums written, then read back (~3 kB per clock chip-wide)
+    cost += (double)p.splits * 2.0 * p.tiles * p.ct_pad * 256 * 4 / 3.0e3;
   return cost;
 }
 
-bool make_plan(const ConvShape& s, FlatPlan* out) {
-  if (s.stride != 1 || s.pad > s.dk - 1) return false;
-  if (s.dk != 1 && s.dk != 3) return false;
-  if (s.Csp > 8 || s.K > 16 * kMaxKB) return false;
-  FlatParams p{};
-  p.N = s.N; p.Cs = s.Cs; p.H = s.H; p.W = s.W; p.M = s.M; p.K = s.K; p.Csp = s.Csp; p.Ct = s.Ct;
-  p.dk = s.dk; p.pad = s.pad; p.Ho = s.Ho; p.Wo = s.Wo;
-  p.Wg = s.W + s.pad;
-  p.Hg = s.H + s.pad;
-  const long long slots = (long long)s.N * p.Hg * p.Wg;
-  const long long gpos = ((long long)s.N * p.Hg + s.pad) * p.Wg;
-  if (gpos + 4096 > (1LL << 31) || (long long)s.N * s.Cs * s.H * s.W * 4 > (1LL << 31) - 1) return false;
-  p.grid_pos = (int)gpos;
-  p.tiles = (int)((slots + kTileSlots - 1) / kTileSlots);
-  const int dmax = (s.dk - 1) * p.Wg + (s.dk - 1);
+// A family of layouts: tap grid rows x cols, G row groups, and whether
+// neighbouring images share their zero halo.
+struct Layout {
+  int rows, cols, G;
+  bool shared, gen;
+};
+
+// Grid geometry for layout L with S strips per image; false when the table
+// does not fit.
+bool set_geometry(const ConvShape& s, const Layout& L, int S, FlatParams* p, size_t* lds) {
+  if (S == 1) {
+    p->sw = s.Wo;
+    p->Wg = L.shared ? s.W + s.pad : s.Wo + L.cols - 1;
+  } else {
+    p->sw = ceil_div(s.Wo, S);
+    if ((S - 1) * p->sw >= s.Wo) return false;  // an empty last strip
+    p->Wg = p->sw + L.cols - 1;
+  }
+  p->S = S;
+  p->Hg = L.shared ? s.H + s.pad : s.Ho + L.rows - 1;
+  p->G = L.G;
+  const long long slots = (long long)s.N * S * p->Hg * p->Wg;
+  const long long gpos = ((long long)s.N * S * p->Hg + (L.shared ? s.pad : 0)) * p->Wg;
+  if (gpos + 4096 > (1LL << 31)) return false;
+  p->grid_pos = (int)gpos;
+  p->tiles = (int)((slots + kTileSlots - 1) / kTileSlots);
+  const int dmax = (L.rows - 1) * p->Wg + (L.cols - 1);
   const int PT = 4 * (kWave + (dmax >> 2));
   const int PT16 = (PT + 15) / 16 * 16;
-  p.npb = PT16 / 16;
-  if (p.npb > kWaves * kMaxPB) return false;
-  p.PR = (PT16 / 4) % 2 == 1 ? PT16 : PT16 + 4;
-  const size_t lds = (size_t)((s.K + 15) / 16 * 16) * p.PR * sizeof(float);
-  (void)kMaxKB;
-  if (lds > kLdsMax) return false;
+  p->npb = PT16 / 16;
+  if (p->npb > kWaves * kMaxPB) return false;
+  p->PR = (PT16 / 4) % 2 == 1 ? PT16 : PT16 + 4;
+  const int kpad = (s.K + 15) / 16 * 16;
+  const bool dummies = s.stride * s.stride * L.G * L.rows * L.cols > s.dk * s.dk;
+  p->zrow = dummies ? kpad : -1;
+  *lds = (size_t)(kpad + (dummies ? 1 : 0)) * p->PR * sizeof(float);
+  return *lds <= kLdsMax;
+}
+
+bool make_plan(const ConvShape& s, FlatPlan* out) {
+  if (s.Csp > 8 || s.K > 16 * kMaxKB) return false;
+  if ((long long)s.N * s.Cs * s.H * s.W * 4 > (1LL << 31) - 1) return false;  // 32-bit buffer offsets
+  // Candidate layouts.  Shared halos need stride 1, pad <= d_k - 1, and for
+  // several row groups pad + ROWS - 1 < d_k (no output reads a neighbour's
+  // rows through a shifted group).
+  Layout cand[4];
+  int nc = 0;
+  if (s.stride == 1 && (s.dk == 1 || s.dk == 3) && s.pad <= s.dk - 1) cand[nc++] = {s.dk, s.dk, 1, true, false};
+  if (s.stride == 1 && s.dk == 5 && s.pad + 1 < 5) cand[nc++] = {2, 5, 3, true, true};
+  const int r = ceil_div(s.dk, s.stride);  // tap grid of a stride phase
+  if ((r == 2 || r == 3) && !(s.stride == 1 && s.dk == 1)) cand[nc++] = {r, r, 1, false, true};
+  if (s.stride == 1 && s.dk == 1) cand[nc++] = {1, 1, 1, true, false};
+  FlatParams p{};
+  p.N = s.N; p.Cs = s.Cs; p.H = s.H; p.W = s.W; p.M = s.M; p.K = s.K; p.Csp = s.Csp; p.Ct = s.Ct;
+  p.dk = s.dk; p.stride = s.stride; p.pad = s.pad; p.Ho = s.Ho; p.Wo = s.Wo;
   bool found = false;
   double best = 0;
-  for (int TW : {12}) {
-    const int tc = kWaves * TW;
-    const int tblocks = ceil_div(s.Ct, tc);
-    for (int splits = 1; splits <= 16 && splits <= s.M; ++splits) {
-      FlatParams q = p;
-      q.tc = tc;
-      q.tblocks = tblocks;
-      q.m_per_split = ceil_div(s.M, splits);
-      q.splits = ceil_div(s.M, q.m_per_split);
-      if (q.splits != splits) continue;
-      const long long work = (long long)p.tiles * tblocks * q.splits;
-      if (work > (1LL << 30)) continue;
-      q.work = (int)work;
-      q.per_xcd = ceil_div(q.work, 8);
-      q.ct_pad = tblocks * tc;
-      if ((long long)s.M * q.ct_pad * s.dk * s.dk + 4 > (1LL << 31)) continue;
-      const double c = plan_cost(q, TW);
-      if (!found || c < best) {
-        found = true;
-        best = c;
-        *out = {q, TW, lds};
+  for (int ci = 0; ci < nc; ++ci) {
+    const Layout& L = cand[ci];
+    const int taps = L.rows * L.cols;
+    p.V = s.M * s.stride * s.stride * L.G;
+    for (int S = 1; S <= 16 && S <= s.Wo; ++S) {
+      size_t lds = 0;
+      if (!set_geometry(s, L, S, &p, &lds)) continue;
+      for (int TW : {8, 12}) {
+        // two channel groups, ten taps or moving offsets with 12 channels per
+        // wave do not fit the registers
+        if (TW == 12 && (s.Csp > 4 || L.gen)) continue;
+        const int tc = kWaves * TW;
+        const int tblocks = ceil_div(s.Ct, tc);
+        for (int splits = 1; splits <= 16 && splits <= p.V; ++splits) {
+          FlatParams q = p;
+          q.tc = tc;
+          q.tblocks = tblocks;
+          q.v_per_split = ceil_div(p.V, splits);
+          q.splits = ceil_div(p.V, q.v_per_split);
+          if (q.splits != splits) continue;
+          const long long work = (long long)p.tiles * tblocks * q.splits;
+          if (work > (1LL << 30)) continue;
+          q.work = (int)work;
+          q.per_xcd = ceil_div(q.work, 8);
+          q.ct_pad = tblocks * tc;
+          if ((long long)p.V * q.ct_pad * taps + 4 > (1LL << 31)) continue;
+          const double c = plan_cost(q, taps, TW);
+          if (!found || c < best) {
+            found = true;
+            best = c;
+            *out = {q, L.rows, L.cols, L.gen, TW, lds};
+          }
+        }
       }
     }
   }
   return found;
 }
 
-template <int DK, int WG4, int NC, int TW>
+template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
 hipError_t launch_main(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
                        float* y, float* partial, hipStream_t stream) {
-  auto k = conv_flat_kernel<DK, WG4, NC, TW>;
+  auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN>;
   hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes8, bias, y, partial, pl.p);
   return hipGetLastError();
 }
 
-template <int DK, int WG4, int NC>
-hipError_t launch_tw(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
-                     float* y, float* partial, hipStream_t stream) {
-  return launch_main<DK, WG4, NC, 12>(pl, x, D, codes8, bias, y, partial, stream);
-}
+struct LaunchArgs {
+  const float* x;
+  const float* D;
+  const uint8_t* codes8;
+  const float* bias;
+  float* y;
+  float* partial;
+  hipStream_t stream;
+};
 
-template <int DK, int WG4>
-hipError_t launch_nc(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
-                     float* y, float* partial, hipStream_t stream) {
-  if (pl.p.Csp <= 4) return launch_tw<DK, WG4, 1>(pl, x, D, codes8, bias, y, partial, stream);
-  return launch_tw<DK, WG4, 2>(pl, x, D, codes8, bias, y, partial, stream);
-}
-
-template <int DK>
-hipError_t launch_wg(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
-                     float* y, float* partial, hipStream_t stream) {
-  if constexpr (DK == 1) return launch_nc<DK, 0>(pl, x, D, codes8, bias, y, partial, stream);  // one tap: no shift
-  else switch (pl.p.Wg & 3) {
-    case 0: return launch_nc<DK, 0>(pl, x, D, codes8, bias, y, partial, stream);
-    case 1: return launch_nc<DK, 1>(pl, x, D, codes8, bias, y, partial, stream);
-    case 2: return launch_nc<DK, 2>(pl, x, D, codes8, bias, y, partial, stream);
-    default: return launch_nc<DK, 3>(pl, x, D, codes8, bias, y, partial, stream);
+template <int ROWS, int COLS, int WG4, bool GEN>
+hipError_t launch_nc(const FlatPlan& pl, const LaunchArgs& a) {
+  if (pl.p.Csp <= 4) {
+    if constexpr (!GEN) {
+      if (pl.TW == 12) return launch_main<ROWS, COLS, WG4, 1, 12, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial,
+                                                                       a.stream);
+    }
+    return launch_main<ROWS, COLS, WG4, 1, 8, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream);
   }
+  return launch_main<ROWS, COLS, WG4, 2, 8, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream);
+}
+
+template <int ROWS, int COLS, bool GEN>
+hipError_t launch_wg(const FlatPlan& pl, const LaunchArgs& a) {
+  if constexpr (ROWS == 1 && COLS == 1) {
+    return launch_nc<1, 1, 0, GEN>(pl, a);  // one tap: no shift
+  } else {
+    switch (pl.p.Wg & 3) {
+      case 0: return launch_nc<ROWS, COLS, 0, GEN>(pl, a);
+      case 1: return launch_nc<ROWS, COLS, 1, GEN>(pl, a);
+      case 2: return launch_nc<ROWS, COLS, 2, GEN>(pl, a);
+      default: return launch_nc<ROWS, COLS, 3, GEN>(pl, a);
+    }
+  }
+}
+
+hipError_t launch_plan(const FlatPlan& pl, const LaunchArgs& a) {
+  const int shape = pl.rows * 10 + pl.cols;
+  if (!pl.gen) {
+    if (shape == 11) return launch_wg<1, 1, false>(pl, a);
+    if (shape == 33) return launch_wg<3, 3, false>(pl, a);
+  } else {
+    if (shape == 22) return launch_wg<2, 2, true>(pl, a);
+    if (shape == 33) return launch_wg<3, 3, true>(pl, a);
+    if (shape == 25) return launch_wg<2, 5, true>(pl, a);
+  }
+  return hipErrorInvalidConfiguration;
 }
 
 }  // namespace
@@ -429,33 +600,33 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
   pl.p.relu = relu;
   static const bool trace = getenv("QCNN_TRACE_PLAN") && *getenv("QCNN_TRACE_PLAN") == '1';
   if (trace)
-    fprintf(stderr, "qcnn conv_flat: tiles=%d tc=%d tblocks=%d splits=%d work=%d PR=%d npb=%d lds=%zu\n",
-            pl.p.tiles, pl.p.tc, pl.p.tblocks, pl.p.splits, pl.p.work, pl.p.PR, pl.p.npb, pl.lds);
+    fprintf(stderr, "qcnn conv_flat: taps %dx%d%s G=%d V=%d S=%d sw=%d Wg=%d Hg=%d tiles=%d TW=%d tc=%d tblocks=%d "
+            "splits=%d work=%d PR=%d npb=%d zrow=%d lds=%zu\n", pl.rows, pl.cols, pl.gen ? " gen" : "", pl.p.G,
+            pl.p.V, pl.p.S, pl.p.sw, pl.p.Wg, pl.p.Hg, pl.p.tiles, pl.TW, pl.p.tc, pl.p.tblocks, pl.p.splits,
+            pl.p.work, pl.p.PR, pl.p.npb, pl.p.zrow, pl.lds);
   const FlatParams& p = pl.p;
-  const size_t n_codes = (size_t)p.M * p.ct_pad * p.dk * p.dk;
-  const size_t out_elems = (size_t)p.N * p.Ct * p.Ho * p.Wo;
+  const int taps = pl.rows * pl.cols;
+  const size_t n_codes = (size_t)p.V * p.ct_pad * taps;
   const size_t code_bytes = (n_codes + 4 + 255) & ~(size_t)255;  // + the tail of the last dword load
-  const size_t ws = code_bytes + (p.splits > 1 ? (size_t)p.splits * out_elems * sizeof(float) : 0);
+  const size_t partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 256;
+  const size_t ws = code_bytes + (p.splits > 1 ? partial_elems * sizeof(float) : 0);
   char* base = nullptr;
   hipError_t e = hipMallocAsync((void**)&base, ws, stream);
   if (e != hipSuccess) return e;
   uint8_t* codes8 = reinterpret_cast<uint8_t*>(base);
   float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
   const size_t nwords = (n_codes + 3) / 4;
+  const CodeMap cm{p.Ct, p.dk, p.stride, p.M, p.G, pl.rows, pl.cols, p.K, p.ct_pad, p.zrow, p.V};
   hipLaunchKernelGGL(flat_codes_kernel, dim3((unsigned)std::min<size_t>(2048, ceil_div_z(nwords, 256))), dim3(256), 0,
-                     stream, codes, p.Ct, p.dk * p.dk, p.M, p.K, p.ct_pad, reinterpret_cast<uint32_t*>(codes8));
+                     stream, codes, cm, reinterpret_cast<uint32_t*>(codes8));
   e = hipGetLastError();
   if (e == hipSuccess) {
     KernelTimer timer(stream);
-    switch (p.dk) {
-      case 1: e = launch_wg<1>(pl, x, D, codes8, bias, y, partial, stream); break;
-      case 3: e = launch_wg<3>(pl, x, D, codes8, bias, y, partial, stream); break;
-      default: e = hipErrorInvalidConfiguration; break;
-    }
+    e = launch_plan(pl, LaunchArgs{x, D, codes8, bias, y, partial, stream});
   }
   if (e == hipSuccess && partial) {
-    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)ceil_div_z(out_elems, 256)), dim3(256), 0, stream,
-                       partial, p.splits, out_elems, p.Ho * p.Wo, p.Ct, bias, relu, y);
+    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)ceil_div_z(partial_elems / p.splits, 256)), dim3(256), 0,
+                       stream, partial, p, bias, y);
     e = hipGetLastError();
   }
   hipError_t e2 = hipFreeAsync(base, stream);

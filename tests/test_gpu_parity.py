@@ -209,6 +209,10 @@ CONV_EDGE = [
     (2, 512, 6, 6, 16, 3, 1, 1, 2, 16),
     (4, 32, 8, 8, 40, 1, 1, 0, 4, 128),
     (1, 7, 3, 3, 5, 3, 1, 1, 1, 7),
+    # maps too wide for one table row: cut into column strips (ragged last strip)
+    (2, 16, 10, 90, 20, 3, 1, 1, 4, 128),
+    (1, 8, 12, 201, 4, 3, 1, 0, 8, 64),
+    (1, 16, 5, 61, 140, 3, 1, 1, 8, 128),
 ]
 
 
