@@ -124,6 +124,8 @@ __global__ __launch_bounds__(256) void fc_reduce_kernel(const float* __restrict_
 
 hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
                              const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream) {
+  if (fc_tiled_supported(N, Cs, M, K, Csp, Ct))
+    return launch_fc_tiled(N, Cs, M, K, Csp, Ct, x, D, codes, bias, relu, y, stream);
   FcParams p;
   float* partial = nullptr;
   p.N = N;

@@ -71,6 +71,12 @@ class KernelTimer {
   hipEvent_t start_ = nullptr;
 };
 
+// FC layer with tables of 4 subspaces per phase and 128-bit gathers over
+// images (fc_tiled.hip): K <= 64, C's <= 8.
+bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct);
+hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
+                           const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream);
+
 // Keep freed stream-ordered allocations in the device's default pool
 // (called once per device before the first hipMallocAsync).
 hipError_t retain_pool_memory();
