@@ -34,10 +34,11 @@ namespace qcnn {
 
 struct FcTParams {
   int N, Cs, M, K, Csp, Ct;
-  int NS, RS;              // images per workgroup (4 LPC), table row stride in floats (RS / 4 odd)
+  int NS, RS;              // images per workgroup (4 LPC), table row stride in floats
   int KP;                  // table rows: K rounded up to 16
   int mgroups;             // ceil(M / 4): dword code groups
-  int tc, tblocks, nblocks, splits, g_per_split;  // g_per_split: 4-subspace groups per split
+  int MC, nphases;         // subspaces per phase (4 or 8), ceil(M / MC)
+  int tc, tblocks, nblocks, splits, ph_per_split;
   int work, per_xcd;
   int ct_pad;
   int relu;
@@ -47,15 +48,15 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kMC = 4;   // subspaces per phase (one code dword)
 constexpr int kNI = 8;   // gather instructions per wave and subspace
 constexpr size_t kLdsMax = 160 * 1024;
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
 // LPC: lanes per channel (16 or 32); NC: 4-channel groups of a subspace (1
-// or 2); KB: 16-row codeword blocks (1..4).
-template <int LPC, int NC, int KB>
+// or 2); KB: 16-row codeword blocks (1..4); MC: subspaces per phase (4 or 8,
+// i.e. one or two code dwords per channel).
+template <int LPC, int NC, int KB, int MC>
 __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __restrict__ x,
                                                                const float* __restrict__ D,
                                                                const uint32_t* __restrict__ codes4,
@@ -68,7 +69,8 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
   constexpr int TW = kNI * CPI;           // channels per wave
   constexpr int NS = 4 * LPC;             // images per workgroup
   constexpr int NB = NS / 16;             // 16-image blocks
-  constexpr int TASKS = kMC * NB;         // (subspace, image block) MFMA tasks per phase
+  constexpr int GPP = MC / 4;             // code dwords per channel and phase
+  constexpr int TASKS = MC * NB;          // (subspace, image block) MFMA tasks per phase
   constexpr int TPW = (TASKS + kWaves - 1) / kWaves;  // tasks per wave (1 or 2)
   constexpr int PD = 8;                   // table reads kept in flight
   const int lane = threadIdx.x & (kWave - 1);
@@ -86,8 +88,8 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
   const int nblk = r0 / p.splits;
   const int n0 = nblk * NS;
   const int t0 = tb * p.tc + wave * TW;
-  const int gq0 = split * p.g_per_split;
-  const int gq1 = min(p.mgroups, gq0 + p.g_per_split);
+  const int ph0 = split * p.ph_per_split;
+  const int ph1 = min(p.nphases, ph0 + p.ph_per_split);
 
   constexpr uint32_t kOOB = 0x80000000u;
   const int arow = lane & 15, acol = lane >> 4;
@@ -97,19 +99,19 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
       const_cast<float*>(D), 0, (int)((size_t)p.M * p.K * p.Csp * 4), 0x00020000);
   const int tbuf = p.KP * p.RS;  // floats per subspace table
 
-  // ---- build operands of a phase (4 subspaces of group gq): task k of this
+  // ---- build operands of phase ph (subspaces ph MC ..): task k of this
   // wave is (subspace ml, image block nb) = ((wave + 16 k) / NB, % NB).
   // A operand (x): image n0 + 16 nb + l % 16, channel m C's + 4 c + l / 16;
   // B operand (D): codeword 16 kb + l % 16 of subspace m, channel 4 c + l / 16.
   // Offsets past a buffer's end (image >= N, channel >= C's, codeword >= K,
   // subspace >= M) read 0.
   float av[TPW][NC], bv[TPW][KB][NC];
-  auto load_ops = [&](int gq) {
+  auto load_ops = [&](int ph) {
 #pragma unroll
     for (int k = 0; k < TPW; ++k) {
       const int task = wave + kWaves * k;
       const int ml = task / NB, nb = task - ml * NB;
-      const int m = gq * kMC + ml;
+      const int m = ph * MC + ml;
       const bool mok = task < TASKS && m < p.M;
       const int n = n0 + nb * 16 + arow;
 #pragma unroll
@@ -135,7 +137,7 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
       const int task = wave + kWaves * k;
       if (task < TASKS) {
         const int ml = task / NB, nb = task - ml * NB;
-        float* base = lut + (buf * kMC + ml) * tbuf + nb * 16 + 4 * acol;
+        float* base = lut + (buf * MC + ml) * tbuf + nb * 16 + 4 * acol;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
           f4v d = {0.f, 0.f, 0.f, 0.f};
@@ -146,13 +148,16 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
       }
     }
   };
-  // Codes of a phase: instruction i serves channel t0 + i CPI + g; its dword
-  // holds that channel's codes of the phase's 4 subspaces.
-  uint32_t cur[kNI], nxt[kNI];
-  auto load_codes = [&](int gq, uint32_t (&dst)[kNI]) {
-    const uint32_t* src = codes4 + (size_t)gq * p.ct_pad + t0 + g;
+  // Codes of a phase: instruction i serves channel t0 + i CPI + g; dword gg
+  // holds that channel's codes of the phase's subspaces 4 gg .. 4 gg + 3.
+  uint32_t cur[GPP][kNI], nxt[GPP][kNI];
+  auto load_codes = [&](int ph, uint32_t (&dst)[GPP][kNI]) {
 #pragma unroll
-    for (int i = 0; i < kNI; ++i) dst[i] = src[i * CPI];
+    for (int gg = 0; gg < GPP; ++gg) {
+      const uint32_t* src = codes4 + (size_t)(ph * GPP + gg) * p.ct_pad + t0 + g;
+#pragma unroll
+      for (int i = 0; i < kNI; ++i) dst[gg][i] = src[i * CPI];
+    }
   };
 
   float acc[kNI][4];
@@ -167,27 +172,34 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
   const uint32_t lane_off = (uint32_t)qd * 16u;
   const char* lbase = reinterpret_cast<const char*>(lut4);
 
-  if (gq0 < gq1) {
-    load_ops(gq0);
-    load_codes(gq0, cur);
+  if (ph0 < ph1) {
+    load_ops(ph0);
+    load_codes(ph0, cur);
     build(0);
+    // Settle the first codes here: the loop below is entered with no load
+    // pending on them, so its start does not wait for the next phase's loads
+    // (the load counter is in order).
+#pragma unroll
+    for (int gg = 0; gg < GPP; ++gg)
+#pragma unroll
+      for (int i = 0; i < kNI; ++i) asm volatile("" : "+v"(cur[gg][i]));
   }
   int buf = 0;
-  for (int gq = gq0; gq < gq1; ++gq) {
-    const bool more = gq + 1 < gq1;
+  for (int ph = ph0; ph < ph1; ++ph) {
+    const bool more = ph + 1 < ph1;
     if (more) {
-      load_ops(gq + 1);
-      load_codes(gq + 1, nxt);
+      load_ops(ph + 1);
+      load_codes(ph + 1, nxt);
     }
     __syncthreads();  // tables of this phase are complete; the other buffer is free
-    // ---- gather, Eq. (5): 4 subspaces x kNI instructions
+    // ---- gather, Eq. (5): MC subspaces x kNI instructions
 #pragma unroll
-    for (int ml = 0; ml < kMC; ++ml) {
-      if (gq * kMC + ml >= p.M) break;  // the last group may hold fewer than 4 subspaces
-      const uint32_t tb_off = (uint32_t)((buf * kMC + ml) * tbuf) * 4u + lane_off;
+    for (int ml = 0; ml < MC; ++ml) {
+      if (ph * MC + ml >= p.M) break;  // the last phase may hold fewer subspaces
+      const uint32_t tb_off = (uint32_t)((buf * MC + ml) * tbuf) * 4u + lane_off;
       f4v qb[PD];
       auto addr = [&](int i) -> uint32_t {
-        const uint32_t code = (cur[i] >> (8 * ml)) & 0xffu;
+        const uint32_t code = (cur[ml >> 2][i] >> (8 * (ml & 3))) & 0xffu;
         return __umul24(code, row_bytes) + tb_off;
       };
 #pragma unroll
@@ -205,7 +217,12 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
     if (more) {
       build(buf ^ 1);
 #pragma unroll
-      for (int i = 0; i < kNI; ++i) cur[i] = nxt[i];
+      for (int gg = 0; gg < GPP; ++gg)
+#pragma unroll
+        for (int i = 0; i < kNI; ++i) {
+          cur[gg][i] = nxt[gg][i];
+          asm volatile("" : "+v"(cur[gg][i]));
+        }
     }
     buf ^= 1;
   }
@@ -335,7 +352,7 @@ double fc_cost(const FcTParams& p, int LPC) {
   const double vals = 40.0;  // table values gathered per clock per CU
   const double gather = (double)kWaves * kNI * kWave * 4 / vals;             // per subspace
   const double build = (double)p.NS * p.KP * 4 * ((p.Csp + 3) / 4) * 2 / 256.0;  // MFMA flops / 256 per clock
-  const double per_wg = (double)p.g_per_split * (kMC * (gather + build) + 800.0);
+  const double per_wg = (double)p.ph_per_split * (p.MC * (gather + build) + 800.0);
   const double rounds = (double)((p.work + 255) / 256);
   double cost = rounds * per_wg;
   if (p.splits > 1) cost += (double)p.splits * 2.0 * p.ct_pad * p.nblocks * p.NS * 4 / 2.0e3;
@@ -348,26 +365,34 @@ bool make_fc_plan(int N, int Cs, int M, int K, int Csp, int Ct, FcPlan* out) {
   if ((long long)N * Cs * 4 > (1LL << 31) - 1 || (long long)M * K * Csp * 4 > (1LL << 31) - 1) return false;
   bool found = false;
   double best = 0;
-  for (int LPC : {16, 32}) {
+  for (int LPC : {16, 32})
+  for (int MC : {4, 8}) {
     const int NS = 4 * LPC;
     if (LPC == 32 && (K > 32 || N <= 64)) continue;
     FcTParams p{};
     p.N = N; p.Cs = Cs; p.M = M; p.K = K; p.Csp = Csp; p.Ct = Ct;
     p.NS = NS;
-    p.RS = NS + 4;
+    // Rows a multiple of 256 bytes apart: every 16-lane group of a gather
+    // then reads one aligned 256-byte run, which the LDS serves at full
+    // rate even when the groups read different rows (rows offset by other
+    // amounts cost about 40 %).  The MFMA result stores (16 rows, one
+    // column each) conflict instead; the gather dominates.
+    p.RS = NS;
     p.KP = (K + 15) / 16 * 16;
-    p.mgroups = ceil_div(M, kMC);
-    const size_t lds = (size_t)2 * kMC * p.KP * p.RS * sizeof(float);
-    if (lds > kLdsMax) continue;
+    p.MC = MC;
+    p.nphases = ceil_div(M, MC);
+    p.mgroups = p.nphases * (MC / 4);  // code dwords per channel, whole phases
+    const size_t lds = (size_t)2 * MC * p.KP * p.RS * sizeof(float);
+    if (lds > kLdsMax || (MC == 8 && (LPC != 16 || p.KP > 32))) continue;
     p.tc = kWaves * kNI * (kWave / LPC);
     p.tblocks = ceil_div(Ct, p.tc);
     p.nblocks = ceil_div(N, NS);
     p.ct_pad = p.tblocks * p.tc;
     if ((long long)p.nblocks * NS * p.ct_pad * 16 > (1LL << 40)) continue;
-    for (int splits = 1; splits <= 64 && splits <= p.mgroups; ++splits) {
+    for (int splits = 1; splits <= 64 && splits <= p.nphases; ++splits) {
       FcTParams q = p;
-      q.g_per_split = ceil_div(p.mgroups, splits);
-      q.splits = ceil_div(p.mgroups, q.g_per_split);
+      q.ph_per_split = ceil_div(p.nphases, splits);
+      q.splits = ceil_div(p.nphases, q.ph_per_split);
       if (q.splits != splits) continue;
       const long long work = (long long)p.nblocks * p.tblocks * q.splits;
       if (work > (1LL << 30)) continue;
@@ -387,7 +412,10 @@ bool make_fc_plan(int N, int Cs, int M, int K, int Csp, int Ct, FcPlan* out) {
 template <int LPC, int NC, int KB>
 hipError_t launch_t(const FcPlan& pl, const float* x, const float* D, const uint32_t* codes4, const float* bias,
                     float* y, float* partial, hipStream_t stream) {
-  auto k = fc_tiled_kernel<LPC, NC, KB>;
+  auto k = fc_tiled_kernel<LPC, NC, KB, 4>;
+  if constexpr (LPC == 16 && KB <= 2) {  // the only tables small enough for 8 subspaces per phase
+    if (pl.p.MC == 8) k = fc_tiled_kernel<LPC, NC, KB, 8>;
+  }
   hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes4, bias, y, partial, pl.p);
@@ -419,9 +447,9 @@ hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const f
   pl.p.relu = relu;
   static const bool trace = getenv("QCNN_TRACE_PLAN") && *getenv("QCNN_TRACE_PLAN") == '1';
   if (trace)
-    fprintf(stderr, "qcnn fc_tiled: LPC=%d NC=%d KB=%d NS=%d tc=%d tblocks=%d nblocks=%d splits=%d groups/split=%d "
-            "work=%d lds=%zu\n", pl.LPC, pl.NC, pl.KB, pl.p.NS, pl.p.tc, pl.p.tblocks, pl.p.nblocks, pl.p.splits,
-            pl.p.g_per_split, pl.p.work, pl.lds);
+    fprintf(stderr, "qcnn fc_tiled: LPC=%d NC=%d KB=%d MC=%d NS=%d tc=%d tblocks=%d nblocks=%d splits=%d "
+            "phases/split=%d work=%d lds=%zu\n", pl.LPC, pl.NC, pl.KB, pl.p.MC, pl.p.NS, pl.p.tc, pl.p.tblocks,
+            pl.p.nblocks, pl.p.splits, pl.p.ph_per_split, pl.p.work, pl.lds);
   const FcTParams& p = pl.p;
   const size_t code_bytes = ((size_t)p.mgroups * p.ct_pad * 4 + 255) & ~(size_t)255;
   const size_t partial_elems = (size_t)p.splits * p.ct_pad * p.nblocks * p.NS;
