@@ -213,6 +213,12 @@ CONV_EDGE = [
     (2, 16, 10, 90, 20, 3, 1, 1, 4, 128),
     (1, 8, 12, 201, 4, 3, 1, 0, 8, 64),
     (1, 16, 5, 61, 140, 3, 1, 1, 8, 128),
+    # stride phases and kernel-row groups (virtual subspaces), incl. padded tap grids
+    (2, 12, 21, 19, 30, 3, 2, 1, 6, 40),     # 3x3 stride 2, two 4-channel groups
+    (1, 9, 33, 29, 10, 7, 3, 2, 3, 24),      # 7x7 stride 3: 9 phases of 3x3 grids
+    (3, 20, 9, 40, 70, 5, 1, 2, 5, 128),     # 5x5 pad 2, row groups, C's = 5
+    (2, 8, 11, 11, 9, 5, 1, 0, 8, 100),      # 5x5 pad 0
+    (1, 6, 12, 12, 5, 4, 2, 1, 2, 16),       # even kernel, stride 2
 ]
 
 
@@ -239,6 +245,9 @@ FC_EDGE = [
     (7, 48, 33, 1, 16),       # C's = 1, K = 16 (the paper's fc8 setting)
     (5, 80, 70, 8, 256),
     (3, 10, 5, 5, 1),         # K = 1, runtime-length C's
+    (96, 640, 300, 8, 64),    # K = 64 (four codeword blocks), C's = 8
+    (200, 192, 70, 4, 48),    # K = 48, two image blocks, ragged channels
+    (128, 68, 40, 4, 32),     # M = 17: the last phase holds one subspace
 ]
 
 
