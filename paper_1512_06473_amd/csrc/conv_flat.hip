@@ -240,12 +240,13 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         a[i][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xres, off, m * p.Csp * HW * 4, 0));
       }
     }
+    // Blocks kb >= kblocks hold codewords >= K: their offsets are past the
+    // buffer's end, so the loads return 0 without a branch.
 #pragma unroll
     for (int kb = 0; kb < kMaxKB; ++kb)
 #pragma unroll
       for (int c = 0; c < NC; ++c)
-        bb[kb][c] = kb < kblocks ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, dlane[c] + kb * dstep, 0, 0))
-                                 : 0.f;
+        bb[kb][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, dlane[c] + kb * dstep, 0, 0));
   };
   load_operands(v0, av, bv);
   // This wave's codes for virtual subspace v: TW x TAPS consecutive bytes, in SGPRs.
@@ -277,8 +278,10 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         }
       }
     }
-    if (v + 1 < v1) load_operands(v + 1, av, bv);  // registers are free again after the build
     __syncthreads();
+    // Operands of v+1, issued after the barrier: issued before it, the burst
+    // of loads held every wave at the barrier for about as long as the build.
+    if (v + 1 < v1) load_operands(v + 1, av, bv);
     // ---- gather-accumulate, Eq. (7).  The (channel, tap) pairs of this wave
     // form one stream of NQ table reads; PD of them are kept in flight.
     auto tap_addr = [&](int k) -> uint32_t {
