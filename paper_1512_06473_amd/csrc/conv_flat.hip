@@ -264,18 +264,34 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     // latency.)
     load_codes(v, cw);
     // ---- table build: lut[k][pos] = sum_j D[m][k][j] x[pos][m C's + j]
+    // d[r] = lut[k = kb*16 + lane%16][pos = 16 pb + 4 (lane/16) + r]
+    auto tile = [&](int i, int kb) -> f4v {
+      f4v d = zero4;
 #pragma unroll
-    for (int kb = 0; kb < kMaxKB; ++kb) {
+      for (int c = 0; c < NC; ++c) d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], bv[kb][c], d, 0, 0, 0);
+      return d;
+    };
+    auto put = [&](int i, int kb, const f4v& d) {
+      *reinterpret_cast<f4v*>(lut + (kb * 16 + arow) * p.PR + 16 * (wave + kWaves * i) + 4 * acol) = d;
+    };
 #pragma unroll
-      for (int i = 0; i < kMaxPB; ++i) {
-        const int pb = wave + kWaves * i;
-        if (kb < kblocks && pb < p.npb) {
-          f4v d = zero4;
+    for (int i = 0; i < kMaxPB; ++i) {
+      if (wave + kWaves * i >= p.npb) continue;  // wave-uniform
+      if (kblocks == kMaxKB) {
+        // All blocks: straight-line code, each store one MFMA behind so
+        // that the next MFMA is issued while the previous result drains.
+        f4v prev = tile(i, 0);
 #pragma unroll
-          for (int c = 0; c < NC; ++c) d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], bv[kb][c], d, 0, 0, 0);
-          // d[r] = lut[k = kb*16 + lane%16][pos = 16 pb + 4 (lane/16) + r]; rows k >= K are never read
-          *reinterpret_cast<f4v*>(lut + (kb * 16 + arow) * p.PR + 16 * pb + 4 * acol) = d;
+        for (int kb = 1; kb < kMaxKB; ++kb) {
+          const f4v d = tile(i, kb);
+          put(i, kb - 1, prev);
+          prev = d;
         }
+        put(i, kMaxKB - 1, prev);
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < kMaxKB; ++kb)
+          if (kb < kblocks) put(i, kb, tile(i, kb));  // rows k >= kblocks*16 are not in the table
       }
     }
     __syncthreads();
