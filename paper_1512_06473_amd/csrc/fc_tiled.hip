@@ -10,7 +10,7 @@
 //   * a workgroup owns NS = 4 LPC images (64 or 128), a block of output
 //     channels and a range of subspaces; per subspace its table
 //     lut[k][image] (K rows of NS floats) is built in LDS by MFMA
-//     (v_mfma_f32_16x16x4_f32: 16 images x 16 codewords x 4 input channels);
+//     (v_mfma_f32_16x16x4_f32: 16 codewords x 16 images x 4 input channels);
 //   * a gather instruction serves 64 / LPC output channels: LPC lanes per
 //     channel, each lane reading the 16-byte quad of 4 images of that
 //     channel's table row, so every table read is one aligned ds_read_b128
@@ -130,20 +130,25 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
       }
     }
   };
-  // MFMA: d[r] = table value of codeword 16 kb + l % 16 at image 16 nb + 4 (l / 16) + r.
+  // MFMA with the codebook as the A operand: d[r] = table value of codeword
+  // 16 kb + 4 (l / 16) + r at image 16 nb + l % 16.  Each 32-bit store then
+  // writes 16 consecutive images of one row per 16-lane group (rows whose
+  // stride is a multiple of 256 bytes would make a 16-rows-per-store layout
+  // conflict 16 ways).
   auto build = [&](int buf) {
 #pragma unroll
     for (int k = 0; k < TPW; ++k) {
       const int task = wave + kWaves * k;
       if (task < TASKS) {
         const int ml = task / NB, nb = task - ml * NB;
-        float* base = lut + (buf * MC + ml) * tbuf + nb * 16 + 4 * acol;
+        float* base = lut + (buf * MC + ml) * tbuf + nb * 16 + arow;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
           f4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int c = 0; c < NC; ++c) d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[k][c], bv[k][kb][c], d, 0, 0, 0);
-          *reinterpret_cast<f4v*>(base + (kb * 16 + arow) * p.RS) = d;
+          for (int c = 0; c < NC; ++c) d = __builtin_amdgcn_mfma_f32_16x16x4f32(bv[k][kb][c], av[k][c], d, 0, 0, 0);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) base[(kb * 16 + 4 * acol + r) * p.RS] = d[r];
         }
       }
     }
@@ -375,8 +380,7 @@ bool make_fc_plan(int N, int Cs, int M, int K, int Csp, int Ct, FcPlan* out) {
     // Rows a multiple of 256 bytes apart: every 16-lane group of a gather
     // then reads one aligned 256-byte run, which the LDS serves at full
     // rate even when the groups read different rows (rows offset by other
-    // amounts cost about 40 %).  The MFMA result stores (16 rows, one
-    // column each) conflict instead; the gather dominates.
+    // amounts cost about 40 %).
     p.RS = NS;
     p.KP = (K + 15) / 16 * 16;
     p.MC = MC;
