@@ -64,6 +64,7 @@ struct FlatParams {
   int tiles;             // ceil(N S Hg Wg / 252)
   int G, V;              // kernel-row groups; virtual subspaces M s^2 G
   int zrow;              // table row of zeros for grid taps past the kernel, or -1
+  int dstage;            // float offset in LDS of the staged codebook (after the table)
   int PR;                // table row stride in floats (PR / 4 odd: conflict-free MFMA stores)
   int npb;               // 16-position blocks per table tile
   int tc, tblocks, splits, v_per_split;
@@ -210,8 +211,19 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
 
   // Table-build operands, double-buffered: those of virtual subspace v+1 are
   // loaded while the waves gather from the table of v.
-  float av[kMaxPB][NC], bv[kMaxKB][NC];
-  auto load_operands = [&](int vv, float (&a)[kMaxPB][NC], float (&bb)[kMaxKB][NC]) {
+  // The codebook of a subspace (the B operands of every wave) is staged in
+  // LDS, dstage[(kb NC + c) 64 + l] = D[m][16 kb + l % 16][4 c + l / 16]:
+  // wave q < kMaxKB NC loads entry q of each lane's set once for the whole
+  // workgroup (a load per wave per 16-codeword block made the build issue
+  // bound on vector memory instructions), and writes it to LDS near the end
+  // of the previous gather.  Waves past the last entry keep 0 in slots
+  // that no build reads.
+  static_assert(kMaxKB * NC <= kWaves, "one staging wave per codebook block and channel group");
+  float* dstage = lut + p.dstage;
+  const bool dloader = wave < kMaxKB * NC;
+  const int dkb = wave / NC, dc = wave % NC;
+  float av[kMaxPB][NC], dnext = 0.f;
+  auto load_operands = [&](int vv, float (&a)[kMaxPB][NC], float& dv) {
     int m = vv, dy = 0, dx = 0;
     if constexpr (GEN) {  // v = ((m s + a) s + b) G + g
       const int g = vv % p.G;
@@ -242,13 +254,16 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     }
     // Blocks kb >= kblocks hold codewords >= K: their offsets are past the
     // buffer's end, so the loads return 0 without a branch.
-#pragma unroll
-    for (int kb = 0; kb < kMaxKB; ++kb)
+    if (dloader) {
+      uint32_t off = kOOB;
 #pragma unroll
       for (int c = 0; c < NC; ++c)
-        bb[kb][c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, dlane[c] + kb * dstep, 0, 0));
+        if (c == dc) off = dlane[c] + dkb * dstep;
+      dv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dres, off, 0, 0));
+    }
   };
-  load_operands(v0, av, bv);
+  load_operands(v0, av, dnext);
+  dstage[wave * 64 + lane] = dnext;  // published by the loop's first barrier
   // This wave's codes for virtual subspace v: TW x TAPS consecutive bytes, in SGPRs.
   auto load_codes = [&](int vv, uint32_t (&cwv)[CW]) {
     const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)vv * p.ct_pad + t0) * TAPS);
@@ -268,7 +283,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     auto tile = [&](int i, int kb) -> f4v {
       f4v d = zero4;
 #pragma unroll
-      for (int c = 0; c < NC; ++c) d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], bv[kb][c], d, 0, 0, 0);
+      for (int c = 0; c < NC; ++c)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], dstage[(kb * NC + c) * 64 + lane], d, 0, 0, 0);
       return d;
     };
     auto put = [&](int i, int kb, const f4v& d) {
@@ -297,7 +313,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     __syncthreads();
     // Operands of v+1, issued after the barrier: issued before it, the burst
     // of loads held every wave at the barrier for about as long as the build.
-    if (v + 1 < v1) load_operands(v + 1, av, bv);
+    if (v + 1 < v1) load_operands(v + 1, av, dnext);
     // ---- gather-accumulate, Eq. (7).  The (channel, tap) pairs of this wave
     // form one stream of NQ table reads; PD of them are kept in flight.
     auto tap_addr = [&](int k) -> uint32_t {
@@ -320,6 +336,11 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         default: tap_add<3>(acc[i], q); break;
       }
     }
+    // Stage the codebook of v+1 (its loads have had the whole gather to land).
+    // Every wave stores, into a slot of its own, without a branch: a branch
+    // here made the compiler spill the accumulators.  After the last subspace
+    // the store rewrites what is already there.
+    dstage[wave * 64 + lane] = dnext;
   }
 
   // ---- epilogue
@@ -494,7 +515,8 @@ bool set_geometry(const ConvShape& s, const Layout& L, int S, FlatParams* p, siz
   const int kpad = (s.K + 15) / 16 * 16;
   const bool dummies = s.stride * s.stride * L.G * L.rows * L.cols > s.dk * s.dk;
   p->zrow = dummies ? kpad : -1;
-  *lds = (size_t)(kpad + (dummies ? 1 : 0)) * p->PR * sizeof(float);
+  p->dstage = (kpad + (dummies ? 1 : 0)) * p->PR;
+  *lds = ((size_t)p->dstage + (size_t)kThreads) * sizeof(float);
   return *lds <= kLdsMax;
 }
 
