@@ -274,6 +274,21 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
 
   for (int v = v0; v < v1; ++v) {
     __syncthreads();  // every wave is done reading the previous table
+    // The build's B operands are read from the staged codebook before any
+    // table store (as far as the compiler knows, the stores could overwrite
+    // them) and waited for before the codes' scalar loads are issued: LDS
+    // reads and scalar loads share one wait counter, so a later wait for the
+    // operands would also wait for the codes.
+    float bv[kMaxKB][NC];
+#pragma unroll
+    for (int kb = 0; kb < kMaxKB; ++kb)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) bv[kb][c] = dstage[(kb * NC + c) * 64 + lane];
+#pragma unroll
+    for (int kb = 0; kb < kMaxKB; ++kb)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) asm volatile("" ::"v"(bv[kb][c]));
+    __builtin_amdgcn_sched_barrier(0);
     // The codes of v arrive during the build.  (A barrier waits for every
     // outstanding scalar load, so issuing them before one would expose their
     // latency.)
@@ -284,7 +299,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
       f4v d = zero4;
 #pragma unroll
       for (int c = 0; c < NC; ++c)
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], dstage[(kb * NC + c) * 64 + lane], d, 0, 0, 0);
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], bv[kb][c], d, 0, 0, 0);
       return d;
     };
     auto put = [&](int i, int kb, const f4v& d) {
