@@ -49,9 +49,13 @@
  *     C++ exception crosses the ABI.
  *   - Execution is asynchronous on `stream` (a hipStream_t; NULL = the legacy
  *     default stream): a call returns once its kernels are enqueued.  Calls
- *     are reentrant; work that needs temporary device memory allocates it
- *     stream-ordered on `stream` (hipMallocAsync / hipFreeAsync), so
- *     concurrent calls on different streams never share it.
+ *     are reentrant.  A conv or FC call that needs temporary device memory
+ *     (re-laid-out codes, partial sums) uses a library-owned workspace, one
+ *     per (device, stream): grown in stream order on `stream` (the old one
+ *     released with hipFreeAsync, a larger one taken with hipMallocAsync),
+ *     locked for the enqueue of one call, and held until the process ends.
+ *     Concurrent calls on different streams never share it; calls on one
+ *     stream use it one after the other in stream order.
  */
 #ifndef QCNN_H
 #define QCNN_H

@@ -468,7 +468,6 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   y[(((size_t)n * p.Ct + t) * p.Ho + yo) * p.Wo + xo] = s;
 }
 
-constexpr size_t kLdsMax = 160 * 1024;
 
 
 struct FlatPlan {
@@ -532,7 +531,7 @@ bool set_geometry(const ConvShape& s, const Layout& L, int S, FlatParams* p, siz
   p->zrow = dummies ? kpad : -1;
   p->dstage = (kpad + (dummies ? 1 : 0)) * p->PR;
   *lds = ((size_t)p->dstage + (size_t)kThreads) * sizeof(float);
-  return *lds <= kLdsMax;
+  return *lds <= kLdsBytes;
 }
 
 bool make_plan(const ConvShape& s, FlatPlan* out) {
@@ -596,7 +595,7 @@ template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
 hipError_t launch_main(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
                        float* y, float* partial, hipStream_t stream) {
   auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN>;
-  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
+  hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes8, bias, y, partial, pl.p);
   return hipGetLastError();
@@ -675,9 +674,10 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
   const size_t code_bytes = (n_codes + 4 + 255) & ~(size_t)255;  // + the tail of the last dword load
   const size_t partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 256;
   const size_t ws = code_bytes + (p.splits > 1 ? partial_elems * sizeof(float) : 0);
-  char* base = nullptr;
-  hipError_t e = hipMallocAsync((void**)&base, ws, stream);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, ws);
   if (e != hipSuccess) return e;
+  char* base = scratch.get();
   uint8_t* codes8 = reinterpret_cast<uint8_t*>(base);
   float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
   const size_t nwords = (n_codes + 3) / 4;
@@ -694,8 +694,7 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
                        stream, partial, p, bias, y);
     e = hipGetLastError();
   }
-  hipError_t e2 = hipFreeAsync(base, stream);
-  return e == hipSuccess ? e2 : e;
+  return e;
 }
 
 }  // namespace qcnn

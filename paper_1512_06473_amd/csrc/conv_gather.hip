@@ -180,7 +180,7 @@ struct ConvPtrs {
 template <int CSP, int G>
 hipError_t launch_g(const ConvPtrs& a, const ConvParams& p, dim3 grid, size_t lds, hipStream_t stream) {
   auto k = conv_pq_generic<CSP, G, kTW>;
-  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
   KernelTimer timer(stream);
   hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, stream, a.x, a.D, a.codes, a.bias, a.y, p);

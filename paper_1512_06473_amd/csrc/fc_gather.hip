@@ -148,9 +148,11 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
   const size_t lds = (size_t)p.mchunk * per_m;
 
   hipError_t e;
+  Scratch scratch;
   if (splits > 1) {
-    e = hipMallocAsync((void**)&partial, (size_t)splits * N * Ct * sizeof(float), stream);
+    e = scratch.acquire(stream, (size_t)splits * N * Ct * sizeof(float));
     if (e != hipSuccess) return e;
+    partial = reinterpret_cast<float*>(scratch.get());
   }
   dim3 grid(tblocks, nblocks, splits);
   void (*kern)(const float*, const float*, const uint8_t*, const float*, float*, float*, FcParams);
@@ -162,7 +164,7 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
     case 8: kern = fc_pq_kernel<8>; break;
     default: kern = fc_pq_kernel<0>; break;
   }
-  e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  e = allow_max_lds((const void*)kern);
   if (e == hipSuccess) {
     KernelTimer timer(stream);
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, x, D, codes, bias, y, partial, p);
@@ -173,10 +175,6 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
     hipLaunchKernelGGL(fc_reduce_kernel, dim3((unsigned)ceil_div_z(total, 256)), dim3(256), 0, stream,
                        partial, splits, N, Ct, bias, relu, y);
     e = hipGetLastError();
-  }
-  if (partial) {
-    hipError_t e2 = hipFreeAsync(partial, stream);
-    if (e == hipSuccess) e = e2;
   }
   return e;
 }

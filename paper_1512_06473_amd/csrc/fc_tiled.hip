@@ -49,7 +49,6 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kNI = 8;   // gather instructions per wave and subspace
-constexpr size_t kLdsMax = 160 * 1024;
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
@@ -387,7 +386,7 @@ bool make_fc_plan(int N, int Cs, int M, int K, int Csp, int Ct, FcPlan* out) {
     p.nphases = ceil_div(M, MC);
     p.mgroups = p.nphases * (MC / 4);  // code dwords per channel, whole phases
     const size_t lds = (size_t)2 * MC * p.KP * p.RS * sizeof(float);
-    if (lds > kLdsMax || (MC == 8 && (LPC != 16 || p.KP > 32))) continue;
+    if (lds > kLdsBytes || (MC == 8 && (LPC != 16 || p.KP > 32))) continue;
     p.tc = kWaves * kNI * (kWave / LPC);
     p.tblocks = ceil_div(Ct, p.tc);
     p.nblocks = ceil_div(N, NS);
@@ -420,7 +419,7 @@ hipError_t launch_t(const FcPlan& pl, const float* x, const float* D, const uint
   if constexpr (LPC == 16 && KB <= 2) {  // the only tables small enough for 8 subspaces per phase
     if (pl.p.MC == 8) k = fc_tiled_kernel<LPC, NC, KB, 8>;
   }
-  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
+  hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes4, bias, y, partial, pl.p);
   return hipGetLastError();
@@ -458,9 +457,10 @@ hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const f
   const size_t code_bytes = ((size_t)p.mgroups * p.ct_pad * 4 + 255) & ~(size_t)255;
   const size_t partial_elems = (size_t)p.splits * p.ct_pad * p.nblocks * p.NS;
   const size_t ws = code_bytes + (p.splits > 1 ? partial_elems * sizeof(float) : 0);
-  char* base = nullptr;
-  hipError_t e = hipMallocAsync((void**)&base, ws, stream);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, ws);
   if (e != hipSuccess) return e;
+  char* base = scratch.get();
   uint32_t* codes4 = reinterpret_cast<uint32_t*>(base);
   float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
   hipLaunchKernelGGL(fc_codes_kernel, dim3((unsigned)ceil_div(p.mgroups, 64), (unsigned)ceil_div(p.ct_pad, 64)),
@@ -481,8 +481,7 @@ hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const f
                        dim3(1024), 0, stream, partial, p, bias, y);
     e = hipGetLastError();
   }
-  hipError_t e2 = hipFreeAsync(base, stream);
-  return e == hipSuccess ? e2 : e;
+  return e;
 }
 
 }  // namespace qcnn

@@ -81,4 +81,28 @@ hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const f
 // (called once per device before the first hipMallocAsync).
 hipError_t retain_pool_memory();
 
+// LDS per workgroup on gfx950.
+constexpr size_t kLdsBytes = 160 * 1024;
+
+// The library's workspace for one call on `stream` (scratch.cpp): a buffer
+// per (device, stream), grown in stream order and kept until the process
+// ends.  The object holds that buffer's lock until it is destroyed, so it
+// must live until every kernel of the call has been enqueued.
+class Scratch {
+ public:
+  Scratch() = default;
+  ~Scratch();
+  Scratch(const Scratch&) = delete;
+  Scratch& operator=(const Scratch&) = delete;
+  hipError_t acquire(hipStream_t stream, size_t bytes);
+  char* get() const { return static_cast<char*>(ptr_); }
+
+ private:
+  void* slot_ = nullptr;
+  void* ptr_ = nullptr;
+};
+
+// Lets `kernel` take up to kLdsBytes of dynamic LDS (once per device).
+hipError_t allow_max_lds(const void* kernel);
+
 }  // namespace qcnn

@@ -290,6 +290,39 @@ def test_side_stream_and_determinism(api, dev, oracle):
     assert_bound(y1.cpu().numpy(), ref, A, "fc on a side stream")
 
 
+def test_workspace_streams_and_growth(api, dev, oracle):
+    # Conv and FC calls interleaved over two streams with no syncs between
+    # them, in an order that grows each stream's workspace and shrinks it
+    # back: every output must still match the oracle exactly.
+    rng = np.random.Generator(np.random.PCG64(2024))
+    conv_shapes = [(1, 16, 14, 14, 32, 3, 1, 1, 4, 16), (4, 64, 13, 13, 48, 3, 1, 1, 4, 64),
+                   (2, 24, 15, 15, 17, 5, 1, 2, 4, 128)]
+    fc_shapes = [(65, 96, 257, 4, 32), (7, 48, 33, 1, 16)]
+    conv_in = [wl.random_conv(rng, *sh, integer=True) for sh in conv_shapes]
+    fc_in = [wl.random_fc(rng, *sh, integer=True) for sh in fc_shapes]
+    streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
+    jobs = []
+    for rep in range(2):
+        for i, (sh, (x, D, c)) in enumerate(zip(conv_shapes, conv_in)):
+            with torch.cuda.stream(streams[(i + rep) % 2]):
+                y = api.conv_forward(T(x, dev), T(D, dev), T(c, dev), sh[6], sh[7])
+            jobs.append(("conv", i, y))
+        for i, (x, D, c) in enumerate(fc_in):
+            with torch.cuda.stream(streams[(i + rep + 1) % 2]):
+                y = api.fc_forward(T(x, dev), T(D, dev), T(c, dev))
+            jobs.append(("fc", i, y))
+    for st in streams:
+        st.synchronize()
+    for kind, i, y in jobs:
+        if kind == "conv":
+            x, D, c = conv_in[i]
+            ref = oracle.conv_lut(x, D, c, conv_shapes[i][6], conv_shapes[i][7])
+        else:
+            x, D, c = fc_in[i]
+            ref = oracle.fc_lut(x, D, c)
+        assert_exact(y.cpu().numpy(), ref, "%s %d across streams" % (kind, i))
+
+
 def test_out_of_range_codes_are_clamped(api, dev, oracle):
     # Precondition violation: codes >= K.  The kernels clamp them to K - 1.
     rng = np.random.Generator(np.random.PCG64(77))
