@@ -46,6 +46,9 @@ def _signatures():
         "qo_fc_direct": [P, I, I, P, I, I, I, P, I, P, I, P],
         "qo_fc_points": [P, I, I, P, I, I, I, P, I, P, I, P, I, P, P],
         "qo_maxpool": [P, I, I, I, I, I, I, P],
+        "qo_pq_assign": [P, I, I, I, P, I, I, I, P, P, P],
+        "qo_pq_update": [P, I, I, I, P, I, I, I, P, P, P],
+        "qo_pq_kmeans": [P, I, I, I, I, I, I, I, P, P, P, P],
         "qo_threads": [],
     }
 
@@ -264,3 +267,63 @@ def network(x, layers, absolute=False, layer_inputs=None):
         else:
             h = fc_lut(h32.reshape(h32.shape[0], -1), D, L["codes"], None, relu)
     return h
+
+
+# ---------------------------------------------------------------- quantizer
+# Sec. 3.1 Eq. (4) and Sec. 3.2 Eq. (6): k-means per subspace over the
+# sub-vectors of W [C_t][C_s][d_k][d_k] (d_k = 1: a fully-connected layer).
+
+def _wshape(W):
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    if W.ndim == 2:
+        W = W.reshape(W.shape[0], W.shape[1], 1, 1)
+    Ct, Cs, dk, dk2 = W.shape
+    assert dk == dk2
+    return W, Ct, Cs, dk
+
+
+def pq_assign(W, D):
+    """Nearest sub-codeword per sub-vector (fp32 decision, ties to the lowest
+    index).  Returns codes [C_t][d_k][d_k][M] (FC: [C_t][M]), the per-subspace
+    sums of the fp32 minimum distances and the exact float64 objective."""
+    fc = np.ndim(W) == 2
+    W, Ct, Cs, dk = _wshape(W)
+    D, Dp = _f32(D)
+    M, K, Csp = D.shape
+    codes = np.empty((Ct, dk, dk, M), np.uint8)
+    o32 = np.empty(M, np.float64)
+    o64 = np.empty(M, np.float64)
+    _chk(lib().qo_pq_assign(W.ctypes.data, Ct, Cs, dk, Dp, M, K, Csp, codes.ctypes.data,
+                            o32.ctypes.data, o64.ctypes.data))
+    return (codes.reshape(Ct, M) if fc else codes), o32, o64
+
+
+def pq_update(W, codes, D):
+    """Each sub-codeword becomes the mean of its sub-vectors (float64 sum in
+    sub-vector order, rounded to fp32); unused ones keep their value.
+    Returns the new codebooks [M][K][C'_s] fp32 and the counts [M][K]."""
+    W, Ct, Cs, dk = _wshape(W)
+    D, Dp = _f32(D)
+    M, K, Csp = D.shape
+    codes, cp = _u8(np.asarray(codes).reshape(Ct, dk, dk, M))
+    out = np.empty_like(D)
+    counts = np.empty((M, K), np.int32)
+    _chk(lib().qo_pq_update(W.ctypes.data, Ct, Cs, dk, cp, M, K, Csp, Dp, out.ctypes.data,
+                            counts.ctypes.data))
+    return out, counts
+
+
+def pq_kmeans(W, D_init, iters):
+    """iters x (assign, update) then a final assignment.  Returns the learned
+    codebooks, the codes and the per-assignment objective totals (fp32-distance
+    sums and exact float64 values), each of length iters + 1."""
+    fc = np.ndim(W) == 2
+    W, Ct, Cs, dk = _wshape(W)
+    D = np.array(D_init, dtype=np.float32, copy=True, order="C")
+    M, K, Csp = D.shape
+    codes = np.empty((Ct, dk, dk, M), np.uint8)
+    o32 = np.empty(iters + 1, np.float64)
+    o64 = np.empty(iters + 1, np.float64)
+    _chk(lib().qo_pq_kmeans(W.ctypes.data, Ct, Cs, dk, M, K, Csp, int(iters), D.ctypes.data,
+                            codes.ctypes.data, o32.ctypes.data, o64.ctypes.data))
+    return D, (codes.reshape(Ct, M) if fc else codes), o32, o64

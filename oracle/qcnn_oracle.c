@@ -418,6 +418,147 @@ int qo_maxpool(const float* x, int N, int C, int H, int W, int k, int s, double*
 }
 
 /* Threads the OpenMP runtime will use (1 when built without OpenMP). */
+/* ------------------------------------------------------------------------ */
+/* Parameter quantization: how the sub-codebooks and codes are learned.
+ * Sec. 3.1, Eq. (4): for subspace m, minimise || D^(m) B^(m) - W^(m) ||_F^2
+ * over D^(m) (K sub-codewords of C'_s entries) and B^(m) (one indicator
+ * column per sub-vector); the paper solves it by k-means over the sub-vectors.
+ * Sec. 3.2, Eq. (6): a conv layer shares D^(m) over every kernel position
+ * p_k, so subspace m's k-means runs over the sub-vectors of all (c_t, p_k)
+ * and its objective is the sum over p_k of Eq. (4)'s.
+ *
+ * Weights W: [C_t][C_s][d_k][d_k] (a fully-connected layer is d_k = 1, i.e.
+ * W[c_t][c_s], the transpose of the paper's C_s x C_t matrix); the sub-vector
+ * of (c_t, p_k = (ky, kx), m) is ( W[c_t][m C'_s + j][ky][kx] )_{j < C'_s}.
+ * Codes [C_t][d_k][d_k][M] and codebooks [M][K][C'_s] as in the forward.
+ *
+ * Readings of what the paper leaves open (it names k-means only):
+ *   Q1 the distance is the squared Euclidean one (the Frobenius objective
+ *      taken column by column).
+ *   Q2 assignment: the nearest sub-codeword, decided on fp32 distances
+ *      accumulated as d = fmaf(w_j - c_j, w_j - c_j, d) over j in order
+ *      (the precision of the kernel that implements it), ties going to the
+ *      lowest index.
+ *   Q3 update: a sub-codeword becomes the mean of the sub-vectors assigned to
+ *      it, summed in double in sub-vector order (c_t, ky, kx) and rounded to
+ *      fp32; a sub-codeword that no sub-vector chose keeps its value.
+ *   Q4 the initial sub-codewords are an input (the caller draws them).
+ *   Q5 an iteration is an assignment followed by an update; after the last
+ *      one a final assignment makes the codes match the final sub-codewords.
+ * The objective of an assignment is reported twice: the sum of the fp32
+ * minimum distances (what the assignment decided on) and the exact double
+ * value of || D B - W ||^2 for the chosen codes.                             */
+
+static float pq_dist32(const float* W, int Cs, int dk, int t, int p, int m, int Csp, const float* c) {
+  float d = 0.0f;
+  for (int j = 0; j < Csp; ++j) {
+    float w = W[(((size_t)t * Cs + (size_t)m * Csp + j) * dk * dk) + p];
+    float diff = w - c[j];
+    d = fmaf(diff, diff, d);
+  }
+  return d;
+}
+
+static int check_quant(int Ct, int Cs, int dk, int M, int K, int Csp) {
+  if (Ct < 1 || Cs < 1 || dk < 1 || M < 1 || Csp < 1) return QO_EARG;
+  if (K < 1 || K > 256) return QO_EK;
+  if (Cs != M * Csp) return QO_ESHAPE;
+  return 0;
+}
+
+/* Assignment step.  codes: [C_t][d_k][d_k][M]; obj32, obj64: [M] or NULL. */
+int qo_pq_assign(const float* W, int Ct, int Cs, int dk, const float* D, int M, int K, int Csp,
+                 uint8_t* codes, double* obj32, double* obj64) {
+  int e;
+  if (!W || !D || !codes) return QO_EARG;
+  if ((e = check_quant(Ct, Cs, dk, M, K, Csp))) return e;
+  const int P = dk * dk;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = 0; m < M; ++m) {
+    const float* Dm = D + (size_t)m * K * Csp;
+    double s32 = 0.0, s64 = 0.0;
+    for (int t = 0; t < Ct; ++t)
+      for (int p = 0; p < P; ++p) {
+        int best = 0;
+        float bd = pq_dist32(W, Cs, dk, t, p, m, Csp, Dm);
+        for (int k = 1; k < K; ++k) {
+          float d = pq_dist32(W, Cs, dk, t, p, m, Csp, Dm + (size_t)k * Csp);
+          if (d < bd) { bd = d; best = k; }
+        }
+        codes[((size_t)t * P + p) * M + m] = (uint8_t)best;
+        s32 += (double)bd;
+        for (int j = 0; j < Csp; ++j) {
+          double diff = (double)W[(((size_t)t * Cs + (size_t)m * Csp + j) * P) + p] -
+                        (double)Dm[(size_t)best * Csp + j];
+          s64 += diff * diff;
+        }
+      }
+    if (obj32) obj32[m] = s32;
+    if (obj64) obj64[m] = s64;
+  }
+  return 0;
+}
+
+/* Update step.  D_in, D_out: [M][K][C'_s] (may be the same array);
+ * counts: [M][K] sub-vectors per sub-codeword, or NULL.                     */
+int qo_pq_update(const float* W, int Ct, int Cs, int dk, const uint8_t* codes, int M, int K, int Csp,
+                 const float* D_in, float* D_out, int* counts) {
+  int e;
+  if (!W || !codes || !D_in || !D_out) return QO_EARG;
+  if ((e = check_quant(Ct, Cs, dk, M, K, Csp))) return e;
+  if ((e = check_codes(codes, (size_t)Ct * dk * dk * M, K))) return e;
+  const int P = dk * dk;
+  int failed = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = 0; m < M; ++m) {
+    double* sum = (double*)calloc((size_t)K * Csp, sizeof(double));
+    int* cnt = (int*)calloc((size_t)K, sizeof(int));
+    if (!sum || !cnt) { free(sum); free(cnt); failed = 1; continue; }
+    for (int t = 0; t < Ct; ++t)
+      for (int p = 0; p < P; ++p) {
+        int k = codes[((size_t)t * P + p) * M + m];
+        cnt[k] += 1;
+        for (int j = 0; j < Csp; ++j)
+          sum[(size_t)k * Csp + j] += (double)W[(((size_t)t * Cs + (size_t)m * Csp + j) * P) + p];
+      }
+    for (int k = 0; k < K; ++k) {
+      for (int j = 0; j < Csp; ++j) {
+        size_t o = ((size_t)m * K + k) * Csp + j;
+        D_out[o] = cnt[k] ? (float)(sum[(size_t)k * Csp + j] / (double)cnt[k]) : D_in[o];
+      }
+      if (counts) counts[(size_t)m * K + k] = cnt[k];
+    }
+    free(sum);
+    free(cnt);
+  }
+  return failed ? QO_ENOMEM : 0;
+}
+
+/* k-means (Q5): iters x (assign, update), then a final assignment.
+ * D: [M][K][C'_s] in: initial sub-codewords, out: learned ones.
+ * obj32, obj64: [iters + 1] totals over m of each assignment's objective.  */
+int qo_pq_kmeans(const float* W, int Ct, int Cs, int dk, int M, int K, int Csp, int iters,
+                 float* D, uint8_t* codes, double* obj32, double* obj64) {
+  int e;
+  if (!W || !D || !codes || iters < 0) return QO_EARG;
+  if ((e = check_quant(Ct, Cs, dk, M, K, Csp))) return e;
+  double* o32 = (double*)malloc((size_t)M * sizeof(double));
+  double* o64 = (double*)malloc((size_t)M * sizeof(double));
+  if (!o32 || !o64) { free(o32); free(o64); return QO_ENOMEM; }
+  for (int it = 0; it <= iters && !e; ++it) {
+    e = qo_pq_assign(W, Ct, Cs, dk, D, M, K, Csp, codes, o32, o64);
+    if (e) break;
+    double a = 0.0, b = 0.0;
+    for (int m = 0; m < M; ++m) { a += o32[m]; b += o64[m]; }
+    if (obj32) obj32[it] = a;
+    if (obj64) obj64[it] = b;
+    if (it < iters) e = qo_pq_update(W, Ct, Cs, dk, codes, M, K, Csp, D, D, NULL);
+  }
+  free(o32);
+  free(o64);
+  return e;
+}
+
 #ifdef _OPENMP
 #include <omp.h>
 int qo_threads(void) { return omp_get_max_threads(); }

@@ -177,3 +177,30 @@ def random_fc(rng: np.random.Generator, N, Cs, Ct, Csp, K, integer=False, sigma=
     x = draw_input(rng, (N, Cs), integer)
     D, codes = draw_layer(rng, L, integer)
     return x, D, codes
+
+
+# ------------------------------------------------------------ quantizer inputs
+# Dense weights for the parameter quantization (Eq. (4), (6)): W [C_t][C_s]
+# [d_k][d_k] (d_k = 1: a fully-connected layer) = sigma * N(0, 1), and initial
+# sub-codebooks [M][K][C'_s] drawn from the same distribution (the k-means
+# start is an input).  ``integer=True`` draws both in {-4..4}: every distance
+# and every mean of such vectors is then exact or nearly so, which pins ties.
+
+QUANT_LAYERS = {
+    # name: (C_t, C_s, d_k, C'_s, K) -- AlexNet conv3 and fc6 shapes of the headline workloads
+    "conv3": (384, 256, 3, 4, 128),
+    "fc6": (4096, 9216, 1, 4, 32),
+}
+
+
+def random_quant(rng: np.random.Generator, Ct, Cs, dk, Csp, K, integer=False, sigma=0.05):
+    M = Cs // Csp
+    if integer:
+        W = rng.integers(-4, 5, (Ct, Cs, dk, dk)).astype(np.float32)
+        D = rng.integers(-4, 5, (M, K, Csp)).astype(np.float32)
+    else:
+        W = (sigma * rng.standard_normal((Ct, Cs, dk, dk))).astype(np.float32)
+        D = (sigma * rng.standard_normal((M, K, Csp))).astype(np.float32)
+    if dk == 1:
+        W = W.reshape(Ct, Cs)
+    return W, D

@@ -48,6 +48,92 @@ def rebuilt_fc(D, codes):
     return sub.reshape(codes.shape[0], -1).astype(np.float64)
 
 
+def subvectors(W, Csp):
+    """Sub-vectors of W [C_t][C_s][d_k][d_k] grouped by subspace:
+    [M][C_t d_k d_k][C'_s], in (c_t, ky, kx) order (numpy reshapes only)."""
+    Ct, Cs, dk, _ = W.shape
+    return W.reshape(Ct, Cs // Csp, Csp, dk, dk).transpose(1, 0, 3, 4, 2).reshape(Cs // Csp, -1, Csp)
+
+
+def quant_checks(rng):
+    out = []
+    # K = 1: the single sub-codeword is the mean of every sub-vector (Eq. (4)
+    # with one indicator row), the objective the total squared deviation.
+    W = rng.standard_normal((5, 6, 3, 3)).astype(np.float32)
+    V = subvectors(W.astype(np.float64), 3)
+    D, codes, o32, o64 = O.pq_kmeans(W, np.zeros((2, 1, 3), np.float32), 1)
+    mean = V.mean(axis=1)
+    out.append(("quant K=1 mean", np.allclose(D[:, 0], mean, rtol=1e-6, atol=1e-7) and not codes.any()))
+    dev = ((V - mean[:, None, :]) ** 2).sum()
+    out.append(("quant K=1 objective", abs(o64[-1] - dev) <= 1e-6 * dev))
+    # A pool of R distinct sub-vectors per subspace and the pool among the
+    # initial sub-codewords: every sub-vector is matched exactly, error 0.
+    Ct, Cs, dk, Csp, K, R = 7, 8, 2, 4, 16, 5
+    M = Cs // Csp
+    pool = rng.integers(-9, 10, (M, R, Csp)).astype(np.float32)
+    pool[:, :, 0] = np.arange(R)[None, :] * 20  # distinct rows
+    r = rng.integers(0, R, (M, Ct * dk * dk))
+    V = pool[np.arange(M)[:, None], r]  # [M][n][Csp]
+    W = V.reshape(M, Ct, dk, dk, Csp).transpose(1, 0, 4, 2, 3).reshape(Ct, Cs, dk, dk)
+    D0 = (rng.standard_normal((M, K, Csp)) * 100 + 1000).astype(np.float32)
+    perm = rng.permutation(K)[:R]
+    D0[:, perm] = pool
+    codes, o32, o64 = O.pq_assign(W, D0)
+    got = codes.reshape(Ct * dk * dk, M).T
+    out.append(("quant exact pool", np.array_equal(got, perm[r]) and o64.sum() == 0.0 and o32.sum() == 0.0))
+    # Nearest sub-codeword: against float64 distances from numpy.
+    for shape in [(9, 12, 3, 4, 16), (33, 8, 1, 2, 64), (4, 6, 5, 3, 7)]:
+        Ct, Cs, dk, Csp, K = shape
+        W, D = wl.random_quant(rng, Ct, Cs, dk, Csp, K)
+        W4 = W.reshape(Ct, Cs, dk, dk)
+        codes, o32, o64 = O.pq_assign(W, D)
+        V = subvectors(W4.astype(np.float64), Csp)
+        dist = ((V[:, :, None, :] - D.astype(np.float64)[:, None, :, :]) ** 2).sum(-1)  # [M][n][K]
+        got = codes.reshape(Ct * dk * dk, Cs // Csp).T
+        chosen = np.take_along_axis(dist, got[:, :, None].astype(np.int64), 2)[..., 0]
+        best = dist.min(-1)
+        out.append(("quant nearest %s" % (shape,), np.all(chosen <= best * (1 + 1e-5) + 1e-12)))
+        rec = ((V - D.astype(np.float64)[np.arange(Cs // Csp)[:, None], got]) ** 2).sum(axis=(1, 2))
+        out.append(("quant objective = ||DB - W||^2 %s" % (shape,), np.allclose(o64, rec, rtol=1e-10, atol=1e-14)))
+        # Update: the mean of each cluster; an unused sub-codeword keeps its value.
+        D[:, -1] = 1e3  # far from every sub-vector: never chosen
+        codes, _, _ = O.pq_assign(W, D)
+        got = codes.reshape(Ct * dk * dk, Cs // Csp).T
+        Dn, cnt = O.pq_update(W, codes, D)
+        ok = True
+        for m in range(Cs // Csp):
+            for k in range(K):
+                sel = V[m][got[m] == k]
+                ok &= cnt[m, k] == len(sel)
+                if len(sel):
+                    ok &= np.allclose(Dn[m, k], sel.mean(0), rtol=1e-6, atol=1e-8)
+                else:
+                    ok &= np.array_equal(Dn[m, k], D[m, k])
+        out.append(("quant update means %s" % (shape,), bool(ok) and (cnt[:, -1] == 0).all()))
+    # Integer data: distances are exact, so the decision must be numpy's
+    # argmin (the first minimum: ties to the lowest index).
+    Ct, Cs, dk, Csp, K = 20, 12, 3, 3, 40
+    W, D = wl.random_quant(rng, Ct, Cs, dk, Csp, K, integer=True)
+    codes, _, _ = O.pq_assign(W, D)
+    V = subvectors(W.astype(np.float64), Csp)
+    dist = ((V[:, :, None, :] - D.astype(np.float64)[:, None, :, :]) ** 2).sum(-1)
+    out.append(("quant ties to lowest index", np.array_equal(codes.reshape(-1, Cs // Csp).T, dist.argmin(-1))))
+    # Lloyd iterations never raise the objective; the final codes are the
+    # assignment to the final sub-codewords.
+    W, D0 = wl.random_quant(rng, 40, 16, 3, 4, 32)
+    D, codes, o32, o64 = O.pq_kmeans(W, D0, 6)
+    out.append(("quant objective non-increasing", np.all(np.diff(o64) <= 1e-6 * o64[:-1])))
+    c2, _, _ = O.pq_assign(W, D)
+    out.append(("quant final codes match codebooks", np.array_equal(codes, c2)))
+    # Eq. (6) = Eq. (4) over the gathered sub-vectors: quantizing a conv layer
+    # is quantizing the FC matrix whose rows are its (c_t, p_k) kernels' columns.
+    Wf = W.transpose(0, 2, 3, 1).reshape(-1, W.shape[1])
+    Df, cf, o32f, o64f = O.pq_kmeans(Wf, D0, 6)
+    out.append(("quant conv = fc on gathered sub-vectors",
+                np.array_equal(D, Df) and np.array_equal(codes.reshape(cf.shape), cf) and np.array_equal(o64, o64f)))
+    return out
+
+
 def checks():
     out = []
     # hand-worked (see test_oracle.py for the arithmetic)
@@ -106,6 +192,7 @@ def checks():
     ref = np.array([[[[xm[0, ch, 2 * i:2 * i + 3, 2 * j:2 * j + 3].max() for j in range(4)] for i in range(3)]
                      for ch in range(2)]])
     out.append(("maxpool", np.array_equal(ym, ref)))
+    out += quant_checks(rng)
     return out
 
 

@@ -316,3 +316,23 @@ def test_workload_generator_is_deterministic():
     assert np.array_equal(a["layers"][0]["codes"], b["layers"][0]["codes"])
     assert a["x"].dtype == np.float32 and a["x"].min() >= 0
     assert a["layers"][0]["codes"].max() < 16
+
+
+# ------------------------------------------------------------ quantizer pins
+
+def test_quantizer_pins(oracle):
+    """Eq. (4), (6): the k-means pins of the battery (K = 1 mean, exact pool,
+    nearest against numpy distances, ||DB - W||^2, cluster means, ties,
+    monotone objective, conv = FC on gathered sub-vectors), in process."""
+    import pin_battery
+    res = pin_battery.quant_checks(np.random.Generator(np.random.PCG64(99)))
+    bad = [name for name, ok in res if not ok]
+    assert not bad, bad
+
+
+def test_quantizer_errors(oracle):
+    W = np.zeros((4, 8), np.float32)
+    with pytest.raises(oracle.OracleError):
+        oracle.pq_assign(W, np.zeros((3, 4, 2), np.float32))  # C_s != M C'_s
+    with pytest.raises(oracle.OracleError):
+        oracle.pq_update(W, np.full((4, 2), 9, np.uint8), np.zeros((2, 4, 4), np.float32))  # code >= K

@@ -42,11 +42,26 @@ MUTANTS = [
     ("qo_conv_points", "int xi = xo * stride - pad + kx;", "int xi = xo * stride - pad + ky;", "point: kx read as ky"),
     ("qo_fc_direct", "for (int c = 0; c < Cs; ++c) s +=", "for (int c = 0; c < Cs - 1; ++c) s +=", "FC last input dropped"),
     ("qo_maxpool", "if (v > best) best = v;", "if (v < best || best == -INFINITY) best = v;", "min instead of max"),
+    ("pq_dist32", "* dk * dk) + p]", "* dk) + p]", "quantizer: sub-vector stride over kernel positions"),
+    ("pq_dist32", "d = fmaf(diff, diff, d);", "d = fmaf(diff, fabsf(w), d);", "quantizer: distance not squared"),
+    ("qo_pq_assign", "if (d < bd) { bd = d; best = k; }", "if (d <= bd) { bd = d; best = k; }",
+     "quantizer: ties to the highest index"),
+    ("qo_pq_assign", "for (int k = 1; k < K; ++k) {", "for (int k = 1; k < K - 1; ++k) {",
+     "quantizer: last sub-codeword never considered"),
+    ("qo_pq_assign", "s64 += diff * diff;", "s64 += fabs(diff);", "quantizer: objective not squared"),
+    ("qo_pq_update", "int k = codes[((size_t)t * P + p) * M + m];", "int k = codes[((size_t)p * Ct + t) * M + m];",
+     "quantizer: update reads the codes transposed"),
+    ("qo_pq_update", "/ (double)cnt[k])", "/ (double)(cnt[k] + 1))", "quantizer: mean divided by count + 1"),
+    ("qo_pq_update", ": D_in[o];", ": 0.0f;", "quantizer: unused sub-codeword zeroed"),
+    ("qo_pq_kmeans", "for (int it = 0; it <= iters && !e; ++it) {", "for (int it = 0; it < iters && !e; ++it) {",
+     "quantizer: no final assignment"),
 ]
 
 
 def _mutate(src: str, func: str, old: str, new: str) -> str:
-    start = src.index("int %s(" % func)
+    start = src.find("int %s(" % func)
+    if start < 0:
+        start = src.index("float %s(" % func)
     end = src.index("\n}\n", start)
     body = src[start:end]
     assert old in body, (func, old)
