@@ -109,6 +109,48 @@ qcnn_status qcnn_fc_forward(const float* x, int N, int C_s,
                             const uint8_t* codes, int C_t,
                             const float* bias, int relu, float* y, void* stream);
 
+/* ---- Parameter quantization (the step that produces codebooks and codes).
+ * Sec. 3.1, Eq. (4): for each subspace m, minimise || D^(m) B^(m) - W^(m) ||_F^2
+ * over the K sub-codewords D^(m) and the indicator columns B^(m), by k-means
+ * over the sub-vectors; Sec. 3.2, Eq. (6): a conv layer shares D^(m) over all
+ * kernel positions p_k, so subspace m's k-means runs over the sub-vectors of
+ * every (c_t, p_k).
+ * W: [C_t][C_s][d_k][d_k] fp32 (a fully-connected layer is d_k = 1, W[c_t][c_s]);
+ * the sub-vector of (c_t, p_k, m) is W[c_t][m C'_s + j][p_k], j < C'_s.
+ * codebooks: [M][K][C'_s]; codes: uint8 [C_t][d_k][d_k][M] (FC: [C_t][M]),
+ * the layouts qcnn_conv_forward / qcnn_fc_forward read.
+ * Assignment: the nearest sub-codeword in squared Euclidean distance,
+ * accumulated in fp32 as d = fma(w_j - c_j, w_j - c_j, d) over j in order,
+ * the first minimum winning (ties go to the lowest index).  Update: each
+ * sub-codeword becomes the mean of its sub-vectors, summed in float64 in
+ * sub-vector order (c_t, p_k) and rounded to fp32; one that no sub-vector
+ * chose keeps its value.  Objectives are float64 sums of the fp32 minimum
+ * distances.  Limits as for the forward: 1 <= K <= 256, C'_s <= 16, C_s =
+ * M C'_s, M <= 65535.  All pointers are device pointers; inputs and outputs
+ * must not overlap (codebooks are updated in place where stated). */
+
+/* One assignment.  codes (output); objective (output, nullable): [M] float64,
+ * per subspace the sum of the minimum distances. */
+qcnn_status qcnn_pq_assign(const float* W, int C_t, int C_s, int d_k,
+                           const float* codebooks, int M, int K, int Csp,
+                           uint8_t* codes, double* objective, void* stream);
+
+/* One update from given codes (every code must be < K): codebooks is read
+ * and replaced in place; counts (output, nullable): int [M][K], sub-vectors
+ * per sub-codeword. */
+qcnn_status qcnn_pq_update(const float* W, int C_t, int C_s, int d_k,
+                           const uint8_t* codes, int M, int K, int Csp,
+                           float* codebooks, int* counts, void* stream);
+
+/* k-means: iters x (assignment, update), then a final assignment, so that
+ * the codes match the returned sub-codewords.  codebooks: in, the initial
+ * sub-codewords (the caller draws them); out, the learned ones.  codes
+ * (output); objective (output, nullable): [iters + 1] float64, the total
+ * over m after each assignment.  iters >= 0. */
+qcnn_status qcnn_pq_kmeans(const float* W, int C_t, int C_s, int d_k,
+                           int M, int K, int Csp, int iters,
+                           float* codebooks, uint8_t* codes, double* objective, void* stream);
+
 /* Network glue between PQ layers (not part of the paper's method): max
  * pooling over k x k windows with stride s and no padding,
  *   y[n][c][yo][xo] = max_{dy,dx < k} x[n][c][yo s + dy][xo s + dx],
@@ -128,8 +170,9 @@ int qcnn_version(void);
 /* Kernel timing, for benchmarks and profiling.  While enabled, every
  * compute call above records a pair of HIP events on its stream around its
  * main kernel (the gather kernel of qcnn_conv_forward and qcnn_fc_forward,
- * the table kernel of qcnn_lut_build); code re-layout and split-sum kernels
- * are outside the pair.  Off by default; when off the calls create no events.
+ * the table kernel of qcnn_lut_build, the assignment or update kernels of
+ * qcnn_pq_assign / qcnn_pq_update, the whole iteration loop of
+ * qcnn_pq_kmeans); code re-layout and split-sum kernels are outside the pair.  Off by default; when off the calls create no events.
  * Enabling and disabling are process-wide and take effect for later calls. */
 qcnn_status qcnn_timing_enable(int enable);
 

@@ -19,6 +19,9 @@ SIGNATURES = {
     "qcnn_conv_forward": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
     "qcnn_fc_forward": ([P, I, I, P, I, I, I, P, I, P, I, P, P], I),
     "qcnn_maxpool2d": ([P, I, I, I, I, I, I, P, P], I),
+    "qcnn_pq_assign": ([P, I, I, I, P, I, I, I, P, P, P], I),
+    "qcnn_pq_update": ([P, I, I, I, P, I, I, I, P, P, P], I),
+    "qcnn_pq_kmeans": ([P, I, I, I, I, I, I, I, P, P, P, P], I),
     "qcnn_out_size": ([I, I, I, I], I),
     "qcnn_status_string": ([I], ctypes.c_char_p),
     "qcnn_version": ([], I),

@@ -149,3 +149,73 @@ def timing_read() -> Tuple[float, int]:
     n = ctypes.c_longlong(0)
     check(lib().qcnn_timing_read(ctypes.byref(ms), ctypes.byref(n)), "qcnn_timing_read")
     return ms.value, n.value
+
+
+# ------------------------------------------------------ parameter quantization
+
+def _quant_w(W: torch.Tensor):
+    """W [C_t][C_s][d_k][d_k] (or [C_t][C_s] for an FC layer) -> (C_t, C_s, d_k)."""
+    if W.dim() == 2:
+        return W.shape[0], W.shape[1], 1
+    _need(W, "W", torch.float32, 4)
+    Ct, Cs, dk, dk2 = W.shape
+    if dk != dk2:
+        raise ValueError("W must be [C_t][C_s][d_k][d_k]")
+    return Ct, Cs, dk
+
+
+def _codes_shape(W, M):
+    return (W.shape[0], M) if W.dim() == 2 else (W.shape[0], W.shape[2], W.shape[3], M)
+
+
+def pq_assign(W: torch.Tensor, codebooks: torch.Tensor, codes: Optional[torch.Tensor] = None,
+              objective: Optional[torch.Tensor] = None):
+    """Nearest sub-codeword of every sub-vector (Eq. (4)/(6) assignment step,
+    qcnn_pq_assign).  Returns (codes uint8, per-subspace objective float64 [M])."""
+    if W.dim() == 2:
+        _need(W, "W", torch.float32, 2)
+    Ct, Cs, dk = _quant_w(W)
+    _need(codebooks, "codebooks", torch.float32, 3, W.device)
+    M, K, Csp = codebooks.shape
+    if codes is None:
+        codes = torch.empty(_codes_shape(W, M), dtype=torch.uint8, device=W.device)
+    if objective is None:
+        objective = torch.empty(M, dtype=torch.float64, device=W.device)
+    check(lib().qcnn_pq_assign(W.data_ptr(), Ct, Cs, dk, codebooks.data_ptr(), M, K, Csp, codes.data_ptr(),
+                               objective.data_ptr(), _stream(W)), "qcnn_pq_assign")
+    return codes, objective
+
+
+def pq_update(W: torch.Tensor, codes: torch.Tensor, codebooks: torch.Tensor, counts: Optional[torch.Tensor] = None):
+    """Each sub-codeword becomes the mean of its sub-vectors (update step,
+    qcnn_pq_update); ``codebooks`` is updated in place and returned with the
+    counts [M][K] int32."""
+    if W.dim() == 2:
+        _need(W, "W", torch.float32, 2)
+    Ct, Cs, dk = _quant_w(W)
+    _need(codebooks, "codebooks", torch.float32, 3, W.device)
+    M, K, Csp = codebooks.shape
+    if codes.dtype != torch.uint8 or not codes.is_contiguous() or tuple(codes.shape) != _codes_shape(W, M):
+        raise ValueError("codes must be contiguous uint8 %s" % (_codes_shape(W, M),))
+    if counts is None:
+        counts = torch.empty((M, K), dtype=torch.int32, device=W.device)
+    check(lib().qcnn_pq_update(W.data_ptr(), Ct, Cs, dk, codes.data_ptr(), M, K, Csp, codebooks.data_ptr(),
+                               counts.data_ptr(), _stream(W)), "qcnn_pq_update")
+    return codebooks, counts
+
+
+def pq_kmeans(W: torch.Tensor, init_codebooks: torch.Tensor, iters: int):
+    """Learn sub-codebooks and codes by k-means (qcnn_pq_kmeans): iters x
+    (assignment, update) and a final assignment.  Returns (codebooks, codes,
+    objective float64 [iters + 1]); ``init_codebooks`` is not modified."""
+    if W.dim() == 2:
+        _need(W, "W", torch.float32, 2)
+    Ct, Cs, dk = _quant_w(W)
+    _need(init_codebooks, "init_codebooks", torch.float32, 3, W.device)
+    D = init_codebooks.clone()
+    M, K, Csp = D.shape
+    codes = torch.empty(_codes_shape(W, M), dtype=torch.uint8, device=W.device)
+    objective = torch.empty(int(iters) + 1, dtype=torch.float64, device=W.device)
+    check(lib().qcnn_pq_kmeans(W.data_ptr(), Ct, Cs, dk, M, K, Csp, int(iters), D.data_ptr(), codes.data_ptr(),
+                               objective.data_ptr(), _stream(W)), "qcnn_pq_kmeans")
+    return D, codes, objective

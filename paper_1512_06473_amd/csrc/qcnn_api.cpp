@@ -247,6 +247,69 @@ qcnn_status qcnn_fc_forward(const float* x, int N, int C_s, const float* codeboo
   return hip_status(qcnn::launch_fc_forward(N, C_s, M, K, Csp, C_t, x, codebooks, codes, bias, relu ? 1 : 0, y, st));
 }
 
+// Shared validation of the quantizer entry points (host only).
+static qcnn_status check_quant(const float* W, int C_t, int C_s, int d_k, int M, int K, int Csp, size_t* nw,
+                               size_t* nd, size_t* nc) {
+  if (!W) return QCNN_ERR_NULL;
+  if (C_t < 1 || d_k < 1) return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(1, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  *nw = elems({C_t, C_s, d_k, d_k});
+  *nd = elems({M, K, Csp});
+  *nc = elems({C_t, d_k, d_k, M});
+  if (!*nw || !*nd || !*nc) return QCNN_ERR_SHAPE;
+  if ((long long)C_t * d_k * d_k > (1LL << 30)) return QCNN_ERR_UNSUPPORTED;
+  return QCNN_OK;
+}
+
+qcnn_status qcnn_pq_assign(const float* W, int C_t, int C_s, int d_k, const float* codebooks, int M, int K, int Csp,
+                           uint8_t* codes, double* objective, void* stream) {
+  size_t nw, nd, nc;
+  qcnn_status s = check_quant(W, C_t, C_s, d_k, M, K, Csp, &nw, &nd, &nc);
+  if (s != QCNN_OK) return s;
+  if (!codebooks || !codes) return QCNN_ERR_NULL;
+  if (overlap(codes, nc, W, nw * 4) || overlap(codes, nc, codebooks, nd * 4) ||
+      overlap(objective, (size_t)M * 8, W, nw * 4) || overlap(objective, (size_t)M * 8, codebooks, nd * 4) ||
+      overlap(objective, (size_t)M * 8, codes, nc))
+    return QCNN_ERR_ALIAS;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  return hip_status(qcnn::launch_pq_assign(C_t, C_s, d_k, W, codebooks, M, K, Csp, codes, objective,
+                                           (hipStream_t)stream));
+}
+
+qcnn_status qcnn_pq_update(const float* W, int C_t, int C_s, int d_k, const uint8_t* codes, int M, int K, int Csp,
+                           float* codebooks, int* counts, void* stream) {
+  size_t nw, nd, nc;
+  qcnn_status s = check_quant(W, C_t, C_s, d_k, M, K, Csp, &nw, &nd, &nc);
+  if (s != QCNN_OK) return s;
+  if (!codebooks || !codes) return QCNN_ERR_NULL;
+  if (overlap(codebooks, nd * 4, W, nw * 4) || overlap(codebooks, nd * 4, codes, nc) ||
+      overlap(counts, nd / Csp * 4, W, nw * 4) || overlap(counts, nd / Csp * 4, codes, nc) ||
+      overlap(counts, nd / Csp * 4, codebooks, nd * 4))
+    return QCNN_ERR_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  s = check_codes(codes, nc, K, st);
+  if (s != QCNN_OK) return s;
+  return hip_status(qcnn::launch_pq_update(C_t, C_s, d_k, W, codes, M, K, Csp, codebooks, counts, st));
+}
+
+qcnn_status qcnn_pq_kmeans(const float* W, int C_t, int C_s, int d_k, int M, int K, int Csp, int iters,
+                           float* codebooks, uint8_t* codes, double* objective, void* stream) {
+  size_t nw, nd, nc;
+  qcnn_status s = check_quant(W, C_t, C_s, d_k, M, K, Csp, &nw, &nd, &nc);
+  if (s != QCNN_OK) return s;
+  if (!codebooks || !codes) return QCNN_ERR_NULL;
+  if (iters < 0) return QCNN_ERR_SHAPE;
+  const size_t no = ((size_t)iters + 1) * 8;
+  if (overlap(codebooks, nd * 4, W, nw * 4) || overlap(codebooks, nd * 4, codes, nc) || overlap(codes, nc, W, nw * 4) ||
+      overlap(objective, no, W, nw * 4) || overlap(objective, no, codebooks, nd * 4) || overlap(objective, no, codes, nc))
+    return QCNN_ERR_ALIAS;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  return hip_status(qcnn::launch_pq_kmeans(C_t, C_s, d_k, W, M, K, Csp, iters, codebooks, codes, objective,
+                                           (hipStream_t)stream));
+}
+
 qcnn_status qcnn_maxpool2d(const float* x, int N, int C, int H, int W, int k, int s, float* y, void* stream) {
   if (!x || !y) return QCNN_ERR_NULL;
   if (N < 1 || C < 1 || H < 1 || W < 1 || k < 1 || s < 1) return QCNN_ERR_SHAPE;

@@ -77,6 +77,14 @@ bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct);
 hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
                            const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream);
 
+// Parameter quantization (quantize.hip); objective arrays are device float64.
+hipError_t launch_pq_assign(int Ct, int Cs, int dk, const float* W, const float* D, int M, int K, int Csp,
+                            uint8_t* codes, double* objective, hipStream_t stream);
+hipError_t launch_pq_update(int Ct, int Cs, int dk, const float* W, const uint8_t* codes, int M, int K, int Csp,
+                            float* D, int* counts, hipStream_t stream);
+hipError_t launch_pq_kmeans(int Ct, int Cs, int dk, const float* W, int M, int K, int Csp, int iters, float* D,
+                            uint8_t* codes, double* objective, hipStream_t stream);
+
 // Keep freed stream-ordered allocations in the device's default pool
 // (called once per device before the first hipMallocAsync).
 hipError_t retain_pool_memory();

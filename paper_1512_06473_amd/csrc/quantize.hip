@@ -1,0 +1,215 @@
+// Parameter quantization on the GPU: the k-means that produces the
+// sub-codebooks and codes the forward uses (Sec. 3.1, Eq. (4): per subspace,
+// minimise || D^(m) B^(m) - W^(m) ||_F^2 by k-means over the sub-vectors;
+// Sec. 3.2, Eq. (6): a conv layer shares D^(m) over every kernel position,
+// so the k-means of subspace m runs over the sub-vectors of all (c_t, p_k)).
+//
+// Weights W [C_t][C_s][d_k][d_k] (FC: d_k = 1); the sub-vector i = c_t P + p
+// (P = d_k^2 kernel positions) of subspace m is W[c_t][m C'_s + j][p],
+// j < C'_s.  Codes [C_t][d_k][d_k][M] = [n][M], codebooks [M][K][C'_s].
+//
+// * Assignment (pq_assign_kernel): one thread per sub-vector, the subspace's
+//   codebook in LDS (every thread reads the same sub-codeword at a time, a
+//   broadcast).  The distance is accumulated in fp32 as
+//   d = fma(w_j - c_j, w_j - c_j, d) over j in order and the first minimum
+//   wins, so the decision is reproducible bit for bit.  The minimum
+//   distances are summed in float64 in a fixed tree order per block, then
+//   per subspace (pq_objective_kernel).
+// * Update (pq_update_kernel): one workgroup per subspace and one thread per
+//   sub-codeword.  Chunks of the subspace's sub-vectors and their codes are
+//   staged in LDS with coalesced loads; thread k then walks the chunk in
+//   sub-vector order and adds the sub-vectors coded k in float64, so each
+//   mean is summed in a fixed order and rounded once to fp32.  A
+//   sub-codeword that no sub-vector chose keeps its value.
+#include "qcnn_internal.h"
+
+namespace qcnn {
+namespace {
+
+constexpr int kQThreads = 256;
+constexpr int kMaxCsp = 16;
+constexpr int kChunkFloats = 8192;  // LDS floats of staged sub-vectors per update chunk
+
+struct QShape {
+  int Ct, Cs, P, M, K, Csp;
+  int n;  // sub-vectors per subspace, C_t P
+};
+
+__device__ __forceinline__ double block_sum_fixed(double v, double* red) {
+  // Tree over the wave (fixed shuffle order), then the waves in order.
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+  if (threadIdx.x == 0)
+    for (int w = 0; w < (int)(blockDim.x / kWave); ++w) s += red[w];
+  return s;
+}
+
+__global__ __launch_bounds__(kQThreads) void pq_assign_kernel(const float* __restrict__ W,
+                                                              const float* __restrict__ D, QShape q,
+                                                              uint8_t* __restrict__ codes,
+                                                              double* __restrict__ part) {
+  extern __shared__ float cb[];  // K x C'_s sub-codewords of subspace m
+  __shared__ double red[kQThreads / kWave];
+  const int m = blockIdx.y;
+  const float* Dm = D + (size_t)m * q.K * q.Csp;
+  for (int i = threadIdx.x; i < q.K * q.Csp; i += kQThreads) cb[i] = Dm[i];
+  __syncthreads();
+  const int i = blockIdx.x * kQThreads + threadIdx.x;
+  double mine = 0.0;
+  if (i < q.n) {
+    const int t = i / q.P, p = i - t * q.P;
+    const float* src = W + ((size_t)t * q.Cs + (size_t)m * q.Csp) * q.P + p;
+    float w[kMaxCsp];
+#pragma unroll
+    for (int j = 0; j < kMaxCsp; ++j) w[j] = j < q.Csp ? src[(size_t)j * q.P] : 0.f;
+    int best = 0;
+    float bd = 0.f;
+    for (int k = 0; k < q.K; ++k) {
+      const float* c = cb + k * q.Csp;
+      float d = 0.f;
+#pragma unroll
+      for (int j = 0; j < kMaxCsp; ++j) {
+        if (j < q.Csp) {
+          const float diff = w[j] - c[j];
+          d = fmaf(diff, diff, d);
+        }
+      }
+      if (k == 0 || d < bd) {
+        bd = d;
+        best = k;
+      }
+    }
+    codes[(size_t)i * q.M + m] = (uint8_t)best;
+    mine = (double)bd;
+  }
+  const double s = block_sum_fixed(mine, red);
+  if (threadIdx.x == 0) part[(size_t)m * gridDim.x + blockIdx.x] = s;
+}
+
+// obj_m[m] = sum over the assignment blocks of subspace m (in block order);
+// total = the sum over m (per-thread runs in m order, then a fixed tree).
+__global__ __launch_bounds__(kQThreads) void pq_objective_kernel(const double* __restrict__ part, int nblk, int M,
+                                                                 double* __restrict__ obj_m,
+                                                                 double* __restrict__ total) {
+  __shared__ double red[kQThreads / kWave];
+  double mine = 0.0;
+  for (int m = threadIdx.x; m < M; m += kQThreads) {
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += part[(size_t)m * nblk + b];
+    if (obj_m) obj_m[m] = s;
+    mine += s;
+  }
+  const double s = block_sum_fixed(mine, red);
+  if (threadIdx.x == 0 && total) *total = s;
+}
+
+__global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __restrict__ W,
+                                                              const uint8_t* __restrict__ codes, QShape q,
+                                                              float* __restrict__ D, int* __restrict__ counts) {
+  __shared__ float sv[kChunkFloats];            // staged sub-vectors, [i][C'_s]
+  __shared__ uint8_t sc[kChunkFloats];          // their codes (chunk <= kChunkFloats sub-vectors)
+  const int m = blockIdx.x;
+  const int k = threadIdx.x;
+  const int chunk = kChunkFloats / q.Csp;
+  double sum[kMaxCsp];
+#pragma unroll
+  for (int j = 0; j < kMaxCsp; ++j) sum[j] = 0.0;
+  int cnt = 0;
+  for (int base = 0; base < q.n; base += chunk) {
+    const int len = min(chunk, q.n - base);
+    __syncthreads();  // the previous chunk has been walked
+    for (int e = threadIdx.x; e < len * q.Csp; e += kQThreads) {
+      // Element (i, j), j slowest, so that consecutive threads read
+      // consecutive kernel positions of one input channel.
+      const int j = e / len, il = e - j * len;
+      const int i = base + il;
+      const int t = i / q.P, p = i - t * q.P;
+      sv[il * q.Csp + j] = W[((size_t)t * q.Cs + (size_t)m * q.Csp + j) * q.P + p];
+    }
+    for (int il = threadIdx.x; il < len; il += kQThreads) sc[il] = codes[(size_t)(base + il) * q.M + m];
+    __syncthreads();
+    if (k < q.K) {
+      for (int il = 0; il < len; ++il) {
+        if (sc[il] == k) {
+          ++cnt;
+#pragma unroll
+          for (int j = 0; j < kMaxCsp; ++j)
+            if (j < q.Csp) sum[j] += (double)sv[il * q.Csp + j];
+        }
+      }
+    }
+  }
+  if (k < q.K) {
+    float* dst = D + ((size_t)m * q.K + k) * q.Csp;
+    if (cnt) {
+#pragma unroll
+      for (int j = 0; j < kMaxCsp; ++j)
+        if (j < q.Csp) dst[j] = (float)(sum[j] / (double)cnt);
+    }
+    if (counts) counts[(size_t)m * q.K + k] = cnt;
+  }
+}
+
+QShape make_shape(int Ct, int Cs, int dk, int M, int K, int Csp) {
+  return QShape{Ct, Cs, dk * dk, M, K, Csp, Ct * dk * dk};
+}
+
+// Assignment plus the objective reduction; obj_m and/or total may be null.
+hipError_t assign(const QShape& q, const float* W, const float* D, uint8_t* codes, double* part, double* obj_m,
+                  double* total, hipStream_t stream) {
+  const int nblk = ceil_div(q.n, kQThreads);
+  hipLaunchKernelGGL(pq_assign_kernel, dim3((unsigned)nblk, (unsigned)q.M), dim3(kQThreads),
+                     (size_t)q.K * q.Csp * sizeof(float), stream, W, D, q, codes, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || (!obj_m && !total)) return e;
+  hipLaunchKernelGGL(pq_objective_kernel, dim3(1), dim3(kQThreads), 0, stream, part, nblk, q.M, obj_m, total);
+  return hipGetLastError();
+}
+
+hipError_t update(const QShape& q, const float* W, const uint8_t* codes, float* D, int* counts,
+                  hipStream_t stream) {
+  hipLaunchKernelGGL(pq_update_kernel, dim3((unsigned)q.M), dim3(kQThreads), 0, stream, W, codes, q, D, counts);
+  return hipGetLastError();
+}
+
+size_t part_bytes(const QShape& q) { return (size_t)q.M * ceil_div(q.n, kQThreads) * sizeof(double); }
+
+}  // namespace
+
+hipError_t launch_pq_assign(int Ct, int Cs, int dk, const float* W, const float* D, int M, int K, int Csp,
+                            uint8_t* codes, double* objective, hipStream_t stream) {
+  const QShape q = make_shape(Ct, Cs, dk, M, K, Csp);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, part_bytes(q));
+  if (e != hipSuccess) return e;
+  KernelTimer timer(stream);
+  return assign(q, W, D, codes, reinterpret_cast<double*>(scratch.get()), objective, nullptr, stream);
+}
+
+hipError_t launch_pq_update(int Ct, int Cs, int dk, const float* W, const uint8_t* codes, int M, int K, int Csp,
+                            float* D, int* counts, hipStream_t stream) {
+  const QShape q = make_shape(Ct, Cs, dk, M, K, Csp);
+  KernelTimer timer(stream);
+  return update(q, W, codes, D, counts, stream);
+}
+
+hipError_t launch_pq_kmeans(int Ct, int Cs, int dk, const float* W, int M, int K, int Csp, int iters, float* D,
+                            uint8_t* codes, double* objective, hipStream_t stream) {
+  const QShape q = make_shape(Ct, Cs, dk, M, K, Csp);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, part_bytes(q));
+  if (e != hipSuccess) return e;
+  double* part = reinterpret_cast<double*>(scratch.get());
+  KernelTimer timer(stream);
+  for (int it = 0; it <= iters && e == hipSuccess; ++it) {
+    e = assign(q, W, D, codes, part, nullptr, objective ? objective + it : nullptr, stream);
+    if (e == hipSuccess && it < iters) e = update(q, W, codes, D, nullptr, stream);
+  }
+  return e;
+}
+
+}  // namespace qcnn

@@ -146,3 +146,21 @@ def test_timing_calls_without_gpu(L):
     assert L.qcnn_timing_enable(0) == 0
     assert L.qcnn_timing_read(ctypes.byref(ms), ctypes.byref(n)) == 0
     assert ms.value == 0.0 and n.value == 0
+
+
+def test_quantizer_rejects(L):
+    # W [4][8][3][3] at FAKE, codebooks [2][16][4] at FAKE2, codes elsewhere.
+    C = 0x2000000
+    assert L.qcnn_pq_assign(None, 4, 8, 3, FAKE2, 2, 16, 4, C, None, None) == NULL
+    assert L.qcnn_pq_assign(FAKE, 4, 8, 3, None, 2, 16, 4, C, None, None) == NULL
+    assert L.qcnn_pq_assign(FAKE, 0, 8, 3, FAKE2, 2, 16, 4, C, None, None) == SHAPE
+    assert L.qcnn_pq_assign(FAKE, 4, 8, 0, FAKE2, 2, 16, 4, C, None, None) == SHAPE
+    assert L.qcnn_pq_assign(FAKE, 4, 8, 3, FAKE2, 3, 16, 4, C, None, None) == SHAPE
+    assert L.qcnn_pq_assign(FAKE, 4, 8, 3, FAKE2, 2, 257, 4, C, None, None) == KR
+    assert L.qcnn_pq_assign(FAKE, 4, 34, 3, FAKE2, 2, 16, 17, C, None, None) == UNSUP
+    assert L.qcnn_pq_assign(FAKE, 4, 8, 3, FAKE2, 2, 16, 4, FAKE + 8, None, None) == ALIAS
+    assert L.qcnn_pq_update(FAKE, 4, 8, 3, C, 2, 16, 4, None, None, None) == NULL
+    assert L.qcnn_pq_update(FAKE, 4, 8, 3, C, 2, 0, 4, FAKE2, None, None) == KR
+    assert L.qcnn_pq_update(FAKE, 4, 8, 3, C, 2, 16, 4, FAKE + 4, None, None) == ALIAS
+    assert L.qcnn_pq_kmeans(FAKE, 4, 8, 3, 2, 16, 4, -1, FAKE2, C, None, None) == SHAPE
+    assert L.qcnn_pq_kmeans(FAKE, 4, 8, 3, 2, 16, 4, 3, FAKE2, C, FAKE2 + 8, None) == ALIAS
