@@ -156,6 +156,30 @@ def main():
         print(json.dumps({"only": "copy", "bytes_read": nbytes, "bytes_written": nbytes, "ms_per_step": ms,
                           "GB_s": 2 * nbytes / ms / 1e6}))
         return
+    def make_quant_step(name):
+        """One k-means iteration (assignment then update) of the parameter
+        quantizer on a dense synthetic layer of the named AlexNet shape."""
+        Ct, Cs, dk, Csp, K = workloads.QUANT_LAYERS[name]
+        W, D0 = workloads.random_quant(np.random.Generator(np.random.PCG64(7)), Ct, Cs, dk, Csp, K)
+        Wd, D = T(W), T(D0)
+        M = Cs // Csp
+        codes = torch.empty((Ct, M) if dk == 1 else (Ct, dk, dk, M), dtype=torch.uint8, device=dev)
+        obj = torch.empty(M, dtype=torch.float64, device=dev)
+        cnt = torch.empty((M, K), dtype=torch.int32, device=dev)
+
+        def step():
+            api.pq_assign(Wd, D, codes=codes, objective=obj)
+            api.pq_update(Wd, codes, D, counts=cnt)
+        # HBM bytes an iteration must move: W read by both steps, the codes
+        # written then read, the codebooks read and written.
+        nbytes = 2 * W.nbytes + 2 * codes.numel() + 2 * D0.nbytes
+        return step, nbytes, (Ct, Cs, dk, Csp, K)
+
+    if args.only and args.only.startswith("quant_"):
+        step, nbytes, _ = make_quant_step(args.only[len("quant_"):])
+        ms, _ = time_steps(step, args.steps, args.warmup)
+        print(json.dumps({"only": args.only, "ms_per_step": ms, "hbm_bytes_per_step": nbytes}))
+        return
     if args.only:
         step, wl, _ = make_step(args.only)
         ms, _ = time_steps(step, args.steps, args.warmup)
@@ -221,6 +245,17 @@ def main():
                     "main_kernels_ms_per_step": km * kn / steps, "main_kernel_launches_per_step": kn // steps}
         del st
     line["per_config"] = per
+
+    # ---------------------------------------------- parameter quantizer (k-means)
+    quant = {}
+    for name in ([] if args.configs == "none" else list(workloads.QUANT_LAYERS)):
+        st, nbytes, shape = make_quant_step(name)
+        m, _ = time_steps(st, 20, 3)
+        quant[name] = {"layer": "C_t=%d C_s=%d d_k=%d C's=%d K=%d" % shape, "ms_per_iteration": m,
+                       "hbm_bytes_per_iteration": nbytes,
+                       "hbm_frac": nbytes / (m * 1e-3) / workmodel.HBM_PEAK_BPS}
+        del st
+    line["quantizer"] = quant
 
     # ------------------------------------------------------------ CPU baseline
     if not args.no_cpu:

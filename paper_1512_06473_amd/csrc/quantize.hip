@@ -17,10 +17,10 @@
 //   per subspace (pq_objective_kernel).
 // * Update (pq_update_kernel): one workgroup per subspace and one thread per
 //   sub-codeword.  Chunks of the subspace's sub-vectors and their codes are
-//   staged in LDS with coalesced loads; thread k then walks the chunk in
-//   sub-vector order and adds the sub-vectors coded k in float64, so each
-//   mean is summed in a fixed order and rounded once to fp32.  A
-//   sub-codeword that no sub-vector chose keeps its value.
+//   staged in LDS with coalesced loads and sorted stably by code; thread k
+//   adds the sub-vectors coded k in float64 in sub-vector order, so each mean
+//   is summed in a fixed order and rounded once to fp32.  A sub-codeword that
+//   no sub-vector chose keeps its value.
 #include "qcnn_internal.h"
 
 namespace qcnn {
@@ -28,7 +28,7 @@ namespace {
 
 constexpr int kQThreads = 256;
 constexpr int kMaxCsp = 16;
-constexpr int kChunkFloats = 8192;  // LDS floats of staged sub-vectors per update chunk
+constexpr int kChunkFloats = 4096;  // LDS floats of staged sub-vectors per update chunk
 
 struct QShape {
   int Ct, Cs, P, M, K, Csp;
@@ -90,67 +90,143 @@ __global__ __launch_bounds__(kQThreads) void pq_assign_kernel(const float* __res
   if (threadIdx.x == 0) part[(size_t)m * gridDim.x + blockIdx.x] = s;
 }
 
-// obj_m[m] = sum over the assignment blocks of subspace m (in block order);
-// total = the sum over m (per-thread runs in m order, then a fixed tree).
+// obj_m[m] = sum over the assignment blocks of subspace m, in block order.
 __global__ __launch_bounds__(kQThreads) void pq_objective_kernel(const double* __restrict__ part, int nblk, int M,
-                                                                 double* __restrict__ obj_m,
-                                                                 double* __restrict__ total) {
-  __shared__ double red[kQThreads / kWave];
-  double mine = 0.0;
-  for (int m = threadIdx.x; m < M; m += kQThreads) {
-    double s = 0.0;
-    for (int b = 0; b < nblk; ++b) s += part[(size_t)m * nblk + b];
-    if (obj_m) obj_m[m] = s;
-    mine += s;
-  }
-  const double s = block_sum_fixed(mine, red);
-  if (threadIdx.x == 0 && total) *total = s;
+                                                                 double* __restrict__ obj_m) {
+  const int m = blockIdx.x * kQThreads + threadIdx.x;
+  if (m >= M) return;
+  double s = 0.0;
+  for (int b = 0; b < nblk; ++b) s += part[(size_t)m * nblk + b];
+  obj_m[m] = s;
 }
 
+// total = the sum over m of obj_m (per-thread runs in m order, then a fixed tree).
+__global__ __launch_bounds__(kQThreads) void pq_total_kernel(const double* __restrict__ obj_m, int M,
+                                                             double* __restrict__ total) {
+  __shared__ double red[kQThreads / kWave];
+  double mine = 0.0;
+  for (int m = threadIdx.x; m < M; m += kQThreads) mine += obj_m[m];
+  const double s = block_sum_fixed(mine, red);
+  if (threadIdx.x == 0) *total = s;
+}
+
+// Update of one subspace per workgroup.  Sub-vectors are taken in chunks:
+// the chunk's sub-vectors and codes are staged in LDS, a stable counting sort
+// by code lists every sub-codeword's members in sub-vector order, and thread
+// k then adds its members in that order (float64), continuing its sums from
+// the previous chunk.  The stable order comes from wave ballots: the lanes
+// holding the same code are found bit by bit, a lane's rank is the number of
+// such lanes below it, earlier waves of the same round and earlier rounds
+// add their counts.
 __global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __restrict__ W,
                                                               const uint8_t* __restrict__ codes, QShape q,
                                                               float* __restrict__ D, int* __restrict__ counts) {
-  __shared__ float sv[kChunkFloats];            // staged sub-vectors, [i][C'_s]
-  __shared__ uint8_t sc[kChunkFloats];          // their codes (chunk <= kChunkFloats sub-vectors)
+  __shared__ float sv[kChunkFloats];        // staged sub-vectors, [il][C'_s]
+  __shared__ uint8_t sc[kChunkFloats];      // their codes
+  __shared__ uint16_t perm[kChunkFloats];   // chunk positions sorted by code, stable
+  __shared__ int cnt[256], start[256], run[256];
+  __shared__ int wcnt[kQThreads / kWave][256];
   const int m = blockIdx.x;
-  const int k = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int chunk = kChunkFloats / q.Csp;
   double sum[kMaxCsp];
 #pragma unroll
   for (int j = 0; j < kMaxCsp; ++j) sum[j] = 0.0;
-  int cnt = 0;
+  int total = 0;  // members of sub-codeword tid over all chunks (tid < K)
   for (int base = 0; base < q.n; base += chunk) {
     const int len = min(chunk, q.n - base);
-    __syncthreads();  // the previous chunk has been walked
-    for (int e = threadIdx.x; e < len * q.Csp; e += kQThreads) {
-      // Element (i, j), j slowest, so that consecutive threads read
-      // consecutive kernel positions of one input channel.
-      const int j = e / len, il = e - j * len;
+    __syncthreads();  // the previous chunk is done
+    for (int e = tid; e < len * q.Csp; e += kQThreads) {
+      // Element (il, j).  Conv: j slowest, so that consecutive threads read
+      // consecutive kernel positions of one input channel; FC (one position):
+      // j fastest, so that they read the contiguous C'_s floats of a row.
+      int j, il;
+      if (q.P == 1) {
+        il = e / q.Csp;
+        j = e - il * q.Csp;
+      } else {
+        j = e / len;
+        il = e - j * len;
+      }
       const int i = base + il;
       const int t = i / q.P, p = i - t * q.P;
       sv[il * q.Csp + j] = W[((size_t)t * q.Cs + (size_t)m * q.Csp + j) * q.P + p];
     }
-    for (int il = threadIdx.x; il < len; il += kQThreads) sc[il] = codes[(size_t)(base + il) * q.M + m];
+    for (int il = tid; il < len; il += kQThreads) sc[il] = codes[(size_t)(base + il) * q.M + m];
+    for (int k = tid; k < 256; k += kQThreads) {
+      cnt[k] = 0;
+      run[k] = 0;
+    }
+    for (int k = tid; k < (kQThreads / kWave) * 256; k += kQThreads) (&wcnt[0][0])[k] = 0;
     __syncthreads();
-    if (k < q.K) {
-      for (int il = 0; il < len; ++il) {
-        if (sc[il] == k) {
-          ++cnt;
+    for (int il = tid; il < len; il += kQThreads) atomicAdd(&cnt[sc[il]], 1);  // counts: order-free
+    __syncthreads();
+    {  // exclusive scan of the 256 counts: within each wave, then across waves
+      static_assert(kQThreads == 256, "one count per thread");
+      const int own = cnt[tid];
+      int incl = own;
 #pragma unroll
-          for (int j = 0; j < kMaxCsp; ++j)
-            if (j < q.Csp) sum[j] += (double)sv[il * q.Csp + j];
-        }
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += o;
       }
+      if (lane == kWave - 1) wcnt[wave][0] = incl;  // wave totals (wcnt is zero again below)
+      __syncthreads();
+      int before = 0;
+      for (int w = 0; w < wave; ++w) before += wcnt[w][0];
+      start[tid] = before + incl - own;
+      __syncthreads();
+      if (lane == kWave - 1) wcnt[wave][0] = 0;
+      __syncthreads();
+    }
+    for (int r0 = 0; r0 < len; r0 += kQThreads) {
+      const int il = r0 + tid;
+      const bool valid = il < len;
+      const uint32_t c = valid ? sc[il] : 0u;
+      uint64_t same = __ballot(valid);
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const uint64_t ones = __ballot(valid && ((c >> b) & 1u));
+        same &= ((c >> b) & 1u) ? ones : ~ones;
+      }
+      const int below = __popcll(same & ((1ull << lane) - 1ull));
+      if (valid && below == 0) wcnt[wave][c] = __popcll(same);  // the group's lowest lane
+      __syncthreads();
+      if (valid) {
+        int off = start[c] + run[c] + below;
+        for (int w = 0; w < wave; ++w) off += wcnt[w][c];
+        perm[off] = (uint16_t)il;
+      }
+      __syncthreads();
+      for (int k = tid; k < 256; k += kQThreads) {
+        int add = 0;
+        for (int w = 0; w < kQThreads / kWave; ++w) {
+          add += wcnt[w][k];
+          wcnt[w][k] = 0;
+        }
+        run[k] += add;
+      }
+      __syncthreads();
+    }
+    if (tid < q.K) {
+      const int s0 = start[tid], n_k = cnt[tid];
+      for (int r = 0; r < n_k; ++r) {
+        const float* v = sv + perm[s0 + r] * q.Csp;
+#pragma unroll
+        for (int j = 0; j < kMaxCsp; ++j)
+          if (j < q.Csp) sum[j] += (double)v[j];
+      }
+      total += n_k;
     }
   }
-  if (k < q.K) {
-    float* dst = D + ((size_t)m * q.K + k) * q.Csp;
-    if (cnt) {
+  if (tid < q.K) {
+    float* dst = D + ((size_t)m * q.K + tid) * q.Csp;
+    if (total) {
 #pragma unroll
       for (int j = 0; j < kMaxCsp; ++j)
-        if (j < q.Csp) dst[j] = (float)(sum[j] / (double)cnt);
+        if (j < q.Csp) dst[j] = (float)(sum[j] / (double)total);
     }
-    if (counts) counts[(size_t)m * q.K + k] = cnt;
+    if (counts) counts[(size_t)m * q.K + tid] = total;
   }
 }
 
@@ -158,15 +234,21 @@ QShape make_shape(int Ct, int Cs, int dk, int M, int K, int Csp) {
   return QShape{Ct, Cs, dk * dk, M, K, Csp, Ct * dk * dk};
 }
 
-// Assignment plus the objective reduction; obj_m and/or total may be null.
+// Assignment plus the objective reduction: obj_m ([M], may be null) and
+// total (may be null); obj_tmp is room for M doubles when obj_m is null.
 hipError_t assign(const QShape& q, const float* W, const float* D, uint8_t* codes, double* part, double* obj_m,
-                  double* total, hipStream_t stream) {
+                  double* obj_tmp, double* total, hipStream_t stream) {
   const int nblk = ceil_div(q.n, kQThreads);
   hipLaunchKernelGGL(pq_assign_kernel, dim3((unsigned)nblk, (unsigned)q.M), dim3(kQThreads),
                      (size_t)q.K * q.Csp * sizeof(float), stream, W, D, q, codes, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || (!obj_m && !total)) return e;
-  hipLaunchKernelGGL(pq_objective_kernel, dim3(1), dim3(kQThreads), 0, stream, part, nblk, q.M, obj_m, total);
+  double* om = obj_m ? obj_m : obj_tmp;
+  hipLaunchKernelGGL(pq_objective_kernel, dim3((unsigned)ceil_div(q.M, kQThreads)), dim3(kQThreads), 0, stream,
+                     part, nblk, q.M, om);
+  e = hipGetLastError();
+  if (e != hipSuccess || !total) return e;
+  hipLaunchKernelGGL(pq_total_kernel, dim3(1), dim3(kQThreads), 0, stream, om, q.M, total);
   return hipGetLastError();
 }
 
@@ -176,7 +258,8 @@ hipError_t update(const QShape& q, const float* W, const uint8_t* codes, float* 
   return hipGetLastError();
 }
 
-size_t part_bytes(const QShape& q) { return (size_t)q.M * ceil_div(q.n, kQThreads) * sizeof(double); }
+// Workspace: the per-block objective partials, then M doubles.
+size_t part_bytes(const QShape& q) { return ((size_t)q.M * ceil_div(q.n, kQThreads) + q.M) * sizeof(double); }
 
 }  // namespace
 
@@ -187,7 +270,8 @@ hipError_t launch_pq_assign(int Ct, int Cs, int dk, const float* W, const float*
   hipError_t e = scratch.acquire(stream, part_bytes(q));
   if (e != hipSuccess) return e;
   KernelTimer timer(stream);
-  return assign(q, W, D, codes, reinterpret_cast<double*>(scratch.get()), objective, nullptr, stream);
+  double* part = reinterpret_cast<double*>(scratch.get());
+  return assign(q, W, D, codes, part, objective, nullptr, nullptr, stream);
 }
 
 hipError_t launch_pq_update(int Ct, int Cs, int dk, const float* W, const uint8_t* codes, int M, int K, int Csp,
@@ -206,7 +290,8 @@ hipError_t launch_pq_kmeans(int Ct, int Cs, int dk, const float* W, int M, int K
   double* part = reinterpret_cast<double*>(scratch.get());
   KernelTimer timer(stream);
   for (int it = 0; it <= iters && e == hipSuccess; ++it) {
-    e = assign(q, W, D, codes, part, nullptr, objective ? objective + it : nullptr, stream);
+    e = assign(q, W, D, codes, part, nullptr, part + (size_t)q.M * ceil_div(q.n, kQThreads),
+               objective ? objective + it : nullptr, stream);
     if (e == hipSuccess && it < iters) e = update(q, W, codes, D, nullptr, stream);
   }
   return e;
