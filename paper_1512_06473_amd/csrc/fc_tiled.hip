@@ -264,32 +264,45 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(const uint8_t* __restrict
   const int gq0 = blockIdx.x * 64, tt0 = blockIdx.y * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4
   const uint32_t kmax = (uint32_t)(K - 1);
-  for (int r = ty; r < 64; r += 4) {
-    const int t = tt0 + r, gq = gq0 + tx;
-    uint32_t word = 0;
-    if (t < Ct && gq < mgroups) {
-      const uint8_t* src = codes + (size_t)t * M + 4 * gq;
-      if ((M & 3) == 0) {  // 4-byte aligned: the caller's codes are, and so is every row
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(src);
+  // All 16 loads of a thread are issued before its first LDS store (one
+  // load latency per workgroup instead of 16).
+  uint32_t words[16];
+  const bool aligned = (M & 3) == 0;  // then every row starts 4-byte aligned (so does the caller's array)
+  const int gq = gq0 + tx;
+  if (aligned) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t c = (v >> (8 * k)) & 0xffu;
-          word |= (c < kmax ? c : kmax) << (8 * k);
-        }
-      } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (4 * gq + k < M) {
-            const uint32_t c = src[k];
-            word |= (c < kmax ? c : kmax) << (8 * k);
-          }
-        }
-      }
+    for (int rr = 0; rr < 16; ++rr) {
+      const int t = tt0 + ty + 4 * rr;
+      words[rr] = (t < Ct && gq < mgroups) ? *reinterpret_cast<const uint32_t*>(codes + (size_t)t * M + 4 * gq) : 0u;
     }
-    tile[r][tx] = word;
+  } else {
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int t = tt0 + ty + 4 * rr;
+      uint32_t word = 0;
+      if (t < Ct && gq < mgroups) {
+        const uint8_t* src = codes + (size_t)t * M + 4 * gq;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (4 * gq + k < M) word |= (uint32_t)src[k] << (8 * k);
+      }
+      words[rr] = word;
+    }
+  }
+#pragma unroll
+  for (int rr = 0; rr < 16; ++rr) {
+    uint32_t out = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t c = (words[rr] >> (8 * k)) & 0xffu;
+      out |= (c < kmax ? c : kmax) << (8 * k);
+    }
+    tile[ty + 4 * rr][tx] = out;
   }
   __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
+#pragma unroll
+  for (int rr = 0; rr < 16; ++rr) {
+    const int r = ty + 4 * rr;
     const int gq = gq0 + r, t = tt0 + tx;
     if (gq < mgroups && t < ct_pad) codes4[(size_t)gq * ct_pad + t] = tile[tx][r];
   }
