@@ -50,6 +50,9 @@ def _signatures():
         "qo_pq_update": [P, I, I, I, P, I, I, I, P, P, P],
         "qo_pq_kmeans": [P, I, I, I, I, I, I, I, P, P, P, P],
         "qo_threads": [],
+        "qo_code_bits": [I],
+        "qo_pack_codes": [P, ctypes.c_longlong, I, P],
+        "qo_unpack_codes": [P, ctypes.c_longlong, I, P],
     }
 
 
@@ -327,3 +330,37 @@ def pq_kmeans(W, D_init, iters):
     _chk(lib().qo_pq_kmeans(W.ctypes.data, Ct, Cs, dk, M, K, Csp, int(iters), D.ctypes.data,
                             codes.ctypes.data, o32.ctypes.data, o64.ctypes.data))
     return D, (codes.reshape(Ct, M) if fc else codes), o32, o64
+
+
+# ------------------------------------------------------------- packed codes
+# Table 1 (Sec. 3.4): log2 K bits per quantization index.  Stream format in
+# qcnn_oracle.c (reading R6b): code i is bits i b .. i b + b - 1, least
+# significant bit first, b = bits that hold 0 .. K-1.
+
+def code_bits(K: int) -> int:
+    b = lib().qo_code_bits(int(K))
+    _chk(min(b, 0))
+    return b
+
+
+def packed_nbytes(n: int, K: int) -> int:
+    """Bytes of the packed stream of n codes: ceil(n b / 8)."""
+    return (int(n) * code_bits(K) + 7) // 8
+
+
+def pack_codes(codes, K: int):
+    """uint8 codes (any shape, C order) -> the packed stream (uint8, ceil(n b / 8) bytes)."""
+    c, cp = _u8(np.asarray(codes).reshape(-1))
+    out = np.zeros(max(packed_nbytes(c.size, K), 1), np.uint8)
+    _chk(lib().qo_pack_codes(cp, c.size, int(K), out.ctypes.data))
+    return out[:packed_nbytes(c.size, K)]
+
+
+def unpack_codes(packed, n: int, K: int):
+    """The packed stream of n codes -> uint8 codes [n]."""
+    p = np.ascontiguousarray(np.asarray(packed, dtype=np.uint8))
+    if p.size == 0:
+        p = np.zeros(1, np.uint8)
+    out = np.empty(max(int(n), 1), np.uint8)
+    _chk(lib().qo_unpack_codes(p.ctypes.data, int(n), int(K), out.ctypes.data))
+    return out[:int(n)]

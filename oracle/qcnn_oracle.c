@@ -559,6 +559,56 @@ int qo_pq_kmeans(const float* W, int Ct, int Cs, int dk, int M, int K, int Csp, 
   return e;
 }
 
+/* ---------------------------------------------------------- packed codes
+ * Table 1 (Sec. 3.4) stores every quantization index in log2 K bits: the
+ * code bytes of a layer are (1/8) d_k^2 M C_t log2 K (conv) or
+ * (1/8) M C_t log2 K (FC).  The stream format is a reading (the paper fixes
+ * only the width):
+ *   R6b  b = the number of bits that hold 0 .. K-1 (b = 0 for K = 1, else the
+ *        smallest b with 2^b >= K, i.e. log2 K for a power of two); code i of
+ *        the array, in the array's own order, is bits i b .. i b + b - 1 of
+ *        the stream, value bit j at stream bit i b + j; stream bit q is bit
+ *        q % 8 of byte q / 8.  The stream is ceil(n b / 8) bytes.
+ * Both functions go bit by bit, straight from that definition.
+ */
+int qo_code_bits(int K) {
+  if (K < 1 || K > 256) return QO_EK;
+  int b = 0;
+  while ((1 << b) < K) ++b;
+  return b;
+}
+
+int qo_pack_codes(const uint8_t* codes, long long n, int K, uint8_t* out) {
+  const int b = qo_code_bits(K);
+  if (b < 0) return b;
+  if (n < 0 || (n > 0 && !codes) || (n * b > 0 && !out)) return QO_EARG;
+  int e = check_codes(codes, (size_t)n, K);
+  if (e) return e;
+  const long long nbytes = (n * b + 7) / 8;
+  for (long long q = 0; q < nbytes; ++q) out[q] = 0;
+  for (long long i = 0; i < n; ++i)
+    for (int j = 0; j < b; ++j) {
+      const long long q = i * b + j;  /* stream bit of value bit j of code i */
+      out[q / 8] |= (uint8_t)(((codes[i] >> j) & 1) << (q % 8));
+    }
+  return 0;
+}
+
+int qo_unpack_codes(const uint8_t* in, long long n, int K, uint8_t* codes) {
+  const int b = qo_code_bits(K);
+  if (b < 0) return b;
+  if (n < 0 || (n > 0 && !codes) || (n * b > 0 && !in)) return QO_EARG;
+  for (long long i = 0; i < n; ++i) {
+    int v = 0;
+    for (int j = 0; j < b; ++j) {
+      const long long q = i * b + j;
+      v |= ((in[q / 8] >> (q % 8)) & 1) << j;
+    }
+    codes[i] = (uint8_t)v;
+  }
+  return 0;
+}
+
 #ifdef _OPENMP
 #include <omp.h>
 int qo_threads(void) { return omp_get_max_threads(); }

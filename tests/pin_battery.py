@@ -3,8 +3,11 @@ process against a given build of the oracle (see test_oracle_mutants.py).
 
 Every reference here is independent of the oracle's code: hand-worked values,
 a numpy dense convolution / matrix product on kernels rebuilt from the codes
-(Eq. (4), (6)), and numpy einsum for the table (Sec. 3.1 test phase).
+(Eq. (4), (6)), numpy einsum for the table (Sec. 3.1 test phase), and for the
+packed indices (Table 1) Python integers and the compression ratios the paper
+prints for fc6 (Table 6).
 """
+import json
 import os
 import sys
 
@@ -134,6 +137,34 @@ def quant_checks(rng):
     return out
 
 
+def pack_checks(rng):
+    """Packed quantization indices (Table 1: log2 K bits each; reading R6b)."""
+    out = []
+    gold = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "packed_codes.json")))
+    for c in gold["cases"]:
+        got = O.pack_codes(np.array(c["codes"], np.uint8), c["K"])
+        out.append(("packed hand-worked K=%d" % c["K"], got.tolist() == c["bytes"]))
+        back = O.unpack_codes(np.array(c["bytes"], np.uint8), len(c["codes"]), c["K"])
+        out.append(("unpacked hand-worked K=%d" % c["K"], back.tolist() == c["codes"]))
+    for K in [1, 2, 3, 5, 16, 31, 32, 33, 64, 100, 127, 128, 129, 200, 255, 256]:
+        n = int(rng.integers(1, 300))
+        codes = rng.integers(0, K, n).astype(np.uint8)
+        b = max(K - 1, 0).bit_length()
+        # the stream as one integer, sum code_i 2^(i b), in little-endian bytes
+        ref = sum(int(v) << (i * b) for i, v in enumerate(codes)).to_bytes((n * b + 7) // 8, "little")
+        got = O.pack_codes(codes, K)
+        out.append(("packed big-int K=%d" % K, bytes(got.tobytes()) == ref))
+        out.append(("packed round trip K=%d" % K, np.array_equal(O.unpack_codes(got, n, K), codes)))
+    # the code bytes of Table 1 reproduce the paper's printed compression of
+    # CaffeNet fc6 (Table 6) when the index array is really packed
+    for csp, K, printed in [(2, 16, 15.06), (3, 16, 21.94), (3, 32, 16.70), (4, 32, 21.33)]:
+        M = 9216 // csp
+        nbytes = O.pack_codes(np.zeros(4096 * M, np.uint8), K).size
+        r = 4.0 * 9216 * 4096 / (4.0 * 9216 * K + nbytes)
+        out.append(("packed fc6 compression %d/%d" % (csp, K), abs(r - printed) <= 0.005))
+    return out
+
+
 def checks():
     out = []
     # hand-worked (see test_oracle.py for the arithmetic)
@@ -193,6 +224,7 @@ def checks():
                      for ch in range(2)]])
     out.append(("maxpool", np.array_equal(ym, ref)))
     out += quant_checks(rng)
+    out += pack_checks(rng)
     return out
 
 

@@ -6,6 +6,9 @@ method equals (torch/numpy in float64), Python integer arithmetic, or an
 invariant of the method (Sec. 2 Eq. (3); Sec. 3.1 Eq. (4)-(5); Sec. 3.2
 Eq. (6)-(7)).
 """
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -336,3 +339,39 @@ def test_quantizer_errors(oracle):
         oracle.pq_assign(W, np.zeros((3, 4, 2), np.float32))  # C_s != M C'_s
     with pytest.raises(oracle.OracleError):
         oracle.pq_update(W, np.full((4, 2), 9, np.uint8), np.zeros((2, 4, 4), np.float32))  # code >= K
+
+
+# ----------------------------------------------------------- packed codes
+# Table 1 (Sec. 3.4) stores each quantization index in log2 K bits.
+
+def test_packed_code_pins(oracle):
+    import pin_battery
+    bad = [name for name, ok in pin_battery.pack_checks(np.random.Generator(np.random.PCG64(5))) if not ok]
+    assert not bad, bad
+
+
+def test_packed_all_fc_compression_table7(oracle):
+    """CaffeNet fc6 + fc7 at the row's C'_s/K and fc8 at C'_s = 1, K = 16
+    (Sec. 5.2.2): the printed compression of Table 7, with the index bytes
+    taken from really packed index arrays."""
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_tables.json")))
+    g = gold["table7_caffenet_all_fc_compression"]
+    layers = [(9216, 4096), (4096, 4096), (4096, 1000)]
+    for csp, K, printed in g["rows"]:
+        dense = sum(4.0 * a * b for a, b in layers)
+        q = 0.0
+        for i, (cs, ct) in enumerate(layers):
+            c_, k_ = (1, 16) if i == 2 else (csp, K)
+            M = cs // c_
+            q += 4.0 * cs * k_ + oracle.pack_codes(np.zeros(ct * M, np.uint8), k_).size
+        assert abs(dense / q - printed) <= g["tol"], (csp, K, dense / q, printed)
+
+
+def test_packed_code_errors(oracle):
+    with pytest.raises(oracle.OracleError):
+        oracle.pack_codes(np.array([5], np.uint8), 5)      # a code >= K
+    with pytest.raises(oracle.OracleError):
+        oracle.pack_codes(np.array([0], np.uint8), 0)      # K < 1
+    with pytest.raises(oracle.OracleError):
+        oracle.pack_codes(np.array([0], np.uint8), 257)    # K > 256
+    assert oracle.packed_nbytes(0, 32) == 0 and oracle.pack_codes(np.zeros(0, np.uint8), 32).size == 0

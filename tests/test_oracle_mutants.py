@@ -55,6 +55,13 @@ MUTANTS = [
     ("qo_pq_update", ": D_in[o];", ": 0.0f;", "quantizer: unused sub-codeword zeroed"),
     ("qo_pq_kmeans", "for (int it = 0; it <= iters && !e; ++it) {", "for (int it = 0; it < iters && !e; ++it) {",
      "quantizer: no final assignment"),
+    ("qo_pack_codes", "<< (q % 8));", "<< (7 - q % 8));", "packed codes: most significant bit first in a byte"),
+    ("qo_pack_codes", "const long long q = i * b + j;", "const long long q = (n - 1 - i) * b + j;",
+     "packed codes: codes stored in reverse order"),
+    ("qo_code_bits", "while ((1 << b) < K) ++b;", "while ((2 << b) <= K) ++b;",
+     "packed codes: floor(log2 K) bits"),
+    ("qo_unpack_codes", "v |= ((in[q / 8] >> (q % 8)) & 1) << j;", "v |= ((in[q / 8] >> (q % 8)) & 1) << (b - 1 - j);",
+     "packed codes: value bits reversed on unpack"),
 ]
 
 
