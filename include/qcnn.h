@@ -60,6 +60,7 @@
 #ifndef QCNN_H
 #define QCNN_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -108,6 +109,45 @@ qcnn_status qcnn_fc_forward(const float* x, int N, int C_s,
                             const float* codebooks, int M, int K, int Csp,
                             const uint8_t* codes, int C_t,
                             const float* bias, int relu, float* y, void* stream);
+
+/* ---- Packed codes.  Table 1 (Sec. 3.4) stores every quantization index in
+ * log2 K bits: (1/8) d_k^2 M C_t log2 K bytes for a conv layer,
+ * (1/8) M C_t log2 K for a fully-connected one.  The packed form is a bit
+ * stream of b = qcnn_code_bits(K) bits per code (b = 0 for K = 1, else the
+ * smallest b with 2^b >= K, i.e. log2 K for a power of two): code i of the
+ * array, in the array's own order ([C_t][d_k][d_k][M] or [C_t][M]), is
+ * stream bits i b .. i b + b - 1 with value bit j at stream bit i b + j, and
+ * stream bit q is bit q % 8 of byte q / 8 (least significant bit first).
+ * A packed buffer is qcnn_packed_bytes(n, K) = 4 ceil(n b / 32) bytes: the
+ * ceil(n b / 8) bytes of the stream, then zero bits up to a whole dword.
+ * Buffers are device pointers, 4-byte aligned (else QCNN_ERR_UNSUPPORTED).
+ * The codes must be < K (the precondition of the forward); packing keeps the
+ * low b bits of each code.  With QCNN_CHECK_CODES=1 qcnn_pack_codes verifies
+ * its input first. */
+
+/* Bits per packed code for K sub-codewords, or -1 when K is outside [1, 256]. */
+int qcnn_code_bits(int K);
+
+/* Size in bytes of the packed form of n codes (0 when K is outside [1, 256]). */
+size_t qcnn_packed_bytes(size_t n, int K);
+
+/* codes: uint8 [n] -> packed (output): qcnn_packed_bytes(n, K) bytes. */
+qcnn_status qcnn_pack_codes(const uint8_t* codes, size_t n, int K, uint8_t* packed, void* stream);
+
+/* packed: qcnn_packed_bytes(n, K) bytes -> codes (output): uint8 [n]. */
+qcnn_status qcnn_unpack_codes(const uint8_t* packed, size_t n, int K, uint8_t* codes, void* stream);
+
+/* qcnn_conv_forward and qcnn_fc_forward with the codes in packed form
+ * (qcnn_packed_bytes of C_t d_k^2 M or C_t M codes).  Same arguments, limits
+ * and results: for the same codes the outputs are identical bit for bit. */
+qcnn_status qcnn_conv_forward_packed(const float* x, int N, int C_s, int H, int W,
+                                     const float* codebooks, int M, int K, int Csp,
+                                     const uint8_t* packed_codes, int C_t, int d_k, int stride, int pad,
+                                     const float* bias, int relu, float* y, void* stream);
+qcnn_status qcnn_fc_forward_packed(const float* x, int N, int C_s,
+                                   const float* codebooks, int M, int K, int Csp,
+                                   const uint8_t* packed_codes, int C_t,
+                                   const float* bias, int relu, float* y, void* stream);
 
 /* ---- Parameter quantization (the step that produces codebooks and codes).
  * Sec. 3.1, Eq. (4): for each subspace m, minimise || D^(m) B^(m) - W^(m) ||_F^2

@@ -25,6 +25,12 @@ SIGNATURES = {
     "qcnn_out_size": ([I, I, I, I], I),
     "qcnn_status_string": ([I], ctypes.c_char_p),
     "qcnn_version": ([], I),
+    "qcnn_conv_forward_packed": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
+    "qcnn_fc_forward_packed": ([P, I, I, P, I, I, I, P, I, P, I, P, P], I),
+    "qcnn_code_bits": ([I], I),
+    "qcnn_packed_bytes": ([ctypes.c_size_t, I], ctypes.c_size_t),
+    "qcnn_pack_codes": ([P, ctypes.c_size_t, I, P, P], I),
+    "qcnn_unpack_codes": ([P, ctypes.c_size_t, I, P, P], I),
     "qcnn_timing_enable": ([I], I),
     "qcnn_timing_read": ([ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong)], I),
 }

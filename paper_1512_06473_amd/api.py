@@ -126,6 +126,124 @@ def fc_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor,
     return out
 
 
+# ---------------------------------------------------------------- packed codes
+# Table 1 (Sec. 3.4): log2 K bits per quantization index.  Format and limits
+# are those of include/qcnn.h.
+
+def code_bits(K: int) -> int:
+    """Bits per packed code (qcnn_code_bits): 0 for K = 1, else ceil(log2 K)."""
+    b = lib().qcnn_code_bits(int(K))
+    if b < 0:
+        raise ValueError("K must be in [1, 256], got %d" % K)
+    return b
+
+
+def packed_bytes(n: int, K: int) -> int:
+    """Bytes of the packed form of n codes (qcnn_packed_bytes): 4 ceil(n b / 32)."""
+    code_bits(K)
+    return int(lib().qcnn_packed_bytes(int(n), int(K)))
+
+
+def pack_codes(codes: torch.Tensor, K: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """uint8 codes (any shape, contiguous) -> packed stream, uint8 [packed_bytes(numel, K)]."""
+    _need(codes, "codes", torch.uint8, codes.dim())
+    n = codes.numel()
+    nb = packed_bytes(n, K)
+    if out is None:
+        out = torch.empty(max(nb, 1), dtype=torch.uint8, device=codes.device)[:nb]
+    _need(out, "out", torch.uint8, 1, codes.device)
+    if out.numel() != nb:
+        raise ValueError("out must have %d bytes, got %d" % (nb, out.numel()))
+    check(lib().qcnn_pack_codes(codes.data_ptr(), n, int(K), out.data_ptr() if nb else None, _stream(codes)),
+          "qcnn_pack_codes")
+    return out
+
+
+def unpack_codes(packed: torch.Tensor, shape, K: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Packed stream -> uint8 codes of the given shape (qcnn_unpack_codes)."""
+    _need(packed, "packed", torch.uint8, 1)
+    shape = tuple(int(v) for v in shape)
+    n = 1
+    for v in shape:
+        n *= v
+    if packed.numel() != packed_bytes(n, K):
+        raise ValueError("packed must have %d bytes, got %d" % (packed_bytes(n, K), packed.numel()))
+    if out is None:
+        out = torch.empty(shape, dtype=torch.uint8, device=packed.device)
+    _need(out, "out", torch.uint8, len(shape), packed.device)
+    if tuple(out.shape) != shape:
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), shape))
+    check(lib().qcnn_unpack_codes(packed.data_ptr() if packed.numel() else None, n, int(K), out.data_ptr(),
+                                  _stream(packed)), "qcnn_unpack_codes")
+    return out
+
+
+def _packed_codes_arg(packed: torch.Tensor, n: int, K: int, device) -> int:
+    _need(packed, "packed_codes", torch.uint8, 1, device)
+    if packed.numel() != packed_bytes(n, K):
+        raise ValueError("packed_codes must have %d bytes, got %d" % (packed_bytes(n, K), packed.numel()))
+    if packed.numel() == 0:  # K = 1 stores nothing; the library still wants an aligned pointer
+        packed = torch.zeros(4, dtype=torch.uint8, device=device)
+    return packed.data_ptr(), packed
+
+
+def conv_forward_packed(x: torch.Tensor, codebooks: torch.Tensor, packed_codes: torch.Tensor, C_t: int, d_k: int,
+                        stride: int = 1, pad: int = 0, bias: Optional[torch.Tensor] = None, relu: bool = False,
+                        out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """conv_forward with packed codes (qcnn_conv_forward_packed): packed_codes is
+    the packed stream of codes [C_t][d_k][d_k][M]."""
+    _need(x, "x", torch.float32, 4)
+    _need(codebooks, "codebooks", torch.float32, 3, x.device)
+    N, Cs, H, W = x.shape
+    M, K, Csp = codebooks.shape
+    ptr, keep = _packed_codes_arg(packed_codes, C_t * d_k * d_k * M, K, x.device)
+    Ho, Wo = out_size(H, d_k, stride, pad), out_size(W, d_k, stride, pad)
+    bp = 0
+    if bias is not None:
+        _need(bias, "bias", torch.float32, 1, x.device)
+        if bias.shape[0] != C_t:
+            raise ValueError("bias must have C_t=%d entries" % C_t)
+        bp = bias.data_ptr()
+    if out is None:
+        out = torch.empty((N, C_t, max(Ho, 0), max(Wo, 0)), dtype=torch.float32, device=x.device)
+    _need(out, "out", torch.float32, 4, x.device)
+    if tuple(out.shape) != (N, C_t, Ho, Wo):
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, C_t, Ho, Wo)))
+    check(lib().qcnn_conv_forward_packed(x.data_ptr(), N, Cs, H, W, codebooks.data_ptr(), M, K, Csp, ptr, C_t, d_k,
+                                         stride, pad, bp or None, int(bool(relu)), out.data_ptr(), _stream(x)),
+          "qcnn_conv_forward_packed")
+    return out
+
+
+def fc_forward_packed(x: torch.Tensor, codebooks: torch.Tensor, packed_codes: torch.Tensor, C_t: int,
+                      bias: Optional[torch.Tensor] = None, relu: bool = False,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """fc_forward with packed codes (qcnn_fc_forward_packed): packed_codes is the
+    packed stream of codes [C_t][M]."""
+    if x.dim() != 2:
+        x = x.reshape(x.shape[0], -1)
+    _need(x, "x", torch.float32, 2)
+    _need(codebooks, "codebooks", torch.float32, 3, x.device)
+    N, Cs = x.shape
+    M, K, Csp = codebooks.shape
+    ptr, keep = _packed_codes_arg(packed_codes, C_t * M, K, x.device)
+    bp = 0
+    if bias is not None:
+        _need(bias, "bias", torch.float32, 1, x.device)
+        if bias.shape[0] != C_t:
+            raise ValueError("bias must have C_t=%d entries" % C_t)
+        bp = bias.data_ptr()
+    if out is None:
+        out = torch.empty((N, C_t), dtype=torch.float32, device=x.device)
+    _need(out, "out", torch.float32, 2, x.device)
+    if tuple(out.shape) != (N, C_t):
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, C_t)))
+    check(lib().qcnn_fc_forward_packed(x.data_ptr(), N, Cs, codebooks.data_ptr(), M, K, Csp, ptr, C_t,
+                                       bp or None, int(bool(relu)), out.data_ptr(), _stream(x)),
+          "qcnn_fc_forward_packed")
+    return out
+
+
 def maxpool2d(x: torch.Tensor, k: int = 3, s: int = 2, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """k x k / stride s max pooling, no padding (qcnn_maxpool2d): network glue."""
     _need(x, "x", torch.float32, 4)

@@ -399,7 +399,7 @@ struct CodeMap {
   int Ct, dk, stride, M, G, rows, cols, K, ct_pad, zrow, V;
 };
 
-__global__ __launch_bounds__(256) void flat_codes_kernel(const uint8_t* __restrict__ codes, CodeMap q,
+__global__ __launch_bounds__(256) void flat_codes_kernel(CodeStream codes, CodeMap q,
                                                          uint32_t* __restrict__ codes8) {
   const int taps = q.rows * q.cols;
   const int per_v = q.ct_pad * taps;
@@ -421,7 +421,7 @@ __global__ __launch_bounds__(256) void flat_codes_kernel(const uint8_t* __restri
         const int pa = rr % q.stride, m = rr / q.stride;
         const int ky = q.stride * (g * q.rows + tap / q.cols) + pa, kx = q.stride * (tap % q.cols) + pb;
         if (ky < q.dk && kx < q.dk) {
-          val = codes[(((size_t)t * q.dk + ky) * q.dk + kx) * q.M + m];
+          val = code_at(codes, (((size_t)t * q.dk + ky) * q.dk + kx) * q.M + m);
           val = val < (uint32_t)(q.K - 1) ? val : (uint32_t)(q.K - 1);
         } else {
           val = (uint32_t)q.zrow;
@@ -657,7 +657,7 @@ bool conv_flat_supported(const ConvShape& s) {
   return make_plan(s, &pl);
 }
 
-hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
+hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                             const float* bias, int relu, float* y, hipStream_t stream) {
   FlatPlan pl;
   if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;

@@ -36,9 +36,8 @@ struct ConvParams {
 
 template <int CSP, int G, int TW>
 __global__ __launch_bounds__(kThreads) void conv_pq_generic(const float* __restrict__ x, const float* __restrict__ D,
-                                                            const uint8_t* __restrict__ codes,
-                                                            const float* __restrict__ bias, float* __restrict__ y,
-                                                            ConvParams p) {
+                                                            CodeStream codes, const float* __restrict__ bias,
+                                                            float* __restrict__ y, ConvParams p) {
   extern __shared__ float lut[];  // [K][ih * iw]
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -172,7 +171,7 @@ bool choose_tiling(const ConvShape& s, Tiling* best) {
 struct ConvPtrs {
   const float* x;
   const float* D;
-  const uint8_t* codes;
+  CodeStream codes;
   const float* bias;
   float* y;
 };
@@ -204,7 +203,7 @@ bool conv_supported(const ConvShape& s) {
   return conv_flat_supported(s) || choose_tiling(s, &t);
 }
 
-hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
+hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                                const float* bias, int relu, float* y, hipStream_t stream) {
   if (conv_flat_supported(s)) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream);
   Tiling t;

@@ -35,9 +35,9 @@ struct FcParams {
 // partial: [splits][N][Ct], or null when the kernel writes y itself.
 template <int CSP>
 __global__ __launch_bounds__(kThreads) void fc_pq_kernel(const float* __restrict__ x, const float* __restrict__ D,
-                                                         const uint8_t* __restrict__ codes,
-                                                         const float* __restrict__ bias, float* __restrict__ y,
-                                                         float* __restrict__ partial, FcParams p) {
+                                                         CodeStream codes, const float* __restrict__ bias,
+                                                         float* __restrict__ y, float* __restrict__ partial,
+                                                         FcParams p) {
   extern __shared__ float lut[];  // [mchunk][K][64]
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256) void fc_reduce_kernel(const float* __restrict_
 }  // namespace
 
 hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
-                             const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream) {
+                             CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream) {
   if (fc_tiled_supported(N, Cs, M, K, Csp, Ct))
     return launch_fc_tiled(N, Cs, M, K, Csp, Ct, x, D, codes, bias, relu, y, stream);
   FcParams p;
@@ -155,7 +155,7 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
     partial = reinterpret_cast<float*>(scratch.get());
   }
   dim3 grid(tblocks, nblocks, splits);
-  void (*kern)(const float*, const float*, const uint8_t*, const float*, float*, float*, FcParams);
+  void (*kern)(const float*, const float*, CodeStream, const float*, float*, float*, FcParams);
   switch (Csp) {
     case 1: kern = fc_pq_kernel<1>; break;
     case 2: kern = fc_pq_kernel<2>; break;

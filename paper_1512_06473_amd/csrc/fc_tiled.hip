@@ -258,7 +258,7 @@ __global__ __launch_bounds__(kThreads, 1) void fc_tiled_kernel(const float* __re
 // A transpose of [C_t][M] bytes into [M / 4][ct_pad] dwords through LDS:
 // a 64 (t) x 64 (gq) tile per workgroup, read along the subspaces, written
 // along the channels.
-__global__ __launch_bounds__(256) void fc_codes_kernel(const uint8_t* __restrict__ codes, int Ct, int M, int K,
+__global__ __launch_bounds__(256) void fc_codes_kernel(CodeStream codes, int Ct, int M, int K,
                                                        int mgroups, int ct_pad, uint32_t* __restrict__ codes4) {
   __shared__ uint32_t tile[64][65];
   const int gq0 = blockIdx.x * 64, tt0 = blockIdx.y * 64;
@@ -267,13 +267,15 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(const uint8_t* __restrict
   // All 16 loads of a thread are issued before its first LDS store (one
   // load latency per workgroup instead of 16).
   uint32_t words[16];
-  const bool aligned = (M & 3) == 0;  // then every row starts 4-byte aligned (so does the caller's array)
+  // One byte per code and M % 4 == 0: every row starts 4-byte aligned (so
+  // does the caller's array) and a dword holds the 4 codes of a group.
+  const bool aligned = codes.bits == 8 && (M & 3) == 0;
   const int gq = gq0 + tx;
   if (aligned) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
       const int t = tt0 + ty + 4 * rr;
-      words[rr] = (t < Ct && gq < mgroups) ? *reinterpret_cast<const uint32_t*>(codes + (size_t)t * M + 4 * gq) : 0u;
+      words[rr] = (t < Ct && gq < mgroups) ? *reinterpret_cast<const uint32_t*>(codes.p + (size_t)t * M + 4 * gq) : 0u;
     }
   } else {
 #pragma unroll
@@ -281,10 +283,9 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(const uint8_t* __restrict
       const int t = tt0 + ty + 4 * rr;
       uint32_t word = 0;
       if (t < Ct && gq < mgroups) {
-        const uint8_t* src = codes + (size_t)t * M + 4 * gq;
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-          if (4 * gq + k < M) word |= (uint32_t)src[k] << (8 * k);
+          if (4 * gq + k < M) word |= code_at(codes, (size_t)t * M + 4 * gq + k) << (8 * k);
       }
       words[rr] = word;
     }
@@ -457,7 +458,7 @@ bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct) {
 }
 
 hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
-                           const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream) {
+                           CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream) {
   FcPlan pl;
   if (!make_fc_plan(N, Cs, M, K, Csp, Ct, &pl)) return hipErrorInvalidConfiguration;
   pl.p.relu = relu;

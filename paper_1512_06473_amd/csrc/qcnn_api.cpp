@@ -72,10 +72,16 @@ bool prepare_device() {
   return true;
 }
 
+// Bytes of the stream of n codes of `bits` bits each as the library writes
+// it (whole dwords), or of one byte per code when bits == 8.
+size_t code_stream_bytes(size_t n, int bits) {
+  return bits == 8 ? n : (n * (size_t)bits + 31) / 32 * 4;
+}
+
 // QCNN_CHECK_CODES=1: count codes >= K on the device and wait for the answer.
-qcnn_status check_codes(const uint8_t* codes, size_t n, int K, hipStream_t st) {
+qcnn_status check_codes(qcnn::CodeStream codes, size_t n, int K, hipStream_t st) {
   static const bool enabled = env_flag("QCNN_CHECK_CODES");
-  if (!enabled || K >= 256) return QCNN_OK;  // uint8 codes are always < 256
+  if (!enabled || (1 << codes.bits) <= K) return QCNN_OK;  // no stored value can reach K
   int* bad = nullptr;
   int host = 0;
   hipError_t e = hipMallocAsync((void**)&bad, sizeof(int), st);
@@ -202,9 +208,14 @@ qcnn_status qcnn_lut_build(const float* x, int N, int C_s, int H, int W, const f
   return hip_status(qcnn::launch_lut_build(x, N, C_s, H, W, codebooks, M, K, Csp, lut, (hipStream_t)stream));
 }
 
-qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
-                              int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
-                              const float* bias, int relu, float* y, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Body of qcnn_conv_forward (bits = 8) and qcnn_conv_forward_packed.
+qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
+                         int Csp, const uint8_t* codes, int bits, int C_t, int d_k, int stride, int pad,
+                         const float* bias, int relu, float* y, void* stream) {
   if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
   if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0) return QCNN_ERR_SHAPE;
   qcnn_status s = check_pq(N, C_s, M, K, Csp);
@@ -214,7 +225,8 @@ qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, cons
   const size_t nx = elems({N, C_s, H, W}), nd = elems({M, K, Csp}), nc = elems({C_t, d_k, d_k, M});
   const size_t ny = elems({N, C_t, Ho, Wo});
   if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
-  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, nc) ||
+  const size_t cb = code_stream_bytes(nc, bits);
+  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, cb) ||
       overlap(y, ny * 4, bias, (size_t)C_t * 4))
     return QCNN_ERR_ALIAS;
   if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
@@ -223,28 +235,101 @@ qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, cons
   if (qcnn::ceil_div(C_t, 32) > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
   hipStream_t st = (hipStream_t)stream;
   if (!prepare_device()) return QCNN_ERR_HIP;
-  s = check_codes(codes, nc, K, st);
+  const qcnn::CodeStream cs{codes, bits};
+  s = check_codes(cs, nc, K, st);
   if (s != QCNN_OK) return s;
-  return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, codes, bias, relu ? 1 : 0, y, st));
+  return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0, y, st));
 }
 
-qcnn_status qcnn_fc_forward(const float* x, int N, int C_s, const float* codebooks, int M, int K, int Csp,
-                            const uint8_t* codes, int C_t, const float* bias, int relu, float* y, void* stream) {
+// Body of qcnn_fc_forward (bits = 8) and qcnn_fc_forward_packed.
+qcnn_status fc_forward(const float* x, int N, int C_s, const float* codebooks, int M, int K, int Csp,
+                       const uint8_t* codes, int bits, int C_t, const float* bias, int relu, float* y, void* stream) {
   if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
   if (C_t < 1) return QCNN_ERR_SHAPE;
   qcnn_status s = check_pq(N, C_s, M, K, Csp);
   if (s != QCNN_OK) return s;
   const size_t nx = elems({N, C_s}), nd = elems({M, K, Csp}), nc = elems({C_t, M}), ny = elems({N, C_t});
   if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
-  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, nc) ||
+  const size_t cb = code_stream_bytes(nc, bits);
+  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, cb) ||
       overlap(y, ny * 4, bias, (size_t)C_t * 4))
     return QCNN_ERR_ALIAS;
   if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
   hipStream_t st = (hipStream_t)stream;
   if (!prepare_device()) return QCNN_ERR_HIP;
-  s = check_codes(codes, nc, K, st);
+  const qcnn::CodeStream cs{codes, bits};
+  s = check_codes(cs, nc, K, st);
   if (s != QCNN_OK) return s;
-  return hip_status(qcnn::launch_fc_forward(N, C_s, M, K, Csp, C_t, x, codebooks, codes, bias, relu ? 1 : 0, y, st));
+  return hip_status(qcnn::launch_fc_forward(N, C_s, M, K, Csp, C_t, x, codebooks, cs, bias, relu ? 1 : 0, y, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
+                              int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                              const float* bias, int relu, float* y, void* stream) {
+  return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, codes, 8, C_t, d_k, stride, pad, bias, relu, y, stream);
+}
+
+qcnn_status qcnn_conv_forward_packed(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M,
+                                     int K, int Csp, const uint8_t* packed_codes, int C_t, int d_k, int stride,
+                                     int pad, const float* bias, int relu, float* y, void* stream) {
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, packed_codes, qcnn::code_bits(K), C_t, d_k, stride,
+                      pad, bias, relu, y, stream);
+}
+
+qcnn_status qcnn_fc_forward(const float* x, int N, int C_s, const float* codebooks, int M, int K, int Csp,
+                            const uint8_t* codes, int C_t, const float* bias, int relu, float* y, void* stream) {
+  return fc_forward(x, N, C_s, codebooks, M, K, Csp, codes, 8, C_t, bias, relu, y, stream);
+}
+
+qcnn_status qcnn_fc_forward_packed(const float* x, int N, int C_s, const float* codebooks, int M, int K, int Csp,
+                                   const uint8_t* packed_codes, int C_t, const float* bias, int relu, float* y,
+                                   void* stream) {
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  return fc_forward(x, N, C_s, codebooks, M, K, Csp, packed_codes, qcnn::code_bits(K), C_t, bias, relu, y, stream);
+}
+
+int qcnn_code_bits(int K) {
+  if (K < 1 || K > 256) return -1;
+  return qcnn::code_bits(K);
+}
+
+size_t qcnn_packed_bytes(size_t n, int K) {
+  if (K < 1 || K > 256 || n > kMaxElems) return 0;
+  return (n * (size_t)qcnn::code_bits(K) + 31) / 32 * 4;
+}
+
+qcnn_status qcnn_pack_codes(const uint8_t* codes, size_t n, int K, uint8_t* packed, void* stream) {
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  if (n > kMaxElems) return QCNN_ERR_SHAPE;
+  const int bits = qcnn::code_bits(K);
+  const size_t pb = (n * (size_t)bits + 31) / 32 * 4;
+  if ((n > 0 && !codes) || (pb > 0 && !packed)) return QCNN_ERR_NULL;
+  if (pb == 0) return QCNN_OK;
+  if (((uintptr_t)packed & 3) || ((uintptr_t)codes & 3)) return QCNN_ERR_UNSUPPORTED;
+  if (overlap(packed, pb, codes, n)) return QCNN_ERR_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  qcnn_status s = check_codes(qcnn::CodeStream{codes, 8}, n, K, st);
+  if (s != QCNN_OK) return s;
+  return hip_status(qcnn::launch_pack_codes(codes, n, bits, reinterpret_cast<uint32_t*>(packed), st));
+}
+
+qcnn_status qcnn_unpack_codes(const uint8_t* packed, size_t n, int K, uint8_t* codes, void* stream) {
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  if (n > kMaxElems) return QCNN_ERR_SHAPE;
+  const int bits = qcnn::code_bits(K);
+  const size_t pb = (n * (size_t)bits + 31) / 32 * 4;
+  if ((n > 0 && !codes) || (pb > 0 && !packed)) return QCNN_ERR_NULL;
+  if (n == 0) return QCNN_OK;
+  if (pb > 0 && ((uintptr_t)packed & 3)) return QCNN_ERR_UNSUPPORTED;
+  if (overlap(codes, n, packed, pb)) return QCNN_ERR_ALIAS;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  return hip_status(qcnn::launch_unpack_codes(qcnn::CodeStream{packed, bits}, n, codes, (hipStream_t)stream));
 }
 
 // Shared validation of the quantizer entry points (host only).
@@ -289,7 +374,7 @@ qcnn_status qcnn_pq_update(const float* W, int C_t, int C_s, int d_k, const uint
     return QCNN_ERR_ALIAS;
   hipStream_t st = (hipStream_t)stream;
   if (!prepare_device()) return QCNN_ERR_HIP;
-  s = check_codes(codes, nc, K, st);
+  s = check_codes(qcnn::CodeStream{codes, 8}, nc, K, st);
   if (s != QCNN_OK) return s;
   return hip_status(qcnn::launch_pq_update(C_t, C_s, d_k, W, codes, M, K, Csp, codebooks, counts, st));
 }

@@ -16,13 +16,37 @@ constexpr int kWave = 64;  // CDNA wavefront width
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 inline size_t ceil_div_z(size_t a, size_t b) { return (a + b - 1) / b; }
 
-// Read byte `idx` of a code array whose base is 4-byte aligned (the C ABI
-// checks this).  The dword holding the byte is loaded instead of the byte, so
-// a wave-uniform index becomes one scalar load; an aligned dword never
-// straddles a page, so the bytes next to the last code cannot fault.
-__device__ __forceinline__ uint32_t code_at(const uint8_t* __restrict__ codes, size_t idx) {
-  const uint32_t word = reinterpret_cast<const uint32_t*>(codes)[idx >> 2];
-  return (word >> ((uint32_t)(idx & 3) * 8u)) & 0xffu;
+// The caller's codes as a stream of `bits` bits per code, base 4-byte
+// aligned (the C ABI checks it): bits = 8 is one byte per code
+// (qcnn_conv_forward, qcnn_fc_forward); otherwise the packed form of Table 1
+// (qcnn_pack_codes): code i is stream bits i bits .. i bits + bits - 1, value
+// bit j at stream bit i bits + j, stream bit q = bit q % 8 of byte q / 8;
+// bits = 0 when K = 1 (every code is 0 and nothing is stored).
+struct CodeStream {
+  const uint8_t* p;
+  int bits;
+};
+
+// Bits per packed code for K codewords: 0 for K = 1, else ceil(log2 K).
+inline int code_bits(int K) {
+  int b = 0;
+  while ((1 << b) < K) ++b;
+  return b;
+}
+
+// Code `idx` of a stream.  Whole aligned dwords are loaded, so a wave-uniform
+// index becomes scalar loads; an aligned dword never straddles a page, and a
+// dword that holds any bit of a code lies within the stream's last dword, so
+// the bytes past the last code cannot fault.
+__device__ __forceinline__ uint32_t code_at(const CodeStream& s, size_t idx) {
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(s.p);
+  if (s.bits == 8) return (w[idx >> 2] >> ((uint32_t)(idx & 3) * 8u)) & 0xffu;
+  if (s.bits == 0) return 0u;
+  const size_t bit = idx * (size_t)s.bits;
+  const uint32_t sh = (uint32_t)(bit & 31);
+  uint32_t v = w[bit >> 5] >> sh;
+  if (sh + (uint32_t)s.bits > 32u) v |= w[(bit >> 5) + 1] << (32u - sh);
+  return v & ((1u << s.bits) - 1u);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -36,24 +60,30 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
                             int Csp, float* lut, hipStream_t stream);
 
 // Returns hipErrorInvalidConfiguration when no tiling fits the device.
-hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
+hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                                const float* bias, int relu, float* y, hipStream_t stream);
 
 hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
-                             const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream);
+                             CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream);
 
 hipError_t launch_maxpool(const float* x, int N, int C, int H, int W, int k, int s, int Ho, int Wo, float* y,
                           hipStream_t stream);
 
 // Zeroes *bad (a device int), then counts the codes >= K into it.
-hipError_t launch_code_check(const uint8_t* codes, size_t n, int K, int* bad, hipStream_t stream);
+hipError_t launch_code_check(CodeStream codes, size_t n, int K, int* bad, hipStream_t stream);
+
+// Packed codes (glue.hip): byte codes -> the stream of `bits` bits per code,
+// written as ceil(n bits / 32) whole dwords (bits past the last code are 0);
+// and back, one byte per code.
+hipError_t launch_pack_codes(const uint8_t* codes, size_t n, int bits, uint32_t* packed, hipStream_t stream);
+hipError_t launch_unpack_codes(CodeStream packed, size_t n, uint8_t* codes, hipStream_t stream);
 
 // True when the conv kernels can tile this layer (host-side, no HIP call).
 bool conv_supported(const ConvShape& s);
 
 // Stride-1 kernel on the flattened padded grid (conv_flat.hip).
 bool conv_flat_supported(const ConvShape& s);
-hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, const uint8_t* codes,
+hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                             const float* bias, int relu, float* y, hipStream_t stream);
 
 // Brackets the main kernel of a call with a pair of HIP events on its
@@ -75,7 +105,7 @@ class KernelTimer {
 // images (fc_tiled.hip): K <= 64, C's <= 8.
 bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct);
 hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
-                           const uint8_t* codes, const float* bias, int relu, float* y, hipStream_t stream);
+                           CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream);
 
 // Parameter quantization (quantize.hip); objective arrays are device float64.
 hipError_t launch_pq_assign(int Ct, int Cs, int dk, const float* W, const float* D, int M, int K, int Csp,

@@ -164,3 +164,61 @@ def test_quantizer_rejects(L):
     assert L.qcnn_pq_update(FAKE, 4, 8, 3, C, 2, 16, 4, FAKE + 4, None, None) == ALIAS
     assert L.qcnn_pq_kmeans(FAKE, 4, 8, 3, 2, 16, 4, -1, FAKE2, C, None, None) == SHAPE
     assert L.qcnn_pq_kmeans(FAKE, 4, 8, 3, 2, 16, 4, 3, FAKE2, C, FAKE2 + 8, None) == ALIAS
+
+
+# ------------------------------------------------------------- packed codes
+
+def test_code_bits_and_packed_bytes(L):
+    # Table 1 (Sec. 3.4): log2 K bits per index; whole dwords per stream.
+    assert [L.qcnn_code_bits(K) for K in (1, 2, 3, 4, 16, 32, 33, 100, 128, 129, 256)] == \
+        [0, 1, 2, 2, 4, 5, 6, 7, 7, 8, 8]
+    assert L.qcnn_code_bits(0) == -1 and L.qcnn_code_bits(257) == -1
+    assert L.qcnn_packed_bytes(0, 32) == 0
+    assert L.qcnn_packed_bytes(3, 32) == 4          # 15 bits -> one dword
+    assert L.qcnn_packed_bytes(7, 32) == 8          # 35 bits -> two dwords
+    assert L.qcnn_packed_bytes(4096 * 2304, 32) == 4096 * 2304 * 5 // 8  # fc6 at 4/32: Table 1's bytes exactly
+    assert L.qcnn_packed_bytes(1000, 1) == 0
+    assert L.qcnn_packed_bytes(5, 0) == 0 and L.qcnn_packed_bytes(5, 300) == 0
+
+
+def test_pack_unpack_rejects_bad_arguments(L):
+    assert L.qcnn_pack_codes(FAKE, 4, 0, FAKE2, None) == KR
+    assert L.qcnn_pack_codes(FAKE, 4, 257, FAKE2, None) == KR
+    assert L.qcnn_pack_codes(None, 4, 16, FAKE2, None) == NULL
+    assert L.qcnn_pack_codes(FAKE, 4, 16, None, None) == NULL
+    assert L.qcnn_pack_codes(FAKE, 4, 16, FAKE2 + 2, None) == UNSUP     # packed not 4-byte aligned
+    assert L.qcnn_pack_codes(FAKE + 1, 4, 16, FAKE2, None) == UNSUP     # codes not 4-byte aligned
+    assert L.qcnn_pack_codes(FAKE, 64, 16, FAKE + 8, None) == ALIAS     # packed overlaps codes
+    assert L.qcnn_pack_codes(None, 0, 16, None, None) == 0              # nothing to do, nothing launched
+    assert L.qcnn_pack_codes(FAKE, 9, 1, None, None) == 0               # K = 1 stores nothing
+    assert L.qcnn_unpack_codes(FAKE, 4, 0, FAKE2, None) == KR
+    assert L.qcnn_unpack_codes(None, 4, 16, FAKE2, None) == NULL
+    assert L.qcnn_unpack_codes(FAKE, 4, 16, None, None) == NULL
+    assert L.qcnn_unpack_codes(FAKE + 2, 4, 16, FAKE2, None) == UNSUP
+    assert L.qcnn_unpack_codes(FAKE, 64, 16, FAKE + 4, None) == ALIAS
+    assert L.qcnn_unpack_codes(None, 0, 16, None, None) == 0
+
+
+def test_packed_forwards_reject_bad_arguments(L):
+    def convp(**kw):
+        a = dict(x=FAKE, N=2, Cs=8, H=5, W=5, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, Ct=4, dk=3, s=1, p=1,
+                 bias=None, relu=0, y=FAKE2, stream=None)
+        a.update(kw)
+        return L.qcnn_conv_forward_packed(a["x"], a["N"], a["Cs"], a["H"], a["W"], a["D"], a["M"], a["K"], a["Csp"],
+                                          a["codes"], a["Ct"], a["dk"], a["s"], a["p"], a["bias"], a["relu"], a["y"],
+                                          a["stream"])
+
+    def fcp(**kw):
+        a = dict(x=FAKE, N=2, Cs=8, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, Ct=4, bias=None, relu=0, y=FAKE2,
+                 stream=None)
+        a.update(kw)
+        return L.qcnn_fc_forward_packed(a["x"], a["N"], a["Cs"], a["D"], a["M"], a["K"], a["Csp"], a["codes"],
+                                        a["Ct"], a["bias"], a["relu"], a["y"], a["stream"])
+
+    assert convp(K=0) == KR and fcp(K=300) == KR
+    assert convp(codes=None) == NULL and fcp(codes=None) == NULL
+    assert convp(Cs=9) == SHAPE and fcp(Cs=9) == SHAPE
+    assert convp(codes=FAKE + 2) == UNSUP and fcp(codes=FAKE + 2) == UNSUP
+    # the packed stream is smaller than the byte codes: y may start right after it
+    assert convp(y=FAKE + 32) == ALIAS       # 72 codes at 4 bits = 36 bytes: y overlaps their last dword
+    assert fcp(y=FAKE + 4) == ALIAS          # 8 codes at 4 bits = one dword

@@ -1,0 +1,171 @@
+"""GPU checks of the packed code format (Table 1, Sec. 3.4: log2 K bits per
+quantization index) through the C ABI.
+
+* qcnn_pack_codes writes, byte for byte, the stream the oracle builds from the
+  format's definition (then zero bits up to a whole dword); qcnn_unpack_codes
+  gives the codes back.
+* The forwards with packed codes return exactly (bit for bit) what the
+  forwards with byte codes return, on every kernel path (flat and generic
+  conv, tiled and generic FC, stride phases, K = 1 and K = 256), and match
+  the oracle within the fp32 bound; integer data (exact in fp32) is checked
+  bit-exact against the oracle, which pins the index handling.
+* The paper's fc8 setting (C'_s = 1, K = 16, Sec. 5.2.2) runs on both code
+  forms.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1512_06473_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+RTOL, ATOL = 1e-5, 1e-6
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_1512_06473_amd import api as a
+    return a
+
+
+def T(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def within_bound(y, ref, A):
+    return bool(np.all(np.abs(np.asarray(y, np.float64) - ref) <= RTOL * A + ATOL))
+
+
+KS = [1, 2, 3, 5, 16, 31, 32, 33, 64, 100, 127, 128, 129, 200, 255, 256]
+
+
+@pytest.mark.parametrize("K", KS)
+def test_pack_matches_oracle_and_round_trips(api, dev, oracle, K):
+    rng = np.random.Generator(np.random.PCG64(1000 + K))
+    for n in [1, 3, 7, 33, 1000, 4099, 65537]:
+        codes = rng.integers(0, K, n).astype(np.uint8)
+        print("pack K=%d n=%d" % (K, n), flush=True)
+        packed = api.pack_codes(T(codes, dev), K)
+        torch.cuda.synchronize()
+        got = packed.cpu().numpy()
+        want = oracle.pack_codes(codes, K)
+        assert got.size == api.packed_bytes(n, K) == 4 * ((n * oracle.code_bits(K) + 31) // 32)
+        assert np.array_equal(got[:want.size], want), (K, n)
+        assert not got[want.size:].any(), "padding past the stream must be zero"
+        back = api.unpack_codes(packed, (n,), K)
+        torch.cuda.synchronize()
+        assert np.array_equal(back.cpu().numpy(), codes), (K, n)
+
+
+def test_unpack_reads_oracle_stream(api, dev, oracle):
+    rng = np.random.Generator(np.random.PCG64(77))
+    for K in [3, 32, 100, 129]:
+        n = 5001
+        codes = rng.integers(0, K, n).astype(np.uint8)
+        stream = oracle.pack_codes(codes, K)
+        buf = np.zeros(api.packed_bytes(n, K), np.uint8)
+        buf[:stream.size] = stream
+        back = api.unpack_codes(T(buf, dev), (n,), K)
+        torch.cuda.synchronize()
+        assert np.array_equal(back.cpu().numpy(), codes), K
+
+
+# (N, C_s, H, W, C_t, d_k, stride, pad, C'_s, K): the flat kernel (3x3 stride 1,
+# stride phases of an 11x11 stride-4 layer, 5x5 row groups, 1x1), the generic
+# kernel (C'_s = 12, K = 256), K = 1 and non-power-of-two K.
+CONV = [
+    (1, 16, 14, 14, 32, 3, 1, 1, 4, 16),
+    (2, 32, 13, 13, 40, 3, 1, 1, 4, 100),
+    (1, 3, 35, 35, 24, 11, 4, 0, 3, 64),
+    (2, 24, 12, 12, 20, 5, 1, 2, 4, 33),
+    (2, 24, 9, 9, 16, 1, 1, 0, 4, 3),
+    (1, 24, 10, 10, 16, 3, 1, 1, 12, 256),
+    (1, 16, 8, 8, 8, 3, 1, 1, 4, 1),
+    (3, 8, 7, 7, 12, 3, 2, 1, 8, 129),
+]
+
+
+@pytest.mark.parametrize("shape", CONV, ids=[str(s) for s in CONV])
+@pytest.mark.parametrize("integer", [False, True])
+def test_conv_packed_equals_byte_codes(api, dev, oracle, shape, integer):
+    N, Cs, H, W, Ct, dk, s, p, Csp, K = shape
+    rng = np.random.Generator(np.random.PCG64(hash(shape) % (2 ** 32)))
+    x, D, codes = wl.random_conv(rng, N, Cs, H, W, Ct, dk, s, p, Csp, K, integer=integer)
+    # integer data: an integer bias keeps every partial sum exact in fp32
+    bias = (rng.integers(-8, 9, Ct) if integer else rng.standard_normal(Ct)).astype(np.float32)
+    print("conv packed", shape, integer, flush=True)
+    xd, Dd, bd = T(x, dev), T(D, dev), T(bias, dev)
+    y8 = api.conv_forward(xd, Dd, T(codes, dev), s, p, bd, True)
+    packed = api.pack_codes(T(codes, dev), K)
+    yp = api.conv_forward_packed(xd, Dd, packed, Ct, dk, s, p, bd, True)
+    torch.cuda.synchronize()
+    y8, yp = y8.cpu().numpy(), yp.cpu().numpy()
+    assert np.array_equal(y8, yp), "packed and byte codes must give identical outputs"
+    ref, A = oracle.conv_lut(x, D, codes, s, p, bias=bias, relu=True, with_bound=True)
+    if integer:
+        assert np.array_equal(yp.astype(np.float64), ref)
+    else:
+        assert within_bound(yp, ref, A)
+
+
+# (N, C_s, C_t, C'_s, K): tiled FC (K <= 64), generic FC (K = 128, C'_s = 12),
+# the fc8 setting C'_s = 1, K = 16 at its full size, K = 1 and odd K.
+FC = [
+    (64, 9216 // 4, 512, 4, 32),
+    (16, 1024, 300, 4, 128),
+    (64, 4096, 1000, 1, 16),
+    (8, 192, 100, 12, 3),
+    (5, 64, 33, 4, 1),
+    (130, 512, 257, 8, 61),
+]
+
+
+@pytest.mark.parametrize("shape", FC, ids=[str(s) for s in FC])
+@pytest.mark.parametrize("integer", [False, True])
+def test_fc_packed_equals_byte_codes(api, dev, oracle, shape, integer):
+    N, Cs, Ct, Csp, K = shape
+    rng = np.random.Generator(np.random.PCG64(hash(shape) % (2 ** 32)))
+    x, D, codes = wl.random_fc(rng, N, Cs, Ct, Csp, K, integer=integer)
+    print("fc packed", shape, integer, flush=True)
+    xd, Dd = T(x, dev), T(D, dev)
+    y8 = api.fc_forward(xd, Dd, T(codes, dev))
+    packed = api.pack_codes(T(codes, dev), K)
+    yp = api.fc_forward_packed(xd, Dd, packed, Ct)
+    torch.cuda.synchronize()
+    y8, yp = y8.cpu().numpy(), yp.cpu().numpy()
+    assert np.array_equal(y8, yp), "packed and byte codes must give identical outputs"
+    ref, A = oracle.fc_lut(x, D, codes, with_bound=True)
+    if integer:
+        assert np.array_equal(yp.astype(np.float64), ref)
+    else:
+        assert within_bound(yp, ref, A)
+
+
+def test_headline_conv_packed(api, dev, oracle):
+    """The AlexNet-conv3-shaped layer (K = 128, 7-bit codes): packed equals
+    byte codes bit for bit, and sampled outputs match the oracle."""
+    d = wl.generate("cfg2")
+    L = d["layers"][0]
+    xd, Dd = T(d["x"], dev), T(L["D"], dev)
+    print("headline packed", flush=True)
+    y8 = api.conv_forward(xd, Dd, T(L["codes"], dev), 1, 1)
+    packed = api.pack_codes(T(L["codes"], dev), 128)
+    assert packed.numel() == L["codes"].size * 7 // 8
+    yp = api.conv_forward_packed(xd, Dd, packed, 384, 3, 1, 1)
+    torch.cuda.synchronize()
+    y8, yp = y8.cpu().numpy(), yp.cpu().numpy()
+    assert np.array_equal(y8, yp)
+    rng = np.random.Generator(np.random.PCG64(3))
+    pts = np.stack([rng.integers(0, 32, 256), rng.integers(0, 384, 256), rng.integers(0, 13, 256),
+                    rng.integers(0, 13, 256)], 1).astype(np.int32)
+    v, a = oracle.conv_points(d["x"], L["D"], L["codes"], pts, 1, 1)
+    got = yp[tuple(pts.T)].astype(np.float64)
+    assert np.all(np.abs(got - v) <= RTOL * a + ATOL)
