@@ -165,6 +165,84 @@ def pack_checks(rng):
     return out
 
 
+def ec_checks(rng, E=None):
+    """Error correction for a FC layer (Sec. 3.3.1, Eq. (8)-(12)); E is the
+    module under test (default: the oracle's)."""
+    if E is None:
+        from oracle import ec as E
+    out = []
+    # Eq. (8) with S = I is || W - D B ||^2 column by column: one round of
+    # (sub-codebook, assignment) update is a k-means update then an
+    # assignment (Eq. (4)).  Well separated clusters, so no decision is close.
+    Ct, Cs, Csp, K = 60, 12, 4, 5
+    M = Cs // Csp
+    centers = rng.standard_normal((M, K, Csp)) * 10
+    lab = rng.integers(0, K, (Ct, M))
+    W = np.stack([centers[m][lab[:, m]] for m in range(M)], 1).reshape(Ct, Cs)
+    W = (W + 0.01 * rng.standard_normal(W.shape)).astype(np.float32)
+    D0 = (centers + rng.standard_normal(centers.shape)).astype(np.float32)
+    c0, _, _ = O.pq_assign(W, D0)
+    D, codes, hist = E.ec_fc(np.eye(Cs), W.T.astype(np.float64), D0, c0, sweeps=1, inner=1)
+    D1, _ = O.pq_update(W, c0, D0)
+    c1, _, _ = O.pq_assign(W, D1)
+    out.append(("ec S=I sub-codebooks = k-means update", np.allclose(D, D1, rtol=1e-6, atol=1e-6)))
+    out.append(("ec S=I assignment = k-means assignment", np.array_equal(codes, c1)))
+    # general inputs
+    N, Cs, Ct, Csp, K = 40, 12, 30, 3, 6
+    M = Cs // Csp
+    S = rng.standard_normal((N, Cs))
+    Wt = rng.standard_normal((Ct, Cs))
+    T = S @ Wt.T + 0.1 * rng.standard_normal((N, Ct))
+    D0 = rng.standard_normal((M, K, Csp))
+    c0 = rng.integers(0, K, (Ct, M)).astype(np.uint8)
+    D, codes, hist = E.ec_fc(S, T, D0, c0, sweeps=2, inner=2)
+    out.append(("ec objective non-increasing", bool(np.all(np.diff(hist) <= 1e-9 * hist[0]))))
+    out.append(("ec objective decreases", hist[-1] < 0.9 * hist[0]))
+    What = np.stack([D[m][codes[:, m]] for m in range(M)], 1).reshape(Ct, Cs)
+    out.append(("ec objective = response error", abs(float(np.sum((T - S @ What.T) ** 2)) - hist[-1])
+                <= 1e-9 * hist[0]))
+    # one subspace step against library least squares and a brute-force argmin
+    m = 1
+    Sm = S[:, m * Csp:(m + 1) * Csp]
+    R = rng.standard_normal((N, Ct))
+    Dm, cm = E.subspace_step(Sm, R, D0[m], c0[:, m], inner=1)
+    ok = True
+    for k in range(K):
+        Lk = np.flatnonzero(c0[:, m] == k)
+        if Lk.size:
+            A = np.vstack([Sm] * Lk.size)
+            bb = np.concatenate([R[:, c] for c in Lk])
+            ok &= np.allclose(Dm[k], np.linalg.lstsq(A, bb, rcond=None)[0], rtol=1e-9, atol=1e-12)
+        else:
+            ok &= np.array_equal(Dm[k], D0[m][k])
+    out.append(("ec sub-codebook = least squares (lstsq)", bool(ok)))
+    brute = np.array([np.argmin([np.sum((R[:, c] - Sm @ Dm[k]) ** 2) for k in range(K)]) for c in range(Ct)])
+    out.append(("ec assignment = brute-force Eq. (12)", np.array_equal(cm, brute)))
+    # a channel that is zero on every image: its coordinate of every updated
+    # sub-codeword is 0 (reading E4), and the fit equals least squares
+    S2 = S.copy()
+    S2[:, m * Csp + 1] = 0.0
+    Sm2 = S2[:, m * Csp:(m + 1) * Csp]
+    Dz, _ = E.subspace_step(Sm2, R, D0[m], c0[:, m], inner=1)
+    used = np.unique(c0[:, m])
+    out.append(("ec dead channel gives a zero coordinate", bool(np.all(Dz[used, 1] == 0.0))))
+    ok = True
+    for k in used:
+        Lk = np.flatnonzero(c0[:, m] == k)
+        ok &= np.allclose(Dz[k], np.linalg.lstsq(np.vstack([Sm2] * Lk.size),
+                                                 np.concatenate([R[:, c] for c in Lk]), rcond=None)[0],
+                          rtol=1e-9, atol=1e-12)
+    out.append(("ec dead channel fit = min-norm least squares", bool(ok)))
+    # an exact quantized layer stays exact
+    Dt = rng.standard_normal((M, K, Csp))
+    ct = rng.integers(0, K, (Ct, M)).astype(np.uint8)
+    Wq = np.stack([Dt[m][ct[:, m]] for m in range(M)], 1).reshape(Ct, Cs)
+    D, codes, hist = E.ec_fc(S, S @ Wq.T, Dt, ct, sweeps=1, inner=1)
+    out.append(("ec lossless start stays lossless", hist[-1] <= 1e-18 * float(np.sum((S @ Wq.T) ** 2)) + 1e-20
+                and np.array_equal(codes, ct)))
+    return out
+
+
 def checks():
     out = []
     # hand-worked (see test_oracle.py for the arithmetic)
@@ -225,6 +303,7 @@ def checks():
     out.append(("maxpool", np.array_equal(ym, ref)))
     out += quant_checks(rng)
     out += pack_checks(rng)
+    out += ec_checks(rng)
     return out
 
 

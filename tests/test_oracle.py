@@ -375,3 +375,32 @@ def test_packed_code_errors(oracle):
     with pytest.raises(oracle.OracleError):
         oracle.pack_codes(np.array([0], np.uint8), 257)    # K > 256
     assert oracle.packed_nbytes(0, 32) == 0 and oracle.pack_codes(np.zeros(0, np.uint8), 32).size == 0
+
+
+# ---------------------------------------------------- error correction (FC)
+# Sec. 3.3.1, Eq. (8)-(12): block coordinate descent over the subspaces.
+
+def test_ec_pins(oracle):
+    """S = I reduces to k-means; sub-codebooks = library least squares;
+    assignments = brute force of Eq. (12); monotone objective equal to the
+    response error; dead channels; a lossless start stays lossless."""
+    import pin_battery
+    bad = [name for name, ok in pin_battery.ec_checks(np.random.Generator(np.random.PCG64(21))) if not ok]
+    assert not bad, bad
+
+
+def test_ec_reduces_error_of_kmeans_on_layer_responses(oracle):
+    """Starting from the k-means quantizer (Eq. (4)), error correction lowers
+    the response error of Eq. (8), which is what it minimises, while k-means
+    minimises the weight error."""
+    from oracle import ec
+    rng = np.random.Generator(np.random.PCG64(4))
+    N, Cs, Ct, Csp, K = 200, 32, 48, 4, 8
+    S = np.maximum(rng.standard_normal((N, Cs)), 0).astype(np.float32)   # post-ReLU-like inputs
+    S[:, :8] *= 5.0                                                        # channels of unequal scale
+    W = (0.1 * rng.standard_normal((Ct, Cs))).astype(np.float32)
+    T = S.astype(np.float64) @ W.T.astype(np.float64)
+    D0 = (0.1 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32)
+    Dk, ck, _, _ = oracle.pq_kmeans(W, D0, 10)
+    D, codes, hist = ec.ec_fc(S, T, Dk, ck, sweeps=3, inner=2)
+    assert hist[-1] < 0.8 * hist[0], hist[[0, -1]]

@@ -100,3 +100,59 @@ def test_pins_catch_mutant(tmp_path, mut):
     lib = _build(_mutate(open(SRC).read(), func, old, new), tmp_path, "mut")
     r = _battery(lib)
     assert r.returncode == 1 and "FAILED" in r.stdout, "mutant survived: %s\n%s%s" % (what, r.stdout, r.stderr)
+
+
+# Mistakes planted in a copy of the error-correction oracle (oracle/ec.py,
+# Eq. (8)-(12)); the module copy is loaded on its own and the battery's EC
+# checks must flag each one.
+EC_SRC = os.path.join(ROOT, "oracle", "ec.py")
+EC_MUTANTS = [
+    ("Dm[k] = solve_normal(G, P[:, Lk].sum(axis=1)) / Lk.sum()",
+     "Dm[k] = solve_normal(G, P[:, Lk].sum(axis=1))", "sub-codebook: sum not divided by |L_k|"),
+    ("cost = q[:, None] - 2.0 * (Dm @ P)", "cost = q[:, None] - (Dm @ P)", "assignment: cross term not doubled"),
+    ("codes_m = np.argmin(cost, axis=0)", "codes_m = np.argmax(cost, axis=0)", "assignment: argmax"),
+    ("R = T - Y + old", "R = T - Y", "residual keeps the subspace's own contribution"),
+    ("for _ in range(inner):\n        for k in range(K):",
+     "for _ in range(inner):\n        for k in range(K - 1):", "last sub-codeword never updated"),
+    ("P = Sm.T @ R ", "P = Sm.T @ (R - R.mean(axis=0)) ", "residual centred"),
+    ("if A[j, j] <= PIVOT_REL * scale or A[j, j] <= 0.0:", "if A[j, j] < 0.0:", "dead directions not dropped"),
+    ("Y = Y - old + Sm @ D[m][codes[:, m]].T", "Y = Y + Sm @ D[m][codes[:, m]].T",
+     "response not updated correctly after a subspace"),
+]
+
+
+def _ec_module(text, tmp_path, name):
+    import importlib.util
+    path = tmp_path / (name + ".py")
+    path.write_text(text)
+    spec = importlib.util.spec_from_file_location(name, str(path))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_unmodified_ec_passes(tmp_path):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    mod = _ec_module(open(EC_SRC).read(), tmp_path, "ec_orig")
+    bad = [n for n, ok in pin_battery.ec_checks(np.random.Generator(np.random.PCG64(11)), mod) if not ok]
+    assert not bad, bad
+
+
+@pytest.mark.filterwarnings("ignore::RuntimeWarning")  # some mutants divide by a zero pivot
+@pytest.mark.parametrize("mut", EC_MUTANTS, ids=[m[2] for m in EC_MUTANTS])
+def test_ec_pins_catch_mutant(tmp_path, mut):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    old, new, what = mut
+    src = open(EC_SRC).read()
+    assert old in src, old
+    mod = _ec_module(src.replace(old, new, 1), tmp_path, "ec_mut")
+    try:
+        res = pin_battery.ec_checks(np.random.Generator(np.random.PCG64(11)), mod)
+        survived = all(ok for _, ok in res)
+    except Exception:  # a crash is a caught mistake too
+        survived = False
+    assert not survived, "mutant survived: " + what
