@@ -195,6 +195,34 @@ qcnn_status qcnn_pq_kmeans(const float* W, int C_t, int C_s, int d_k,
  * pooling over k x k windows with stride s and no padding,
  *   y[n][c][yo][xo] = max_{dy,dx < k} x[n][c][yo s + dy][xo s + dx],
  * H_o = floor((H - k) / s) + 1.  x: [N][C][H][W]; y (output): [N][C][H_o][W_o]. */
+/* ---- Error-corrected quantization of a fully-connected layer (Sec. 3.3.1).
+ * Minimises the response error of Eq. (8),
+ *   sum_n || T_n - sum_m (D^(m) B^(m))^T S_n^(m) ||^2,
+ * over the sub-codebooks and assignments by block coordinate descent over
+ * the subspaces: for subspace m, with R^(m) the residual of the others
+ * (Eq. (9)), `inner` rounds of the sub-codebook update of Eq. (11) (each
+ * sub-codeword the least-squares fit over the images and the output
+ * channels assigned to it) then the assignment update of Eq. (12) (each
+ * channel the sub-codeword of least residual error).  A call runs `sweeps`
+ * sweeps over m = 0 .. M-1 in order, starting from the codebooks and codes
+ * given (normally those of qcnn_pq_kmeans).
+ * S: [N][C_s] the layer's inputs; T: [N][C_t] the desired responses (fp32);
+ * codebooks [M][K][C'_s] fp32 and codes uint8 [C_t][M]: updated in place;
+ * objective (output, nullable): [1 + sweeps M] float64, Eq. (8) before the
+ * first step and after every subspace step (non-increasing up to rounding).
+ * Arithmetic is float64 throughout (the residual E = T - S W-hat is kept in
+ * a library workspace of 8 N C_t bytes plus partial sums); the codebooks
+ * are rounded to fp32 once at the end.  A sub-codeword no channel uses keeps
+ * its value; the normal equations |L_k| G D_k = sum_{c in L_k} S^(m)T r_c,
+ * G = S^(m)T S^(m), are solved by elimination in channel order, a pivot
+ * <= 1e-12 x max diag(G) (a direction the inputs do not span, such as a
+ * channel that is zero on every image) setting that coordinate to 0;
+ * assignment ties go to the lowest index.  Limits: those of the forward,
+ * N <= 2^20; codes >= K are read as K - 1 (checked with QCNN_CHECK_CODES=1). */
+qcnn_status qcnn_ec_fc(const float* S, int N, int C_s, const float* T, int C_t,
+                       float* codebooks, int M, int K, int Csp, uint8_t* codes,
+                       int sweeps, int inner, double* objective, void* stream);
+
 qcnn_status qcnn_maxpool2d(const float* x, int N, int C, int H, int W, int k, int s,
                            float* y, void* stream);
 

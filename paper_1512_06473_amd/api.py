@@ -244,6 +244,34 @@ def fc_forward_packed(x: torch.Tensor, codebooks: torch.Tensor, packed_codes: to
     return out
 
 
+def ec_fc(S: torch.Tensor, T: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, sweeps: int = 1,
+          inner: int = 1, objective: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Error-corrected quantization of a FC layer, Eq. (8)-(12) (qcnn_ec_fc).
+
+    S [N][C_s] layer inputs, T [N][C_t] desired responses (fp32); codebooks
+    [M][K][C'_s] fp32 and codes uint8 [C_t][M] are updated in place.  Returns
+    the objective history, float64 [1 + sweeps M].
+    """
+    _need(S, "S", torch.float32, 2)
+    _need(T, "T", torch.float32, 2, S.device)
+    _need(codebooks, "codebooks", torch.float32, 3, S.device)
+    _need(codes, "codes", torch.uint8, 2, S.device)
+    N, Cs = S.shape
+    Ct = T.shape[1]
+    M, K, Csp = codebooks.shape
+    if T.shape[0] != N or tuple(codes.shape) != (Ct, M):
+        raise ValueError("shapes: S %s, T %s, codes %s, codebooks %s" % (tuple(S.shape), tuple(T.shape),
+                                                                          tuple(codes.shape), tuple(codebooks.shape)))
+    if objective is None:
+        objective = torch.empty(1 + sweeps * M, dtype=torch.float64, device=S.device)
+    _need(objective, "objective", torch.float64, 1, S.device)
+    if objective.numel() != 1 + sweeps * M:
+        raise ValueError("objective must have 1 + sweeps M = %d entries" % (1 + sweeps * M))
+    check(lib().qcnn_ec_fc(S.data_ptr(), N, Cs, T.data_ptr(), Ct, codebooks.data_ptr(), M, K, Csp, codes.data_ptr(),
+                           int(sweeps), int(inner), objective.data_ptr(), _stream(S)), "qcnn_ec_fc")
+    return objective
+
+
 def maxpool2d(x: torch.Tensor, k: int = 3, s: int = 2, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """k x k / stride s max pooling, no padding (qcnn_maxpool2d): network glue."""
     _need(x, "x", torch.float32, 4)

@@ -115,6 +115,12 @@ hipError_t launch_pq_update(int Ct, int Cs, int dk, const float* W, const uint8_
 hipError_t launch_pq_kmeans(int Ct, int Cs, int dk, const float* W, int M, int K, int Csp, int iters, float* D,
                             uint8_t* codes, double* objective, hipStream_t stream);
 
+// Error-corrected quantization of a fully-connected layer (ec_fc.hip):
+// S [N][C_s], T [N][C_t] fp32; D [M][K][C'_s] and codes [C_t][M] updated in
+// place; objective (nullable) [1 + sweeps M] float64.
+hipError_t launch_ec_fc(int N, int Cs, int Ct, int M, int K, int Csp, const float* S, const float* T, float* D,
+                        uint8_t* codes, int sweeps, int inner, double* objective, hipStream_t stream);
+
 // Keep freed stream-ordered allocations in the device's default pool
 // (called once per device before the first hipMallocAsync).
 hipError_t retain_pool_memory();

@@ -222,3 +222,21 @@ def test_packed_forwards_reject_bad_arguments(L):
     # the packed stream is smaller than the byte codes: y may start right after it
     assert convp(y=FAKE + 32) == ALIAS       # 72 codes at 4 bits = 36 bytes: y overlaps their last dword
     assert fcp(y=FAKE + 4) == ALIAS          # 8 codes at 4 bits = one dword
+
+
+def test_ec_fc_rejects_bad_arguments(L):
+    def ec(**kw):
+        a = dict(S=FAKE, N=8, Cs=8, T=FAKE2, Ct=4, D=FAKE2 + 4096, M=2, K=16, Csp=4, codes=FAKE2 + 8192,
+                 sweeps=1, inner=1, obj=None, stream=None)
+        a.update(kw)
+        return L.qcnn_ec_fc(a["S"], a["N"], a["Cs"], a["T"], a["Ct"], a["D"], a["M"], a["K"], a["Csp"], a["codes"],
+                            a["sweeps"], a["inner"], a["obj"], a["stream"])
+
+    assert ec(S=None) == NULL and ec(T=None) == NULL and ec(D=None) == NULL and ec(codes=None) == NULL
+    assert ec(Cs=9) == SHAPE and ec(Ct=0) == SHAPE and ec(N=0) == SHAPE
+    assert ec(sweeps=-1) == SHAPE and ec(inner=0) == SHAPE
+    assert ec(K=0) == KR and ec(K=257) == KR
+    assert ec(M=1, Csp=17, Cs=17) == UNSUP
+    assert ec(D=FAKE + 16) == ALIAS                  # codebooks inside S
+    assert ec(codes=FAKE2 + 4) == ALIAS              # codes inside T
+    assert ec(obj=FAKE2 + 4096 + 8) == ALIAS         # objective inside the codebooks
