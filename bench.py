@@ -257,6 +257,75 @@ def main():
         del st
     line["quantizer"] = quant
 
+    # ------------------------------------------ packed codes (Table 1 storage)
+    # The same layers with their codes in the packed log2 K-bit form; the
+    # forward reads the packed stream directly.  fc6 at N = 1 is where code
+    # streaming dominates a step.
+    packed = {}
+    if args.configs != "none":
+        def packed_case(cfg, n_images=None):
+            d = workloads.generate(cfg)
+            L = d["layers"][0]
+            x = T(d["x"] if n_images is None else d["x"][:n_images])
+            D, c = T(L["D"]), T(L["codes"])
+            K = L["D"].shape[1]
+            pc = api.pack_codes(c, K)
+            Ct = L["codes"].shape[0]
+            if L["kind"] == "conv":
+                dk = L["codes"].shape[1]
+                y = api.conv_forward(x, D, c, L["stride"], L["pad"])
+                f8 = lambda: api.conv_forward(x, D, c, L["stride"], L["pad"], out=y)
+                fp = lambda: api.conv_forward_packed(x, D, pc, Ct, dk, L["stride"], L["pad"], out=y)
+            else:
+                y = api.fc_forward(x, D, c)
+                f8 = lambda: api.fc_forward(x, D, c, out=y)
+                fp = lambda: api.fc_forward_packed(x, D, pc, Ct, out=y)
+            m8, _ = time_steps(f8, 100, 5)
+            mp, _ = time_steps(fp, 100, 5)
+            return {"code_bytes": int(L["codes"].size), "packed_bytes": int(pc.numel()),
+                    "bits_per_code": api.code_bits(K), "ms_byte_codes": m8, "ms_packed_codes": mp}
+        packed["cfg2_conv3"] = packed_case("cfg2")
+        packed["cfg3_fc6"] = packed_case("cfg3")
+        packed["fc6_one_image"] = packed_case("cfg3", 1)
+    line["packed_codes"] = packed
+
+    # -------------------------- error-corrected quantization of fc6 (Eq. (8)-(12))
+    # One sweep over the 2304 subspaces of a 9216 -> 4096 layer (C's = 4,
+    # K = 32) from the k-means solution, on 256 synthetic calibration images:
+    # S = |N(0,1)|, T = S W^T for W = 0.01 N(0,1).
+    ecr = {}
+    if args.configs != "none":
+        rng = np.random.Generator(np.random.PCG64(31))
+        Nimg, Cs, Ct, Csp, K = 256, 9216, 4096, 4, 32
+        S = np.abs(rng.standard_normal((Nimg, Cs))).astype(np.float32)
+        W = (0.01 * rng.standard_normal((Ct, Cs))).astype(np.float32)
+        Tn = S @ W.T
+        Sd, Td, Wd = T(S), T(Tn), T(W)
+        D0 = T((0.01 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32))
+        Dk, ck, _ = api.pq_kmeans(Wd, D0, 4)
+        torch.cuda.synchronize(dev)
+        times, objs = [], None
+        for _ in range(3):
+            D, c = Dk.clone(), ck.clone()
+            torch.cuda.synchronize(dev)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            objs = api.ec_fc(Sd, Td, D, c, 1, 1)
+            e1.record()
+            torch.cuda.synchronize(dev)
+            times.append(e0.elapsed_time(e1))
+        o = objs.cpu().numpy()
+        M = Cs // Csp
+        # HBM bytes a sweep must move: the float64 residual read and written once
+        # per subspace step, plus the subspace's inputs
+        nbytes = M * (16.0 * Nimg * Ct + 4.0 * Nimg * Csp)
+        ecr = {"layer": "fc6 9216 -> 4096, C's=4, K=32, 256 images", "ms_per_sweep": min(times),
+               "hbm_bytes_per_sweep": nbytes, "hbm_frac": nbytes / (min(times) * 1e-3) / workmodel.HBM_PEAK_BPS,
+               "response_error_kmeans": float(o[0]), "response_error_after_sweep": float(o[-1])}
+        del Sd, Td, Wd
+    line["error_correction_fc"] = ecr
+
     # ------------------------------------------------------------ CPU baseline
     if not args.no_cpu:
         from oracle import oracle

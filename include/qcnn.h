@@ -218,7 +218,8 @@ qcnn_status qcnn_pq_kmeans(const float* W, int C_t, int C_s, int d_k,
  * <= 1e-12 x max diag(G) (a direction the inputs do not span, such as a
  * channel that is zero on every image) setting that coordinate to 0;
  * assignment ties go to the lowest index.  Limits: those of the forward,
- * N <= 2^20; codes >= K are read as K - 1 (checked with QCNN_CHECK_CODES=1). */
+ * N <= 2^20, C_t <= 65536; codes >= K are read as K - 1 (checked with
+ * QCNN_CHECK_CODES=1). */
 qcnn_status qcnn_ec_fc(const float* S, int N, int C_s, const float* T, int C_t,
                        float* codebooks, int M, int K, int Csp, uint8_t* codes,
                        int sweeps, int inner, double* objective, void* stream);

@@ -19,7 +19,9 @@
 //                    partial products S^(m)T E over chunks of images;
 //   ec_reduce_kernel P = sum of the partials (fixed order) + G W^(m), so that
 //                    P = S^(m)T R^(m) with R^(m) = E + S^(m) W^(m);
-//   ec_update_kernel one workgroup: `inner` rounds of Eq. (11) then Eq. (12).
+//   ec_fit_kernel    one workgroup: Eq. (11) for every sub-codeword;
+//   ec_assign_kernel one thread per output channel: Eq. (12);
+//                    the last two `inner` times.
 // Readings (shared with the oracle): the descent starts from the given
 // sub-codebooks and codes; a sweep visits m in order; a sub-codeword no
 // channel uses keeps its value; the normal equations are solved by
@@ -28,7 +30,7 @@
 // assignment ties go to the lowest index.
 //
 // Bound: HBM.  A subspace step reads and writes E once (16 N C_t bytes) and
-// reads S^(m) (4 N C'_s bytes); the update kernel is latency-bound on one CU.
+// reads S^(m) (4 N C'_s bytes); the fit kernel is latency-bound on one CU.
 #include "qcnn_internal.h"
 
 namespace qcnn {
@@ -156,7 +158,7 @@ __global__ __launch_bounds__(kEcThreads) void ec_reduce_kernel(const double* __r
 
 // x with G x = b by elimination in channel order without row exchanges; a
 // pivot <= 1e-12 x max diag(G) (or <= 0) drops that coordinate (x = 0).
-__device__ void solve_normal(const double* __restrict__ Gm, const double* __restrict__ bin, int n, double* x) {
+__device__ __forceinline__ void solve_normal(const double* __restrict__ Gm, const double* __restrict__ bin, int n, double* x) {
   double A[kMaxCsp][kMaxCsp], y[kMaxCsp];
   bool live[kMaxCsp];
   double scale = 0.0;
@@ -184,95 +186,156 @@ __device__ void solve_normal(const double* __restrict__ Gm, const double* __rest
   }
 }
 
-// One workgroup: the objective after the previous step (from the pass
-// kernel's block sums), the old sub-codebook / codes of subspace m kept for
-// the next pass, then `inner` rounds of Eq. (11) and Eq. (12).
+// Eq. (11), one workgroup.  On the first round of a subspace (`first`) it
+// also records the objective after the previous step (from the pass
+// kernel's block sums) and keeps the subspace's old sub-codebook and codes
+// for the next pass.  Then each sub-codeword used by some channel becomes
+// the least-squares fit, and qv[k] = D_k^T G D_k for the assignment.
 template <int CSP>
-__global__ __launch_bounds__(kUpdThreads) void ec_update_kernel(const double* __restrict__ P, EcParams p, int m,
-                                                              const double* __restrict__ G,
-                                                              double* __restrict__ D64, uint8_t* __restrict__ codes,
-                                                              double* __restrict__ Dold,
-                                                              uint8_t* __restrict__ codes_old,
-                                                              const double* __restrict__ opart, int nopart,
-                                                              double* __restrict__ objective) {
+__global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __restrict__ P, EcParams p, int m,
+                                                           const double* __restrict__ G, double* __restrict__ D64,
+                                                           const uint8_t* __restrict__ codes, int first,
+                                                           double* __restrict__ Dold,
+                                                           uint8_t* __restrict__ codes_old,
+                                                           const double* __restrict__ opart, int nopart,
+                                                           double* __restrict__ objective, double* __restrict__ qv) {
+  // All LDS is dynamic (the kernel may take up to the whole 160 KB, so it
+  // cannot also have static LDS).
   extern __shared__ double sh[];
   double* Gs = sh;                               // [C's][C's]
   double* Ds = Gs + kMaxCsp * kMaxCsp;           // [K][C's]
-  double* q = Ds + 256 * kMaxCsp;                // [K]
+  double* red = Ds + 256 * kMaxCsp;              // [threads] objective tree
+  // this subspace's codes, read from the [C_t][M] array (stride M) once
+  uint8_t* cs = reinterpret_cast<uint8_t*>(red + kUpdThreads);
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   constexpr int Csp = CSP;
   const int K = p.K;
-  if (tid == 0 && objective) {
+  if (first && objective) {
+    // the pass kernel's block sums: thread strides, then a fixed tree
     double s = 0.0;
-    for (int i = 0; i < nopart; ++i) s += opart[i];
-    *objective = s;
+    for (int i = tid; i < nopart; i += kUpdThreads) s += opart[i];
+    red[tid] = s;
+    __syncthreads();
+    for (int h = kUpdThreads / 2; h > 0; h >>= 1) {
+      if (tid < h) red[tid] += red[tid + h];
+      __syncthreads();
+    }
+    if (tid == 0) *objective = red[0];
   }
   for (int i = tid; i < Csp * Csp; i += kUpdThreads) Gs[i] = G[(size_t)m * Csp * Csp + i];
   for (int i = tid; i < K * Csp; i += kUpdThreads) {
     Ds[i] = D64[(size_t)m * K * Csp + i];
-    Dold[i] = Ds[i];
+    if (first) Dold[i] = Ds[i];
   }
-  for (int c = tid; c < p.Ct; c += kUpdThreads) codes_old[c] = (uint8_t)ec_code(codes, c, p.M, m, K);
+  // the codes (stride M bytes apart): eight loads in flight per thread
+  for (int c0 = tid; c0 < p.Ct; c0 += 8 * kUpdThreads) {
+    uint8_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int c = c0 + u * kUpdThreads;
+      v[u] = c < p.Ct ? (uint8_t)ec_code(codes, c, p.M, m, K) : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int c = c0 + u * kUpdThreads;
+      if (c < p.Ct) {
+        if (first) codes_old[c] = v[u];
+        cs[c] = v[u];
+      }
+    }
+  }
   __syncthreads();
-  for (int it = 0; it < p.inner; ++it) {
-    // Eq. (11): wave w fits sub-codewords k = w, w + 16, ...; its lanes scan
-    // the channels c = lane, lane + 64, ... in order, and the wave adds the
-    // lanes' sums in a fixed tree.
-    for (int k = wave; k < K; k += kUpdThreads / kWave) {
-      double b[CSP];
+  // Wave w fits sub-codewords in groups of KC (k = KC w .. KC w + KC - 1,
+  // then KC (w + 4) ...; KC C'_s <= 32 bins per lane): its lanes read the
+  // channels c = lane, lane + 64, ... in
+  // order, each channel's P_c once and unconditionally (coalesced, several
+  // loads in flight), adding it to the bin of its code; the wave then adds
+  // the lanes' bins in a fixed tree.
+  constexpr int KC = CSP <= 4 ? 8 : (CSP <= 8 ? 4 : 2);
+  for (int kbase = wave * KC; kbase < K; kbase += (kUpdThreads / kWave) * KC) {
+    double b[KC][CSP];
+    int cnt[KC];
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) b[j] = 0.0;
-      int cnt = 0;
-      for (int c = lane; c < p.Ct; c += kWave)
-        if (ec_code(codes, c, p.M, m, K) == (uint32_t)k) {
-          ++cnt;
+    for (int u = 0; u < KC; ++u) {
+      cnt[u] = 0;
 #pragma unroll
-          for (int j = 0; j < CSP; ++j) b[j] += P[(size_t)j * p.Ct + c];
-        }
-      for (int off = kWave / 2; off > 0; off >>= 1) {
-        cnt += __shfl_down(cnt, off, kWave);
-#pragma unroll
-        for (int j = 0; j < CSP; ++j) b[j] += __shfl_down(b[j], off, kWave);
-      }
-      if (lane == 0 && cnt > 0) {
-        double x[kMaxCsp];
-        solve_normal(Gs, b, Csp, x);
-        for (int j = 0; j < Csp; ++j) Ds[k * Csp + j] = x[j] / cnt;
-      }
+      for (int j = 0; j < CSP; ++j) b[u][j] = 0.0;
     }
-    __syncthreads();
-    for (int k = tid; k < K; k += kUpdThreads) {  // D_k^T G D_k
-      double s = 0.0;
-      for (int i = 0; i < Csp; ++i) {
-        double g = 0.0;
-        for (int j = 0; j < Csp; ++j) g += Gs[i * Csp + j] * Ds[k * Csp + j];
-        s += Ds[k * Csp + i] * g;
-      }
-      q[k] = s;
-    }
-    __syncthreads();
-    // Eq. (12): the first k minimising D_k^T G D_k - 2 D_k^T P_c.
-    for (int c = tid; c < p.Ct; c += kUpdThreads) {
+    for (int c = lane; c < p.Ct; c += kWave) {
+      const int kc = (int)cs[c] - kbase;
       double pc[CSP];
 #pragma unroll
       for (int j = 0; j < CSP; ++j) pc[j] = P[(size_t)j * p.Ct + c];
-      int best = 0;
-      double bv = 0.0;
-      for (int k = 0; k < K; ++k) {
-        double d = 0.0;
 #pragma unroll
-        for (int j = 0; j < CSP; ++j) d += Ds[k * CSP + j] * pc[j];
-        const double v = q[k] - 2.0 * d;
-        if (k == 0 || v < bv) {
-          bv = v;
-          best = k;
+      for (int u = 0; u < KC; ++u) {
+        const bool hit = kc == u;
+        cnt[u] += hit ? 1 : 0;
+#pragma unroll
+        for (int j = 0; j < CSP; ++j) b[u][j] += hit ? pc[j] : 0.0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < KC; ++u)
+      for (int off = kWave / 2; off > 0; off >>= 1) {
+        cnt[u] += __shfl_down(cnt[u], off, kWave);
+#pragma unroll
+        for (int j = 0; j < CSP; ++j) b[u][j] += __shfl_down(b[u][j], off, kWave);
+      }
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < KC; ++u) {
+        const int k = kbase + u;
+        if (k < K && cnt[u] > 0) {
+          double x[kMaxCsp];
+          solve_normal(Gs, b[u], Csp, x);
+          for (int j = 0; j < Csp; ++j) Ds[k * Csp + j] = x[j] / cnt[u];
         }
       }
-      codes[(size_t)c * p.M + m] = (uint8_t)best;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  for (int k = tid; k < K; k += kUpdThreads) {  // D_k^T G D_k
+    double s = 0.0;
+    for (int i = 0; i < Csp; ++i) {
+      double g = 0.0;
+      for (int j = 0; j < Csp; ++j) g += Gs[i * Csp + j] * Ds[k * Csp + j];
+      s += Ds[k * Csp + i] * g;
+    }
+    qv[k] = s;
   }
   for (int i = tid; i < K * Csp; i += kUpdThreads) D64[(size_t)m * K * Csp + i] = Ds[i];
+}
+
+// Eq. (12), one thread per output channel: the first k minimising
+// D_k^T G D_k - 2 D_k^T P_c.
+template <int CSP>
+__global__ __launch_bounds__(kEcThreads) void ec_assign_kernel(const double* __restrict__ P, EcParams p, int m,
+                                                             const double* __restrict__ D64,
+                                                             const double* __restrict__ qv,
+                                                             uint8_t* __restrict__ codes) {
+  extern __shared__ double sd[];  // [K][C's], then [K]
+  double* q = sd + (size_t)p.K * CSP;
+  for (int i = threadIdx.x; i < p.K * CSP; i += kEcThreads) sd[i] = D64[(size_t)m * p.K * CSP + i];
+  for (int i = threadIdx.x; i < p.K; i += kEcThreads) q[i] = qv[i];
+  __syncthreads();
+  const int c = blockIdx.x * kEcThreads + threadIdx.x;
+  if (c >= p.Ct) return;
+  double pc[CSP];
+#pragma unroll
+  for (int j = 0; j < CSP; ++j) pc[j] = P[(size_t)j * p.Ct + c];
+  int best = 0;
+  double bv = 0.0;
+  for (int k = 0; k < p.K; ++k) {
+    double d = 0.0;
+#pragma unroll
+    for (int j = 0; j < CSP; ++j) d += sd[k * CSP + j] * pc[j];
+    const double v = q[k] - 2.0 * d;
+    if (k == 0 || v < bv) {
+      bv = v;
+      best = k;
+    }
+  }
+  codes[(size_t)c * p.M + m] = (uint8_t)best;
 }
 
 __global__ __launch_bounds__(kEcThreads) void ec_finish_kernel(const double* __restrict__ D64, size_t nd,
@@ -280,7 +343,7 @@ __global__ __launch_bounds__(kEcThreads) void ec_finish_kernel(const double* __r
                                                              int nopart, double* __restrict__ objective) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nd) D[i] = (float)D64[i];
-  if (i == 0 && objective) {
+  if (i == 0 && objective) {  // once per call: a serial sum is fine here
     double s = 0.0;
     for (int b = 0; b < nopart; ++b) s += opart[b];
     *objective = s;
@@ -299,9 +362,10 @@ size_t ec_fc_workspace(int N, int Ct, int M, int K, int Csp) {
   b += (size_t)M * Csp * Csp * 8;                // G
   b += (size_t)M * K * Csp * 8;                  // D64
   b += (size_t)K * Csp * 8;                      // Dold
+  b += (size_t)K * 8;                            // q
   b += cblocks * nchunks * 8;                    // objective partials
   b += (size_t)Ct + 64;                          // codes_old
-  return b + 8 * 256;                            // alignment slack
+  return b + 16 * 256;                           // each slice is rounded up to 256 bytes
 }
 
 template <int CSP>
@@ -314,7 +378,8 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   Scratch scratch;
   hipError_t e = scratch.acquire(stream, ec_fc_workspace(N, Ct, M, K, Csp));
   auto pass = ec_pass_kernel<CSP>;
-  auto update = ec_update_kernel<CSP>;
+  auto fit = ec_fit_kernel<CSP>;
+  auto assign = ec_assign_kernel<CSP>;
   if (e != hipSuccess) return e;
   char* w = scratch.get();
   auto take = [&](size_t bytes) {
@@ -328,6 +393,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   double* G = reinterpret_cast<double*>(take((size_t)M * Csp * Csp * 8));
   double* D64 = reinterpret_cast<double*>(take((size_t)M * K * Csp * 8));
   double* Dold = reinterpret_cast<double*>(take((size_t)K * Csp * 8));
+  double* qv = reinterpret_cast<double*>(take((size_t)K * 8));
   double* opart = reinterpret_cast<double*>(take((size_t)nopart * 8));
   uint8_t* codes_old = reinterpret_cast<uint8_t*>(take((size_t)Ct));
 
@@ -343,7 +409,10 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
                        m == M - 1 ? opart : nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  const size_t upd_lds = (kMaxCsp * kMaxCsp + 256 * kMaxCsp + 256) * sizeof(double);
+  const size_t fit_lds = (kMaxCsp * kMaxCsp + 256 * kMaxCsp + kUpdThreads) * sizeof(double) + (size_t)Ct;
+  const size_t asg_lds = (size_t)K * (Csp + 1) * sizeof(double);
+  if (fit_lds > kLdsBytes) return hipErrorInvalidValue;
+  if ((e = allow_max_lds((const void*)fit)) != hipSuccess) return e;
   int step = 0;
   int ma = -1;  // subspace updated by the previous step, whose change the next pass applies
   for (int s = 0; s < sweeps; ++s) {
@@ -355,10 +424,16 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
       hipLaunchKernelGGL(ec_reduce_kernel, dim3((unsigned)ceil_div_z((size_t)Csp * Ct, kEcThreads)),
                          dim3(kEcThreads), 0, stream, part, p, m, G, D64, (const uint8_t*)codes, P);
       if ((e = hipGetLastError()) != hipSuccess) return e;
-      // objective[step] is the value before this step (after the previous one)
-      hipLaunchKernelGGL(update, dim3(1), dim3(kUpdThreads), upd_lds, stream, P, p, m, G, D64, codes,
-                         Dold, codes_old, opart, nopart, objective ? objective + step : nullptr);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
+      for (int it = 0; it < inner; ++it) {
+        // objective[step] is the value before this step (after the previous one)
+        hipLaunchKernelGGL(fit, dim3(1), dim3(kUpdThreads), fit_lds, stream, P, p, m, G, D64,
+                           (const uint8_t*)codes, it == 0 ? 1 : 0, Dold, codes_old, opart, nopart,
+                           objective ? objective + step : nullptr, qv);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(assign, dim3((unsigned)cblocks), dim3(kEcThreads), asg_lds, stream, P, p, m,
+                           (const double*)D64, (const double*)qv, codes);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+      }
       ma = m;
     }
   }

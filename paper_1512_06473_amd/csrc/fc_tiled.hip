@@ -277,7 +277,7 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(CodeStream codes, int Ct,
       const int t = tt0 + ty + 4 * rr;
       words[rr] = (t < Ct && gq < mgroups) ? *reinterpret_cast<const uint32_t*>(codes.p + (size_t)t * M + 4 * gq) : 0u;
     }
-  } else {
+  } else if (codes.bits == 8) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
       const int t = tt0 + ty + 4 * rr;
@@ -286,6 +286,28 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(CodeStream codes, int Ct,
 #pragma unroll
         for (int k = 0; k < 4; ++k)
           if (4 * gq + k < M) word |= code_at(codes, (size_t)t * M + 4 * gq + k) << (8 * k);
+      }
+      words[rr] = word;
+    }
+  } else {
+    // Packed codes: the group's (up to) 4 codes are 4 b <= 28 consecutive
+    // stream bits, read as one 64-bit window of two aligned dwords (the
+    // second only when the bits reach into it, so it is inside the stream).
+    const uint32_t* w = reinterpret_cast<const uint32_t*>(codes.p);
+    const int b = codes.bits;
+    const uint32_t mask = b ? (1u << b) - 1u : 0u;
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int t = tt0 + ty + 4 * rr;
+      uint32_t word = 0;
+      if (t < Ct && gq < mgroups && b > 0) {
+        const int n = min(4, M - 4 * gq);
+        const size_t bit = ((size_t)t * M + 4 * gq) * (size_t)b;
+        const uint32_t sh = (uint32_t)(bit & 31);
+        uint64_t win = w[bit >> 5];
+        if (sh + (uint32_t)(n * b) > 32u) win |= (uint64_t)w[(bit >> 5) + 1] << 32;
+        win >>= sh;
+        for (int k = 0; k < n; ++k) word |= (uint32_t)((win >> (k * b)) & mask) << (8 * k);
       }
       words[rr] = word;
     }

@@ -403,7 +403,7 @@ qcnn_status qcnn_ec_fc(const float* S, int N, int C_s, const float* T, int C_t, 
   if (s != QCNN_OK) return s;
   const size_t ns = elems({N, C_s}), nt = elems({N, C_t}), nd = elems({M, K, Csp}), nc = elems({C_t, M});
   if (!ns || !nt || !nd || !nc || (long long)sweeps * M > (1LL << 30)) return QCNN_ERR_SHAPE;
-  if (N > (1 << 20) || nt > ((size_t)1 << 32)) return QCNN_ERR_UNSUPPORTED;
+  if (N > (1 << 20) || C_t > 65536 || nt > ((size_t)1 << 32)) return QCNN_ERR_UNSUPPORTED;
   const size_t no = ((size_t)sweeps * M + 1) * 8;
   if (overlap(codebooks, nd * 4, S, ns * 4) || overlap(codebooks, nd * 4, T, nt * 4) ||
       overlap(codes, nc, S, ns * 4) || overlap(codes, nc, T, nt * 4) || overlap(codes, nc, codebooks, nd * 4) ||

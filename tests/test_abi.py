@@ -240,3 +240,8 @@ def test_ec_fc_rejects_bad_arguments(L):
     assert ec(D=FAKE + 16) == ALIAS                  # codebooks inside S
     assert ec(codes=FAKE2 + 4) == ALIAS              # codes inside T
     assert ec(obj=FAKE2 + 4096 + 8) == ALIAS         # objective inside the codebooks
+
+
+def test_ec_fc_rejects_too_many_outputs(L):
+    assert L.qcnn_ec_fc(FAKE, 8, 8, FAKE2, 65537, FAKE2 + (1 << 24), 2, 16, 4, FAKE2 + (1 << 25), 1, 1, None,
+                        None) == UNSUP
