@@ -191,10 +191,6 @@ qcnn_status qcnn_pq_kmeans(const float* W, int C_t, int C_s, int d_k,
                            int M, int K, int Csp, int iters,
                            float* codebooks, uint8_t* codes, double* objective, void* stream);
 
-/* Network glue between PQ layers (not part of the paper's method): max
- * pooling over k x k windows with stride s and no padding,
- *   y[n][c][yo][xo] = max_{dy,dx < k} x[n][c][yo s + dy][xo s + dx],
- * H_o = floor((H - k) / s) + 1.  x: [N][C][H][W]; y (output): [N][C][H_o][W_o]. */
 /* ---- Error-corrected quantization of a fully-connected layer (Sec. 3.3.1).
  * Minimises the response error of Eq. (8),
  *   sum_n || T_n - sum_m (D^(m) B^(m))^T S_n^(m) ||^2,
@@ -218,12 +214,16 @@ qcnn_status qcnn_pq_kmeans(const float* W, int C_t, int C_s, int d_k,
  * <= 1e-12 x max diag(G) (a direction the inputs do not span, such as a
  * channel that is zero on every image) setting that coordinate to 0;
  * assignment ties go to the lowest index.  Limits: those of the forward,
- * N <= 2^20, C_t <= 65536; codes >= K are read as K - 1 (checked with
- * QCNN_CHECK_CODES=1). */
+ * N <= 2^20, C_t <= 65536; codes >= K are read, and written back, as K - 1
+ * (checked with QCNN_CHECK_CODES=1). */
 qcnn_status qcnn_ec_fc(const float* S, int N, int C_s, const float* T, int C_t,
                        float* codebooks, int M, int K, int Csp, uint8_t* codes,
                        int sweeps, int inner, double* objective, void* stream);
 
+/* Network glue between PQ layers (not part of the paper's method): max
+ * pooling over k x k windows with stride s and no padding,
+ *   y[n][c][yo][xo] = max_{dy,dx < k} x[n][c][yo s + dy][xo s + dx],
+ * H_o = floor((H - k) / s) + 1.  x: [N][C][H][W]; y (output): [N][C][H_o][W_o]. */
 qcnn_status qcnn_maxpool2d(const float* x, int N, int C, int H, int W, int k, int s,
                            float* y, void* stream);
 

@@ -61,6 +61,8 @@ CASES = [
     (80, 32, 300, 4, 256, 1, 1, None),    # K = 256, most sub-codewords unused
     (60, 32, 40, 4, 8, 1, 2, [1, 2, 9]),  # channels zero on every image
     (300, 128, 70, 4, 32, 1, 1, None),    # more images than one pass chunk
+    (40, 48, 600, 12, 32, 2, 2, None),    # three channel blocks, C'_s > 8
+    (30, 16, 20, 4, 8, 0, 1, None),       # no sweep: the starting objective only
 ]
 
 
