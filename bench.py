@@ -175,6 +175,36 @@ def main():
         nbytes = 2 * W.nbytes + 2 * codes.numel() + 2 * D0.nbytes
         return step, nbytes, (Ct, Cs, dk, Csp, K)
 
+    def make_ec_step():
+        """One error-correction sweep over the 2304 subspaces of a 9216 -> 4096
+        layer (C's = 4, K = 32) from the k-means solution, on 256 synthetic
+        calibration images: S = |N(0,1)|, T = S W^T for W = 0.01 N(0,1).  Each
+        call restarts from the k-means codebooks and codes (a device copy)."""
+        rng = np.random.Generator(np.random.PCG64(31))
+        Nimg, Cs, Ct, Csp, K = 256, 9216, 4096, 4, 32
+        S = np.abs(rng.standard_normal((Nimg, Cs))).astype(np.float32)
+        W = (0.01 * rng.standard_normal((Ct, Cs))).astype(np.float32)
+        Sd, Td, Wd = T(S), T(S @ W.T), T(W)
+        D0 = T((0.01 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32))
+        Dk, ck, _ = api.pq_kmeans(Wd, D0, 4)
+        D, c = Dk.clone(), ck.clone()
+        torch.cuda.synchronize(dev)
+
+        def step():
+            D.copy_(Dk)
+            c.copy_(ck)
+            return api.ec_fc(Sd, Td, D, c, 1, 1)
+        # HBM bytes a sweep must move: the float64 residual read and written
+        # once per subspace step, plus the subspace's inputs
+        M = Cs // Csp
+        nbytes = M * (16.0 * Nimg * Ct + 4.0 * Nimg * Csp)
+        return step, nbytes, "fc6 9216 -> 4096, C's=4, K=32, 256 images"
+
+    if args.only == "ec_fc6":
+        step, nbytes, _ = make_ec_step()
+        ms, _ = time_steps(step, args.steps, args.warmup)
+        print(json.dumps({"only": args.only, "ms_per_step": ms, "hbm_bytes_per_step": nbytes}))
+        return
     if args.only and args.only.startswith("quant_"):
         step, nbytes, _ = make_quant_step(args.only[len("quant_"):])
         ms, _ = time_steps(step, args.steps, args.warmup)
@@ -290,40 +320,23 @@ def main():
     line["packed_codes"] = packed
 
     # -------------------------- error-corrected quantization of fc6 (Eq. (8)-(12))
-    # One sweep over the 2304 subspaces of a 9216 -> 4096 layer (C's = 4,
-    # K = 32) from the k-means solution, on 256 synthetic calibration images:
-    # S = |N(0,1)|, T = S W^T for W = 0.01 N(0,1).
     ecr = {}
     if args.configs != "none":
-        rng = np.random.Generator(np.random.PCG64(31))
-        Nimg, Cs, Ct, Csp, K = 256, 9216, 4096, 4, 32
-        S = np.abs(rng.standard_normal((Nimg, Cs))).astype(np.float32)
-        W = (0.01 * rng.standard_normal((Ct, Cs))).astype(np.float32)
-        Tn = S @ W.T
-        Sd, Td, Wd = T(S), T(Tn), T(W)
-        D0 = T((0.01 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32))
-        Dk, ck, _ = api.pq_kmeans(Wd, D0, 4)
-        torch.cuda.synchronize(dev)
+        step_ec, nbytes, meta = make_ec_step()
         times, objs = [], None
         for _ in range(3):
-            D, c = Dk.clone(), ck.clone()
-            torch.cuda.synchronize(dev)
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
-            objs = api.ec_fc(Sd, Td, D, c, 1, 1)
+            objs = step_ec()
             e1.record()
             torch.cuda.synchronize(dev)
             times.append(e0.elapsed_time(e1))
         o = objs.cpu().numpy()
-        M = Cs // Csp
-        # HBM bytes a sweep must move: the float64 residual read and written once
-        # per subspace step, plus the subspace's inputs
-        nbytes = M * (16.0 * Nimg * Ct + 4.0 * Nimg * Csp)
-        ecr = {"layer": "fc6 9216 -> 4096, C's=4, K=32, 256 images", "ms_per_sweep": min(times),
+        ecr = {"layer": meta, "ms_per_sweep": min(times),
                "hbm_bytes_per_sweep": nbytes, "hbm_frac": nbytes / (min(times) * 1e-3) / workmodel.HBM_PEAK_BPS,
                "response_error_kmeans": float(o[0]), "response_error_after_sweep": float(o[-1])}
-        del Sd, Td, Wd
+        del step_ec
     line["error_correction_fc"] = ecr
 
     # ------------------------------------------------------------ CPU baseline
