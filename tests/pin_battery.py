@@ -243,6 +243,133 @@ def ec_checks(rng, E=None):
     return out
 
 
+def _bf_patch(Sm, n, yo, xo, ky, kx, stride, pad):
+    """The input sub-vector at p_s = p_t s - pad + p_k, or 0 outside."""
+    y, x = yo * stride - pad + ky, xo * stride - pad + kx
+    if 0 <= y < Sm.shape[2] and 0 <= x < Sm.shape[3]:
+        return Sm[n, :, y, x].astype(np.float64)
+    return np.zeros(Sm.shape[1])
+
+
+def _bf_channel(Sm, Dm, codes_c, dk, stride, pad, Ho, Wo, skip=()):
+    """One channel's response of subspace m, [N][H_o][W_o], by loops: the sum
+    over kernel positions (except those in `skip`) of D_{code}^T S_{p_s}."""
+    N = Sm.shape[0]
+    out = np.zeros((N, Ho, Wo))
+    for n in range(N):
+        for yo in range(Ho):
+            for xo in range(Wo):
+                for ky in range(dk):
+                    for kx in range(dk):
+                        if ky * dk + kx not in skip:
+                            out[n, yo, xo] += Dm[codes_c[ky * dk + kx]] @ _bf_patch(Sm, n, yo, xo, ky, kx,
+                                                                                     stride, pad)
+    return out
+
+
+def ec_conv_checks(rng, E=None):
+    """Error correction for a conv layer (Sec. 3.3.2 Eq. (13), App. B Eq.
+    (14)-(21)); E is the module under test (default: the oracle's)."""
+    if E is None:
+        from oracle import ec_conv as E
+    from oracle import ec as F
+    out = []
+    # the quantized response equals the C oracle's conv forward (Eq. (7))
+    ok = True
+    for (N, Cs, H, W, Ct, dk, st, pd, Csp, K) in [(2, 6, 7, 6, 5, 3, 1, 1, 3, 4), (1, 4, 9, 8, 3, 3, 2, 2, 2, 5),
+                                                  (2, 4, 5, 5, 4, 2, 1, 0, 4, 3)]:
+        S = rng.standard_normal((N, Cs, H, W)).astype(np.float32)
+        D = rng.standard_normal((Cs // Csp, K, Csp)).astype(np.float32)
+        c = rng.integers(0, K, (Ct, dk, dk, Cs // Csp)).astype(np.uint8)
+        ok &= np.allclose(E.forward(S, D, c, st, pd), O.conv_direct(S, D, c, st, pd), rtol=1e-12, atol=1e-12)
+    out.append(("ec conv response = C oracle conv", bool(ok)))
+    # a 1x1 kernel (stride 1, no padding) is the FC case over every pixel
+    N, Cs, H, W, Ct, Csp, K = 3, 8, 3, 2, 7, 2, 4
+    M = Cs // Csp
+    S = rng.standard_normal((N, Cs, H, W))
+    T = rng.standard_normal((N, Ct, H, W))
+    D0 = rng.standard_normal((M, K, Csp))
+    c0 = rng.integers(0, K, (Ct, 1, 1, M)).astype(np.uint8)
+    D, codes, hist = E.ec_conv(S, T, D0, c0, 1, 0, sweeps=2, inner=2)
+    Df, cf, hf = F.ec_fc(S.transpose(0, 2, 3, 1).reshape(-1, Cs), T.transpose(0, 2, 3, 1).reshape(-1, Ct),
+                         D0, c0[:, 0, 0, :], sweeps=2, inner=2)
+    out.append(("ec conv 1x1 = FC over pixels: codes", np.array_equal(codes[:, 0, 0, :], cf)))
+    out.append(("ec conv 1x1 = FC over pixels: sub-codebooks", np.allclose(D, Df, rtol=1e-9, atol=1e-12)))
+    out.append(("ec conv 1x1 = FC over pixels: objective", np.allclose(hist, hf, rtol=1e-9)))
+    # one subspace: the codebook update against least squares built by loops
+    # (sub-codewords in order, each with the latest others), and the
+    # assignment update against every candidate's error for that channel
+    # (inputs with a strong per-channel mean, so that neighbouring kernel
+    # positions see correlated inputs and one position's code moves the
+    # best code of another)
+    N, Csp, H, W, Ct, dk, st, pd, K = 2, 2, 4, 5, 8, 2, 1, 1, 3
+    Sm = 0.3 * rng.standard_normal((N, Csp, H, W)) + rng.standard_normal((1, Csp, 1, 1))
+    Ho, Wo = (H + 2 * pd - dk) // st + 1, (W + 2 * pd - dk) // st + 1
+    R = rng.standard_normal((N, Ct, Ho, Wo))
+    Dm0 = rng.standard_normal((K, Csp))
+    cm = rng.integers(0, K, (Ct, dk * dk)).astype(np.uint8)
+    cm[0, :2] = 1  # a channel with two positions on one sub-codeword
+    s = E.shifted(Sm, dk, st, pd)
+    Rf = R.reshape(N, Ct, -1)
+    Dg = E.update_codebook(s, Rf, Dm0.copy(), cm)
+    Db = Dm0.copy()
+    for k in range(K):
+        rows, rhs = [], []
+        for c in range(Ct):
+            mine = [p for p in range(dk * dk) if cm[c, p] == k]
+            if not mine:
+                continue
+            Q = R[:, c] - _bf_channel(Sm, Db, cm[c], dk, st, pd, Ho, Wo, skip=mine)
+            for n in range(N):
+                for yo in range(Ho):
+                    for xo in range(Wo):
+                        rows.append(sum(_bf_patch(Sm, n, yo, xo, p // dk, p % dk, st, pd) for p in mine))
+                        rhs.append(Q[n, yo, xo])
+        if rows:
+            Db[k] = np.linalg.lstsq(np.array(rows), np.array(rhs), rcond=None)[0]
+    out.append(("ec conv codebook update = sequential least squares", np.allclose(Dg, Db, rtol=1e-9, atol=1e-12)))
+    cg = E.update_assignment(s, Rf, Dg.copy(), cm.copy())
+    cb = cm.copy()
+    for p in range(dk * dk):
+        for c in range(Ct):
+            errs = []
+            for k in range(K):
+                trial = cb[c].copy()
+                trial[p] = k
+                errs.append(np.sum((R[:, c] - _bf_channel(Sm, Dg, trial, dk, st, pd, Ho, Wo)) ** 2))
+            cb[c, p] = int(np.argmin(errs))
+    out.append(("ec conv assignment update = brute force, positions in order", np.array_equal(cg, cb)))
+    # whole descent: monotone, ends at the response error it reports
+    N, Cs, H, W, Ct, dk, st, pd, Csp, K = 2, 6, 6, 5, 5, 3, 1, 1, 3, 4
+    M = Cs // Csp
+    S = rng.standard_normal((N, Cs, H, W))
+    Wt = rng.standard_normal((Ct, Cs, dk, dk))
+    T = dense_conv(S, Wt, st, pd) + 0.1 * rng.standard_normal((N, Ct, H, W))
+    D0 = rng.standard_normal((M, K, Csp))
+    c0 = rng.integers(0, K, (Ct, dk, dk, M)).astype(np.uint8)
+    D, codes, hist = E.ec_conv(S, T, D0, c0, st, pd, sweeps=2, inner=1)
+    out.append(("ec conv objective non-increasing", bool(np.all(np.diff(hist) <= 1e-9 * hist[0]))))
+    out.append(("ec conv objective decreases", hist[-1] < 0.9 * hist[0]))
+    Y = dense_conv(S, rebuilt_conv(D, codes), st, pd)
+    out.append(("ec conv objective = response error", abs(float(np.sum((T - Y) ** 2)) - hist[-1])
+                <= 1e-9 * hist[0]))
+    # an exactly quantized layer stays exact
+    Dt = rng.standard_normal((M, K, Csp))
+    ct = rng.integers(0, K, (Ct, dk, dk, M)).astype(np.uint8)
+    Tq = dense_conv(S, rebuilt_conv(Dt, ct), st, pd)
+    D, codes, hist = E.ec_conv(S, Tq, Dt, ct, st, pd, sweeps=1, inner=1)
+    out.append(("ec conv lossless start stays lossless",
+                hist[-1] <= 1e-18 * float(np.sum(Tq ** 2)) + 1e-20 and np.array_equal(codes, ct)))
+    # an input channel that is zero everywhere: its coordinate of every
+    # updated sub-codeword is 0 (pivot rule)
+    S2 = S.copy()
+    S2[:, 1] = 0.0
+    D, codes, hist = E.ec_conv(S2, T, D0, c0, st, pd, sweeps=1, inner=1)
+    used = np.unique(codes[:, :, :, 0])
+    out.append(("ec conv dead channel gives a zero coordinate", bool(np.all(D[0][used, 1] == 0.0))))
+    return out
+
+
 def checks():
     out = []
     # hand-worked (see test_oracle.py for the arithmetic)

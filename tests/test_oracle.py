@@ -389,6 +389,17 @@ def test_ec_pins(oracle):
     assert not bad, bad
 
 
+def test_ec_conv_pins(oracle):
+    """Conv error correction (App. B): the response equals the C oracle's
+    conv; a 1x1 kernel is the FC case over pixels; the codebook update equals
+    sequential least squares built by loops; the assignment update equals
+    brute force over each channel's error, positions in order; monotone
+    objective equal to the response error; lossless start; dead channel."""
+    import pin_battery
+    bad = [name for name, ok in pin_battery.ec_conv_checks(np.random.Generator(np.random.PCG64(23))) if not ok]
+    assert not bad, bad
+
+
 def test_ec_reduces_error_of_kmeans_on_layer_responses(oracle):
     """Starting from the k-means quantizer (Eq. (4)), error correction lowers
     the response error of Eq. (8), which is what it minimises, while k-means

@@ -156,3 +156,55 @@ def test_ec_pins_catch_mutant(tmp_path, mut):
     except Exception:  # a crash is a caught mistake too
         survived = False
     assert not survived, "mutant survived: " + what
+
+
+# Mistakes planted in a copy of the conv error-correction oracle
+# (oracle/ec_conv.py, App. B); each entry is a list of replacements.
+ECC_SRC = os.path.join(ROOT, "oracle", "ec_conv.py")
+ECC_MUTANTS = [
+    ([("for p in other:", "for p in range(P):")], "Q takes out every position, its own too"),
+    ([("A = s[:, :, mine[c], :].sum(axis=2)", "A = s[:, :, np.flatnonzero(mine[c])[:1], :].sum(axis=2)")],
+     "only the first position of a channel on sub-codeword k fitted"),
+    ([("    for k in range(K):\n        mine = codes_m == k", "    Dz = Dm.copy()\n    for k in range(K):\n        mine = codes_m == k"),
+      ("Q -= s[:, :, p, :] @ Dm[codes_m[c, p]]", "Q -= s[:, :, p, :] @ Dz[codes_m[c, p]]")],
+     "codebook update not sequential (old sub-codewords in Q)"),
+    ([("if q != p:", "if True:")], "P takes out the position being assigned"),
+    ([("    for p in range(P):\n        for c in range(Ct):", "    cz = codes_m.copy()\n    for p in range(P):\n        for c in range(Ct):"),
+      ("Pp -= s[:, :, q, :] @ Dm[codes_m[c, q]]", "Pp -= s[:, :, q, :] @ Dm[cz[c, q]]")],
+     "assignment update not sequential (old codes in P)"),
+    ([("codes_m[c, p] = int(np.argmin(err))", "codes_m[c, p] = int(np.argmax(err))")], "assignment: argmax"),
+    ([("Sp[:, :, pad:pad + H, pad:pad + W] = Sm", "Sp[:, :, :H, :W] = Sm")], "padding ignored"),
+    ([("s[:, :, ky * dk + kx, :] = win", "s[:, :, kx * dk + ky, :] = win")], "kernel positions transposed"),
+    ([("R = Tf - Y + old", "R = Tf - Y")], "residual keeps the subspace's own contribution"),
+    ([("for _ in range(inner):\n        update_codebook(s, R, Dm, codes_m)\n",
+       "for _ in range(inner):\n")], "codebook never updated"),
+]
+
+
+def test_unmodified_ec_conv_passes(tmp_path):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    mod = _ec_module(open(ECC_SRC).read(), tmp_path, "ecc_orig")
+    bad = [n for n, ok in pin_battery.ec_conv_checks(np.random.Generator(np.random.PCG64(13)), mod) if not ok]
+    assert not bad, bad
+
+
+@pytest.mark.filterwarnings("ignore::RuntimeWarning")
+@pytest.mark.parametrize("mut", ECC_MUTANTS, ids=[m[1] for m in ECC_MUTANTS])
+def test_ec_conv_pins_catch_mutant(tmp_path, mut):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    reps, what = mut
+    src = open(ECC_SRC).read()
+    for old, new in reps:
+        assert old in src, old
+        src = src.replace(old, new, 1)
+    mod = _ec_module(src, tmp_path, "ecc_mut")
+    try:
+        res = pin_battery.ec_conv_checks(np.random.Generator(np.random.PCG64(13)), mod)
+        survived = all(ok for _, ok in res)
+    except Exception:  # a crash is a caught mistake too
+        survived = False
+    assert not survived, "mutant survived: " + what
