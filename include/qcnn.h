@@ -220,6 +220,40 @@ qcnn_status qcnn_ec_fc(const float* S, int N, int C_s, const float* T, int C_t,
                        float* codebooks, int M, int K, int Csp, uint8_t* codes,
                        int sweeps, int inner, double* objective, void* stream);
 
+/* ---- Error-corrected quantization of a convolutional layer (Sec. 3.3.2
+ * Eq. (13); App. B Eq. (14)-(21)).  Minimises the response error
+ *   sum_{n, p_t} || sum_{(p_k, p_s)} sum_m (D^(m) B^(m)_{p_k})^T S^(m)_{n, p_s} - T_{n, p_t} ||^2
+ * by block coordinate descent over the subspaces; for subspace m, with the
+ * residual of the others (Eq. (15)), `inner` rounds of: the sub-codewords
+ * k = 0 .. K-1 in order, each the least-squares fit of Eq. (19) to the
+ * residual without the other sub-codewords' terms (Eq. (18)); then the
+ * kernel positions in row-major order, each channel taking the sub-codeword
+ * of least error for the residual without the other positions' terms
+ * (Eq. (20)-(21)).  Each step uses the latest values of the others.
+ * Readings of the appendix's garbled indices: Eq. (18) takes out, per
+ * channel, the positions whose sub-codeword is not k, and Eq. (19) sums over
+ * the channels that have a position on k; Eq. (20) takes out every other
+ * position p'_k with its own input position p'_s.  p_s = p_t stride - pad +
+ * p_k (no flip), S = 0 outside the input.
+ * S: [N][C_s][H][W] inputs; T: [N][C_t][H_o][W_o] desired responses (fp32);
+ * codebooks [M][K][C'_s] fp32 and codes uint8 [C_t][d_k][d_k][M] (the
+ * forward's layouts): updated in place; objective (output, nullable):
+ * [1 + sweeps M] float64, the error before the first step and after every
+ * subspace step.  Arithmetic is float64 (a workspace of 8 N C_t H_o W_o
+ * bytes plus small per-subspace arrays); normal equations solved as in
+ * qcnn_ec_fc (elimination in channel order, a pivot <= 1e-12 x the largest
+ * diagonal entry dropping that coordinate); a sub-codeword that no position
+ * uses keeps its value; ties go to the lowest index.  Limits: C'_s <= 8,
+ * C_t d_k^2 <= 16384, N C_t H_o W_o <= 2^31; codes >= K are read, and
+ * written back, as K - 1 (checked with QCNN_CHECK_CODES=1).  Cost per call:
+ * M d_k^4 C'_s^2 N H_o W_o multiply-adds once for the input Gram blocks,
+ * then per subspace step two passes over the residual and a one-workgroup
+ * solve that is sequential over the K sub-codewords. */
+qcnn_status qcnn_ec_conv(const float* S, int N, int C_s, int H, int W,
+                         const float* T, int C_t, int d_k, int stride, int pad,
+                         float* codebooks, int M, int K, int Csp, uint8_t* codes,
+                         int sweeps, int inner, double* objective, void* stream);
+
 /* Network glue between PQ layers (not part of the paper's method): max
  * pooling over k x k windows with stride s and no padding,
  *   y[n][c][yo][xo] = max_{dy,dx < k} x[n][c][yo s + dy][xo s + dx],

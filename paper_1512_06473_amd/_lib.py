@@ -32,6 +32,7 @@ SIGNATURES = {
     "qcnn_pack_codes": ([P, ctypes.c_size_t, I, P, P], I),
     "qcnn_unpack_codes": ([P, ctypes.c_size_t, I, P, P], I),
     "qcnn_ec_fc": ([P, I, I, P, I, P, I, I, I, P, I, I, P, P], I),
+    "qcnn_ec_conv": ([P, I, I, I, I, P, I, I, I, I, P, I, I, I, P, I, I, P, P], I),
     "qcnn_timing_enable": ([I], I),
     "qcnn_timing_read": ([ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong)], I),
 }

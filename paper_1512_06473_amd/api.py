@@ -272,6 +272,38 @@ def ec_fc(S: torch.Tensor, T: torch.Tensor, codebooks: torch.Tensor, codes: torc
     return objective
 
 
+def ec_conv(S: torch.Tensor, T: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, stride: int = 1,
+            pad: int = 0, sweeps: int = 1, inner: int = 1,
+            objective: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Error-corrected quantization of a conv layer, Eq. (13), App. B
+    (qcnn_ec_conv).
+
+    S [N][C_s][H][W] layer inputs, T [N][C_t][H_o][W_o] desired responses
+    (fp32); codebooks [M][K][C'_s] fp32 and codes uint8 [C_t][d_k][d_k][M] are
+    updated in place.  Returns the objective history, float64 [1 + sweeps M].
+    """
+    _need(S, "S", torch.float32, 4)
+    _need(T, "T", torch.float32, 4, S.device)
+    _need(codebooks, "codebooks", torch.float32, 3, S.device)
+    _need(codes, "codes", torch.uint8, 4, S.device)
+    N, Cs, H, W = S.shape
+    Ct, dk = codes.shape[0], codes.shape[1]
+    M, K, Csp = codebooks.shape
+    Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
+    if tuple(T.shape) != (N, Ct, Ho, Wo) or tuple(codes.shape) != (Ct, dk, dk, M):
+        raise ValueError("shapes: S %s, T %s, codes %s, codebooks %s" % (tuple(S.shape), tuple(T.shape),
+                                                                          tuple(codes.shape), tuple(codebooks.shape)))
+    if objective is None:
+        objective = torch.empty(1 + sweeps * M, dtype=torch.float64, device=S.device)
+    _need(objective, "objective", torch.float64, 1, S.device)
+    if objective.numel() != 1 + sweeps * M:
+        raise ValueError("objective must have 1 + sweeps M = %d entries" % (1 + sweeps * M))
+    check(lib().qcnn_ec_conv(S.data_ptr(), N, Cs, H, W, T.data_ptr(), Ct, dk, int(stride), int(pad),
+                             codebooks.data_ptr(), M, K, Csp, codes.data_ptr(), int(sweeps), int(inner),
+                             objective.data_ptr(), _stream(S)), "qcnn_ec_conv")
+    return objective
+
+
 def maxpool2d(x: torch.Tensor, k: int = 3, s: int = 2, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """k x k / stride s max pooling, no padding (qcnn_maxpool2d): network glue."""
     _need(x, "x", torch.float32, 4)

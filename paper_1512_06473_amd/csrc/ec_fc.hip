@@ -348,49 +348,6 @@ __global__ __launch_bounds__(kEcThreads) void ec_reduce_kernel(const double* __r
   }
 }
 
-// x with G x = b by elimination in channel order without row exchanges; a
-// pivot <= 1e-12 x max diag(G) (or <= 0) drops that coordinate (x = 0).
-// A: N x N working storage of the calling lane (registers once the loops
-// are unrolled, or LDS).
-template <int N>
-__device__ __forceinline__ void solve_normal(const double* __restrict__ Gm, const double (&bin)[N], double* A,
-                                             double (&x)[N]) {
-  double y[N];
-  bool live[N];
-  double scale = 0.0;
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-#pragma unroll
-    for (int j = 0; j < N; ++j) A[i * N + j] = Gm[i * N + j];
-    y[i] = bin[i];
-    scale = fmax(scale, Gm[i * N + i]);
-  }
-#pragma unroll
-  for (int j = 0; j < N; ++j) {
-    live[j] = A[j * N + j] > 1e-12 * scale && A[j * N + j] > 0.0;
-    if (live[j]) {
-#pragma unroll
-      for (int i = j + 1; i < N; ++i) {
-        const double f = A[i * N + j] / A[j * N + j];
-#pragma unroll
-        for (int q = j; q < N; ++q) A[i * N + q] -= f * A[j * N + q];
-        y[i] -= f * y[j];
-      }
-    }
-  }
-#pragma unroll
-  for (int j = N - 1; j >= 0; --j) {
-    x[j] = 0.0;
-    if (live[j]) {
-      double s = y[j];
-#pragma unroll
-      for (int i = j + 1; i < N; ++i)
-        if (live[i]) s -= A[j * N + i] * x[i];
-      x[j] = s / A[j * N + j];
-    }
-  }
-}
-
 // Threads of the fit kernel that solve at once, and the LDS each takes for
 // its elimination (registers up to C'_s = 8).
 template <int CSP> constexpr int fit_solvers() { return CSP <= 8 ? kUpdThreads : 16; }

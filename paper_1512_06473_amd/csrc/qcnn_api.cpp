@@ -419,6 +419,38 @@ qcnn_status qcnn_ec_fc(const float* S, int N, int C_s, const float* T, int C_t, 
   return hip_status(qcnn::launch_ec_fc(N, C_s, C_t, M, K, Csp, S, T, codebooks, codes, sweeps, inner, objective, st));
 }
 
+qcnn_status qcnn_ec_conv(const float* S, int N, int C_s, int H, int W, const float* T, int C_t, int d_k,
+                         int stride, int pad, float* codebooks, int M, int K, int Csp, uint8_t* codes, int sweeps,
+                         int inner, double* objective, void* stream) {
+  if (!S || !T || !codebooks || !codes) return QCNN_ERR_NULL;
+  if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0 || sweeps < 0 || inner < 1)
+    return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(N, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  const int Ho = qcnn_out_size(H, d_k, stride, pad), Wo = qcnn_out_size(W, d_k, stride, pad);
+  if (Ho < 1 || Wo < 1) return QCNN_ERR_SHAPE;
+  const size_t ns = elems({N, C_s, H, W}), nt = elems({N, C_t, Ho, Wo}), nd = elems({M, K, Csp});
+  const size_t nc = elems({C_t, d_k, d_k, M});
+  if (!ns || !nt || !nd || !nc || (long long)sweeps * M > (1LL << 30)) return QCNN_ERR_SHAPE;
+  if (Csp > 8 || (long long)C_t * d_k * d_k > 16384 || nt > ((size_t)1 << 31) ||
+      (size_t)M * d_k * d_k * d_k * d_k * Csp * Csp > ((size_t)1 << 31))
+    return QCNN_ERR_UNSUPPORTED;
+  const size_t no = ((size_t)sweeps * M + 1) * 8;
+  if (overlap(codebooks, nd * 4, S, ns * 4) || overlap(codebooks, nd * 4, T, nt * 4) ||
+      overlap(codes, nc, S, ns * 4) || overlap(codes, nc, T, nt * 4) || overlap(codes, nc, codebooks, nd * 4) ||
+      overlap(objective, no, S, ns * 4) || overlap(objective, no, T, nt * 4) ||
+      overlap(objective, no, codebooks, nd * 4) || overlap(objective, no, codes, nc))
+    return QCNN_ERR_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  if (((uintptr_t)codes & 3) == 0) {
+    s = check_codes(qcnn::CodeStream{codes, 8}, nc, K, st);
+    if (s != QCNN_OK) return s;
+  }
+  return hip_status(qcnn::launch_ec_conv(N, C_s, H, W, C_t, d_k, stride, pad, M, K, Csp, S, T, codebooks, codes,
+                                         sweeps, inner, objective, st));
+}
+
 qcnn_status qcnn_maxpool2d(const float* x, int N, int C, int H, int W, int k, int s, float* y, void* stream) {
   if (!x || !y) return QCNN_ERR_NULL;
   if (N < 1 || C < 1 || H < 1 || W < 1 || k < 1 || s < 1) return QCNN_ERR_SHAPE;

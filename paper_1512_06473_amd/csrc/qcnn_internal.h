@@ -115,11 +115,62 @@ hipError_t launch_pq_update(int Ct, int Cs, int dk, const float* W, const uint8_
 hipError_t launch_pq_kmeans(int Ct, int Cs, int dk, const float* W, int M, int K, int Csp, int iters, float* D,
                             uint8_t* codes, double* objective, hipStream_t stream);
 
+// Error correction (Sec. 3.3), the normal equations of one sub-codeword's
+// least-squares fit: x with G x = b by elimination in channel order without
+// row exchanges; a pivot <= 1e-12 x max diag(G) (or <= 0) drops that
+// coordinate (x = 0).  A: N x N working storage of the calling lane
+// (registers once the loops are unrolled, or LDS).
+template <int N>
+__device__ __forceinline__ void solve_normal(const double* __restrict__ Gm, const double (&bin)[N], double* A,
+                                             double (&x)[N]) {
+  double y[N];
+  bool live[N];
+  double scale = 0.0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) A[i * N + j] = Gm[i * N + j];
+    y[i] = bin[i];
+    scale = fmax(scale, Gm[i * N + i]);
+  }
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    live[j] = A[j * N + j] > 1e-12 * scale && A[j * N + j] > 0.0;
+    if (live[j]) {
+#pragma unroll
+      for (int i = j + 1; i < N; ++i) {
+        const double f = A[i * N + j] / A[j * N + j];
+#pragma unroll
+        for (int q = j; q < N; ++q) A[i * N + q] -= f * A[j * N + q];
+        y[i] -= f * y[j];
+      }
+    }
+  }
+#pragma unroll
+  for (int j = N - 1; j >= 0; --j) {
+    x[j] = 0.0;
+    if (live[j]) {
+      double s = y[j];
+#pragma unroll
+      for (int i = j + 1; i < N; ++i)
+        if (live[i]) s -= A[j * N + i] * x[i];
+      x[j] = s / A[j * N + j];
+    }
+  }
+}
+
 // Error-corrected quantization of a fully-connected layer (ec_fc.hip):
 // S [N][C_s], T [N][C_t] fp32; D [M][K][C'_s] and codes [C_t][M] updated in
 // place; objective (nullable) [1 + sweeps M] float64.
 hipError_t launch_ec_fc(int N, int Cs, int Ct, int M, int K, int Csp, const float* S, const float* T, float* D,
                         uint8_t* codes, int sweeps, int inner, double* objective, hipStream_t stream);
+
+// Error-corrected quantization of a conv layer (ec_conv.hip): S [N][C_s][H][W],
+// T [N][C_t][H_o][W_o] fp32; D [M][K][C'_s] and codes [C_t][d_k][d_k][M]
+// updated in place; objective (nullable) [1 + sweeps M] float64.
+hipError_t launch_ec_conv(int N, int Cs, int H, int W, int Ct, int dk, int stride, int pad, int M, int K, int Csp,
+                          const float* S, const float* T, float* D, uint8_t* codes, int sweeps, int inner,
+                          double* objective, hipStream_t stream);
 
 // Keep freed stream-ordered allocations in the device's default pool
 // (called once per device before the first hipMallocAsync).

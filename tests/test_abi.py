@@ -245,3 +245,25 @@ def test_ec_fc_rejects_bad_arguments(L):
 def test_ec_fc_rejects_too_many_outputs(L):
     assert L.qcnn_ec_fc(FAKE, 8, 8, FAKE2, 65537, FAKE2 + (1 << 24), 2, 16, 4, FAKE2 + (1 << 25), 1, 1, None,
                         None) == UNSUP
+
+
+def test_ec_conv_rejects_bad_arguments(L):
+    def ec(**kw):
+        a = dict(S=FAKE, N=2, Cs=8, H=5, W=5, T=FAKE2, Ct=4, dk=3, stride=1, pad=1, D=FAKE2 + 4096, M=2, K=16,
+                 Csp=4, codes=FAKE2 + 8192, sweeps=1, inner=1, obj=None, stream=None)
+        a.update(kw)
+        return L.qcnn_ec_conv(a["S"], a["N"], a["Cs"], a["H"], a["W"], a["T"], a["Ct"], a["dk"], a["stride"],
+                              a["pad"], a["D"], a["M"], a["K"], a["Csp"], a["codes"], a["sweeps"], a["inner"],
+                              a["obj"], a["stream"])
+
+    assert ec(S=None) == NULL and ec(T=None) == NULL and ec(D=None) == NULL and ec(codes=None) == NULL
+    assert ec(Cs=9) == SHAPE and ec(Ct=0) == SHAPE and ec(N=0) == SHAPE and ec(H=0) == SHAPE
+    assert ec(dk=0) == SHAPE and ec(stride=0) == SHAPE and ec(pad=-1) == SHAPE
+    assert ec(dk=7, pad=0) == SHAPE                  # kernel larger than the padded input
+    assert ec(sweeps=-1) == SHAPE and ec(inner=0) == SHAPE
+    assert ec(K=0) == KR and ec(K=257) == KR
+    assert ec(M=1, Csp=16, Cs=16) == UNSUP           # C'_s > 8 on this path
+    assert ec(Ct=2000, dk=3) == UNSUP                # C_t d_k^2 > 16384
+    assert ec(D=FAKE + 16) == ALIAS                  # codebooks inside S
+    assert ec(codes=FAKE2 + 4) == ALIAS              # codes inside T
+    assert ec(obj=FAKE2 + 4096 + 8) == ALIAS         # objective inside the codebooks
