@@ -200,6 +200,38 @@ def main():
         nbytes = M * (16.0 * Nimg * Ct + 4.0 * Nimg * Csp)
         return step, nbytes, "fc6 9216 -> 4096, C's=4, K=32, 256 images"
 
+    def make_ecc_step():
+        """One error-correction sweep over the 64 subspaces of the AlexNet conv3
+        layer shape (256 -> 384, 3x3, pad 1, 13x13 maps, C's = 4, K = 128) from
+        the k-means solution, on 32 synthetic calibration images: S = |N(0,1)|,
+        T = the dense conv of S with W = 0.02 N(0,1).  Each call restarts from
+        the k-means codebooks and codes (a device copy)."""
+        rng = np.random.Generator(np.random.PCG64(37))
+        Nimg, Cs, Hs, Ct, dk, Csp, K = 32, 256, 13, 384, 3, 4, 128
+        S = np.abs(rng.standard_normal((Nimg, Cs, Hs, Hs))).astype(np.float32)
+        Wt = (0.02 * rng.standard_normal((Ct, Cs, dk, dk))).astype(np.float32)
+        Sd, Wd = T(S), T(Wt)
+        Td = torch.nn.functional.conv2d(Sd, Wd, padding=1).contiguous()
+        D0 = T((0.02 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32))
+        Dk, ck, _ = api.pq_kmeans(Wd, D0, 3)
+        D, c = Dk.clone(), ck.clone()
+        torch.cuda.synchronize(dev)
+
+        def step():
+            D.copy_(Dk)
+            c.copy_(ck)
+            return api.ec_conv(Sd, Td, D, c, 1, 1, 1, 1)
+        # HBM bytes a sweep must move: the float64 residual read twice (the
+        # correlation pass and the update pass) and written once per subspace
+        M = Cs // Csp
+        nbytes = M * 24.0 * Nimg * Ct * Hs * Hs
+        return step, nbytes, "conv3 256 -> 384, 3x3 p1, 13x13, C's=4, K=128, 32 images"
+
+    if args.only == "ec_conv3":
+        step, nbytes, _ = make_ecc_step()
+        ms, _ = time_steps(step, args.steps, args.warmup)
+        print(json.dumps({"only": args.only, "ms_per_step": ms, "hbm_bytes_per_step": nbytes}))
+        return
     if args.only == "ec_fc6":
         step, nbytes, _ = make_ec_step()
         ms, _ = time_steps(step, args.steps, args.warmup)
@@ -338,6 +370,26 @@ def main():
                "response_error_kmeans": float(o[0]), "response_error_after_sweep": float(o[-1])}
         del step_ec
     line["error_correction_fc"] = ecr
+
+    # ------------------------ error-corrected quantization of conv3 (App. B)
+    eccr = {}
+    if args.configs != "none":
+        step_ecc, nbytes, meta = make_ecc_step()
+        times, objs = [], None
+        for _ in range(3):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            objs = step_ecc()
+            e1.record()
+            torch.cuda.synchronize(dev)
+            times.append(e0.elapsed_time(e1))
+        o = objs.cpu().numpy()
+        eccr = {"layer": meta, "ms_per_sweep": min(times), "hbm_bytes_per_sweep": nbytes,
+                "hbm_frac": nbytes / (min(times) * 1e-3) / workmodel.HBM_PEAK_BPS,
+                "response_error_kmeans": float(o[0]), "response_error_after_sweep": float(o[-1])}
+        del step_ecc
+    line["error_correction_conv"] = eccr
 
     # ------------------------------------------------------------ CPU baseline
     if not args.no_cpu:

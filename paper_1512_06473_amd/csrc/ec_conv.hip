@@ -35,8 +35,11 @@
 //   ecc_corr_kernel   partial sum_{n,o} s_p E(c) per chunk of images;
 //   ecc_reduce_kernel H = the partials in chunk order + sum_p' G[p][p'] W(c, p')
 //                     (so H is taken against R = E + this subspace's terms);
-//   ecc_solve_kernel  one workgroup: `inner` rounds of the two updates, then
-//                     delta for the next apply.
+//   ecc_dupdate_kernel one workgroup: Eq. (17)-(19), the sub-codewords in
+//                     order;
+//   ecc_bupdate_kernel one wave per channel: Eq. (20)-(21), the positions in
+//                     order; after the last of `inner` rounds, delta for the
+//                     next apply.
 #include "qcnn_internal.h"
 
 namespace qcnn {
@@ -48,17 +51,6 @@ struct EccParams {
   int N, Cs, H, W, Ct, Ho, Wo, dk, stride, pad, M, K, Csp, P, O;
   int chunk, nchunks;  // images per correlation chunk, number of chunks
 };
-
-// Coordinate j of the input sub-vector of subspace m that kernel position p
-// meets at output o of image n (0 outside the input).
-__device__ __forceinline__ float ecc_s(const float* __restrict__ S, const EccParams& q, int n, int m, int j, int o,
-                                       int p) {
-  const int yo = o / q.Wo, xo = o - yo * q.Wo;
-  const int ky = p / q.dk, kx = p - ky * q.dk;
-  const int y = yo * q.stride - q.pad + ky, x = xo * q.stride - q.pad + kx;
-  if ((unsigned)y >= (unsigned)q.H || (unsigned)x >= (unsigned)q.W) return 0.f;
-  return S[(((size_t)n * q.Cs + (size_t)m * q.Csp + j) * q.H + y) * q.W + x];
-}
 
 // Fixed-order sum of one value per thread into opart[block].
 __device__ __forceinline__ void ecc_block_sum(double v, double* red, double* __restrict__ opart) {
@@ -99,10 +91,24 @@ __global__ __launch_bounds__(kCThreads) void ecc_gram_kernel(const float* __rest
   const int i = (int)(r % q.Csp);
   r /= q.Csp;
   const int p2 = (int)(r % q.P), p = (int)(r / q.P);
+  // output positions whose two input positions both lie inside the input
+  // (the others add exact zeros)
+  const int ky = p / q.dk, kx = p - ky * q.dk, ky2 = p2 / q.dk, kx2 = p2 - ky2 * q.dk;
+  const size_t HW = (size_t)q.H * q.W;
   double s = 0.0;
-  for (int n = 0; n < q.N; ++n)
-    for (int o = 0; o < q.O; ++o)
-      s += (double)ecc_s(S, q, n, m, i, o, p) * (double)ecc_s(S, q, n, m, j, o, p2);
+  for (int n = 0; n < q.N; ++n) {
+    const float* si = S + ((size_t)n * q.Cs + (size_t)m * q.Csp + i) * HW;
+    const float* sj = S + ((size_t)n * q.Cs + (size_t)m * q.Csp + j) * HW;
+    for (int yo = 0; yo < q.Ho; ++yo) {
+      const int y = yo * q.stride - q.pad + ky, y2 = yo * q.stride - q.pad + ky2;
+      if ((unsigned)y >= (unsigned)q.H || (unsigned)y2 >= (unsigned)q.H) continue;
+      for (int xo = 0; xo < q.Wo; ++xo) {
+        const int x = xo * q.stride - q.pad + kx, x2 = xo * q.stride - q.pad + kx2;
+        if ((unsigned)x >= (unsigned)q.W || (unsigned)x2 >= (unsigned)q.W) continue;
+        s += (double)si[y * q.W + x] * (double)sj[y2 * q.W + x2];
+      }
+    }
+  }
   G[i0] = s;
 }
 
@@ -123,13 +129,22 @@ __global__ __launch_bounds__(kCThreads) void ecc_start_kernel(const float* __res
     const int c = (int)((i / q.O) % q.Ct);
     const int n = (int)(i / ((size_t)q.O * q.Ct));
     e = (double)T[i];
+    const int yo = o / q.Wo, xo = o - yo * q.Wo;
+    const size_t HW = (size_t)q.H * q.W;
     for (int m = 0; m < q.M; ++m) {
       const uint8_t* km = ct + ((size_t)m * q.Ct + c) * q.P;
-      double d = 0.0;
-      for (int p = 0; p < q.P; ++p) {
-        const double* w = D64 + ((size_t)m * q.K + km[p]) * CSP;
+      const float* sn = S + ((size_t)n * q.Cs + (size_t)m * CSP) * HW;
+      double d = 0.0;  // positions outside the input add exact zeros: skipped
+      for (int ky = 0; ky < q.dk; ++ky) {
+        const int y = yo * q.stride - q.pad + ky;
+        if ((unsigned)y >= (unsigned)q.H) continue;
+        for (int kx = 0; kx < q.dk; ++kx) {
+          const int x = xo * q.stride - q.pad + kx;
+          if ((unsigned)x >= (unsigned)q.W) continue;
+          const double* w = D64 + ((size_t)m * q.K + km[ky * q.dk + kx]) * CSP;
 #pragma unroll
-        for (int j = 0; j < CSP; ++j) d += (double)ecc_s(S, q, n, m, j, o, p) * w[j];
+          for (int j = 0; j < CSP; ++j) d += (double)sn[j * HW + (size_t)y * q.W + x] * w[j];
+        }
       }
       e -= d;
     }
@@ -152,11 +167,22 @@ __global__ __launch_bounds__(kCThreads) void ecc_apply_kernel(const float* __res
     const int c = (int)((i / q.O) % q.Ct);
     const int n = (int)(i / ((size_t)q.O * q.Ct));
     e = E[i];
+    const int yo = o / q.Wo, xo = o - yo * q.Wo;
+    const size_t HW = (size_t)q.H * q.W;
+    const float* sn = S + ((size_t)n * q.Cs + (size_t)ma * CSP) * HW;
     const double* dl = delta + (size_t)c * q.P * CSP;
-    double d = 0.0;
-    for (int p = 0; p < q.P; ++p)
+    double d = 0.0;  // positions outside the input add exact zeros: skipped
+    for (int ky = 0; ky < q.dk; ++ky) {
+      const int y = yo * q.stride - q.pad + ky;
+      if ((unsigned)y >= (unsigned)q.H) continue;
+      for (int kx = 0; kx < q.dk; ++kx) {
+        const int x = xo * q.stride - q.pad + kx;
+        if ((unsigned)x >= (unsigned)q.W) continue;
+        const double* dp = dl + (ky * q.dk + kx) * CSP;
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) d += (double)ecc_s(S, q, n, ma, j, o, p) * dl[p * CSP + j];
+        for (int j = 0; j < CSP; ++j) d += (double)sn[j * HW + (size_t)y * q.W + x] * dp[j];
+      }
+    }
     e -= d;
     E[i] = e;
   }
@@ -176,12 +202,24 @@ __global__ __launch_bounds__(kCThreads) void ecc_corr_kernel(const float* __rest
   double acc[CSP];
 #pragma unroll
   for (int j = 0; j < CSP; ++j) acc[j] = 0.0;
+  const int ky = p / q.dk, kx = p - ky * q.dk;
+  const size_t HW = (size_t)q.H * q.W;
   for (int n = n0; n < n1; ++n) {
     const double* er = E + ((size_t)n * q.Ct + c) * q.O;
-    for (int o = 0; o < q.O; ++o) {
-      const double e = er[o];
+    const float* sn = S + ((size_t)n * q.Cs + (size_t)m * CSP) * HW;
+    for (int yo = 0; yo < q.Ho; ++yo) {
+      const int y = yo * q.stride - q.pad + ky;
+      if ((unsigned)y >= (unsigned)q.H) continue;  // exact zeros: skipped
+      const double* erow = er + (size_t)yo * q.Wo;
+      const float* srow = sn + (size_t)y * q.W;
+#pragma unroll 4
+      for (int xo = 0; xo < q.Wo; ++xo) {
+        const int x = xo * q.stride - q.pad + kx;
+        if ((unsigned)x >= (unsigned)q.W) continue;
+        const double e = erow[xo];
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) acc[j] += (double)ecc_s(S, q, n, m, j, o, p) * e;
+        for (int j = 0; j < CSP; ++j) acc[j] += (double)srow[j * HW + x] * e;
+      }
     }
   }
   double* dst = part + (((size_t)blockIdx.y * q.Ct + c) * q.P + p) * CSP;
@@ -226,45 +264,65 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// Doubles and bytes of the solve kernel's LDS.
-template <int CSP> size_t solve_lds_bytes(int K, int npairs) {
-  const size_t dbl = (size_t)2 * K * CSP + K + kCThreads + (size_t)kWave * (CSP + 1);
+// Bytes of the D-update kernel's LDS, with (gl) or without the Gram blocks.
+template <int CSP> size_t solve_lds_bytes(int K, int npairs, int P, bool gl) {
+  constexpr int QS = kWave / CSP;
+  const size_t dbl = (size_t)2 * K * CSP + kCThreads + (size_t)(kCThreads / kWave) * QS * CSP * (CSP + 1) +
+                     (size_t)(kCThreads / kWave) * CSP * (CSP + 1) + (gl ? (size_t)P * P * CSP * CSP : 0);
   const size_t ints = 3 * 256 + (kCThreads / kWave) * 256;
-  return dbl * 8 + ints * 4 + (size_t)npairs * 2 + (size_t)npairs * 2;
+  return dbl * 8 + ints * 4 + (size_t)npairs * 2 + (size_t)npairs;
 }
 
-// One workgroup per subspace step: the objective before the step (from the
-// apply kernel's block sums), `inner` rounds of Eq. (17)-(19) then Eq.
-// (20)-(21), and delta for the next apply.
-template <int CSP>
-__global__ __launch_bounds__(kCThreads) void ecc_solve_kernel(const double* __restrict__ H, EccParams q, int m,
-                                                            const double* __restrict__ G, double* __restrict__ D64,
-                                                            uint8_t* __restrict__ ct, double* __restrict__ delta,
-                                                            const double* __restrict__ opart, int nopart,
-                                                            double* __restrict__ objective, int inner) {
+// Eq. (17)-(19), one workgroup: the sub-codewords in order.  On the first
+// round of a step (`first`) it also records the objective before the step
+// (from the apply kernel's block sums) and keeps the subspace's sub-codebook
+// and codes as they were (Dold, cold) for delta.  At the end it stores
+// qkg[p][k] = D_k^T G[p][p] D_k for the assignment kernel.  GL: the
+// subspace's Gram blocks are staged in LDS.
+template <int CSP, bool GL>
+__global__ __launch_bounds__(kCThreads) void ecc_dupdate_kernel(const double* __restrict__ H, EccParams q, int m,
+                                                              const double* __restrict__ G, double* __restrict__ D64,
+                                                              const uint8_t* __restrict__ ct, int first,
+                                                              double* __restrict__ Dold, uint8_t* __restrict__ cold,
+                                                              double* __restrict__ qkg,
+                                                              const double* __restrict__ opart, int nopart,
+                                                              double* __restrict__ objective) {
   extern __shared__ double sh[];
+  constexpr int NW = kCThreads / kWave;
+  constexpr int QS = kWave / CSP;               // pair slots per wave
+  constexpr int NE = CSP * (CSP + 1);           // entries of [rhs | normal matrix]
   const int K = q.K, P = q.P, Ct = q.Ct, npairs = Ct * P;
   double* Ds = sh;                              // [K][C's] current sub-codewords
-  double* Do = Ds + K * CSP;                    // [K][C's] at the start of the step
-  double* qk = Do + K * CSP;                    // [K]
-  double* red = qk + K;                         // [256]
-  double* wred = red + kCThreads;               // [64][C's + 1] slot partials
-  int* cnt = reinterpret_cast<int*>(wred + kWave * (CSP + 1));  // [256]
+  double* hs = Ds + K * CSP;                    // [K][C's] sums of H over each sub-codeword's pairs
+  double* red = hs + K * CSP;                   // [256]
+  double* wred = red + kCThreads;               // [4][QS][C's][C's + 1] slot partials
+  double* wpart = wred + NW * QS * NE;          // [4][C's][C's + 1] wave partials
+  double* Gl = wpart + NW * NE;                 // [P][P][C's][C's] (GL)
+  int* cnt = reinterpret_cast<int*>(Gl + (GL ? (size_t)P * P * CSP * CSP : 0));  // [256]
   int* start = cnt + 256;                       // [256]
   int* run = start + 256;                       // [256]
   int* wcnt = run + 256;                        // [4][256]
-  uint16_t* list = reinterpret_cast<uint16_t*>(wcnt + (kCThreads / kWave) * 256);  // pairs by code
-  uint8_t* cs = reinterpret_cast<uint8_t*>(list + npairs);  // [C_t][P] codes
-  uint8_t* cso = cs + npairs;                               // [C_t][P] at the start of the step
+  uint16_t* list = reinterpret_cast<uint16_t*>(wcnt + NW * 256);  // pairs by code
+  uint8_t* cs = reinterpret_cast<uint8_t*>(list + npairs);        // [C_t][P] codes
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const double* Gm = G + (size_t)m * P * P * CSP * CSP;
+  const double* Gg = G + (size_t)m * P * P * CSP * CSP;
+  const double* Gm = GL ? Gl : Gg;
 
+  const bool obj = first && objective;
   double os = 0.0;
-  if (objective)
+  if (obj)
     for (int i = tid; i < nopart; i += kCThreads) os += opart[i];
-  for (int i = tid; i < K * CSP; i += kCThreads) Ds[i] = Do[i] = D64[(size_t)m * K * CSP + i];
-  for (int i = tid; i < npairs; i += kCThreads) cs[i] = cso[i] = ct[(size_t)m * npairs + i];
-  if (objective) {
+  for (int i = tid; i < K * CSP; i += kCThreads) {
+    Ds[i] = D64[(size_t)m * K * CSP + i];
+    if (first) Dold[i] = Ds[i];
+  }
+  for (int i = tid; i < npairs; i += kCThreads) {
+    cs[i] = ct[(size_t)m * npairs + i];
+    if (first) cold[i] = cs[i];
+  }
+  if (GL)
+    for (int i = tid; i < P * P * CSP * CSP; i += kCThreads) Gl[i] = Gg[i];
+  if (obj) {
     red[tid] = os;
     __syncthreads();
     for (int h = kCThreads / 2; h > 0; h >>= 1) {
@@ -275,10 +333,10 @@ __global__ __launch_bounds__(kCThreads) void ecc_solve_kernel(const double* __re
   }
   __syncthreads();
 
-  for (int it = 0; it < inner; ++it) {
+  {
     // ---- the (c, p) pairs sorted stably by code: list[start[k] ..]
     for (int k = tid; k < 256; k += kCThreads) cnt[k] = run[k] = 0;
-    for (int k = tid; k < (kCThreads / kWave) * 256; k += kCThreads) wcnt[k] = 0;
+    for (int k = tid; k < NW * 256; k += kCThreads) wcnt[k] = 0;
     __syncthreads();
     for (int i = tid; i < npairs; i += kCThreads) atomicAdd(&cnt[cs[i]], 1);  // counts: order-free
     __syncthreads();
@@ -311,7 +369,7 @@ __global__ __launch_bounds__(kCThreads) void ecc_solve_kernel(const double* __re
       __syncthreads();
       for (int k = tid; k < 256; k += kCThreads) {
         int add = 0;
-        for (int w = 0; w < kCThreads / kWave; ++w) {
+        for (int w = 0; w < NW; ++w) {
           add += wcnt[w * 256 + k];
           wcnt[w * 256 + k] = 0;
         }
@@ -320,126 +378,229 @@ __global__ __launch_bounds__(kCThreads) void ecc_solve_kernel(const double* __re
       __syncthreads();
     }
 
-    // ---- Eq. (17)-(19): sub-codewords in order, on wave 0.  Lane l works
-    // on row j = l % C's of the pairs slot, slot + QS, ... (slot = l / C's);
-    // the slots' sums are then added in order.
-    if (wave == 0) {
-      constexpr int QS = kWave / CSP;
+    // the H part of each sub-codeword's right-hand side (it does not depend
+    // on the sub-codewords), its pairs in list order
+    for (int e = tid; e < K * CSP; e += kCThreads) {
+      const int k = e / CSP, j = e - k * CSP;
+      const int s0 = start[k], n_k = cnt[k];
+      double v = 0.0;
+      for (int r0 = 0; r0 < n_k; r0 += 4) {
+        double h[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) h[u] = r0 + u < n_k ? H[(size_t)list[s0 + r0 + u] * CSP + j] : 0.0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (r0 + u < n_k) v += h[u];
+      }
+      hs[e] = v;
+    }
+    __syncthreads();
+
+    // ---- Eq. (17)-(19): sub-codewords in order.  Pair slot g = wave QS +
+    // lane / C's takes pairs g, g + 4 QS, ... of the sub-codeword's list;
+    // lane % C's is its row j of [rhs | normal matrix].  Slot sums are added
+    // in slot order within each wave, then the waves in order.
+    {
       const int slot = lane / CSP, j = lane - slot * CSP;
       const bool act = slot < QS;
+      const int g0 = wave * QS + slot;
       for (int k = 0; k < K; ++k) {
-        const int n_k = cnt[k];
+        const int n_k = cnt[k];  // uniform
         if (n_k == 0) continue;  // unused: keeps its value
         double rhs = 0.0, mat[CSP];
 #pragma unroll
         for (int i = 0; i < CSP; ++i) mat[i] = 0.0;
         if (act) {
-          for (int r = slot; r < n_k; r += QS) {
+          for (int r = g0; r < n_k; r += NW * QS) {
             const int pr = list[start[k] + r];
             const int c = pr / P, p = pr - c * P;
-            rhs += H[(size_t)pr * CSP + j];
-            for (int p2 = 0; p2 < P; ++p2) {
-              const int k2 = cs[c * P + p2];
-              const double* g = Gm + (((size_t)p * P + p2) * CSP + j) * CSP;  // G[p][p2][j][.]
-              if (k2 == k) {
+            const uint8_t* kc = cs + c * P;
+            const double* grow = Gm + ((size_t)p * P * CSP + j) * CSP;  // G[p][p2][j][.] at p2 * C's^2
+            constexpr int PB = CSP <= 4 ? 9 : 5;  // positions whose loads are in flight together
+            for (int p0 = 0; p0 < P; p0 += PB) {
+              int k2[PB];
 #pragma unroll
-                for (int i = 0; i < CSP; ++i) mat[i] += g[i];
-              } else {
-                double t = 0.0;
+              for (int u = 0; u < PB; ++u) k2[u] = p0 + u < P ? kc[p0 + u] : 0;
+              double gv[PB][CSP], dv[PB][CSP];
 #pragma unroll
-                for (int i = 0; i < CSP; ++i) t += g[i] * Ds[k2 * CSP + i];
-                rhs -= t;
+              for (int u = 0; u < PB; ++u)
+#pragma unroll
+                for (int i = 0; i < CSP; ++i) {
+                  gv[u][i] = p0 + u < P ? grow[(size_t)(p0 + u) * CSP * CSP + i] : 0.0;
+                  dv[u][i] = Ds[k2[u] * CSP + i];
+                }
+#pragma unroll
+              for (int u = 0; u < PB; ++u) {
+                if (p0 + u < P) {
+                  const bool on = k2[u] == k;
+                  double t = 0.0;
+#pragma unroll
+                  for (int i = 0; i < CSP; ++i) {
+                    t += gv[u][i] * dv[u][i];
+                    mat[i] += on ? gv[u][i] : 0.0;
+                  }
+                  rhs -= on ? 0.0 : t;
+                }
               }
             }
           }
-          double* w = wred + (size_t)(slot * CSP + j) * (CSP + 1);
+          double* w = wred + ((size_t)(wave * QS + slot) * CSP + j) * (CSP + 1);
           w[0] = rhs;
 #pragma unroll
           for (int i = 0; i < CSP; ++i) w[1 + i] = mat[i];
         }
         wave_sync_lds();
-        // entry e = (row j, column col) of [rhs | matrix]: the used slots in order
-        const int used = min(QS, n_k);
-        double* rb = red;        // [C's] rhs
-        double* rA = red + CSP;  // [C's][C's] normal matrix
-        for (int e = lane; e < CSP * (CSP + 1); e += kWave) {
-          double v = 0.0;
-          for (int s = 0; s < used; ++s) v += wred[(size_t)s * CSP * (CSP + 1) + e];
-          const int jr = e / (CSP + 1), col = e - jr * (CSP + 1);
-          if (col == 0)
-            rb[jr] = v;
-          else
-            rA[jr * CSP + col - 1] = v;
-        }
-        wave_sync_lds();
-        if (lane == 0) {
-          double b[CSP], x[CSP], Aw[CSP * CSP];
+        {  // this wave's slots, in order
+          const int used = max(0, min(QS, n_k - wave * QS));
+          for (int e = lane; e < NE; e += kWave) {
+            double v = 0.0;
+            for (int s0 = 0; s0 < used; s0 += 4) {
+              double w4[4];
 #pragma unroll
-          for (int r = 0; r < CSP; ++r) b[r] = rb[r];
-          solve_normal<CSP>(rA, b, Aw, x);
+              for (int u = 0; u < 4; ++u) w4[u] = s0 + u < used ? wred[(size_t)(wave * QS + s0 + u) * NE + e] : 0.0;
 #pragma unroll
-          for (int r = 0; r < CSP; ++r) Ds[k * CSP + r] = x[r];
+              for (int u = 0; u < 4; ++u)
+                if (s0 + u < used) v += w4[u];
+            }
+            wpart[wave * NE + e] = v;
+          }
         }
-        wave_sync_lds();
+        __syncthreads();
+        if (wave == 0) {
+          double* rb = red;        // [C's] rhs
+          double* rA = red + CSP;  // [C's][C's] normal matrix
+          for (int e = lane; e < NE; e += kWave) {
+            double v = 0.0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) v += wpart[w * NE + e];
+            const int jr = e / (CSP + 1), col = e - jr * (CSP + 1);
+            if (col == 0)
+              rb[jr] = v;
+            else
+              rA[jr * CSP + col - 1] = v;
+          }
+          wave_sync_lds();
+          if (lane == 0) {
+            double b[CSP], x[CSP], Aw[CSP * CSP];
+#pragma unroll
+            for (int r = 0; r < CSP; ++r) b[r] = hs[k * CSP + r] + rb[r];
+            solve_normal<CSP>(rA, b, Aw, x);
+#pragma unroll
+            for (int r = 0; r < CSP; ++r) Ds[k * CSP + r] = x[r];
+          }
+        }
+        __syncthreads();
       }
     }
-    __syncthreads();
 
-    // ---- Eq. (20)-(21): kernel positions in order, one channel per thread
-    for (int p = 0; p < P; ++p) {
-      const double* Gpp = Gm + ((size_t)p * P + p) * CSP * CSP;
-      for (int k = tid; k < K; k += kCThreads) {
-        double s = 0.0;
-#pragma unroll
-        for (int r = 0; r < CSP; ++r) {
-          double g = 0.0;
-#pragma unroll
-          for (int i = 0; i < CSP; ++i) g += Gpp[r * CSP + i] * Ds[k * CSP + i];
-          s += Ds[k * CSP + r] * g;
-        }
-        qk[k] = s;
-      }
-      __syncthreads();
-      for (int c = tid; c < Ct; c += kCThreads) {
-        double b[CSP];
-        const double* hc = H + ((size_t)c * P + p) * CSP;
-#pragma unroll
-        for (int r = 0; r < CSP; ++r) b[r] = hc[r];
-        for (int p2 = 0; p2 < P; ++p2) {
-          if (p2 == p) continue;
-          const int k2 = cs[c * P + p2];
-          const double* g = Gm + ((size_t)p * P + p2) * CSP * CSP;
-#pragma unroll
-          for (int r = 0; r < CSP; ++r) {
-            double t = 0.0;
-#pragma unroll
-            for (int i = 0; i < CSP; ++i) t += g[r * CSP + i] * Ds[k2 * CSP + i];
-            b[r] -= t;
-          }
-        }
-        int best = 0;
-        double bv = 0.0;
-        for (int k = 0; k < K; ++k) {
-          double d = 0.0;
-#pragma unroll
-          for (int r = 0; r < CSP; ++r) d += Ds[k * CSP + r] * b[r];
-          const double v = qk[k] - 2.0 * d;
-          if (k == 0 || v < bv) {
-            bv = v;
-            best = k;
-          }
-        }
-        cs[c * P + p] = (uint8_t)best;
-      }
-      __syncthreads();
-    }
   }
 
   for (int i = tid; i < K * CSP; i += kCThreads) D64[(size_t)m * K * CSP + i] = Ds[i];
-  for (int i = tid; i < npairs; i += kCThreads) {
-    ct[(size_t)m * npairs + i] = cs[i];
+  for (int e = tid; e < P * K; e += kCThreads) {  // D_k^T G[p][p] D_k
+    const int p = e / K, k = e - p * K;
+    const double* Gpp = Gm + ((size_t)p * P + p) * CSP * CSP;
+    double s2 = 0.0;
 #pragma unroll
-    for (int r = 0; r < CSP; ++r) delta[(size_t)i * CSP + r] = Ds[cs[i] * CSP + r] - Do[cso[i] * CSP + r];
+    for (int r = 0; r < CSP; ++r) {
+      double g = 0.0;
+#pragma unroll
+      for (int i = 0; i < CSP; ++i) g += Gpp[r * CSP + i] * Ds[k * CSP + i];
+      s2 += Ds[k * CSP + r] * g;
+    }
+    qkg[e] = s2;
+  }
+}
+
+// Eq. (20)-(21): one wave per output channel c, the kernel positions in
+// order.  For position p, b = H[c][p] - sum_{p' != p} G[p][p'] D_{k(c,p')}
+// (lanes take (p', row) terms; the rows are added over p' in a fixed order),
+// then lane l tries candidates l, l + 64, ... and the wave keeps the first
+// minimum of qkg[p][k] - 2 D_k^T b (ties to the lowest k).  On the last round
+// it also writes delta[c][p] = D_{k_new} - Dold_{k_old}.
+template <int CSP>
+__global__ __launch_bounds__(kCThreads) void ecc_bupdate_kernel(const double* __restrict__ H, EccParams q, int m,
+                                                              const double* __restrict__ G,
+                                                              const double* __restrict__ D64,
+                                                              const double* __restrict__ qkg,
+                                                              uint8_t* __restrict__ ct,
+                                                              const double* __restrict__ Dold,
+                                                              const uint8_t* __restrict__ cold,
+                                                              double* __restrict__ delta, int last) {
+  extern __shared__ double sb[];
+  constexpr int NW = kCThreads / kWave;
+  constexpr int QS = kWave / CSP;
+  const int K = q.K, P = q.P;
+  double* Ds = sb;                                   // [K][C's]
+  double* part = Ds + K * CSP;                       // [4][QS][C's] row partials per wave
+  double* bb = part + NW * QS * CSP;                 // [4][C's]
+  uint8_t* kc = reinterpret_cast<uint8_t*>(bb + NW * CSP);  // [4][P] this wave's codes
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  for (int i = tid; i < K * CSP; i += kCThreads) Ds[i] = D64[(size_t)m * K * CSP + i];
+  const int c = blockIdx.x * NW + wave;
+  const bool col = c < q.Ct;
+  uint8_t* kw = kc + wave * P;
+  if (col)
+    for (int p = lane; p < P; p += kWave) kw[p] = ct[((size_t)m * q.Ct + c) * P + p];
+  __syncthreads();
+  if (!col) return;  // no barriers below
+  const double* Gg = G + (size_t)m * P * P * CSP * CSP;
+  const int g = lane / CSP, j = lane - g * CSP;
+  for (int p = 0; p < P; ++p) {
+    // row j of sum_{p' != p} G[p][p'] D_{k(c,p')}: group g takes p' = g, g + QS, ...
+    double t = 0.0;
+    if (g < QS) {
+      for (int p2 = g; p2 < P; p2 += QS) {
+        if (p2 == p) continue;
+        const double* gr = Gg + (((size_t)p * P + p2) * CSP + j) * CSP;
+        const double* dk = Ds + kw[p2] * CSP;
+#pragma unroll
+        for (int i = 0; i < CSP; ++i) t += gr[i] * dk[i];
+      }
+      part[(wave * QS + g) * CSP + j] = t;
+    }
+    wave_sync_lds();
+    if (lane < CSP) {
+      double v = H[(((size_t)c * P + p) * CSP) + lane];
+      double sub = 0.0;
+      for (int g2 = 0; g2 < QS; ++g2) sub += part[(wave * QS + g2) * CSP + lane];
+      bb[wave * CSP + lane] = v - sub;
+    }
+    wave_sync_lds();
+    double b[CSP];
+#pragma unroll
+    for (int r = 0; r < CSP; ++r) b[r] = bb[wave * CSP + r];
+    // this lane's candidates, then the wave's first minimum
+    int best = -1;
+    double bv = 0.0;
+    const double* qp = qkg + (size_t)p * K;
+    for (int k = lane; k < K; k += kWave) {
+      double d = 0.0;
+#pragma unroll
+      for (int r = 0; r < CSP; ++r) d += Ds[k * CSP + r] * b[r];
+      const double v = qp[k] - 2.0 * d;
+      if (best < 0 || v < bv) {
+        bv = v;
+        best = k;
+      }
+    }
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      const double ov = __shfl_down(bv, off, kWave);
+      const int ok = __shfl_down(best, off, kWave);
+      if (ok >= 0 && (best < 0 || ov < bv || (ov == bv && ok < best))) {
+        bv = ov;
+        best = ok;
+      }
+    }
+    best = __shfl(best, 0, kWave);
+    if (lane == 0) kw[p] = (uint8_t)best;
+    wave_sync_lds();
+  }
+  for (int p = lane; p < P; p += kWave) {
+    const size_t i = (size_t)c * P + p;
+    ct[(size_t)m * q.Ct * P + i] = kw[p];
+    if (last)
+#pragma unroll
+      for (int r = 0; r < CSP; ++r) delta[i * CSP + r] = Ds[kw[p] * CSP + r] - Dold[cold[i] * CSP + r];
   }
 }
 
@@ -469,9 +630,9 @@ EccParams make_params(int N, int Cs, int H, int W, int Ct, int dk, int stride, i
   q.Ho = (H + 2 * pad - dk) / stride + 1;
   q.Wo = (W + 2 * pad - dk) / stride + 1;
   q.M = M, q.K = K, q.Csp = Csp, q.P = dk * dk, q.O = q.Ho * q.Wo;
-  // about 64 Ki correlation threads: (c, p) pairs times image chunks
+  // about 256 Ki correlation threads: (c, p) pairs times image chunks
   const int pairs = Ct * q.P;
-  const int want = std::max(1, std::min(N, 65536 / std::max(1, pairs)));
+  const int want = std::max(1, std::min(N, 262144 / std::max(1, pairs)));
   q.chunk = ceil_div(N, want);
   q.nchunks = ceil_div(N, q.chunk);
   return q;
@@ -486,17 +647,25 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
   const int npairs = q.Ct * q.P;
   const int eblocks = (int)ceil_div_z(total, kCThreads);
   const int pblocks = ceil_div(npairs, kCThreads);
-  const size_t slds = solve_lds_bytes<CSP>(q.K, npairs);
-  if (slds > kLdsBytes) return hipErrorInvalidValue;
-  auto solve = ecc_solve_kernel<CSP>;
-  hipError_t e = allow_max_lds((const void*)solve);
+  // the Gram blocks go to LDS when they fit beside the rest
+  const bool gl = solve_lds_bytes<CSP>(q.K, npairs, q.P, true) <= kLdsBytes;
+  const size_t slds = solve_lds_bytes<CSP>(q.K, npairs, q.P, gl);
+  constexpr int NW = kCThreads / kWave;
+  const size_t blds = ((size_t)q.K * CSP + NW * (kWave / CSP) * CSP + NW * CSP) * 8 + (size_t)NW * q.P;
+  if (slds > kLdsBytes || blds > kLdsBytes) return hipErrorInvalidValue;
+  auto dupdate = gl ? ecc_dupdate_kernel<CSP, true> : ecc_dupdate_kernel<CSP, false>;
+  auto bupdate = ecc_bupdate_kernel<CSP>;
+  hipError_t e = allow_max_lds((const void*)dupdate);
   if (e != hipSuccess) return e;
+  if ((e = allow_max_lds((const void*)bupdate)) != hipSuccess) return e;
   Scratch scratch;
   size_t bytes = 0;
   const size_t szE = total * 8, szPart = (size_t)q.nchunks * npairs * CSP * 8, szH = (size_t)npairs * CSP * 8;
   const size_t szG = (size_t)q.M * q.P * q.P * CSP * CSP * 8, szD = (size_t)q.M * q.K * CSP * 8;
   const size_t szDelta = (size_t)npairs * CSP * 8, szOp = (size_t)eblocks * 8, szCt = (size_t)q.M * npairs;
-  for (size_t b : {szE, szPart, szH, szG, szD, szDelta, szOp, szCt}) bytes += (b + 255) & ~(size_t)255;
+  const size_t szDold = (size_t)q.K * CSP * 8, szCold = (size_t)npairs, szQk = (size_t)q.P * q.K * 8;
+  for (size_t b : {szE, szPart, szH, szG, szD, szDelta, szOp, szCt, szDold, szCold, szQk})
+    bytes += (b + 255) & ~(size_t)255;
   if ((e = scratch.acquire(stream, bytes)) != hipSuccess) return e;
   char* w = scratch.get();
   auto take = [&](size_t b) {
@@ -512,6 +681,9 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
   double* delta = reinterpret_cast<double*>(take(szDelta));
   double* opart = reinterpret_cast<double*>(take(szOp));
   uint8_t* ct = reinterpret_cast<uint8_t*>(take(szCt));
+  double* Dold = reinterpret_cast<double*>(take(szDold));
+  uint8_t* cold = reinterpret_cast<uint8_t*>(take(szCold));
+  double* qkg = reinterpret_cast<double*>(take(szQk));
 
   const size_t ninit = std::max((size_t)q.M * q.K * CSP, (size_t)q.M * npairs);
   const unsigned iblocks = (unsigned)std::min<size_t>(8192, std::max<size_t>(1, ceil_div_z(ninit, kCThreads)));
@@ -540,10 +712,16 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
       hipLaunchKernelGGL(ecc_reduce_kernel<CSP>, dim3((unsigned)pblocks), dim3(kCThreads), 0, stream,
                          (const double*)part, q, m, (const double*)G, (const double*)D64, (const uint8_t*)ct, Hs);
       if ((e = hipGetLastError()) != hipSuccess) return e;
-      hipLaunchKernelGGL(solve, dim3(1), dim3(kCThreads), slds, stream, (const double*)Hs, q, m, (const double*)G,
-                         D64, ct, delta, (const double*)opart, eblocks, objective ? objective + nstep : nullptr,
-                         inner);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
+      for (int it = 0; it < inner; ++it) {
+        hipLaunchKernelGGL(dupdate, dim3(1), dim3(kCThreads), slds, stream, (const double*)Hs, q, m,
+                           (const double*)G, D64, (const uint8_t*)ct, it == 0 ? 1 : 0, Dold, cold, qkg,
+                           (const double*)opart, eblocks, objective ? objective + nstep : nullptr);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(bupdate, dim3((unsigned)ceil_div(q.Ct, NW)), dim3(kCThreads), blds, stream,
+                           (const double*)Hs, q, m, (const double*)G, (const double*)D64, (const double*)qkg, ct,
+                           (const double*)Dold, (const uint8_t*)cold, delta, it == inner - 1 ? 1 : 0);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+      }
       ma = m;
     }
   }
