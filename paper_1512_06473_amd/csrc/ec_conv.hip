@@ -264,6 +264,47 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// x with A x = b for the normal matrix A of Eq. (19): elimination in channel
+// order without row exchanges, one reciprocal per pivot; a pivot <= 1e-12 x
+// the largest diagonal entry (or <= 0) drops that coordinate (x = 0).  A is
+// read only; W is N x N working storage of the calling lane.
+template <int N>
+__device__ __forceinline__ void solve_rcp(const double* __restrict__ A, const double (&bin)[N], double* W,
+                                          double (&x)[N]) {
+  double y[N], inv[N];
+  bool live[N];
+  double scale = 0.0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) W[i * N + j] = A[i * N + j];
+    y[i] = bin[i];
+    scale = fmax(scale, A[i * N + i]);
+  }
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    live[j] = W[j * N + j] > 1e-12 * scale && W[j * N + j] > 0.0;
+    inv[j] = live[j] ? 1.0 / W[j * N + j] : 0.0;
+    if (live[j]) {
+#pragma unroll
+      for (int i = j + 1; i < N; ++i) {
+        const double f = W[i * N + j] * inv[j];
+#pragma unroll
+        for (int c = j; c < N; ++c) W[i * N + c] -= f * W[j * N + c];
+        y[i] -= f * y[j];
+      }
+    }
+  }
+#pragma unroll
+  for (int j = N - 1; j >= 0; --j) {
+    double s = y[j];
+#pragma unroll
+    for (int i = j + 1; i < N; ++i)
+      if (live[i]) s -= W[j * N + i] * x[i];
+    x[j] = live[j] ? s * inv[j] : 0.0;
+  }
+}
+
 // Bytes of the D-update kernel's LDS, with (gl) or without the Gram blocks.
 template <int CSP> size_t solve_lds_bytes(int K, int npairs, int P, bool gl) {
   constexpr int QS = kWave / CSP;
@@ -484,7 +525,7 @@ __global__ __launch_bounds__(kCThreads) void ecc_dupdate_kernel(const double* __
             double b[CSP], x[CSP], Aw[CSP * CSP];
 #pragma unroll
             for (int r = 0; r < CSP; ++r) b[r] = hs[k * CSP + r] + rb[r];
-            solve_normal<CSP>(rA, b, Aw, x);
+            solve_rcp<CSP>(rA, b, Aw, x);
 #pragma unroll
             for (int r = 0; r < CSP; ++r) Ds[k * CSP + r] = x[r];
           }

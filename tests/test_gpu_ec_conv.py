@@ -74,6 +74,7 @@ CASES = [
     (2, 8, 6, 6, 12, 3, 1, 1, 4, 6, 1, 2, [1, 6]),   # input channels zero everywhere
     (2, 4, 5, 5, 6, 3, 1, 1, 4, 8, 0, 1, None),      # no sweep: the starting objective only
     (1, 4, 4, 4, 600, 3, 1, 1, 4, 32, 1, 1, None),   # 5400 pairs: 22 sort chunks, 3 channel blocks
+    (1, 8, 4, 4, 200, 3, 1, 1, 8, 256, 1, 1, None),  # normal matrices too large to precompute in LDS
 ]
 
 
