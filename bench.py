@@ -227,6 +227,30 @@ def main():
         nbytes = M * 24.0 * Nimg * Ct * Hs * Hs
         return step, nbytes, "conv3 256 -> 384, 3x3 p1, 13x13, C's=4, K=128, 32 images"
 
+    def make_ecn_step():
+        """Multi-layer error correction (Sec. 3.3.3) of the AlexNet conv3 ->
+        conv4 -> conv5 stack (13x13 maps, 3x3, pad 1, ReLU; C's = 4, K = 128)
+        on 32 synthetic images: per layer, k-means on dense synthetic weights
+        W = 0.02 N(0,1), then one error-correction sweep against the original
+        stack's responses, with the quantized stack's own inputs."""
+        from paper_1512_06473_amd import quantize_net
+        rng = np.random.Generator(np.random.PCG64(41))
+        x = T(np.abs(rng.standard_normal((32, 256, 13, 13))).astype(np.float32))
+        specs = []
+        for Cs, Ct in ((256, 384), (384, 384), (384, 256)):
+            specs.append({"kind": "conv", "stride": 1, "pad": 1, "relu": True,
+                          "W": T((0.02 * rng.standard_normal((Ct, Cs, 3, 3))).astype(np.float32)),
+                          "bias": T((0.01 * rng.standard_normal(Ct)).astype(np.float32)),
+                          "D0": T((0.02 * rng.standard_normal((Cs // 4, 128, 4))).astype(np.float32))})
+        torch.cuda.synchronize(dev)
+        return (lambda: quantize_net.quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=3),
+                "AlexNet conv3-conv5 (256->384->384->256, 3x3 p1, 13x13, C's=4, K=128), 32 images")
+
+    if args.only == "ec_net":
+        step, _ = make_ecn_step()
+        ms, _ = time_steps(step, args.steps, args.warmup)
+        print(json.dumps({"only": args.only, "ms_per_step": ms}))
+        return
     if args.only == "ec_conv3":
         step, nbytes, _ = make_ecc_step()
         ms, _ = time_steps(step, args.steps, args.warmup)
@@ -390,6 +414,24 @@ def main():
                 "response_error_kmeans": float(o[0]), "response_error_after_sweep": float(o[-1])}
         del step_ecc
     line["error_correction_conv"] = eccr
+
+    # ------------------- multi-layer error correction of conv3-conv5 (Sec. 3.3.3)
+    ecnr = {}
+    if args.configs != "none":
+        step_ecn, meta = make_ecn_step()
+        times, res = [], None
+        for _ in range(2):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            res = step_ecn()
+            e1.record()
+            torch.cuda.synchronize(dev)
+            times.append(e0.elapsed_time(e1))
+        ecnr = {"network": meta, "ms_per_network": min(times),
+                "response_error_per_layer": [[float(r["objective"][0]), float(r["objective"][-1])] for r in res]}
+        del step_ecn, res
+    line["error_correction_network"] = ecnr
 
     # ------------------------------------------------------------ CPU baseline
     if not args.no_cpu:

@@ -370,6 +370,80 @@ def ec_conv_checks(rng, E=None):
     return out
 
 
+def small_network(rng, lossless=False):
+    """A conv -> pool -> conv -> FC stack with synthetic weights (and, with
+    lossless, weights that are exactly quantized by their D0 and codes)."""
+    specs = []
+    shapes = [("conv", 6, 4, 3, 1, 1, 2, 4), ("pool", 2, 2), ("conv", 8, 6, 3, 1, 1, 3, 4), ("fc", 5, 8 * 3 * 3, 1, 0, 0, 4, 4)]
+    for sh in shapes:
+        if sh[0] == "pool":
+            specs.append({"kind": "pool", "k": sh[1], "s": sh[2]})
+            continue
+        kind, Ct, Cs, dk, st, pd, Csp, K = sh
+        M = Cs // Csp
+        D0 = (0.5 * rng.standard_normal((M, K, Csp))).astype(np.float32)
+        if lossless:
+            codes = rng.integers(0, K, (Ct, dk, dk, M)).astype(np.uint8)
+            W = rebuilt_conv(D0, codes).astype(np.float32)
+        else:
+            W = (0.5 * rng.standard_normal((Ct, Cs, dk, dk))).astype(np.float32)
+        spec = {"kind": kind, "W": W if kind == "conv" else W.reshape(Ct, Cs), "D0": D0,
+                "bias": (0.1 * rng.standard_normal(Ct)).astype(np.float32), "relu": kind == "conv"}
+        if kind == "conv":
+            spec.update(stride=st, pad=pd)
+        specs.append(spec)
+    x = np.maximum(rng.standard_normal((3, 4, 6, 6)), 0).astype(np.float32)
+    return x, specs
+
+
+def ec_network_checks(rng, E=None):
+    """Multi-layer error correction (Sec. 3.3.3); E is the module under test
+    (default: the oracle's)."""
+    if E is None:
+        from oracle import ec_network as E
+    out = []
+    x, specs = small_network(rng)
+    res = E.quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=2)
+    # layer 1: S is the input and T its original linear response
+    D, codes, hist, S, T = res[0]
+    out.append(("ecn layer 1 S = input", np.array_equal(S, x)))
+    W1 = specs[0]["W"].astype(np.float64)
+    out.append(("ecn layer 1 T = W * x", np.allclose(T, dense_conv(x.astype(np.float64), W1, 1, 1), rtol=1e-6,
+                                                    atol=1e-6)))
+    # layer 2: S = max-pool of layer 1's quantized forward (C oracle), T = W2
+    # times the pooled original activations (bias, ReLU)
+    h1q = O.conv_lut(x, D.astype(np.float32), codes, 1, 1, bias=specs[0]["bias"], relu=True).astype(np.float32)
+    S2 = O.maxpool(h1q, 2, 2).astype(np.float32)
+    h1o = np.maximum(dense_conv(x.astype(np.float64), W1, 1, 1) + specs[0]["bias"][None, :, None, None], 0)
+    S2o = O.maxpool(h1o.astype(np.float32), 2, 2)
+    D2, codes2, hist2, S_2, T_2 = res[2]
+    out.append(("ecn layer 2 S = pooled quantized forward", np.array_equal(S_2, S2)))
+    out.append(("ecn layer 2 T = W2 * pooled original activations",
+                np.allclose(T_2, dense_conv(S2o.astype(np.float64), specs[2]["W"].astype(np.float64), 1, 1),
+                            rtol=1e-6, atol=1e-6)))
+    # layer 3 (FC) on the flattened quantized activations
+    h2q = O.conv_lut(S2, D2.astype(np.float32), codes2, 1, 1, bias=specs[2]["bias"], relu=True).astype(np.float32)
+    out.append(("ecn FC S = flattened quantized activations", np.array_equal(res[3][3], h2q.reshape(3, -1))))
+    out.append(("ecn objectives non-increasing",
+                all(np.all(np.diff(r[2]) <= 1e-9 * r[2][0]) for r in res if r is not None)))
+    # every layer's codes are those of error correction from k-means on W
+    D1k, c1k, _, _ = O.pq_kmeans(specs[0]["W"], specs[0]["D0"], 2)
+    from oracle import ec_conv as EC
+    Dr, cr, hr = EC.ec_conv(x, T, D1k, c1k, 1, 1, 1, 1)
+    out.append(("ecn layer 1 = k-means then conv error correction", np.array_equal(cr, codes) and
+                np.allclose(Dr, D, rtol=1e-12, atol=1e-15)))
+    # weights that their D0 quantizes exactly: every layer stays lossless and
+    # the quantized network's activations equal the original's
+    x, specs = small_network(rng, lossless=True)
+    res = E.quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=2)
+    ok = True
+    for r, spec in zip(res, specs):
+        if r is not None:
+            ok &= r[2][-1] <= 1e-12 * max(float(np.sum(r[4].astype(np.float64) ** 2)), 1e-30)
+    out.append(("ecn lossless network stays lossless", bool(ok)))
+    return out
+
+
 def checks():
     out = []
     # hand-worked (see test_oracle.py for the arithmetic)

@@ -400,6 +400,17 @@ def test_ec_conv_pins(oracle):
     assert not bad, bad
 
 
+def test_ec_network_pins(oracle):
+    """Multi-layer error correction (Sec. 3.3.3): each layer's S is the
+    quantized network's input to it and T the original network's linear
+    response, both recomputed here from the C oracle's forward and plain
+    numpy; per layer, k-means then error correction; a lossless network stays
+    lossless."""
+    import pin_battery
+    bad = [name for name, ok in pin_battery.ec_network_checks(np.random.Generator(np.random.PCG64(29))) if not ok]
+    assert not bad, bad
+
+
 def test_ec_reduces_error_of_kmeans_on_layer_responses(oracle):
     """Starting from the k-means quantizer (Eq. (4)), error correction lowers
     the response error of Eq. (8), which is what it minimises, while k-means

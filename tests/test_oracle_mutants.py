@@ -208,3 +208,47 @@ def test_ec_conv_pins_catch_mutant(tmp_path, mut):
     except Exception:  # a crash is a caught mistake too
         survived = False
     assert not survived, "mutant survived: " + what
+
+
+# Mistakes planted in a copy of the multi-layer oracle (oracle/ec_network.py).
+ECN_SRC = os.path.join(ROOT, "oracle", "ec_network.py")
+ECN_MUTANTS = [
+    ([("        lin = dense_linear(ho, spec)                              # M1", "        lin = dense_linear(hq, spec)")],
+     "T from the quantized network"),
+    ([("            S = hq\n", "            S = ho\n")], "conv S from the original network"),
+    ([("        T = lin.astype(np.float32)\n", "        T = (lin + (0.1 if spec.get('bias') is not None else 0.0)).astype(np.float32)\n")],
+     "T shifted (bias folded in)"),
+    ([("        if spec[\"relu\"]:\n            lin = np.maximum(lin, 0.0)", "        if False:\n            lin = np.maximum(lin, 0.0)")],
+     "original network without ReLU"),
+    ([("            ho = O.maxpool(ho, spec[\"k\"], spec[\"s\"]).astype(np.float32)\n", "")],
+     "original network skips the pool"),
+]
+
+
+@pytest.mark.filterwarnings("ignore::RuntimeWarning")
+@pytest.mark.parametrize("mut", ECN_MUTANTS, ids=[m[1] for m in ECN_MUTANTS])
+def test_ec_network_pins_catch_mutant(tmp_path, mut):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    reps, what = mut
+    src = open(ECN_SRC).read()
+    for old, new in reps:
+        assert old in src, old
+        src = src.replace(old, new, 1)
+    mod = _ec_module(src, tmp_path, "ecn_mut")
+    try:
+        res = pin_battery.ec_network_checks(np.random.Generator(np.random.PCG64(17)), mod)
+        survived = all(ok for _, ok in res)
+    except Exception:  # a crash is a caught mistake too
+        survived = False
+    assert not survived, "mutant survived: " + what
+
+
+def test_unmodified_ec_network_passes(tmp_path):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    mod = _ec_module(open(ECN_SRC).read(), tmp_path, "ecn_orig")
+    bad = [n for n, ok in pin_battery.ec_network_checks(np.random.Generator(np.random.PCG64(17)), mod) if not ok]
+    assert not bad, bad
