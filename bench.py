@@ -449,6 +449,53 @@ def main():
                                 "kind": "oracle",
                                 "sample": "%d full passes of the 32-image batch through the oracle's table path "
                                           "(float64, OpenMP over images), %.1f s" % (reps, el)}
+        # the error-correction oracles on bounded samples of the same layers,
+        # scaled to one sweep (their cost is linear in the subspace steps and,
+        # for the conv oracle, in the images)
+        if line.get("error_correction_fc"):
+            from oracle import ec as OE
+            rng = np.random.Generator(np.random.PCG64(31))
+            Nimg, Cs, Ct, Csp, K = 256, 9216, 4096, 4, 32
+            S = np.abs(rng.standard_normal((Nimg, Cs)))
+            W = 0.01 * rng.standard_normal((Ct, Cs))
+            Tn = S @ W.T
+            D = 0.01 * rng.standard_normal((Cs // Csp, K, Csp))
+            codes = rng.integers(0, K, (Ct, Cs // Csp)).astype(np.uint8)
+            t0 = time.perf_counter()
+            Y = OE.forward(S, D, codes)
+            t_start = time.perf_counter() - t0
+            steps = 8
+            t0 = time.perf_counter()
+            for m in range(steps):
+                Sm = S[:, m * Csp:(m + 1) * Csp]
+                old = Sm @ D[m][codes[:, m]].T
+                D[m], codes[:, m] = OE.subspace_step(Sm, Tn - Y + old, D[m], codes[:, m], 1)
+                Y = Y - old + Sm @ D[m][codes[:, m]].T
+            t_step = (time.perf_counter() - t0) / steps
+            line["error_correction_fc"]["cpu_oracle"] = {
+                "ms_per_sweep": (t_start + (Cs // Csp) * t_step) * 1e3, "kind": "oracle",
+                "sample": "the starting residual and %d of the %d subspace steps of the same layer (float64 "
+                          "numpy), scaled to the sweep" % (steps, Cs // Csp)}
+        if line.get("error_correction_conv"):
+            from oracle import ec_conv as OC
+            rng = np.random.Generator(np.random.PCG64(37))
+            Ns, Nimg, Cs, Hs, Ct, dk, Csp, K = 2, 32, 256, 13, 384, 3, 4, 128
+            S = np.abs(rng.standard_normal((Ns, Cs, Hs, Hs)))
+            Wt = 0.02 * rng.standard_normal((Ct, Cs, dk, dk))
+            D = 0.02 * rng.standard_normal((Cs // Csp, K, Csp))
+            codes = rng.integers(0, K, (Ct, dk * dk)).astype(np.uint8)
+            t0 = time.perf_counter()
+            ss = [OC.shifted(S[:, m * Csp:(m + 1) * Csp], dk, 1, 1) for m in range(Cs // Csp)]
+            Y = sum(OC.contribution(ss[m], D[m], codes) for m in range(Cs // Csp))
+            t_start = time.perf_counter() - t0
+            t0 = time.perf_counter()
+            OC.subspace_step(ss[0], Y, D[0], codes, 1)  # any residual of the right shape times the same
+            t_step = time.perf_counter() - t0
+            scale = Nimg / Ns
+            line["error_correction_conv"]["cpu_oracle"] = {
+                "ms_per_sweep": scale * (t_start + (Cs // Csp) * t_step) * 1e3, "kind": "oracle",
+                "sample": "the starting residual and one of the %d subspace steps of the same layer on %d of the "
+                          "%d images (float64 numpy), scaled to the sweep and the images" % (Cs // Csp, Ns, Nimg)}
     print(json.dumps(line))
 
 
