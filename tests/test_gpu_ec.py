@@ -134,3 +134,34 @@ def test_ec_lowers_response_error_of_kmeans(api, dev):
     Wq = np.stack([Dn[m][cn[:, m]] for m in range(Cs // Csp)], 1).reshape(Ct, Cs)
     err = float(np.sum((T.astype(np.float64) - S.astype(np.float64) @ Wq.T) ** 2))
     assert abs(err - o[-1]) <= 1e-5 * o[-1]
+
+
+def test_ec_full_size_first_steps(api, dev):
+    """The fc6 shape (9216 -> 4096, C'_s = 4, K = 32, 256 images) at full size:
+    after one GPU sweep, subspace m's sub-codebook and codes are those of its
+    own step (no later step changes them), so the oracle replays the first
+    steps exactly from the same start and the objective history's first
+    entries must agree too."""
+    from oracle import ec
+    rng = np.random.Generator(np.random.PCG64(12))
+    N, Cs, Ct, Csp, K = 256, 9216, 4096, 4, 32
+    S = np.abs(rng.standard_normal((N, Cs))).astype(np.float32)
+    W = (0.01 * rng.standard_normal((Ct, Cs))).astype(np.float32)
+    T = (S.astype(np.float64) @ W.T.astype(np.float64)).astype(np.float32)
+    D0 = (0.01 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32)
+    c0 = rng.integers(0, K, (Ct, Cs // Csp)).astype(np.uint8)
+    D, c, obj = run_gpu(api, dev, S, T, D0, c0, 1, 1)
+    S64, T64 = S.astype(np.float64), T.astype(np.float64)
+    Dr = D0.astype(np.float64)
+    cr = c0.copy()
+    Y = ec.forward(S64, Dr, cr)
+    hist = [float(np.sum((T64 - Y) ** 2))]
+    for m in range(3):
+        Sm = S64[:, m * Csp:(m + 1) * Csp]
+        old = Sm @ Dr[m][cr[:, m]].T
+        Dr[m], cr[:, m] = ec.subspace_step(Sm, T64 - Y + old, Dr[m], cr[:, m], 1)
+        Y = Y - old + Sm @ Dr[m][cr[:, m]].T
+        hist.append(float(np.sum((T64 - Y) ** 2)))
+        assert np.array_equal(c[:, m], cr[:, m]), m
+        assert np.allclose(D[m], Dr[m], rtol=1e-6, atol=1e-7 * float(np.abs(Dr[m]).max())), m
+    assert np.allclose(obj[:4], hist, rtol=1e-9), (obj[:4], hist)

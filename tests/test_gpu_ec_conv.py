@@ -138,3 +138,29 @@ def test_ec_conv_lowers_response_error_of_kmeans(api, dev):
     y = api.conv_forward(Sd, D, codes, 1, 1)
     err = float(((y.double() - Td.double()) ** 2).sum())
     assert abs(err - o[-1]) <= 1e-4 * o[-1], (err, o[-1])
+
+
+def test_ec_conv_full_size_first_step(api, dev):
+    """The AlexNet conv3 shape (256 -> 384, 3x3, pad 1, 13x13, C'_s = 4,
+    K = 128) at full layer size on 4 images: after one GPU sweep, subspace 0's
+    sub-codebook and codes are those of the first step, which the oracle
+    replays from the same start; the first objective entries agree too."""
+    from oracle import ec_conv
+    rng = np.random.Generator(np.random.PCG64(14))
+    N, Cs, H, Ct, dk, Csp, K = 4, 256, 13, 384, 3, 4, 128
+    S, T, D0, c0 = problem(rng, N, Cs, H, H, Ct, dk, 1, 1, Csp, K)
+    D, c, obj = run_gpu(api, dev, S, T, D0, c0, 1, 1, 1, 1)
+    M = Cs // Csp
+    S64, T64 = S.astype(np.float64), T.astype(np.float64).reshape(N, Ct, -1)
+    Dr = D0.astype(np.float64)
+    cm = [c0[:, :, :, m].reshape(Ct, dk * dk) for m in range(M)]
+    ss = [ec_conv.shifted(S64[:, m * Csp:(m + 1) * Csp], dk, 1, 1) for m in range(M)]
+    Y = sum(ec_conv.contribution(ss[m], Dr[m], cm[m]) for m in range(M))
+    h0 = float(np.sum((T64 - Y) ** 2))
+    old = ec_conv.contribution(ss[0], Dr[0], cm[0])
+    D1, c1 = ec_conv.subspace_step(ss[0], T64 - Y + old, Dr[0], cm[0], 1)
+    Y = Y - old + ec_conv.contribution(ss[0], D1, c1)
+    h1 = float(np.sum((T64 - Y) ** 2))
+    assert np.array_equal(c[:, :, :, 0].reshape(Ct, -1), c1)
+    assert np.allclose(D[0], D1, rtol=1e-6, atol=1e-7 * float(np.abs(D1).max()))
+    assert np.allclose(obj[:2], [h0, h1], rtol=1e-9), (obj[:2], h0, h1)
