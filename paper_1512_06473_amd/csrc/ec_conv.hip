@@ -440,7 +440,8 @@ __global__ __launch_bounds__(kCThreads) void ecc_dupdate_kernel(const double* __
     // ---- Eq. (17)-(19): sub-codewords in order.  Pair slot g = wave QS +
     // lane / C's takes pairs g, g + 4 QS, ... of the sub-codeword's list;
     // lane % C's is its row j of [rhs | normal matrix].  Slot sums are added
-    // in slot order within each wave, then the waves in order.
+    // within each wave (a fixed shuffle tree, or in slot order when C's does
+    // not divide 64), then the waves in order.
     {
       const int slot = lane / CSP, j = lane - slot * CSP;
       const bool act = slot < QS;
@@ -485,13 +486,30 @@ __global__ __launch_bounds__(kCThreads) void ecc_dupdate_kernel(const double* __
               }
             }
           }
-          double* w = wred + ((size_t)(wave * QS + slot) * CSP + j) * (CSP + 1);
-          w[0] = rhs;
+          if constexpr (QS * CSP != kWave) {
+            double* w = wred + ((size_t)(wave * QS + slot) * CSP + j) * (CSP + 1);
+            w[0] = rhs;
 #pragma unroll
-          for (int i = 0; i < CSP; ++i) w[1 + i] = mat[i];
+            for (int i = 0; i < CSP; ++i) w[1 + i] = mat[i];
+          }
         }
-        wave_sync_lds();
-        {  // this wave's slots, in order
+        if constexpr (QS * CSP == kWave) {
+          // C's divides 64: the slots' sums by a fixed shuffle tree over the
+          // lanes of one row (stride C's); slot 0 then holds the wave's sums
+          double vals[CSP + 1];
+          vals[0] = rhs;
+#pragma unroll
+          for (int i = 0; i < CSP; ++i) vals[1 + i] = mat[i];
+#pragma unroll
+          for (int off = kWave / 2; off >= CSP; off >>= 1)
+#pragma unroll
+            for (int e = 0; e <= CSP; ++e) vals[e] += __shfl_down(vals[e], off, kWave);
+          if (slot == 0)
+#pragma unroll
+            for (int e = 0; e <= CSP; ++e) wpart[wave * NE + j * (CSP + 1) + e] = vals[e];
+        } else {
+          wave_sync_lds();
+          // this wave's slots, in order
           const int used = max(0, min(QS, n_k - wave * QS));
           for (int e = lane; e < NE; e += kWave) {
             double v = 0.0;
