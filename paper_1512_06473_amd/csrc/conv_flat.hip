@@ -100,6 +100,81 @@ __device__ __forceinline__ void tap_add(float (&a)[4], const f4v& q) {
   }
 }
 
+// Kernel rows ky = s u + a (u = 0, 1, ...) of stride phase a.
+__device__ __forceinline__ int s_rows_in_kernel(const FlatParams& p, int a) {
+  return (p.dk - a + p.stride - 1) / p.stride;
+}
+
+// Gather-accumulate of Eq. (7) over one virtual subspace's table: the
+// (channel, tap) pairs of a wave form one stream of table reads, PD of them
+// kept in flight.  Per read: the code byte (a scalar), one address
+// multiply-add, one 128-bit LDS read and four adds.  LAST_ROW_AT_END: the
+// taps of the grid's last row come at the end of the stream (every channel's
+// other rows first), and the stream stops before them when that row lies past
+// the kernel (the last row group, or a stride phase with fewer rows: those
+// taps would read the zero row); only the PD reads already in flight are
+// spent on it.  The stream is unrolled by template recursion (a counted loop
+// this long exceeds the compiler's unroll limit).
+template <int ROWS, int COLS, int TW, int CW, bool LAST_ROW_AT_END>
+struct GatherStream {
+  static constexpr int TAPS = ROWS * COLS;
+  static constexpr int NS = TW * TAPS;
+  static constexpr int B = LAST_ROW_AT_END ? TW * (ROWS - 1) * COLS : NS;  // first read of the last row
+  // stream position k -> (channel, tap) index of the full tap grid
+  static constexpr int full(int k) {
+    if (k < B) {
+      constexpr int per = LAST_ROW_AT_END ? (ROWS - 1) * COLS : TAPS;
+      return (k / per) * TAPS + k % per;
+    }
+    return ((k - B) / COLS) * TAPS + (ROWS - 1) * COLS + (k - B) % COLS;
+  }
+
+  const uint32_t (&cw)[CW];
+  const uint32_t (&tapbase)[TAPS];
+  uint32_t row_bytes;
+  const char* lbase;
+  bool last_row;  // read the last row's taps
+
+  template <int KF>
+  __device__ __forceinline__ f4v read() const {
+    const uint32_t code = (cw[KF >> 2] >> (8 * (KF & 3))) & 0xffu;
+    return *reinterpret_cast<const f4v*>(lbase + __umul24(code, row_bytes) + tapbase[KF % TAPS]);
+  }
+
+  template <int K, int WG4, int PD>
+  __device__ __forceinline__ void step(float (&acc)[TW][4], f4v (&qb)[PD]) const {
+    if constexpr (K < NS) {
+      if constexpr (K == B) {
+        if (!last_row) return;  // wave-uniform
+      }
+      const f4v q = qb[K % PD];
+      if constexpr (K + PD < NS) qb[K % PD] = read<full(K + PD)>();
+      constexpr int kf = full(K), i = kf / TAPS, tap = kf % TAPS;
+      constexpr int R = ((tap / COLS) * WG4 + tap % COLS) & 3;
+      tap_add<R>(acc[i], q);
+      step<K + 1, WG4, PD>(acc, qb);
+    }
+  }
+
+  template <int K, int PD>
+  __device__ __forceinline__ void prime(f4v (&qb)[PD]) const {
+    if constexpr (K < PD && K < NS) {
+      qb[K] = read<full(K)>();
+      prime<K + 1, PD>(qb);
+    }
+  }
+};
+
+template <int ROWS, int COLS, int WG4, int TW, int PD, bool LAST_ROW_AT_END, int CW>
+__device__ __forceinline__ void gather_stream(float (&acc)[TW][4], const uint32_t (&cw)[CW],
+                                              const uint32_t (&tapbase)[ROWS * COLS], uint32_t row_bytes,
+                                              const char* lbase, bool last_row) {
+  const GatherStream<ROWS, COLS, TW, CW, LAST_ROW_AT_END> gs{cw, tapbase, row_bytes, lbase, last_row};
+  f4v qb[PD];
+  gs.template prime<0, PD>(qb);
+  gs.template step<0, WG4, PD>(acc, qb);
+}
+
 // GEN = false: one virtual subspace per subspace (stride 1, one row group),
 // so the input offsets of the table build are fixed per lane.  GEN = true:
 // stride phases and/or row groups; the offsets move with the virtual subspace.
@@ -329,26 +404,19 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     // Operands of v+1, issued after the barrier: issued before it, the burst
     // of loads held every wave at the barrier for about as long as the build.
     if (v + 1 < v1) load_operands(v + 1, av, dnext);
-    // ---- gather-accumulate, Eq. (7).  The (channel, tap) pairs of this wave
-    // form one stream of NQ table reads; PD of them are kept in flight.
-    auto tap_addr = [&](int k) -> uint32_t {
-      const uint32_t code = (cw[k >> 2] >> (8 * (k & 3))) & 0xffu;
-      return __umul24(code, row_bytes) + tapbase[k % TAPS];
-    };
+    // ---- gather-accumulate, Eq. (7), over the grid rows and columns of this
+    // virtual subspace that lie inside the kernel.
     const char* lbase = reinterpret_cast<const char*>(lut4);
-    f4v qb[PD];
-#pragma unroll
-    for (int k = 0; k < PD && k < NQ; ++k) qb[k] = *reinterpret_cast<const f4v*>(lbase + tap_addr(k));
-#pragma unroll
-    for (int k = 0; k < NQ; ++k) {
-      const f4v q = qb[k % PD];
-      if (k + PD < NQ) qb[k % PD] = *reinterpret_cast<const f4v*>(lbase + tap_addr(k + PD));
-      const int i = k / TAPS, tap = k % TAPS;
-      switch ((((tap / COLS) * WG4) + (tap % COLS)) & 3) {
-        case 0: tap_add<0>(acc[i], q); break;
-        case 1: tap_add<1>(acc[i], q); break;
-        case 2: tap_add<2>(acc[i], q); break;
-        default: tap_add<3>(acc[i], q); break;
+    // Waves whose channels all lie past C_t (a channel block wider than the
+    // layer) skip the gather: wave-uniform, they only help build the tables.
+    if (t0 < p.Ct) {
+      if constexpr (GEN) {
+        // Grid row u' is kernel row s (g ROWS + u') + a.
+        const int g = v % p.G, a = (v / p.G / p.stride) % p.stride;
+        const bool last_row = s_rows_in_kernel(p, a) - g * ROWS >= ROWS;
+        gather_stream<ROWS, COLS, WG4, TW, PD, (ROWS > 1)>(acc, cw, tapbase, row_bytes, lbase, last_row);
+      } else {
+        gather_stream<ROWS, COLS, WG4, TW, PD, false>(acc, cw, tapbase, row_bytes, lbase, true);
       }
     }
     // Stage the codebook of v+1 (its loads have had the whole gather to land).
