@@ -1,6 +1,6 @@
 """Benchmark of the PQ layer forward on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--configs cfg1,cfg3,...]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--configs small_conv_n1,alexnet_fc6_n128,...]
 
 Headline workload: the AlexNet-conv3-shaped PQ conv layer (32 x 256 x 13 x 13
 -> 384 channels, 3x3, pad 1, C'_s = 4, K = 128), synthetic seeded inputs
@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--configs", default="cfg1,cfg3,cfg4,cfg5",
+    ap.add_argument("--configs", default="small_conv_n1,alexnet_fc6_n128,vgg16_conv3_n16,alexnet_n64",
                     help="extra workloads to time besides the headline (comma list, or 'none')")
     ap.add_argument("--only", default=None, help="time only this workload and exit (profiling runs)")
     return ap.parse_args()
@@ -92,7 +92,7 @@ def main():
     def make_step(cfg):
         d = workloads.generate(cfg)
         wl = d["spec"]
-        if cfg == "cfg5":
+        if cfg == "alexnet_n64":
             net = Network(d["layers"], dev)
             x = T(d["x"])
             return (lambda: net.forward(x)), wl, d
@@ -275,14 +275,14 @@ def main():
         return
 
     # ---------------------------------------------------------------- headline
-    step, wl, data = make_step("cfg2")
+    step, wl, data = make_step("alexnet_conv3_n32")
     ms, wall_ms = time_steps(step, args.steps, args.warmup)
     kms, klaunches = kernel_ms(step, args.steps)
     w = work_of(wl)
     sec = ms * 1e-3
     images_s = wl.N / sec
     lds_achieved = w["lds"] / (kms * 1e-3)
-    traffic = measured_traffic("conv_flat", "cfg2")
+    traffic = measured_traffic("conv_flat", "alexnet_conv3_n32")
     line = {
         "metric": "images/s (AlexNet-conv3-shaped PQ conv layer; also effective dense GFLOP/s and LDS roofline %)",
         "value": images_s,
@@ -296,7 +296,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded |N(0,1)| activations, N(0,0.05^2) codebooks, uniform uint8 codes)",
-        "config": {"workload": "cfg2: PQ conv 32x256x13x13 -> 384, 3x3 s1 p1, C's=4 (M=64), K=128",
+        "config": {"workload": "alexnet_conv3_n32: PQ conv 32x256x13x13 -> 384, 3x3 s1 p1, C's=4 (M=64), K=128",
                    "global_batch": wl.N, "parallelism": "none (1 GPU)"},
         "effective_dense_gflops": w["dense_flops"] / sec / 1e9,
         "roofline": {
@@ -320,7 +320,7 @@ def main():
     extra = [] if args.configs == "none" else [c for c in args.configs.split(",") if c]
     for cfg in extra:
         st, wlc, _ = make_step(cfg)
-        steps = max(5, args.steps // (10 if cfg in ("cfg4", "cfg5") else 1))
+        steps = max(5, args.steps // (10 if cfg in ("vgg16_conv3_n16", "alexnet_n64") else 1))
         m, _ = time_steps(st, steps, max(2, args.warmup // 2))
         km, kn = kernel_ms(st, steps)
         wc = work_of(wlc)
@@ -370,9 +370,9 @@ def main():
             mp, _ = time_steps(fp, 100, 5)
             return {"code_bytes": int(L["codes"].size), "packed_bytes": int(pc.numel()),
                     "bits_per_code": api.code_bits(K), "ms_byte_codes": m8, "ms_packed_codes": mp}
-        packed["cfg2_conv3"] = packed_case("cfg2")
-        packed["cfg3_fc6"] = packed_case("cfg3")
-        packed["fc6_one_image"] = packed_case("cfg3", 1)
+        packed["alexnet_conv3_n32"] = packed_case("alexnet_conv3_n32")
+        packed["alexnet_fc6_n128"] = packed_case("alexnet_fc6_n128")
+        packed["fc6_one_image"] = packed_case("alexnet_fc6_n128", 1)
     line["packed_codes"] = packed
 
     # -------------------------- error-corrected quantization of fc6 (Eq. (8)-(12))

@@ -15,8 +15,8 @@ networks:
 * codes uniform in [0, K) as uint8, conv [C_t][d_k][d_k][M], FC [C_t][M].
 
 Generator: numpy ``Generator(PCG64(seed))``; draw order x, then for each PQ
-layer in network order its D then its codes.  The seed of workload ``cfgN``
-is N.
+layer in network order its D then its codes.  Each workload has a
+seed of its own (1 to 5, in the order of the table below).
 
 ``integer=True`` gives the exact-arithmetic variant used for bit-exact index
 checks: x in {0..7}, D in {-8..8} (integers as fp32), so every partial sum of
@@ -99,15 +99,15 @@ def _alexnet_layers() -> Tuple[Layer, ...]:
 
 
 WORKLOADS = {
-    "cfg1": Workload("cfg1", "single PQ conv 1x16x14x14 -> 32, 3x3 s1 p1, C's=4, K=16",
+    "small_conv_n1": Workload("small_conv_n1", "single PQ conv 1x16x14x14 -> 32, 3x3 s1 p1, C's=4, K=16",
                      1, (16, 14, 14), (Conv(16, 32, 3, 1, 1, 4, 16, False, 0.1),), 1),
-    "cfg2": Workload("cfg2", "AlexNet-conv3-shaped PQ conv 32x256x13x13 -> 384, 3x3 p1, C's=4, K=128",
+    "alexnet_conv3_n32": Workload("alexnet_conv3_n32", "AlexNet-conv3-shaped PQ conv 32x256x13x13 -> 384, 3x3 p1, C's=4, K=128",
                      32, (256, 13, 13), (Conv(256, 384, 3, 1, 1, 4, 128, False, 0.05),), 2),
-    "cfg3": Workload("cfg3", "fc6-shaped PQ FC 128x9216 -> 4096, C's=4, K=32",
+    "alexnet_fc6_n128": Workload("alexnet_fc6_n128", "fc6-shaped PQ FC 128x9216 -> 4096, C's=4, K=32",
                      128, (9216,), (FC(9216, 4096, 4, 32, False, 0.01),), 3),
-    "cfg4": Workload("cfg4", "VGG-16-conv3-shaped PQ conv 16x256x56x56 -> 256, 3x3 p1, C's=8, K=128",
+    "vgg16_conv3_n16": Workload("vgg16_conv3_n16", "VGG-16-conv3-shaped PQ conv 16x256x56x56 -> 256, 3x3 p1, C's=8, K=128",
                      16, (256, 56, 56), (Conv(256, 256, 3, 1, 1, 8, 128, False, 0.05),), 4),
-    "cfg5": Workload("cfg5", "AlexNet-shaped PQ forward, batch 64, 227x227, 5 conv + 3 pool + 3 FC",
+    "alexnet_n64": Workload("alexnet_n64", "AlexNet-shaped PQ forward, batch 64, 227x227, 5 conv + 3 pool + 3 FC",
                      64, (3, 227, 227), _alexnet_layers(), 5),
 }
 

@@ -152,7 +152,7 @@ def test_fc_packed_equals_byte_codes(api, dev, oracle, shape, integer):
 def test_headline_conv_packed(api, dev, oracle):
     """The AlexNet-conv3-shaped layer (K = 128, 7-bit codes): packed equals
     byte codes bit for bit, and sampled outputs match the oracle."""
-    d = wl.generate("cfg2")
+    d = wl.generate("alexnet_conv3_n32")
     L = d["layers"][0]
     xd, Dd = T(d["x"], dev), T(L["D"], dev)
     print("headline packed", flush=True)

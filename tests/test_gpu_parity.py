@@ -82,7 +82,7 @@ def sample_points(rng, N, Ct, Ho, Wo, count):
 # ------------------------------------------------------------ headline configs
 
 @pytest.mark.parametrize("integer", [False, True])
-@pytest.mark.parametrize("cfg", ["cfg1", "cfg2"])
+@pytest.mark.parametrize("cfg", ["small_conv_n1", "alexnet_conv3_n32"])
 def test_conv_config_full(api, dev, oracle, cfg, integer):
     d = wl.generate(cfg, integer=integer)
     L = d["layers"][0]
@@ -96,21 +96,21 @@ def test_conv_config_full(api, dev, oracle, cfg, integer):
 
 @pytest.mark.parametrize("integer", [False, True])
 def test_fc_config_full(api, dev, oracle, integer):
-    d = wl.generate("cfg3", integer=integer)
+    d = wl.generate("alexnet_fc6_n128", integer=integer)
     L = d["layers"][0]
     y = run_fc(api, dev, d["x"], L["D"], L["codes"])
     ref, A = oracle.fc_lut(d["x"], L["D"], L["codes"], with_bound=True)
     if integer:
-        assert_exact(y, ref, "cfg3 integer")
+        assert_exact(y, ref, "alexnet_fc6_n128 integer")
     else:
-        assert_bound(y, ref, A, "cfg3")
+        assert_bound(y, ref, A, "alexnet_fc6_n128")
 
 
 @pytest.mark.parametrize("integer", [False, True])
-def test_cfg4_sampled(api, dev, oracle, integer):
+def test_vgg16_conv3_n16_sampled(api, dev, oracle, integer):
     # Full-size VGG-conv3-shaped layer, checked on sampled outputs (the oracle
     # evaluates each one from its definition).
-    d = wl.generate("cfg4", integer=integer)
+    d = wl.generate("vgg16_conv3_n16", integer=integer)
     L = d["layers"][0]
     y = run_conv(api, dev, d["x"], L["D"], L["codes"], L["stride"], L["pad"])
     rng = np.random.Generator(np.random.PCG64(41))
@@ -118,22 +118,22 @@ def test_cfg4_sampled(api, dev, oracle, integer):
     ref, A = oracle.conv_points(d["x"], L["D"], L["codes"], pts, L["stride"], L["pad"])
     got = y[tuple(pts.T)]
     if integer:
-        assert_exact(got, ref, "cfg4 integer (sampled)")
+        assert_exact(got, ref, "vgg16_conv3_n16 integer (sampled)")
     else:
-        assert_bound(got, ref, A, "cfg4 (sampled)")
+        assert_bound(got, ref, A, "vgg16_conv3_n16 (sampled)")
 
 
-def test_cfg4_two_images_full(api, dev, oracle):
-    d = wl.generate("cfg4", N=2)
+def test_vgg16_conv3_n16_two_images_full(api, dev, oracle):
+    d = wl.generate("vgg16_conv3_n16", N=2)
     L = d["layers"][0]
     y = run_conv(api, dev, d["x"], L["D"], L["codes"], 1, 1)
     ref, A = oracle.conv_lut(d["x"], L["D"], L["codes"], 1, 1, with_bound=True)
-    assert_bound(y, ref, A, "cfg4 N=2")
+    assert_bound(y, ref, A, "vgg16_conv3_n16 N=2")
 
 
-def test_cfg5_per_layer_and_end_to_end(api, dev, oracle):
+def test_alexnet_n64_per_layer_and_end_to_end(api, dev, oracle):
     from paper_1512_06473_amd.network import Network
-    d = wl.generate("cfg5")
+    d = wl.generate("alexnet_n64")
     net = Network(d["layers"], dev)
     keep = []
     out = net.forward(T(d["x"], dev), keep)
@@ -143,7 +143,7 @@ def test_cfg5_per_layer_and_end_to_end(api, dev, oracle):
     # Per layer: the oracle gets the GPU's own fp32 input of that layer.
     for i, spec in enumerate(d["layers"]):
         hin, hout = acts[i], acts[i + 1]
-        what = "cfg5 layer %d (%s)" % (i, spec["kind"])
+        what = "alexnet_n64 layer %d (%s)" % (i, spec["kind"])
         if spec["kind"] == "pool":
             assert_exact(hout, oracle.maxpool(hin, spec["k"], spec["s"]), what)
         elif spec["kind"] == "conv":
@@ -162,7 +162,7 @@ def test_cfg5_per_layer_and_end_to_end(api, dev, oracle):
     xs = d["x"][:2]
     ref = oracle.network(xs, d["layers"])
     A = oracle.network(xs, d["layers"], absolute=True)
-    assert_bound(out.cpu().numpy()[:2], ref, A, "cfg5 end to end")
+    assert_bound(out.cpu().numpy()[:2], ref, A, "alexnet_n64 end to end")
 
 
 # ----------------------------------------------------------------- table export
@@ -277,7 +277,7 @@ def test_maxpool(api, dev, oracle, shape):
 # ------------------------------------------------------------------ semantics
 
 def test_side_stream_and_determinism(api, dev, oracle):
-    d = wl.generate("cfg3", N=64)
+    d = wl.generate("alexnet_fc6_n128", N=64)
     L = d["layers"][0]
     x, D, c = T(d["x"], dev), T(L["D"], dev), T(L["codes"], dev)
     s = torch.cuda.Stream(dev)

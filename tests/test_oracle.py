@@ -313,8 +313,8 @@ def test_errors(oracle):
 
 
 def test_workload_generator_is_deterministic():
-    a = wl.generate("cfg1")
-    b = wl.generate("cfg1")
+    a = wl.generate("small_conv_n1")
+    b = wl.generate("small_conv_n1")
     assert np.array_equal(a["x"], b["x"])
     assert np.array_equal(a["layers"][0]["codes"], b["layers"][0]["codes"])
     assert a["x"].dtype == np.float32 and a["x"].min() >= 0

@@ -118,13 +118,13 @@ def test_valid_taps_brute_force():
 
 def test_workload_counts():
     # Figures quoted for the five workloads: valid gathers and table entries.
-    w2 = wm.workload_work(wl.WORKLOADS["cfg2"])[0][1]
+    w2 = wm.workload_work(wl.WORKLOADS["alexnet_conv3_n32"])[0][1]
     assert w2.gathers == 32 * 384 * 64 * (13 * 13 * 9 - 4 * 13 * 3 + 4)
     assert w2.lut_entries == 32 * 169 * 64 * 128
-    w3 = wm.workload_work(wl.WORKLOADS["cfg3"])[0][1]
+    w3 = wm.workload_work(wl.WORKLOADS["alexnet_fc6_n128"])[0][1]
     assert w3.gathers == 128 * 4096 * 2304
     assert w3.dense_macs == 128 * 9216 * 4096
-    w5 = wm.workload_work(wl.WORKLOADS["cfg5"])
+    w5 = wm.workload_work(wl.WORKLOADS["alexnet_n64"])
     kinds = [k for k, _ in w5]
     assert kinds == ["conv", "pool", "conv", "pool", "conv", "conv", "conv", "pool", "fc", "fc", "fc"]
     # conv1 gathers: 55x55 outputs, all 11x11 taps valid (227 = 54*4 + 11), M = 1.
