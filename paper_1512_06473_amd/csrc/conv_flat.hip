@@ -114,8 +114,14 @@ __device__ __forceinline__ int s_rows_in_kernel(const FlatParams& p, int a) {
 // the kernel (the last row group, or a stride phase with fewer rows: those
 // taps would read the zero row); only the PD reads already in flight are
 // spent on it.  The stream is unrolled by template recursion (a counted loop
-// this long exceeds the compiler's unroll limit).
-template <int ROWS, int COLS, int TW, int CW, bool LAST_ROW_AT_END>
+// this long exceeds the compiler's unroll limit).  PRIO: a
+// wave issues the first half of its stream at raised priority and the rest
+// at the base level, so that waves ahead of the others yield the SIMD to the
+// ones behind and the waves of a workgroup finish their gathers closer
+// together (the last ones alone do not keep the LDS busy).  Only for a
+// workgroup that has its CU to itself: beside a second workgroup, the
+// priority starves that one's table build.
+template <int ROWS, int COLS, int TW, int CW, bool LAST_ROW_AT_END, bool PRIO>
 struct GatherStream {
   static constexpr int TAPS = ROWS * COLS;
   static constexpr int NS = TW * TAPS;
@@ -144,6 +150,8 @@ struct GatherStream {
   template <int K, int WG4, int PD>
   __device__ __forceinline__ void step(float (&acc)[TW][4], f4v (&qb)[PD]) const {
     if constexpr (K < NS) {
+      if constexpr (PRIO && K == 0) __builtin_amdgcn_s_setprio(1);
+      if constexpr (PRIO && K == NS / 2) __builtin_amdgcn_s_setprio(0);
       if constexpr (K == B) {
         if (!last_row) return;  // wave-uniform
       }
@@ -165,11 +173,11 @@ struct GatherStream {
   }
 };
 
-template <int ROWS, int COLS, int WG4, int TW, int PD, bool LAST_ROW_AT_END, int CW>
+template <int ROWS, int COLS, int WG4, int TW, int PD, bool LAST_ROW_AT_END, bool PRIO, int CW>
 __device__ __forceinline__ void gather_stream(float (&acc)[TW][4], const uint32_t (&cw)[CW],
                                               const uint32_t (&tapbase)[ROWS * COLS], uint32_t row_bytes,
                                               const char* lbase, bool last_row) {
-  const GatherStream<ROWS, COLS, TW, CW, LAST_ROW_AT_END> gs{cw, tapbase, row_bytes, lbase, last_row};
+  const GatherStream<ROWS, COLS, TW, CW, LAST_ROW_AT_END, PRIO> gs{cw, tapbase, row_bytes, lbase, last_row};
   f4v qb[PD];
   gs.template prime<0, PD>(qb);
   gs.template step<0, WG4, PD>(acc, qb);
@@ -178,7 +186,7 @@ __device__ __forceinline__ void gather_stream(float (&acc)[TW][4], const uint32_
 // GEN = false: one virtual subspace per subspace (stride 1, one row group),
 // so the input offsets of the table build are fixed per lane.  GEN = true:
 // stride phases and/or row groups; the offsets move with the virtual subspace.
-template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
+template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN, bool PRIO>
 __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __restrict__ x,
                                                                  const float* __restrict__ D,
                                                                  const uint8_t* __restrict__ codes8,
@@ -414,9 +422,10 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         // Grid row u' is kernel row s (g ROWS + u') + a.
         const int g = v % p.G, a = (v / p.G / p.stride) % p.stride;
         const bool last_row = s_rows_in_kernel(p, a) - g * ROWS >= ROWS;
-        gather_stream<ROWS, COLS, WG4, TW, PD, (ROWS > 1)>(acc, cw, tapbase, row_bytes, lbase, last_row);
+        // (no priority steps here: with the early stop they made the compiler spill)
+        gather_stream<ROWS, COLS, WG4, TW, PD, (ROWS > 1), false>(acc, cw, tapbase, row_bytes, lbase, last_row);
       } else {
-        gather_stream<ROWS, COLS, WG4, TW, PD, false>(acc, cw, tapbase, row_bytes, lbase, true);
+        gather_stream<ROWS, COLS, WG4, TW, PD, false, PRIO>(acc, cw, tapbase, row_bytes, lbase, true);
       }
     }
     // Stage the codebook of v+1 (its loads have had the whole gather to land).
@@ -544,6 +553,7 @@ struct FlatPlan {
   bool gen;        // offsets move with the virtual subspace
   int TW;
   size_t lds;
+  bool prio;  // one workgroup per CU: the plain-grid kernels step their waves' issue priority
 };
 
 // Estimated cost (arbitrary units ~ CU clocks) of a plan, for the choice of
@@ -659,14 +669,23 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
   return found;
 }
 
-template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
-hipError_t launch_main(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
-                       float* y, float* partial, hipStream_t stream) {
-  auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN>;
+template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN, bool PRIO>
+hipError_t launch_kernel(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8,
+                         const float* bias, float* y, float* partial, hipStream_t stream) {
+  auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN, PRIO>;
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes8, bias, y, partial, pl.p);
   return hipGetLastError();
+}
+
+template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
+hipError_t launch_main(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
+                       float* y, float* partial, hipStream_t stream) {
+  if constexpr (!GEN) {
+    if (pl.prio) return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, true>(pl, x, D, codes8, bias, y, partial, stream);
+  }
+  return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, false>(pl, x, D, codes8, bias, y, partial, stream);
 }
 
 struct LaunchArgs {
@@ -730,6 +749,7 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
   FlatPlan pl;
   if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;
   pl.p.relu = relu;
+  pl.prio = pl.lds > kLdsBytes / 2;  // no second workgroup fits beside this one
   static const bool trace = getenv("QCNN_TRACE_PLAN") && *getenv("QCNN_TRACE_PLAN") == '1';
   if (trace)
     fprintf(stderr, "qcnn conv_flat: taps %dx%d%s G=%d V=%d S=%d sw=%d Wg=%d Hg=%d tiles=%d TW=%d tc=%d tblocks=%d "
