@@ -115,8 +115,9 @@ __device__ __forceinline__ int s_rows_in_kernel(const FlatParams& p, int a) {
 // taps would read the zero row); only the PD reads already in flight are
 // spent on it.  The stream is unrolled by template recursion (a counted loop
 // this long exceeds the compiler's unroll limit).  PRIO: a
-// wave issues the first half of its stream at raised priority and the rest
-// at the base level, so that waves ahead of the others yield the SIMD to the
+// wave issues the first three quarters of its stream at raised priority and
+// the rest at the base level (a drop at 1/3 or 5/6 was slower, at 1/2 or 2/3
+// up to 1 % slower), so that waves ahead of the others yield the SIMD to the
 // ones behind and the waves of a workgroup finish their gathers closer
 // together (the last ones alone do not keep the LDS busy).  Only for a
 // workgroup that has its CU to itself: beside a second workgroup, the
@@ -151,7 +152,7 @@ struct GatherStream {
   __device__ __forceinline__ void step(float (&acc)[TW][4], f4v (&qb)[PD]) const {
     if constexpr (K < NS) {
       if constexpr (PRIO && K == 0) __builtin_amdgcn_s_setprio(1);
-      if constexpr (PRIO && K == NS / 2) __builtin_amdgcn_s_setprio(0);
+      if constexpr (PRIO && K == (3 * NS) / 4) __builtin_amdgcn_s_setprio(0);
       if constexpr (K == B) {
         if (!last_row) return;  // wave-uniform
       }
