@@ -71,8 +71,8 @@ def measured_traffic(kernel: str, workload: str):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the PQ forward shards over images with no exchange, and this "
-              "build runs on a single MI355X; --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU: the PQ forward shards over images with no exchange, so one "
+              "MI355X's share is the whole measurement; --gpus %d is not supported" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
