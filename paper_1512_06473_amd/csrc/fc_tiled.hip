@@ -271,18 +271,21 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(CodeStream codes, int Ct,
   // does the caller's array) and a dword holds the 4 codes of a group.
   const bool aligned = codes.bits == 8 && (M & 3) == 0;
   const int gq = gq0 + tx;
+  // Groups past the last subspace (mgroups rounds M up to whole phases) hold
+  // no code: nothing of the caller's array is read for them.
+  const bool has_codes = gq < mgroups && 4 * gq < M;
   if (aligned) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
       const int t = tt0 + ty + 4 * rr;
-      words[rr] = (t < Ct && gq < mgroups) ? *reinterpret_cast<const uint32_t*>(codes.p + (size_t)t * M + 4 * gq) : 0u;
+      words[rr] = (t < Ct && has_codes) ? *reinterpret_cast<const uint32_t*>(codes.p + (size_t)t * M + 4 * gq) : 0u;
     }
   } else if (codes.bits == 8) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
       const int t = tt0 + ty + 4 * rr;
       uint32_t word = 0;
-      if (t < Ct && gq < mgroups) {
+      if (t < Ct && has_codes) {
 #pragma unroll
         for (int k = 0; k < 4; ++k)
           if (4 * gq + k < M) word |= code_at(codes, (size_t)t * M + 4 * gq + k) << (8 * k);
@@ -300,8 +303,8 @@ __global__ __launch_bounds__(256) void fc_codes_kernel(CodeStream codes, int Ct,
     for (int rr = 0; rr < 16; ++rr) {
       const int t = tt0 + ty + 4 * rr;
       uint32_t word = 0;
-      if (t < Ct && gq < mgroups && b > 0) {
-        const int n = min(4, M - 4 * gq);
+      if (t < Ct && has_codes && b > 0) {
+        const int n = min(4, M - 4 * gq);  // >= 1 here
         const size_t bit = ((size_t)t * M + 4 * gq) * (size_t)b;
         const uint32_t sh = (uint32_t)(bit & 31);
         uint64_t win = w[bit >> 5];
