@@ -48,22 +48,42 @@ def dense_linear(h, spec):
     return y
 
 
-def quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=4):
-    """Returns, per spec, None for a pool or (D float64, codes, objective
-    history, S, T) for a PQ layer."""
-    hq = np.asarray(x, np.float32)
+def original_responses(x, specs):
+    """The desired responses T of every PQ layer (None for a pool): the
+    original network run on x, T = W * S_orig in float64 rounded to fp32
+    (M1, M2); the next layer sees bias + ReLU of the float64 response,
+    rounded to fp32, or the pool of the fp32 activations (M3)."""
     ho = np.asarray(x, np.float32)
     out = []
     for spec in specs:
         if spec["kind"] == "pool":
-            hq = O.maxpool(hq, spec["k"], spec["s"]).astype(np.float32)
             ho = O.maxpool(ho, spec["k"], spec["s"]).astype(np.float32)
             out.append(None)
             continue
         lin = dense_linear(ho, spec)                              # M1
-        T = lin.astype(np.float32)
+        out.append(lin.astype(np.float32))
+        bias = spec.get("bias")
+        if bias is not None:
+            b = np.asarray(bias, np.float64)
+            lin = lin + (b[None, :, None, None] if spec["kind"] == "conv" else b[None, :])
+        if spec["relu"]:
+            lin = np.maximum(lin, 0.0)
+        ho = lin.astype(np.float32)
+    return out
+
+
+def quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=4):
+    """Returns, per spec, None for a pool or (D float64, codes, objective
+    history, S, T) for a PQ layer."""
+    hq = np.asarray(x, np.float32)
+    out = []
+    for spec, T in zip(specs, original_responses(x, specs)):
+        if spec["kind"] == "pool":
+            hq = O.maxpool(hq, spec["k"], spec["s"]).astype(np.float32)
+            out.append(None)
+            continue
         W = np.asarray(spec["W"], np.float32)
-        D, codes, _, _ = O.pq_kmeans(W, np.asarray(spec["D0"], np.float32), kmeans_iters)
+        D, codes, _ = O.pq_kmeans(W, np.asarray(spec["D0"], np.float32), kmeans_iters)
         bias = spec.get("bias")
         if spec["kind"] == "conv":
             S = hq
@@ -76,11 +96,5 @@ def quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=4):
             D, codes, hist = ec.ec_fc(S, T, D, codes, sweeps, inner)
             D32 = D.astype(np.float32)
             hq = O.fc_lut(S, D32, codes, bias=bias, relu=spec["relu"]).astype(np.float32)
-        if bias is not None:
-            b = np.asarray(bias, np.float64)
-            lin = lin + (b[None, :, None, None] if spec["kind"] == "conv" else b[None, :])
-        if spec["relu"]:
-            lin = np.maximum(lin, 0.0)
-        ho = lin.astype(np.float32)
         out.append((D, codes, hist, S, T))
     return out

@@ -46,9 +46,10 @@ def _signatures():
         "qo_fc_direct": [P, I, I, P, I, I, I, P, I, P, I, P],
         "qo_fc_points": [P, I, I, P, I, I, I, P, I, P, I, P, I, P, P],
         "qo_maxpool": [P, I, I, I, I, I, I, P],
-        "qo_pq_assign": [P, I, I, I, P, I, I, I, P, P, P],
+        "qo_pq_assign": [P, I, I, I, P, I, I, I, P, P],
+        "qo_pq_distances": [P, I, I, I, P, I, I, I, P, P, P],
         "qo_pq_update": [P, I, I, I, P, I, I, I, P, P, P],
-        "qo_pq_kmeans": [P, I, I, I, I, I, I, I, P, P, P, P],
+        "qo_pq_kmeans": [P, I, I, I, I, I, I, I, P, P, P],
         "qo_threads": [],
         "qo_code_bits": [I],
         "qo_pack_codes": [P, ctypes.c_longlong, I, P],
@@ -286,19 +287,32 @@ def _wshape(W):
 
 
 def pq_assign(W, D):
-    """Nearest sub-codeword per sub-vector (fp32 decision, ties to the lowest
-    index).  Returns codes [C_t][d_k][d_k][M] (FC: [C_t][M]), the per-subspace
-    sums of the fp32 minimum distances and the exact float64 objective."""
+    """Nearest sub-codeword per sub-vector (Eq. (4)/(6): float64 distances,
+    ties to the lowest index).  Returns codes [C_t][d_k][d_k][M] (FC:
+    [C_t][M]) and the per-subspace float64 objective ||D B - W||^2."""
     fc = np.ndim(W) == 2
     W, Ct, Cs, dk = _wshape(W)
     D, Dp = _f32(D)
     M, K, Csp = D.shape
     codes = np.empty((Ct, dk, dk, M), np.uint8)
-    o32 = np.empty(M, np.float64)
-    o64 = np.empty(M, np.float64)
-    _chk(lib().qo_pq_assign(W.ctypes.data, Ct, Cs, dk, Dp, M, K, Csp, codes.ctypes.data,
-                            o32.ctypes.data, o64.ctypes.data))
-    return (codes.reshape(Ct, M) if fc else codes), o32, o64
+    obj = np.empty(M, np.float64)
+    _chk(lib().qo_pq_assign(W.ctypes.data, Ct, Cs, dk, Dp, M, K, Csp, codes.ctypes.data, obj.ctypes.data))
+    return (codes.reshape(Ct, M) if fc else codes), obj
+
+
+def pq_distances(W, D, codes):
+    """For an assignment made elsewhere: per sub-vector (codes' shape) the
+    float64 distance to the named sub-codeword and the float64 minimum over
+    all K, as (dcode, dmin)."""
+    W, Ct, Cs, dk = _wshape(W)
+    D, Dp = _f32(D)
+    M, K, Csp = D.shape
+    shape = np.shape(codes)
+    codes, cp = _u8(np.asarray(codes).reshape(Ct, dk, dk, M))
+    dcode = np.empty((Ct, dk, dk, M), np.float64)
+    dmin = np.empty_like(dcode)
+    _chk(lib().qo_pq_distances(W.ctypes.data, Ct, Cs, dk, Dp, M, K, Csp, cp, dcode.ctypes.data, dmin.ctypes.data))
+    return dcode.reshape(shape), dmin.reshape(shape)
 
 
 def pq_update(W, codes, D):
@@ -318,18 +332,17 @@ def pq_update(W, codes, D):
 
 def pq_kmeans(W, D_init, iters):
     """iters x (assign, update) then a final assignment.  Returns the learned
-    codebooks, the codes and the per-assignment objective totals (fp32-distance
-    sums and exact float64 values), each of length iters + 1."""
+    codebooks, the codes and the float64 objective of every assignment
+    (length iters + 1)."""
     fc = np.ndim(W) == 2
     W, Ct, Cs, dk = _wshape(W)
     D = np.array(D_init, dtype=np.float32, copy=True, order="C")
     M, K, Csp = D.shape
     codes = np.empty((Ct, dk, dk, M), np.uint8)
-    o32 = np.empty(iters + 1, np.float64)
-    o64 = np.empty(iters + 1, np.float64)
+    obj = np.empty(iters + 1, np.float64)
     _chk(lib().qo_pq_kmeans(W.ctypes.data, Ct, Cs, dk, M, K, Csp, int(iters), D.ctypes.data,
-                            codes.ctypes.data, o32.ctypes.data, o64.ctypes.data))
-    return D, (codes.reshape(Ct, M) if fc else codes), o32, o64
+                            codes.ctypes.data, obj.ctypes.data))
+    return D, (codes.reshape(Ct, M) if fc else codes), obj
 
 
 # ------------------------------------------------------------- packed codes

@@ -435,26 +435,24 @@ int qo_maxpool(const float* x, int N, int C, int H, int W, int k, int s, double*
  * Readings of what the paper leaves open (it names k-means only):
  *   Q1 the distance is the squared Euclidean one (the Frobenius objective
  *      taken column by column).
- *   Q2 assignment: the nearest sub-codeword, decided on fp32 distances
- *      accumulated as d = fmaf(w_j - c_j, w_j - c_j, d) over j in order
- *      (the precision of the kernel that implements it), ties going to the
- *      lowest index.
+ *   Q2 assignment: the nearest sub-codeword of Eq. (4) / (6), distances
+ *      taken in double from the fp32 values, ties going to the lowest index.
  *   Q3 update: a sub-codeword becomes the mean of the sub-vectors assigned to
  *      it, summed in double in sub-vector order (c_t, ky, kx) and rounded to
  *      fp32; a sub-codeword that no sub-vector chose keeps its value.
  *   Q4 the initial sub-codewords are an input (the caller draws them).
  *   Q5 an iteration is an assignment followed by an update; after the last
  *      one a final assignment makes the codes match the final sub-codewords.
- * The objective of an assignment is reported twice: the sum of the fp32
- * minimum distances (what the assignment decided on) and the exact double
- * value of || D B - W ||^2 for the chosen codes.                             */
+ * The objective of an assignment is || D B - W ||^2 for the chosen codes, in
+ * double (per subspace).                                                     */
 
-static float pq_dist32(const float* W, int Cs, int dk, int t, int p, int m, int Csp, const float* c) {
-  float d = 0.0f;
+/* Squared distance, in double, between sub-vector (t, p, m) of W and the
+ * sub-codeword c (C'_s entries).                                            */
+static double pq_dist(const float* W, int Cs, int dk, int t, int p, int m, int Csp, const float* c) {
+  double d = 0.0;
   for (int j = 0; j < Csp; ++j) {
-    float w = W[(((size_t)t * Cs + (size_t)m * Csp + j) * dk * dk) + p];
-    float diff = w - c[j];
-    d = fmaf(diff, diff, d);
+    double diff = (double)W[(((size_t)t * Cs + (size_t)m * Csp + j) * dk * dk) + p] - (double)c[j];
+    d += diff * diff;
   }
   return d;
 }
@@ -466,9 +464,9 @@ static int check_quant(int Ct, int Cs, int dk, int M, int K, int Csp) {
   return 0;
 }
 
-/* Assignment step.  codes: [C_t][d_k][d_k][M]; obj32, obj64: [M] or NULL. */
+/* Assignment step (Q1, Q2).  codes: [C_t][d_k][d_k][M]; obj: [M] or NULL. */
 int qo_pq_assign(const float* W, int Ct, int Cs, int dk, const float* D, int M, int K, int Csp,
-                 uint8_t* codes, double* obj32, double* obj64) {
+                 uint8_t* codes, double* obj) {
   int e;
   if (!W || !D || !codes) return QO_EARG;
   if ((e = check_quant(Ct, Cs, dk, M, K, Csp))) return e;
@@ -476,25 +474,47 @@ int qo_pq_assign(const float* W, int Ct, int Cs, int dk, const float* D, int M, 
 #pragma omp parallel for schedule(dynamic, 1)
   for (int m = 0; m < M; ++m) {
     const float* Dm = D + (size_t)m * K * Csp;
-    double s32 = 0.0, s64 = 0.0;
+    double s = 0.0;
     for (int t = 0; t < Ct; ++t)
       for (int p = 0; p < P; ++p) {
         int best = 0;
-        float bd = pq_dist32(W, Cs, dk, t, p, m, Csp, Dm);
+        double bd = pq_dist(W, Cs, dk, t, p, m, Csp, Dm);
         for (int k = 1; k < K; ++k) {
-          float d = pq_dist32(W, Cs, dk, t, p, m, Csp, Dm + (size_t)k * Csp);
+          double d = pq_dist(W, Cs, dk, t, p, m, Csp, Dm + (size_t)k * Csp);
           if (d < bd) { bd = d; best = k; }
         }
         codes[((size_t)t * P + p) * M + m] = (uint8_t)best;
-        s32 += (double)bd;
-        for (int j = 0; j < Csp; ++j) {
-          double diff = (double)W[(((size_t)t * Cs + (size_t)m * Csp + j) * P) + p] -
-                        (double)Dm[(size_t)best * Csp + j];
-          s64 += diff * diff;
-        }
+        s += bd;
       }
-    if (obj32) obj32[m] = s32;
-    if (obj64) obj64[m] = s64;
+    if (obj) obj[m] = s;
+  }
+  return 0;
+}
+
+/* For checking an assignment made elsewhere: per sub-vector (in the codes'
+ * order [C_t][d_k][d_k][M]), the double distance to the sub-codeword its
+ * code names (dcode) and the smallest double distance over all K (dmin).   */
+int qo_pq_distances(const float* W, int Ct, int Cs, int dk, const float* D, int M, int K, int Csp,
+                    const uint8_t* codes, double* dcode, double* dmin) {
+  int e;
+  if (!W || !D || !codes || !dcode || !dmin) return QO_EARG;
+  if ((e = check_quant(Ct, Cs, dk, M, K, Csp))) return e;
+  if ((e = check_codes(codes, (size_t)Ct * dk * dk * M, K))) return e;
+  const int P = dk * dk;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = 0; m < M; ++m) {
+    const float* Dm = D + (size_t)m * K * Csp;
+    for (int t = 0; t < Ct; ++t)
+      for (int p = 0; p < P; ++p) {
+        const size_t i = ((size_t)t * P + p) * M + m;
+        double bd = pq_dist(W, Cs, dk, t, p, m, Csp, Dm);
+        for (int k = 1; k < K; ++k) {
+          double d = pq_dist(W, Cs, dk, t, p, m, Csp, Dm + (size_t)k * Csp);
+          if (d < bd) bd = d;
+        }
+        dmin[i] = bd;
+        dcode[i] = pq_dist(W, Cs, dk, t, p, m, Csp, Dm + (size_t)codes[i] * Csp);
+      }
   }
   return 0;
 }
@@ -536,26 +556,23 @@ int qo_pq_update(const float* W, int Ct, int Cs, int dk, const uint8_t* codes, i
 
 /* k-means (Q5): iters x (assign, update), then a final assignment.
  * D: [M][K][C'_s] in: initial sub-codewords, out: learned ones.
- * obj32, obj64: [iters + 1] totals over m of each assignment's objective.  */
+ * obj: [iters + 1] totals over m of each assignment's objective.           */
 int qo_pq_kmeans(const float* W, int Ct, int Cs, int dk, int M, int K, int Csp, int iters,
-                 float* D, uint8_t* codes, double* obj32, double* obj64) {
+                 float* D, uint8_t* codes, double* obj) {
   int e;
   if (!W || !D || !codes || iters < 0) return QO_EARG;
   if ((e = check_quant(Ct, Cs, dk, M, K, Csp))) return e;
-  double* o32 = (double*)malloc((size_t)M * sizeof(double));
-  double* o64 = (double*)malloc((size_t)M * sizeof(double));
-  if (!o32 || !o64) { free(o32); free(o64); return QO_ENOMEM; }
+  double* om = (double*)malloc((size_t)M * sizeof(double));
+  if (!om) return QO_ENOMEM;
   for (int it = 0; it <= iters && !e; ++it) {
-    e = qo_pq_assign(W, Ct, Cs, dk, D, M, K, Csp, codes, o32, o64);
+    e = qo_pq_assign(W, Ct, Cs, dk, D, M, K, Csp, codes, om);
     if (e) break;
-    double a = 0.0, b = 0.0;
-    for (int m = 0; m < M; ++m) { a += o32[m]; b += o64[m]; }
-    if (obj32) obj32[it] = a;
-    if (obj64) obj64[it] = b;
+    double a = 0.0;
+    for (int m = 0; m < M; ++m) a += om[m];
+    if (obj) obj[it] = a;
     if (it < iters) e = qo_pq_update(W, Ct, Cs, dk, codes, M, K, Csp, D, D, NULL);
   }
-  free(o32);
-  free(o64);
+  free(om);
   return e;
 }
 

@@ -346,6 +346,13 @@ def _codes_shape(W, M):
     return (W.shape[0], M) if W.dim() == 2 else (W.shape[0], W.shape[2], W.shape[3], M)
 
 
+def _need_shaped(t: torch.Tensor, name: str, dtype: torch.dtype, shape, device) -> None:
+    """A caller-supplied buffer: dtype, exact shape, device, contiguity."""
+    _need(t, name, dtype, len(shape), device)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+
+
 def pq_assign(W: torch.Tensor, codebooks: torch.Tensor, codes: Optional[torch.Tensor] = None,
               objective: Optional[torch.Tensor] = None):
     """Nearest sub-codeword of every sub-vector (Eq. (4)/(6) assignment step,
@@ -357,8 +364,10 @@ def pq_assign(W: torch.Tensor, codebooks: torch.Tensor, codes: Optional[torch.Te
     M, K, Csp = codebooks.shape
     if codes is None:
         codes = torch.empty(_codes_shape(W, M), dtype=torch.uint8, device=W.device)
+    _need_shaped(codes, "codes", torch.uint8, _codes_shape(W, M), W.device)
     if objective is None:
         objective = torch.empty(M, dtype=torch.float64, device=W.device)
+    _need_shaped(objective, "objective", torch.float64, (M,), W.device)
     check(lib().qcnn_pq_assign(W.data_ptr(), Ct, Cs, dk, codebooks.data_ptr(), M, K, Csp, codes.data_ptr(),
                                objective.data_ptr(), _stream(W)), "qcnn_pq_assign")
     return codes, objective
@@ -373,10 +382,10 @@ def pq_update(W: torch.Tensor, codes: torch.Tensor, codebooks: torch.Tensor, cou
     Ct, Cs, dk = _quant_w(W)
     _need(codebooks, "codebooks", torch.float32, 3, W.device)
     M, K, Csp = codebooks.shape
-    if codes.dtype != torch.uint8 or not codes.is_contiguous() or tuple(codes.shape) != _codes_shape(W, M):
-        raise ValueError("codes must be contiguous uint8 %s" % (_codes_shape(W, M),))
+    _need_shaped(codes, "codes", torch.uint8, _codes_shape(W, M), W.device)
     if counts is None:
         counts = torch.empty((M, K), dtype=torch.int32, device=W.device)
+    _need_shaped(counts, "counts", torch.int32, (M, K), W.device)
     check(lib().qcnn_pq_update(W.data_ptr(), Ct, Cs, dk, codes.data_ptr(), M, K, Csp, codebooks.data_ptr(),
                                counts.data_ptr(), _stream(W)), "qcnn_pq_update")
     return codebooks, counts

@@ -64,7 +64,7 @@ def quant_checks(rng):
     # with one indicator row), the objective the total squared deviation.
     W = rng.standard_normal((5, 6, 3, 3)).astype(np.float32)
     V = subvectors(W.astype(np.float64), 3)
-    D, codes, o32, o64 = O.pq_kmeans(W, np.zeros((2, 1, 3), np.float32), 1)
+    D, codes, o64 = O.pq_kmeans(W, np.zeros((2, 1, 3), np.float32), 1)
     mean = V.mean(axis=1)
     out.append(("quant K=1 mean", np.allclose(D[:, 0], mean, rtol=1e-6, atol=1e-7) and not codes.any()))
     dev = ((V - mean[:, None, :]) ** 2).sum()
@@ -81,26 +81,34 @@ def quant_checks(rng):
     D0 = (rng.standard_normal((M, K, Csp)) * 100 + 1000).astype(np.float32)
     perm = rng.permutation(K)[:R]
     D0[:, perm] = pool
-    codes, o32, o64 = O.pq_assign(W, D0)
+    codes, o64 = O.pq_assign(W, D0)
     got = codes.reshape(Ct * dk * dk, M).T
-    out.append(("quant exact pool", np.array_equal(got, perm[r]) and o64.sum() == 0.0 and o32.sum() == 0.0))
+    out.append(("quant exact pool", np.array_equal(got, perm[r]) and o64.sum() == 0.0))
     # Nearest sub-codeword: against float64 distances from numpy.
     for shape in [(9, 12, 3, 4, 16), (33, 8, 1, 2, 64), (4, 6, 5, 3, 7)]:
         Ct, Cs, dk, Csp, K = shape
         W, D = wl.random_quant(rng, Ct, Cs, dk, Csp, K)
         W4 = W.reshape(Ct, Cs, dk, dk)
-        codes, o32, o64 = O.pq_assign(W, D)
+        codes, o64 = O.pq_assign(W, D)
         V = subvectors(W4.astype(np.float64), Csp)
         dist = ((V[:, :, None, :] - D.astype(np.float64)[:, None, :, :]) ** 2).sum(-1)  # [M][n][K]
         got = codes.reshape(Ct * dk * dk, Cs // Csp).T
         chosen = np.take_along_axis(dist, got[:, :, None].astype(np.int64), 2)[..., 0]
         best = dist.min(-1)
-        out.append(("quant nearest %s" % (shape,), np.all(chosen <= best * (1 + 1e-5) + 1e-12)))
+        # float64 on both sides: the chosen distance is the minimum up to the
+        # order of C's float64 additions
+        out.append(("quant nearest %s" % (shape,), np.all(chosen <= best * (1 + 1e-13) + 1e-300)))
+        # and the distances the oracle reports for a given assignment are
+        # these same float64 distances
+        dcode, dmin = O.pq_distances(W, D, codes)
+        out.append(("quant distances %s" % (shape,),
+                    np.allclose(dcode.reshape(-1, Cs // Csp).T, chosen, rtol=1e-13, atol=0)
+                    and np.allclose(dmin.reshape(-1, Cs // Csp).T, best, rtol=1e-13, atol=0)))
         rec = ((V - D.astype(np.float64)[np.arange(Cs // Csp)[:, None], got]) ** 2).sum(axis=(1, 2))
         out.append(("quant objective = ||DB - W||^2 %s" % (shape,), np.allclose(o64, rec, rtol=1e-10, atol=1e-14)))
         # Update: the mean of each cluster; an unused sub-codeword keeps its value.
         D[:, -1] = 1e3  # far from every sub-vector: never chosen
-        codes, _, _ = O.pq_assign(W, D)
+        codes, _ = O.pq_assign(W, D)
         got = codes.reshape(Ct * dk * dk, Cs // Csp).T
         Dn, cnt = O.pq_update(W, codes, D)
         ok = True
@@ -117,23 +125,107 @@ def quant_checks(rng):
     # argmin (the first minimum: ties to the lowest index).
     Ct, Cs, dk, Csp, K = 20, 12, 3, 3, 40
     W, D = wl.random_quant(rng, Ct, Cs, dk, Csp, K, integer=True)
-    codes, _, _ = O.pq_assign(W, D)
+    codes, _ = O.pq_assign(W, D)
     V = subvectors(W.astype(np.float64), Csp)
     dist = ((V[:, :, None, :] - D.astype(np.float64)[:, None, :, :]) ** 2).sum(-1)
     out.append(("quant ties to lowest index", np.array_equal(codes.reshape(-1, Cs // Csp).T, dist.argmin(-1))))
     # Lloyd iterations never raise the objective; the final codes are the
     # assignment to the final sub-codewords.
     W, D0 = wl.random_quant(rng, 40, 16, 3, 4, 32)
-    D, codes, o32, o64 = O.pq_kmeans(W, D0, 6)
+    D, codes, o64 = O.pq_kmeans(W, D0, 6)
     out.append(("quant objective non-increasing", np.all(np.diff(o64) <= 1e-6 * o64[:-1])))
-    c2, _, _ = O.pq_assign(W, D)
+    c2, _ = O.pq_assign(W, D)
     out.append(("quant final codes match codebooks", np.array_equal(codes, c2)))
     # Eq. (6) = Eq. (4) over the gathered sub-vectors: quantizing a conv layer
     # is quantizing the FC matrix whose rows are its (c_t, p_k) kernels' columns.
     Wf = W.transpose(0, 2, 3, 1).reshape(-1, W.shape[1])
-    Df, cf, o32f, o64f = O.pq_kmeans(Wf, D0, 6)
+    Df, cf, o64f = O.pq_kmeans(Wf, D0, 6)
     out.append(("quant conv = fc on gathered sub-vectors",
                 np.array_equal(D, Df) and np.array_equal(codes.reshape(cf.shape), cf) and np.array_equal(o64, o64f)))
+    return out
+
+
+def _pool_np(h, k, s):
+    N, C, H, W = h.shape
+    Ho, Wo = (H - k) // s + 1, (W - k) // s + 1
+    return np.array([[[[h[n, c, s * i:s * i + k, s * j:s * j + k].max() for j in range(Wo)] for i in range(Ho)]
+                      for c in range(C)] for n in range(N)])
+
+
+def network_checks(rng, Om=None):
+    """Pins of the oracle's network composition (oracle.network): the
+    hand-worked stack of tests/golden/network_handworked.json, and a random
+    conv -> pool -> conv -> pool -> FC -> FC stack against the same layers
+    written as numpy dense products on the rebuilt weights (Eq. (4), (6)),
+    fp32 rounding of every layer's input, NCHW flatten before the first FC;
+    in absolute mode (|x|, |D|, no ReLU) the same composition on magnitudes,
+    which bounds |y| elementwise.  ``Om`` replaces the oracle module (a copy
+    with a planted mistake)."""
+    Om = Om or O
+    out = []
+    g = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                    "network_handworked.json")))
+    x = np.array(g["x"], np.float32)
+    layers = [dict(kind="conv", D=np.array(g["conv"]["D"], np.float32),
+                   codes=np.array(g["conv"]["codes"], np.uint8), stride=1, pad=0, relu=True),
+              dict(kind="pool", k=2, s=1),
+              dict(kind="fc", D=np.array(g["fc"]["D"], np.float32),
+                   codes=np.array(g["fc"]["codes"], np.uint8), relu=False)]
+    try:
+        out.append(("network hand-worked stack",
+                    np.array_equal(Om.network(x, layers), np.array(g["y"], np.float64))))
+        out.append(("network hand-worked absolute stack",
+                    np.array_equal(Om.network(x, layers, absolute=True), np.array(g["y_absolute"], np.float64))))
+    except Exception:
+        out.append(("network hand-worked stack", False))
+
+    def reference(xx, specs, absolute):
+        h = np.abs(xx).astype(np.float64) if absolute else xx.astype(np.float64)
+        for L in specs:
+            h = h.astype(np.float32).astype(np.float64)  # fp32 input of every layer
+            if L["kind"] == "pool":
+                h = _pool_np(h, L["k"], L["s"])
+                continue
+            D = np.abs(L["D"]) if absolute else L["D"]
+            if L["kind"] == "conv":
+                h = dense_conv(h, rebuilt_conv(D, L["codes"]), L["stride"], L["pad"])
+            else:
+                h = h.reshape(h.shape[0], -1) @ rebuilt_fc(D, L["codes"]).T
+            if L["relu"] and not absolute:
+                h = np.maximum(h, 0.0)
+        return h
+
+    Ls = []
+    # 9x9 -> conv p1 9x9 -> pool 3/2 4x4 -> conv p0 2x2 -> pool 2/1 1x1 -> fc 8 -> fc 3
+    for (Cs, Ct, p, Csp, K, pk, ps) in [(4, 6, 1, 2, 8, 3, 2), (6, 8, 0, 3, 16, 2, 1)]:
+        Ls.append(dict(kind="conv", D=(0.3 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32),
+                       codes=rng.integers(0, K, (Ct, 3, 3, Cs // Csp)).astype(np.uint8), stride=1, pad=p,
+                       relu=True))
+        Ls.append(dict(kind="pool", k=pk, s=ps))
+    for (Cs, Ct, Csp, K, relu) in [(8, 10, 2, 4, True), (10, 3, 5, 8, False)]:
+        Ls.append(dict(kind="fc", D=(0.3 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32),
+                       codes=rng.integers(0, K, (Ct, Cs // Csp)).astype(np.uint8), relu=relu))
+    x = rng.standard_normal((3, 4, 9, 9)).astype(np.float32)
+    # a spatial FC input too: conv -> pool 2x2 map -> fc, where the flatten order matters
+    Ls2 = [dict(kind="conv", D=(0.3 * rng.standard_normal((2, 8, 2))).astype(np.float32),
+                codes=rng.integers(0, 8, (3, 3, 3, 2)).astype(np.uint8), stride=1, pad=1, relu=True),
+           dict(kind="pool", k=3, s=2),
+           dict(kind="fc", D=(0.3 * rng.standard_normal((4, 8, 3))).astype(np.float32),
+                codes=rng.integers(0, 8, (5, 4)).astype(np.uint8), relu=False)]
+    x2 = rng.standard_normal((2, 4, 5, 5)).astype(np.float32)
+    for name, xx, specs in [("network stack", x, Ls), ("network spatial flatten", x2, Ls2)]:
+        try:
+            y = Om.network(xx, specs)
+            A = Om.network(xx, specs, absolute=True)
+            r, ra = reference(xx, specs, False), reference(xx, specs, True)
+            # intermediate fp32 roundings may land one unit apart: 1e-6 of the magnitude sum
+            out.append((name + " = numpy composition",
+                        y.shape == r.shape and bool(np.all(np.abs(y - r) <= 1e-6 * ra + 1e-12))))
+            out.append((name + " absolute = numpy composition on magnitudes",
+                        A.shape == ra.shape and bool(np.all(np.abs(A - ra) <= 1e-6 * ra + 1e-12))))
+            out.append((name + " absolute bounds |y|", bool(np.all(np.abs(y) <= A * (1 + 1e-6) + 1e-12))))
+        except Exception:
+            out.append((name + " = numpy composition", False))
     return out
 
 
@@ -181,10 +273,10 @@ def ec_checks(rng, E=None):
     W = np.stack([centers[m][lab[:, m]] for m in range(M)], 1).reshape(Ct, Cs)
     W = (W + 0.01 * rng.standard_normal(W.shape)).astype(np.float32)
     D0 = (centers + rng.standard_normal(centers.shape)).astype(np.float32)
-    c0, _, _ = O.pq_assign(W, D0)
+    c0, _ = O.pq_assign(W, D0)
     D, codes, hist = E.ec_fc(np.eye(Cs), W.T.astype(np.float64), D0, c0, sweeps=1, inner=1)
     D1, _ = O.pq_update(W, c0, D0)
-    c1, _, _ = O.pq_assign(W, D1)
+    c1, _ = O.pq_assign(W, D1)
     out.append(("ec S=I sub-codebooks = k-means update", np.allclose(D, D1, rtol=1e-6, atol=1e-6)))
     out.append(("ec S=I assignment = k-means assignment", np.array_equal(codes, c1)))
     # general inputs
@@ -427,7 +519,7 @@ def ec_network_checks(rng, E=None):
     out.append(("ecn objectives non-increasing",
                 all(np.all(np.diff(r[2]) <= 1e-9 * r[2][0]) for r in res if r is not None)))
     # every layer's codes are those of error correction from k-means on W
-    D1k, c1k, _, _ = O.pq_kmeans(specs[0]["W"], specs[0]["D0"], 2)
+    D1k, c1k, _ = O.pq_kmeans(specs[0]["W"], specs[0]["D0"], 2)
     from oracle import ec_conv as EC
     Dr, cr, hr = EC.ec_conv(x, T, D1k, c1k, 1, 1, 1, 1)
     out.append(("ecn layer 1 = k-means then conv error correction", np.array_equal(cr, codes) and
@@ -503,6 +595,7 @@ def checks():
                      for ch in range(2)]])
     out.append(("maxpool", np.array_equal(ym, ref)))
     out += quant_checks(rng)
+    out += network_checks(rng)
     out += pack_checks(rng)
     out += ec_checks(rng)
     return out

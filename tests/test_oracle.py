@@ -423,6 +423,6 @@ def test_ec_reduces_error_of_kmeans_on_layer_responses(oracle):
     W = (0.1 * rng.standard_normal((Ct, Cs))).astype(np.float32)
     T = S.astype(np.float64) @ W.T.astype(np.float64)
     D0 = (0.1 * rng.standard_normal((Cs // Csp, K, Csp))).astype(np.float32)
-    Dk, ck, _, _ = oracle.pq_kmeans(W, D0, 10)
+    Dk, ck, _ = oracle.pq_kmeans(W, D0, 10)
     D, codes, hist = ec.ec_fc(S, T, Dk, ck, sweeps=3, inner=2)
     assert hist[-1] < 0.8 * hist[0], hist[[0, -1]]

@@ -42,13 +42,15 @@ MUTANTS = [
     ("qo_conv_points", "int xi = xo * stride - pad + kx;", "int xi = xo * stride - pad + ky;", "point: kx read as ky"),
     ("qo_fc_direct", "for (int c = 0; c < Cs; ++c) s +=", "for (int c = 0; c < Cs - 1; ++c) s +=", "FC last input dropped"),
     ("qo_maxpool", "if (v > best) best = v;", "if (v < best || best == -INFINITY) best = v;", "min instead of max"),
-    ("pq_dist32", "* dk * dk) + p]", "* dk) + p]", "quantizer: sub-vector stride over kernel positions"),
-    ("pq_dist32", "d = fmaf(diff, diff, d);", "d = fmaf(diff, fabsf(w), d);", "quantizer: distance not squared"),
+    ("pq_dist", "* dk * dk) + p]", "* dk) + p]", "quantizer: sub-vector stride over kernel positions"),
+    ("pq_dist", "d += diff * diff;", "d += fabs(diff);", "quantizer: distance not squared"),
     ("qo_pq_assign", "if (d < bd) { bd = d; best = k; }", "if (d <= bd) { bd = d; best = k; }",
      "quantizer: ties to the highest index"),
     ("qo_pq_assign", "for (int k = 1; k < K; ++k) {", "for (int k = 1; k < K - 1; ++k) {",
      "quantizer: last sub-codeword never considered"),
-    ("qo_pq_assign", "s64 += diff * diff;", "s64 += fabs(diff);", "quantizer: objective not squared"),
+    ("qo_pq_assign", "s += bd;", "s += sqrt(bd);", "quantizer: objective not squared"),
+    ("qo_pq_distances", "if (d < bd) bd = d;", "if (d > bd) bd = d;", "quantizer check: largest distance as the minimum"),
+    ("qo_pq_distances", "Dm + (size_t)codes[i] * Csp);", "Dm + (size_t)codes[i]);", "quantizer check: code stride"),
     ("qo_pq_update", "int k = codes[((size_t)t * P + p) * M + m];", "int k = codes[((size_t)p * Ct + t) * M + m];",
      "quantizer: update reads the codes transposed"),
     ("qo_pq_update", "/ (double)cnt[k])", "/ (double)(cnt[k] + 1))", "quantizer: mean divided by count + 1"),
@@ -66,9 +68,11 @@ MUTANTS = [
 
 
 def _mutate(src: str, func: str, old: str, new: str) -> str:
-    start = src.find("int %s(" % func)
-    if start < 0:
-        start = src.index("float %s(" % func)
+    for ret in ("int", "float", "double"):
+        start = src.find("%s %s(" % (ret, func))
+        if start >= 0:
+            break
+    assert start >= 0, func
     end = src.index("\n}\n", start)
     body = src[start:end]
     assert old in body, (func, old)
@@ -213,15 +217,21 @@ def test_ec_conv_pins_catch_mutant(tmp_path, mut):
 # Mistakes planted in a copy of the multi-layer oracle (oracle/ec_network.py).
 ECN_SRC = os.path.join(ROOT, "oracle", "ec_network.py")
 ECN_MUTANTS = [
-    ([("        lin = dense_linear(ho, spec)                              # M1", "        lin = dense_linear(hq, spec)")],
-     "T from the quantized network"),
-    ([("            S = hq\n", "            S = ho\n")], "conv S from the original network"),
-    ([("        T = lin.astype(np.float32)\n", "        T = (lin + (0.1 if spec.get('bias') is not None else 0.0)).astype(np.float32)\n")],
+    ([("        out.append(lin.astype(np.float32))\n",
+       "        out.append((lin + (0.1 if spec.get('bias') is not None else 0.0)).astype(np.float32))\n")],
      "T shifted (bias folded in)"),
+    ([("        lin = dense_linear(ho, spec)                              # M1",
+       "        lin = dense_linear(np.maximum(ho, 0.0), spec)                              # M1"),
+      ("            ho = O.maxpool(ho, spec[\"k\"], spec[\"s\"]).astype(np.float32)\n",
+       "            ho = -O.maxpool(ho, spec[\"k\"], spec[\"s\"]).astype(np.float32)\n")],
+     "original network's pool output negated"),
     ([("        if spec[\"relu\"]:\n            lin = np.maximum(lin, 0.0)", "        if False:\n            lin = np.maximum(lin, 0.0)")],
      "original network without ReLU"),
     ([("            ho = O.maxpool(ho, spec[\"k\"], spec[\"s\"]).astype(np.float32)\n", "")],
      "original network skips the pool"),
+    ([("relu=spec[\"relu\"]).astype(np.float32)", "relu=False).astype(np.float32)")],
+     "quantized network without ReLU after a conv"),
+    ([("            S = hq\n", "            S = np.abs(hq - 0.05)\n")], "conv S is not the quantized activations"),
 ]
 
 
@@ -252,3 +262,50 @@ def test_unmodified_ec_network_passes(tmp_path):
     mod = _ec_module(open(ECN_SRC).read(), tmp_path, "ecn_orig")
     bad = [n for n, ok in pin_battery.ec_network_checks(np.random.Generator(np.random.PCG64(17)), mod) if not ok]
     assert not bad, bad
+
+
+# Mistakes planted in a copy of the oracle's network composition
+# (oracle/oracle.py, network()): the copy runs on the same C oracle library and
+# the battery's network checks must flag each one.
+NET_SRC = os.path.join(ROOT, "oracle", "oracle.py")
+NET_MUTANTS = [
+    ('fc_lut(h32.reshape(h32.shape[0], -1), D,',
+     'fc_lut(np.ascontiguousarray(h32.transpose(0, 2, 3, 1) if h32.ndim == 4 else h32)'
+     '.reshape(h32.shape[0], -1), D,', "flatten in NHWC order"),
+    ('h = maxpool(h32, L["k"], L["s"])', 'h = h32', "pool skipped"),
+    ('relu = bool(L["relu"]) and not absolute', 'relu = False', "ReLU dropped"),
+    ('D = np.abs(L["D"]) if absolute else L["D"]', 'D = L["D"]', "absolute network keeps signed codebooks"),
+    ('h = np.abs(x) if absolute else x', 'h = x', "absolute network keeps signed inputs"),
+]
+
+
+def _net_module(text, tmp_path, name):
+    here = '_HERE = os.path.dirname(os.path.abspath(__file__))'
+    assert here in text
+    return _ec_module(text.replace(here, "_HERE = %r" % os.path.join(ROOT, "oracle"), 1), tmp_path, name)
+
+
+def test_unmodified_network_passes(tmp_path):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    mod = _net_module(open(NET_SRC).read(), tmp_path, "net_orig")
+    bad = [n for n, ok in pin_battery.network_checks(np.random.Generator(np.random.PCG64(5)), mod) if not ok]
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("mut", NET_MUTANTS, ids=[m[2] for m in NET_MUTANTS])
+def test_network_pins_catch_mutant(tmp_path, mut):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import pin_battery
+    old, new, what = mut
+    src = open(NET_SRC).read()
+    assert old in src, old
+    mod = _net_module(src.replace(old, new, 1), tmp_path, "net_mut")
+    try:
+        res = pin_battery.network_checks(np.random.Generator(np.random.PCG64(5)), mod)
+        survived = all(ok for _, ok in res)
+    except Exception:  # a crash is a caught mistake too
+        survived = False
+    assert not survived, "mutant survived: " + what
