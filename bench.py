@@ -242,8 +242,18 @@ def main():
                           "W": T((0.02 * rng.standard_normal((Ct, Cs, 3, 3))).astype(np.float32)),
                           "bias": T((0.01 * rng.standard_normal(Ct)).astype(np.float32)),
                           "D0": T((0.02 * rng.standard_normal((Cs // 4, 128, 4))).astype(np.float32))})
+        # The original stack's responses T (the method's input): its dense
+        # layers in float64 (unfold + matmul), rounded to fp32, made once.
+        targets, ho = [], x
+        for sp in specs:
+            Wt = sp["W"].double()
+            N, _, H, Wd = ho.shape
+            cols = torch.nn.functional.unfold(ho.double(), 3, padding=1)
+            lin = torch.matmul(Wt.reshape(Wt.shape[0], -1), cols).reshape(N, Wt.shape[0], H, Wd)
+            targets.append(lin.float().contiguous())
+            ho = torch.clamp_min(lin + sp["bias"].double()[None, :, None, None], 0.0).float()
         torch.cuda.synchronize(dev)
-        return (lambda: quantize_net.quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=3),
+        return (lambda: quantize_net.quantize_network(x, specs, targets, sweeps=1, inner=1, kmeans_iters=3),
                 "AlexNet conv3-conv5 (256->384->384->256, 3x3 p1, 13x13, C's=4, K=128), 32 images")
 
     if args.only == "ec_net":

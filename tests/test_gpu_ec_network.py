@@ -1,6 +1,8 @@
 """Multi-layer error correction (Sec. 3.3.3) on the GPU (quantize_net, which
 chains qcnn_pq_kmeans, qcnn_ec_conv / qcnn_ec_fc and the PQ forward) against
 the oracle chain (oracle/ec_network.py) on a conv -> pool -> conv -> FC stack.
+The original network's responses T are an input of the method; both sides
+take the oracle's (float64 dense layers rounded to fp32).
 
 Layer 1 sees identical inputs on both sides; later layers see the quantized
 network's activations, which the GPU's fp32 forward and the oracle's float64
@@ -46,7 +48,9 @@ def test_network_matches_oracle(dev, seed, lossless):
     x, specs = pin_battery.small_network(np.random.Generator(np.random.PCG64(seed)), lossless)
     print("ec_network seed", seed, flush=True)
     rec = []
-    got = quantize_net.quantize_network(torch.from_numpy(x).to(dev), to_dev(specs, dev), sweeps=1, inner=1,
+    # the original network's responses are the caller's: the oracle's here
+    targets = [None if t is None else torch.from_numpy(t).to(dev) for t in ec_network.original_responses(x, specs)]
+    got = quantize_net.quantize_network(torch.from_numpy(x).to(dev), to_dev(specs, dev), targets, sweeps=1, inner=1,
                                         kmeans_iters=2, record=rec)
     torch.cuda.synchronize()
     ref = ec_network.quantize_network(x, specs, sweeps=1, inner=1, kmeans_iters=2)
