@@ -19,6 +19,9 @@
 //     wave-uniform: one scalar load serves 64 lanes, and the lanes read one
 //     table row at consecutive positions;
 //   * the table never leaves LDS.
+#include <stdlib.h>
+#include <string.h>
+
 #include "qcnn_internal.h"
 
 namespace qcnn {
@@ -200,12 +203,31 @@ hipError_t launch_csp(const ConvPtrs& a, const ConvParams& p, int G, dim3 grid, 
 
 bool conv_supported(const ConvShape& s) {
   Tiling t;
-  return conv_flat_supported(s) || choose_tiling(s, &t);
+  return conv_half_supported(s) || conv_flat_supported(s) || choose_tiling(s, &t);
 }
+
+namespace {
+
+// Which conv kernel family serves a layer: the first of conv_flat,
+// conv_half, conv_pq_generic that can tile it.  QCNN_CONV_KERNEL = half puts
+// the two-table kernel first, = generic skips the first two (for comparisons
+// and for tests of every kernel on shapes the default one also serves).
+int conv_kernel_choice() {
+  const char* v = getenv("QCNN_CONV_KERNEL");  // read per call: tests switch it within one process
+  if (!v) return 0;
+  if (strcmp(v, "half") == 0) return 1;
+  if (strcmp(v, "generic") == 0) return 2;
+  return 0;
+}
+
+}  // namespace
 
 hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                                const float* bias, int relu, float* y, hipStream_t stream) {
-  if (conv_flat_supported(s)) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream);
+  const int choice = conv_kernel_choice();
+  if (choice == 1 && conv_half_supported(s)) return launch_conv_half(s, x, D, codes, bias, relu, y, stream);
+  if (choice != 2 && conv_flat_supported(s)) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream);
+  if (choice != 2 && conv_half_supported(s)) return launch_conv_half(s, x, D, codes, bias, relu, y, stream);
   Tiling t;
   if (!choose_tiling(s, &t)) return hipErrorInvalidConfiguration;
   const ConvPtrs a{x, D, codes, bias, y};

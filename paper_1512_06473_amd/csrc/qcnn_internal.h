@@ -86,6 +86,12 @@ bool conv_flat_supported(const ConvShape& s);
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                             const float* bias, int relu, float* y, hipStream_t stream);
 
+// Stride-1 3x3 / 1x1 kernel with two tables in LDS and half-wave table rows
+// (conv_half.hip): C'_s <= 8, K <= 128.
+bool conv_half_supported(const ConvShape& s);
+hipError_t launch_conv_half(const ConvShape& s, const float* x, const float* D, CodeStream codes,
+                            const float* bias, int relu, float* y, hipStream_t stream);
+
 // Brackets the main kernel of a call with a pair of HIP events on its
 // stream while kernel timing is switched on (qcnn_timing_enable); does
 // nothing otherwise.  The pairs are read back by qcnn_timing_read.
