@@ -75,7 +75,8 @@ typedef enum qcnn_status {
   QCNN_ERR_CODE_RANGE = 4,  /* a code >= K (only with QCNN_CHECK_CODES=1) */
   QCNN_ERR_HIP = 5,         /* a HIP runtime call or kernel launch failed */
   QCNN_ERR_UNSUPPORTED = 6, /* C'_s > 16, codes not 4-byte aligned, grid or LDS limits */
-  QCNN_ERR_ALIAS = 7        /* an output overlaps an input */
+  QCNN_ERR_ALIAS = 7,       /* an output overlaps an input */
+  QCNN_ERR_WORKSPACE = 8    /* qcnn_conv_forward_noalloc: the layer needs more than its static scratch */
 } qcnn_status;
 
 /* Build the table of sub-codeword inner products (Sec. 3.1 test phase;
@@ -109,6 +110,23 @@ qcnn_status qcnn_fc_forward(const float* x, int N, int C_s,
                             const float* codebooks, int M, int K, int Csp,
                             const uint8_t* codes, int C_t,
                             const float* bias, int relu, float* y, void* stream);
+
+/* qcnn_conv_forward for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments, limits, kernels and results (bit for bit),
+ * but every temporary (re-laid-out codes, partial sums of split layers, the
+ * QCNN_CHECK_CODES counter) lives in a static device array of 64 MiB that the
+ * library's code object holds on every device it runs on until the process
+ * ends; nothing is allocated or freed and no timing events are recorded.  A
+ * layer whose temporaries exceed the array returns QCNN_ERR_WORKSPACE before
+ * any HIP call (the AlexNet conv3 layer at N = 32 needs about 49 MiB).  The
+ * array is shared by every call on a device and keeps the last call's
+ * contents: calls that overlap on one device (two streams, or two host
+ * threads) race on it, so serialise them. */
+qcnn_status qcnn_conv_forward_noalloc(const float* x, int N, int C_s, int H, int W,
+                                      const float* codebooks, int M, int K, int Csp,
+                                      const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                                      const float* bias, int relu, float* y, void* stream);
 
 /* ---- Packed codes.  Table 1 (Sec. 3.4) stores every quantization index in
  * log2 K bits: (1/8) d_k^2 M C_t log2 K bytes for a conv layer,

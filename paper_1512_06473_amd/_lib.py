@@ -25,6 +25,7 @@ SIGNATURES = {
     "qcnn_out_size": ([I, I, I, I], I),
     "qcnn_status_string": ([I], ctypes.c_char_p),
     "qcnn_version": ([], I),
+    "qcnn_conv_forward_noalloc": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
     "qcnn_conv_forward_packed": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
     "qcnn_fc_forward_packed": ([P, I, I, P, I, I, I, P, I, P, I, P, P], I),
     "qcnn_code_bits": ([I], I),
@@ -38,7 +39,7 @@ SIGNATURES = {
 }
 
 STATUS = {0: "QCNN_OK", 1: "QCNN_ERR_NULL", 2: "QCNN_ERR_SHAPE", 3: "QCNN_ERR_K_RANGE",
-          4: "QCNN_ERR_CODE_RANGE", 5: "QCNN_ERR_HIP", 6: "QCNN_ERR_UNSUPPORTED", 7: "QCNN_ERR_ALIAS"}
+          4: "QCNN_ERR_CODE_RANGE", 5: "QCNN_ERR_HIP", 6: "QCNN_ERR_UNSUPPORTED", 7: "QCNN_ERR_ALIAS", 8: "QCNN_ERR_WORKSPACE"}
 
 _lib = None
 

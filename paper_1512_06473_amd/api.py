@@ -66,6 +66,21 @@ def conv_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, 
     x [N][C_s][H][W] fp32, codebooks [M][K][C'_s] fp32, codes uint8 [C_t][d_k][d_k][M],
     bias [C_t] fp32 or None.  Returns y [N][C_t][H_o][W_o].
     """
+    return _conv_call("qcnn_conv_forward", x, codebooks, codes, stride, pad, bias, relu, out)
+
+
+def conv_forward_noalloc(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, stride: int, pad: int,
+                         bias: Optional[torch.Tensor], relu: bool, out: torch.Tensor) -> torch.Tensor:
+    """conv_forward that allocates nothing (qcnn_conv_forward_noalloc): the
+    temporaries live in the library's static device scratch; the caller
+    brings ``out``.  Raises QcnnError (QCNN_ERR_WORKSPACE) for a layer whose
+    temporaries do not fit; calls that overlap on one device race."""
+    if out is None:
+        raise ValueError("conv_forward_noalloc needs the caller's output tensor")
+    return _conv_call("qcnn_conv_forward_noalloc", x, codebooks, codes, stride, pad, bias, relu, out)
+
+
+def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out):
     _need(x, "x", torch.float32, 4)
     _need(codebooks, "codebooks", torch.float32, 3, x.device)
     _need(codes, "codes", torch.uint8, 4, x.device)
@@ -86,9 +101,9 @@ def conv_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, 
     _need(out, "out", torch.float32, 4, x.device)
     if tuple(out.shape) != (N, Ct, Ho, Wo):
         raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, Ct, Ho, Wo)))
-    check(lib().qcnn_conv_forward(x.data_ptr(), N, Cs, H, W, codebooks.data_ptr(), M, K, Csp,
-                                  codes.data_ptr(), Ct, dk, stride, pad, bp or None, int(bool(relu)),
-                                  out.data_ptr(), _stream(x)), "qcnn_conv_forward")
+    check(getattr(lib(), entry)(x.data_ptr(), N, Cs, H, W, codebooks.data_ptr(), M, K, Csp,
+                                codes.data_ptr(), Ct, dk, stride, pad, bp or None, int(bool(relu)),
+                                out.data_ptr(), _stream(x)), entry)
     return out
 
 

@@ -745,8 +745,32 @@ bool conv_flat_supported(const ConvShape& s) {
   return make_plan(s, &pl);
 }
 
+namespace {
+
+// Workspace of a plan: the re-laid-out codes, then (split plans) the partials.
+struct FlatWs {
+  size_t n_codes, code_bytes, partial_elems, total;
+};
+
+FlatWs flat_ws(const FlatPlan& pl) {
+  const FlatParams& p = pl.p;
+  FlatWs w;
+  w.n_codes = (size_t)p.V * p.ct_pad * pl.rows * pl.cols;
+  w.code_bytes = (w.n_codes + 4 + 255) & ~(size_t)255;  // + the tail of the last dword load
+  w.partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 256;
+  w.total = w.code_bytes + (p.splits > 1 ? w.partial_elems * sizeof(float) : 0);
+  return w;
+}
+
+}  // namespace
+
+size_t conv_flat_workspace(const ConvShape& s) {
+  FlatPlan pl;
+  return make_plan(s, &pl) ? flat_ws(pl).total : 0;
+}
+
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                            const float* bias, int relu, float* y, hipStream_t stream) {
+                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws) {
   FlatPlan pl;
   if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;
   pl.p.relu = relu;
@@ -758,24 +782,21 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
             pl.p.V, pl.p.S, pl.p.sw, pl.p.Wg, pl.p.Hg, pl.p.tiles, pl.TW, pl.p.tc, pl.p.tblocks, pl.p.splits,
             pl.p.work, pl.p.PR, pl.p.npb, pl.p.zrow, pl.lds);
   const FlatParams& p = pl.p;
-  const int taps = pl.rows * pl.cols;
-  const size_t n_codes = (size_t)p.V * p.ct_pad * taps;
-  const size_t code_bytes = (n_codes + 4 + 255) & ~(size_t)255;  // + the tail of the last dword load
-  const size_t partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 256;
-  const size_t ws = code_bytes + (p.splits > 1 ? partial_elems * sizeof(float) : 0);
+  const FlatWs w = flat_ws(pl);
+  const size_t n_codes = w.n_codes, partial_elems = w.partial_elems;
   Scratch scratch;
-  hipError_t e = scratch.acquire(stream, ws);
+  hipError_t e = scratch.take(stream, w.total, ws);
   if (e != hipSuccess) return e;
   char* base = scratch.get();
   uint8_t* codes8 = reinterpret_cast<uint8_t*>(base);
-  float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
+  float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + w.code_bytes) : nullptr;
   const size_t nwords = (n_codes + 3) / 4;
   const CodeMap cm{p.Ct, p.dk, p.stride, p.M, p.G, pl.rows, pl.cols, p.K, p.ct_pad, p.zrow, p.V};
   hipLaunchKernelGGL(flat_codes_kernel, dim3((unsigned)std::min<size_t>(2048, ceil_div_z(nwords, 256))), dim3(256), 0,
                      stream, codes, cm, reinterpret_cast<uint32_t*>(codes8));
   e = hipGetLastError();
   if (e == hipSuccess) {
-    KernelTimer timer(stream);
+    KernelTimer timer(stream, ws == nullptr);
     e = launch_plan(pl, LaunchArgs{x, D, codes8, bias, y, partial, stream});
   }
   if (e == hipSuccess && partial) {

@@ -177,6 +177,7 @@ struct ConvPtrs {
   CodeStream codes;
   const float* bias;
   float* y;
+  bool timed;  // false on the allocation-free path (no timing events)
 };
 
 template <int CSP, int G>
@@ -184,7 +185,7 @@ hipError_t launch_g(const ConvPtrs& a, const ConvParams& p, dim3 grid, size_t ld
   auto k = conv_pq_generic<CSP, G, kTW>;
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
-  KernelTimer timer(stream);
+  KernelTimer timer(stream, a.timed);
   hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, stream, a.x, a.D, a.codes, a.bias, a.y, p);
   return hipGetLastError();
 }
@@ -220,17 +221,34 @@ int conv_kernel_choice() {
   return 0;
 }
 
+enum class ConvKernel { kFlat, kHalf, kGeneric };
+
+ConvKernel pick_conv_kernel(const ConvShape& s) {
+  const int choice = conv_kernel_choice();
+  if (choice == 1 && conv_half_supported(s)) return ConvKernel::kHalf;
+  if (choice != 2 && conv_flat_supported(s)) return ConvKernel::kFlat;
+  if (choice != 2 && conv_half_supported(s)) return ConvKernel::kHalf;
+  return ConvKernel::kGeneric;
+}
+
 }  // namespace
 
+size_t conv_forward_workspace(const ConvShape& s) {
+  switch (pick_conv_kernel(s)) {
+    case ConvKernel::kFlat: return conv_flat_workspace(s);
+    case ConvKernel::kHalf: return conv_half_workspace(s);
+    default: return 0;  // the generic kernel reads the caller's codes directly
+  }
+}
+
 hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                               const float* bias, int relu, float* y, hipStream_t stream) {
-  const int choice = conv_kernel_choice();
-  if (choice == 1 && conv_half_supported(s)) return launch_conv_half(s, x, D, codes, bias, relu, y, stream);
-  if (choice != 2 && conv_flat_supported(s)) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream);
-  if (choice != 2 && conv_half_supported(s)) return launch_conv_half(s, x, D, codes, bias, relu, y, stream);
+                               const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws) {
+  const ConvKernel kind = pick_conv_kernel(s);
+  if (kind == ConvKernel::kFlat) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream, ws);
+  if (kind == ConvKernel::kHalf) return launch_conv_half(s, x, D, codes, bias, relu, y, stream, ws);
   Tiling t;
   if (!choose_tiling(s, &t)) return hipErrorInvalidConfiguration;
-  const ConvPtrs a{x, D, codes, bias, y};
+  const ConvPtrs a{x, D, codes, bias, y, ws == nullptr};
   ConvParams p;
   p.N = s.N;
   p.Cs = s.Cs;

@@ -714,8 +714,32 @@ bool conv_half_supported(const ConvShape& s) {
   return make_half_plan(s, &pl);
 }
 
+namespace {
+
+// Workspace of a plan: the row offsets, then (split plans) the partials.
+struct HalfWs {
+  size_t n_ro, ro_bytes, partial_elems, total;
+};
+
+HalfWs half_ws(const HalfPlan& pl) {
+  const HalfParams& p = pl.p;
+  HalfWs w;
+  w.n_ro = (size_t)p.M * p.nwslots * p.ngp * 8;  // dwords
+  w.ro_bytes = (w.n_ro * 4 + 255) & ~(size_t)255;
+  w.partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 128;
+  w.total = w.ro_bytes + (p.splits > 1 ? w.partial_elems * sizeof(float) : 0);
+  return w;
+}
+
+}  // namespace
+
+size_t conv_half_workspace(const ConvShape& s) {
+  HalfPlan pl;
+  return make_half_plan(s, &pl) ? half_ws(pl).total : 0;
+}
+
 hipError_t launch_conv_half(const ConvShape& s, const float* x, const float* D, CodeStream codes, const float* bias,
-                            int relu, float* y, hipStream_t stream) {
+                            int relu, float* y, hipStream_t stream, const Workspace* ws) {
   HalfPlan pl;
   if (!make_half_plan(s, &pl)) return hipErrorInvalidConfiguration;
   pl.p.relu = relu;
@@ -726,22 +750,20 @@ hipError_t launch_conv_half(const ConvShape& s, const float* x, const float* D, 
             "splits=%d work=%d PR=%d PT=%d kbl=%d lds=%zu\n", s.dk, s.dk, p.S, p.sw, p.Wg, p.Hg, p.tiles,
             pl.bld ? "builder-wave" : "all-build", pl.twp, p.tc, p.tblocks, p.splits, p.work, p.PR, p.PT, pl.kbl,
             pl.lds);
-  const size_t n_ro = (size_t)p.M * p.nwslots * p.ngp * 8;  // dwords
-  const size_t ro_bytes = (n_ro * 4 + 255) & ~(size_t)255;
-  const size_t partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 128;
-  const size_t ws = ro_bytes + (p.splits > 1 ? partial_elems * sizeof(float) : 0);
+  const HalfWs w = half_ws(pl);
+  const size_t n_ro = w.n_ro, partial_elems = w.partial_elems;
   Scratch scratch;
-  hipError_t e = scratch.acquire(stream, ws);
+  hipError_t e = scratch.take(stream, w.total, ws);
   if (e != hipSuccess) return e;
   char* base = scratch.get();
   uint32_t* rowoff = reinterpret_cast<uint32_t*>(base);
-  float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + ro_bytes) : nullptr;
+  float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + w.ro_bytes) : nullptr;
   const HalfCodeMap cm{p.Ct, p.dk, p.M, p.K, p.PR * 4, p.tc, pl.twp, pl.bld ? kWaves - 1 : kWaves, p.nwslots, p.ngp};
   hipLaunchKernelGGL(half_rowoff_kernel, dim3((unsigned)std::min<size_t>(4096, ceil_div_z(n_ro, 256))), dim3(256), 0,
                      stream, codes, cm, (int)n_ro, rowoff);
   e = hipGetLastError();
   if (e == hipSuccess) {
-    KernelTimer timer(stream);
+    KernelTimer timer(stream, ws == nullptr);
     const HalfArgs a{x, D, rowoff, bias, y, partial, stream};
     e = s.dk == 1 ? launch_taps<1, 1>(pl, a) : launch_taps<3, 3>(pl, a);
   }

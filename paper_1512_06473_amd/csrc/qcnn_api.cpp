@@ -79,16 +79,18 @@ size_t code_stream_bytes(size_t n, int bits) {
 }
 
 // QCNN_CHECK_CODES=1: count codes >= K on the device and wait for the answer.
-qcnn_status check_codes(qcnn::CodeStream codes, size_t n, int K, hipStream_t st) {
+// The counter is `counter` (a device int the caller owns) or a temporary.
+qcnn_status check_codes(qcnn::CodeStream codes, size_t n, int K, hipStream_t st, int* counter = nullptr) {
   static const bool enabled = env_flag("QCNN_CHECK_CODES");
   if (!enabled || (1 << codes.bits) <= K) return QCNN_OK;  // no stored value can reach K
-  int* bad = nullptr;
+  int* bad = counter;
   int host = 0;
-  hipError_t e = hipMallocAsync((void**)&bad, sizeof(int), st);
+  hipError_t e = hipSuccess;
+  if (!bad) e = hipMallocAsync((void**)&bad, sizeof(int), st);
   if (e != hipSuccess) return QCNN_ERR_HIP;
   e = qcnn::launch_code_check(codes, n, K, bad, st);
   if (e == hipSuccess) e = hipMemcpyAsync(&host, bad, sizeof(int), hipMemcpyDeviceToHost, st);
-  hipError_t e2 = hipFreeAsync(bad, st);
+  hipError_t e2 = counter ? hipSuccess : hipFreeAsync(bad, st);
   if (e == hipSuccess) e = e2;
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return QCNN_ERR_HIP;
@@ -113,8 +115,8 @@ TimingState& timing() {
 
 namespace qcnn {
 
-KernelTimer::KernelTimer(hipStream_t stream) : stream_(stream) {
-  if (!timing().on.load(std::memory_order_relaxed)) return;
+KernelTimer::KernelTimer(hipStream_t stream, bool enabled) : stream_(stream) {
+  if (!enabled || !timing().on.load(std::memory_order_relaxed)) return;
   if (hipEventCreate(&start_) != hipSuccess) {
     start_ = nullptr;
   } else if (hipEventRecord(start_, stream_) != hipSuccess) {
@@ -191,6 +193,7 @@ const char* qcnn_status_string(qcnn_status s) {
     case QCNN_ERR_HIP: return "HIP runtime error";
     case QCNN_ERR_UNSUPPORTED: return "layer not supported by the kernels (C's > 16, grid or LDS limits)";
     case QCNN_ERR_ALIAS: return "an output overlaps an input";
+    case QCNN_ERR_WORKSPACE: return "the layer needs more scratch than qcnn_conv_forward_noalloc holds";
   }
   return "unknown status";
 }
@@ -212,10 +215,11 @@ qcnn_status qcnn_lut_build(const float* x, int N, int C_s, int H, int W, const f
 
 namespace {
 
-// Body of qcnn_conv_forward (bits = 8) and qcnn_conv_forward_packed.
+// Body of qcnn_conv_forward (bits = 8), qcnn_conv_forward_packed and (with
+// noalloc) qcnn_conv_forward_noalloc.
 qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
                          int Csp, const uint8_t* codes, int bits, int C_t, int d_k, int stride, int pad,
-                         const float* bias, int relu, float* y, void* stream) {
+                         const float* bias, int relu, float* y, void* stream, bool noalloc = false) {
   if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
   if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0) return QCNN_ERR_SHAPE;
   qcnn_status s = check_pq(N, C_s, M, K, Csp);
@@ -234,8 +238,20 @@ qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const flo
   if (!qcnn::conv_supported(sh)) return QCNN_ERR_UNSUPPORTED;
   if (qcnn::ceil_div(C_t, 32) > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
   hipStream_t st = (hipStream_t)stream;
-  if (!prepare_device()) return QCNN_ERR_HIP;
   const qcnn::CodeStream cs{codes, bits};
+  if (noalloc) {
+    // The static scratch: the layer's temporaries, then 256 bytes for the
+    // code-check counter.  Checked before any HIP call.
+    const size_t room = qcnn::noalloc_scratch_bytes() - 256;
+    if (qcnn::conv_forward_workspace(sh) > room) return QCNN_ERR_WORKSPACE;
+    char* base = nullptr;
+    if (qcnn::noalloc_scratch(&base) != hipSuccess) return QCNN_ERR_HIP;
+    s = check_codes(cs, nc, K, st, reinterpret_cast<int*>(base + room));
+    if (s != QCNN_OK) return s;
+    const qcnn::Workspace ws{base, room};
+    return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0, y, st, &ws));
+  }
+  if (!prepare_device()) return QCNN_ERR_HIP;
   s = check_codes(cs, nc, K, st);
   if (s != QCNN_OK) return s;
   return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0, y, st));
@@ -271,6 +287,13 @@ qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, cons
                               int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
                               const float* bias, int relu, float* y, void* stream) {
   return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, codes, 8, C_t, d_k, stride, pad, bias, relu, y, stream);
+}
+
+qcnn_status qcnn_conv_forward_noalloc(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M,
+                                      int K, int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                                      const float* bias, int relu, float* y, void* stream) {
+  return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, codes, 8, C_t, d_k, stride, pad, bias, relu, y, stream,
+                      true);
 }
 
 qcnn_status qcnn_conv_forward_packed(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M,

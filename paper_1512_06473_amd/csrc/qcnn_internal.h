@@ -59,9 +59,24 @@ struct ConvShape {
 hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const float* D, int M, int K,
                             int Csp, float* lut, hipStream_t stream);
 
+// Device memory a call brings for its temporaries in place of the
+// library's per-stream buffer (the allocation-free entry point's static
+// array): nothing is allocated, and a call that needs more than `bytes`
+// fails with hipErrorOutOfMemory before it launches anything.
+struct Workspace {
+  char* ptr;
+  size_t bytes;
+};
+
 // Returns hipErrorInvalidConfiguration when no tiling fits the device.
+// With `ws` the temporaries live there (nothing allocated, no timing events).
 hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                               const float* bias, int relu, float* y, hipStream_t stream);
+                               const float* bias, int relu, float* y, hipStream_t stream,
+                               const Workspace* ws = nullptr);
+
+// Bytes of temporaries launch_conv_forward needs for this layer with the
+// kernel it would pick now (host-side, no HIP call).
+size_t conv_forward_workspace(const ConvShape& s);
 
 hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
                              CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream);
@@ -83,21 +98,24 @@ bool conv_supported(const ConvShape& s);
 
 // Stride-1 kernel on the flattened padded grid (conv_flat.hip).
 bool conv_flat_supported(const ConvShape& s);
+size_t conv_flat_workspace(const ConvShape& s);
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                            const float* bias, int relu, float* y, hipStream_t stream);
+                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws);
 
 // Stride-1 3x3 / 1x1 kernel with two tables in LDS and half-wave table rows
 // (conv_half.hip): C'_s <= 8, K <= 128.
 bool conv_half_supported(const ConvShape& s);
+size_t conv_half_workspace(const ConvShape& s);
 hipError_t launch_conv_half(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                            const float* bias, int relu, float* y, hipStream_t stream);
+                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws);
 
 // Brackets the main kernel of a call with a pair of HIP events on its
 // stream while kernel timing is switched on (qcnn_timing_enable); does
-// nothing otherwise.  The pairs are read back by qcnn_timing_read.
+// nothing otherwise (or when `enabled` is false: the allocation-free path
+// creates no events).  The pairs are read back by qcnn_timing_read.
 class KernelTimer {
  public:
-  explicit KernelTimer(hipStream_t stream);
+  explicit KernelTimer(hipStream_t stream, bool enabled = true);
   ~KernelTimer();
   KernelTimer(const KernelTimer&) = delete;
   KernelTimer& operator=(const KernelTimer&) = delete;
@@ -196,12 +214,21 @@ class Scratch {
   Scratch(const Scratch&) = delete;
   Scratch& operator=(const Scratch&) = delete;
   hipError_t acquire(hipStream_t stream, size_t bytes);
+  // `bytes` of the caller's workspace when `ws` is given (nothing is
+  // allocated or locked; hipErrorOutOfMemory if it is too small), else
+  // acquire(stream, bytes).
+  hipError_t take(hipStream_t stream, size_t bytes, const Workspace* ws);
   char* get() const { return static_cast<char*>(ptr_); }
 
  private:
   void* slot_ = nullptr;
   void* ptr_ = nullptr;
 };
+
+// The allocation-free conv forward's device scratch (noalloc.hip): its size,
+// and its address on the current device (looked up once per device).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(char** ptr);
 
 // Lets `kernel` take up to kLdsBytes of dynamic LDS (once per device).
 hipError_t allow_max_lds(const void* kernel);

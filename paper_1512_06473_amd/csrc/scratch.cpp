@@ -77,6 +77,13 @@ hipError_t Scratch::acquire(hipStream_t stream, size_t bytes) {
   return hipSuccess;
 }
 
+hipError_t Scratch::take(hipStream_t stream, size_t bytes, const Workspace* ws) {
+  if (!ws) return acquire(stream, bytes);
+  if (bytes > ws->bytes) return hipErrorOutOfMemory;
+  ptr_ = ws->ptr;
+  return hipSuccess;
+}
+
 hipError_t allow_max_lds(const void* kernel) {
   static std::mutex mu;
   static auto* done = new std::set<std::pair<int, const void*>>();

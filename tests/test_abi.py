@@ -60,11 +60,11 @@ def test_version_status_outsize(L):
     assert L.qcnn_out_size(0, 1, 1, 0) == 0
 
 
-def conv(L, **kw):
+def conv(L, entry="qcnn_conv_forward", **kw):
     a = dict(x=FAKE, N=2, Cs=8, H=5, W=5, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, Ct=4, dk=3, s=1, p=1,
              bias=None, relu=0, y=FAKE2, stream=None)
     a.update(kw)
-    return L.qcnn_conv_forward(a["x"], a["N"], a["Cs"], a["H"], a["W"], a["D"], a["M"], a["K"], a["Csp"],
+    return getattr(L, entry)(a["x"], a["N"], a["Cs"], a["H"], a["W"], a["D"], a["M"], a["K"], a["Csp"],
                                a["codes"], a["Ct"], a["dk"], a["s"], a["p"], a["bias"], a["relu"], a["y"],
                                a["stream"])
 
@@ -96,6 +96,18 @@ NULL, SHAPE, KR, UNSUP, ALIAS = 1, 2, 3, 6, 7
 ])
 def test_conv_rejects(L, kw, want):
     assert conv(L, **kw) == want
+    # the allocation-free variant validates the same way, before any HIP call
+    assert conv(L, "qcnn_conv_forward_noalloc", **kw) == want
+
+
+def test_noalloc_rejects_layers_beyond_its_scratch(L):
+    # AlexNet conv3 at N = 64 (256 -> 384, 13x13, 3x3 pad 1, C's = 4, K = 128)
+    # needs more temporaries than the static scratch holds: refused on the
+    # host, before any HIP call (the fake addresses are never touched).
+    X, Y, D, C = 1 << 40, 2 << 40, 3 << 40, 4 << 40
+    st = L.qcnn_conv_forward_noalloc(X, 64, 256, 13, 13, D, 64, 128, 4, C, 384, 3, 1, 1, None, 0, Y, None)
+    assert st == 8 and _lib.STATUS[st] == "QCNN_ERR_WORKSPACE"
+    assert b"noalloc" in L.qcnn_status_string(8)
 
 
 @pytest.mark.parametrize("kw,want", [
