@@ -10,16 +10,26 @@ epilogue, all in the library's HIP kernel.  Prints ONE JSON line.
 
 Timing: W untimed warm-up steps, then K steps between two HIP events on the
 stream the kernels run on, with a device synchronize on both sides; that
-gives `value` and `ms_per_step`.  A second pass of K steps switches on the
-library's kernel timing (HIP events recorded by the library on the same
-stream around the main gather kernel of each call) and gives the kernel's
-average duration, from which the roofline's `achieved` is computed.  A step
-also runs a code re-layout kernel and, when the subspaces are split over
-workgroups, a split-sum kernel; those are outside the kernel timing.
+gives `value` and `ms_per_step`.  Then max(50, K) steps with an event
+between consecutive steps give the per-step median and minimum
+(`step_ms_stats`), and max(50, K) steps with the library's kernel timing on
+(HIP events recorded by the library on the same stream around the main
+gather kernel of each call) give every launch's duration: the roofline's
+`achieved` uses their mean (what a rocprofv3 kernel trace averages), and
+their median and minimum are reported beside it.  A step also runs a code
+re-layout kernel and, when the subspaces are split over workgroups, a
+split-sum kernel; those are outside the kernel timing but inside the step.
+
+Before the headline, the library's peak probes measure this device's LDS
+read rate (bytes per clock per CU, and the shader clock under that load)
+and HBM stream rates; `peaks` reports them beside the published figures and
+the roofline also gives its fraction of the measured LDS peak.
 
 The other four workloads (the small conv, the fc6-shaped FC layer, the
-VGG-conv3-shaped conv and the AlexNet-shaped forward) are timed the same way
-and reported under "per_config".
+VGG-conv3-shaped conv and the AlexNet-shaped forward, with a row per layer)
+are timed the same way and reported under "per_config"; `lut_build` times
+the exported table of the headline layer against its HBM roofline; the CPU
+baseline times the oracle on all threads and on one.
 """
 from __future__ import annotations
 
@@ -145,6 +155,36 @@ def main():
             api.timing_enable(False)
         total, n = api.timing_read()
         return total / n, n
+
+    def kernel_launches(step, n):
+        """Per-launch durations (ms) of the main kernels of `n` back-to-back
+        steps, from the library's HIP events on the launch stream."""
+        api.timing_read_each(1)  # drop anything recorded earlier
+        api.timing_enable(True)
+        try:
+            for _ in range(n):
+                step()
+        finally:
+            api.timing_enable(False)
+        return api.timing_read_each(64 * n)
+
+    def step_times(step, n, warmup):
+        """GPU time of each of `n` back-to-back steps (events between steps)."""
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize(dev)
+        stream = torch.cuda.current_stream(dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record(stream)
+        for i in range(n):
+            step()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize(dev)
+        return [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+
+    def stats(xs, scale=1.0):
+        a = np.asarray(xs, dtype=np.float64) * scale
+        return {"mean": float(a.mean()), "median": float(np.median(a)), "min": float(a.min()), "n": int(a.size)}
 
     if args.only == "copy":
         # Plain device-to-device copy of a known size: the calibration run for
@@ -277,22 +317,53 @@ def main():
         print(json.dumps({"only": args.only, "ms_per_step": ms, "hbm_bytes_per_step": nbytes}))
         return
     if args.only:
-        step, wl, _ = make_step(args.only)
+        if args.only == "lut_build":
+            d = workloads.generate("alexnet_conv3_n32")
+            xl, Dl = T(d["x"]), T(d["layers"][0]["D"])
+            lut = api.lut_build(xl, Dl)
+            step = lambda: api.lut_build(xl, Dl, out=lut)  # noqa: E731
+        else:
+            step, wl, _ = make_step(args.only)
         ms, _ = time_steps(step, args.steps, args.warmup)
         kms, kn = kernel_ms(step, args.steps)
         print(json.dumps({"only": args.only, "ms_per_step": ms, "main_kernel_us": kms * 1e3,
                           "main_kernel_launches": kn}))
         return
 
+    # ------------------------------------------------------ measured peaks
+    # The roofline denominators measured on this device: conflict-free 128-bit
+    # LDS reads on every CU (with the shader clock under that load) and HBM
+    # stream rates, reported beside the published figures.
+    lds_peak = api.probe_lds(dev)
+    hbm_peak = api.probe_hbm(2 << 30, dev)
+    peaks = {
+        "lds": {"measured_bytes_per_clk_cu": lds_peak["bytes_per_clk_cu"],
+                "measured_shader_clock_ghz": lds_peak["clock_ghz"],
+                "measured_GB_s": lds_peak["bytes_per_s"] / 1e9,
+                "spec_bytes_per_clk_cu": workmodel.LDS_READ_BYTES_PER_CLK_PER_CU,
+                "spec_clock_ghz": workmodel.CLOCK_HZ / 1e9,
+                "spec_GB_s": workmodel.LDS_PEAK_BPS / 1e9,
+                "probe": "qcnn_probe_lds: one 1024-thread workgroup per CU, ds_read_b128 in 1 KB contiguous runs"},
+        "hbm": {"measured_read_GB_s": hbm_peak["read_bytes_per_s"] / 1e9,
+                "measured_write_GB_s": hbm_peak["write_bytes_per_s"] / 1e9,
+                "measured_copy_GB_s": hbm_peak["copy_bytes_per_s"] / 1e9,
+                "spec_GB_s": workmodel.HBM_PEAK_BPS / 1e9,
+                "probe": "qcnn_probe_hbm: 16-byte loads, stores, and both, over 2 GiB buffers"},
+    }
+
     # ---------------------------------------------------------------- headline
     step, wl, data = make_step("alexnet_conv3_n32")
     ms, wall_ms = time_steps(step, args.steps, args.warmup)
-    kms, klaunches = kernel_ms(step, args.steps)
+    nl = max(50, args.steps)
+    steps_ms = step_times(step, nl, 2)
+    kl = kernel_launches(step, nl)
+    kms = float(np.mean(kl))
     w = work_of(wl)
     sec = ms * 1e-3
     images_s = wl.N / sec
     lds_achieved = w["lds"] / (kms * 1e-3)
     traffic = measured_traffic("conv_flat", "alexnet_conv3_n32")
+    frac = lds_achieved / workmodel.LDS_PEAK_BPS
     line = {
         "metric": "images/s (AlexNet-conv3-shaped PQ conv layer; also effective dense GFLOP/s and LDS roofline %)",
         "value": images_s,
@@ -309,38 +380,116 @@ def main():
         "config": {"workload": "alexnet_conv3_n32: PQ conv 32x256x13x13 -> 384, 3x3 s1 p1, C's=4 (M=64), K=128",
                    "global_batch": wl.N, "parallelism": "none (1 GPU)"},
         "effective_dense_gflops": w["dense_flops"] / sec / 1e9,
+        "step_ms_stats": stats(steps_ms),
         "roofline": {
             "bound": "lds",
             "achieved": lds_achieved / 1e9,
             "peak": workmodel.LDS_PEAK_BPS / 1e9,
             "unit": "GB/s",
-            "frac": lds_achieved / workmodel.LDS_PEAK_BPS,
+            "frac": frac,
             "traffic": traffic,
             "kernel": "conv_flat_kernel (fused table build + gather-accumulate)",
             "kernel_us": kms * 1e3,
-            "kernel_launches_timed": klaunches,
+            "kernel_us_stats": stats(kl, 1e3),
+            "frac_at_median_kernel": w["lds"] / (float(np.median(kl)) * 1e-3) / workmodel.LDS_PEAK_BPS,
+            "frac_at_best_kernel": w["lds"] / (float(np.min(kl)) * 1e-3) / workmodel.LDS_PEAK_BPS,
+            "frac_of_measured_peak": lds_achieved / lds_peak["bytes_per_s"],
+            "step_frac": w["lds"] / sec / workmodel.LDS_PEAK_BPS,
+            "target_frac": 0.5,
+            "target_met": bool(frac >= 0.5),
+            "kernel_launches_timed": len(kl),
             "algorithmic_bytes_per_launch": w["lds"],
             "hbm_frac": w["hbm"] / (kms * 1e-3) / workmodel.HBM_PEAK_BPS,
         },
+        "peaks": peaks,
         "wall_ms_per_step": wall_ms,
     }
 
     # ------------------------------------------------------------ other configs
     per = {}
     extra = [] if args.configs == "none" else [c for c in args.configs.split(",") if c]
+    main_kernel = {"small_conv_n1": "conv_flat", "alexnet_fc6_n128": "fc_tiled", "vgg16_conv3_n16": "conv_flat"}
     for cfg in extra:
-        st, wlc, _ = make_step(cfg)
+        st, wlc, dc = make_step(cfg)
         steps = max(5, args.steps // (10 if cfg in ("vgg16_conv3_n16", "alexnet_n64") else 1))
         m, _ = time_steps(st, steps, max(2, args.warmup // 2))
-        km, kn = kernel_ms(st, steps)
+        nlc = max(50, steps)
+        kl = kernel_launches(st, nlc)
+        per_step = max(1, len(kl) // nlc)
         wc = work_of(wlc)
-        s = m * 1e-3
-        per[cfg] = {"ms_per_step": m, "images_s": wlc.N / s, "effective_dense_gflops": wc["dense_flops"] / s / 1e9,
-                    "lds_frac": wc["lds"] / s / workmodel.LDS_PEAK_BPS,
-                    "hbm_frac": wc["hbm"] / s / workmodel.HBM_PEAK_BPS, "steps": steps,
-                    "main_kernels_ms_per_step": km * kn / steps, "main_kernel_launches_per_step": kn // steps}
+        s_ = m * 1e-3
+        row = {"ms_per_step": m, "images_s": wlc.N / s_, "effective_dense_gflops": wc["dense_flops"] / s_ / 1e9,
+               "lds_frac": wc["lds"] / s_ / workmodel.LDS_PEAK_BPS,
+               "hbm_frac": wc["hbm"] / s_ / workmodel.HBM_PEAK_BPS, "steps": steps,
+               "step_ms_stats": stats(step_times(st, nlc, 1)),
+               "main_kernels_ms_per_step": float(np.sum(kl)) / nlc, "main_kernel_launches_per_step": per_step}
+        if cfg in main_kernel:
+            row["kernel_us_stats"] = stats(kl, 1e3)
+            row["kernel_lds_frac"] = wc["lds"] / (float(np.mean(kl)) * 1e-3) / workmodel.LDS_PEAK_BPS
+            row["traffic"] = measured_traffic(main_kernel[cfg], cfg)
+        if cfg == "alexnet_n64":
+            # Table 1 per layer: the main kernel of every PQ layer (launch order
+            # = layer order) and each layer's whole GPU time (its code
+            # re-layout and split-sum kernels included; pools are layers too).
+            net = Network(dc["layers"], dev)
+            xin = T(dc["x"])
+            nlayers = len(net.layers)
+            stream = torch.cuda.current_stream(dev)
+            reps = 20
+            acc = np.zeros(nlayers)
+            for r in range(reps + 2):
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(nlayers + 1)]
+                h = xin
+                ev[0].record(stream)
+                for i, Lyr in enumerate(net.layers):
+                    h = Lyr(h)
+                    ev[i + 1].record(stream)
+                torch.cuda.synchronize(dev)
+                if r >= 2:
+                    acc += [ev[i].elapsed_time(ev[i + 1]) for i in range(nlayers)]
+            layer_ms = acc / reps
+            karr = np.asarray(kl[: per_step * nlc]).reshape(nlc, per_step)
+            rows, ki = [], 0
+            names = {"conv": 0, "fc": 5, "pool": 0}
+            for i, ((kind, lw), spec) in enumerate(zip(workmodel.workload_work(wlc), dc["layers"])):
+                names[kind] += 1
+                r_ = {"layer": "%s%d" % (kind, names[kind]), "kind": kind, "layer_ms": float(layer_ms[i]),
+                      "lds_bytes": lw.lds_bytes, "dense_flops": lw.dense_flops, "hbm_bytes": lw.hbm_bytes}
+                if kind != "pool":
+                    kk = karr[:, ki]
+                    ki += 1
+                    r_["kernel_us_stats"] = stats(kk, 1e3)
+                    r_["kernel_lds_frac"] = lw.lds_bytes / (float(np.mean(kk)) * 1e-3) / workmodel.LDS_PEAK_BPS
+                    r_["layer_lds_frac"] = lw.lds_bytes / (layer_ms[i] * 1e-3) / workmodel.LDS_PEAK_BPS
+                else:
+                    r_["layer_hbm_frac"] = lw.hbm_bytes / (layer_ms[i] * 1e-3) / workmodel.HBM_PEAK_BPS
+                rows.append(r_)
+            row["per_layer"] = rows
+            row["step_lds_frac"] = row["lds_frac"]
+            row["target_step_lds_frac"] = 0.35
+            row["target_met"] = bool(row["lds_frac"] >= 0.35)
+            del net, xin, h
+        per[cfg] = row
         del st
     line["per_config"] = per
+
+    # ------------------------------------------- exported table (qcnn_lut_build)
+    # The table of Sec. 3.1's test phase written to HBM for the headline
+    # layer's input: N M K H W fp32 values, bound by HBM writes.
+    if args.configs != "none":
+        Ld = data["layers"][0]
+        xl, Dl = T(data["x"]), T(Ld["D"])
+        lut = api.lut_build(xl, Dl)
+        nl_ = 50
+        kl = kernel_launches(lambda: api.lut_build(xl, Dl, out=lut), nl_)
+        wbytes = lut.numel() * 4
+        rbytes = xl.numel() * 4 + Dl.numel() * 4
+        km = float(np.mean(kl)) * 1e-3
+        line["lut_build"] = {"table_bytes": wbytes, "input_bytes": rbytes, "kernel_us_stats": stats(kl, 1e3),
+                             "hbm_write_roofline_us": wbytes / workmodel.HBM_PEAK_BPS * 1e6,
+                             "hbm_frac": (wbytes + rbytes) / km / workmodel.HBM_PEAK_BPS,
+                             "write_frac_of_measured_write_peak": wbytes / km / hbm_peak["write_bytes_per_s"]}
+        del lut, xl, Dl
 
     # ---------------------------------------------- parameter quantizer (k-means)
     quant = {}
@@ -447,18 +596,39 @@ def main():
     if not args.no_cpu:
         from oracle import oracle
         L = data["layers"][0]
-        t0 = time.perf_counter()
-        reps = 0
-        while True:
-            oracle.conv_lut(data["x"], L["D"], L["codes"], L["stride"], L["pad"])
-            reps += 1
-            if time.perf_counter() - t0 >= 10.0:
-                break
-        el = time.perf_counter() - t0
-        line["cpu_baseline"] = {"value": reps * wl.N / el, "unit": "images/s", "cores": oracle.threads(),
-                                "kind": "oracle",
+        cpu_model = "unknown"
+        try:
+            for ln in open("/proc/cpuinfo"):
+                if ln.startswith("model name"):
+                    cpu_model = ln.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
+        all_threads = oracle.threads()
+
+        def oracle_rate(threads, n_images, seconds):
+            oracle.set_threads(threads)
+            xs = data["x"][:n_images]
+            t0 = time.perf_counter()
+            reps = 0
+            while True:
+                oracle.conv_lut(xs, L["D"], L["codes"], L["stride"], L["pad"])
+                reps += 1
+                if time.perf_counter() - t0 >= seconds:
+                    break
+            el = time.perf_counter() - t0
+            return reps * n_images / el, reps, el
+
+        r_all, reps, el = oracle_rate(all_threads, wl.N, 10.0)
+        r_one, reps1, el1 = oracle_rate(1, 4, 5.0)
+        oracle.set_threads(all_threads)
+        line["cpu_baseline"] = {"value": r_all, "unit": "images/s", "cores": all_threads,
+                                "kind": "oracle", "cpu_model": cpu_model,
                                 "sample": "%d full passes of the 32-image batch through the oracle's table path "
-                                          "(float64, OpenMP over images), %.1f s" % (reps, el)}
+                                          "(float64, OpenMP over images, %d threads), %.1f s" % (reps, all_threads, el),
+                                "one_thread": {"value": r_one, "unit": "images/s", "cores": 1,
+                                               "sample": "%d passes of 4 of the 32 images on one thread, %.1f s"
+                                                         % (reps1, el1)}}
         # the error-correction oracles on bounded samples of the same layers,
         # scaled to one sweep (their cost is linear in the subspace steps and,
         # for the conv oracle, in the images)

@@ -304,6 +304,28 @@ qcnn_status qcnn_timing_enable(int enable);
  * readable pairs only). */
 qcnn_status qcnn_timing_read(double* total_ms, long long* launches);
 
+/* The same drain with each pair's elapsed milliseconds, in launch order,
+ * written to ms_each[0 .. min(*launches, capacity)); *launches is the number
+ * of pairs read (all are destroyed, also those past `capacity`). */
+qcnn_status qcnn_timing_read_each(double* ms_each, long long capacity, long long* launches);
+
+/* Peak probes, for the benchmark's roofline denominators (not part of the
+ * paper's method).  Both synchronise with `stream` and allocate small
+ * temporaries.
+ * qcnn_probe_lds: every CU of the current device streams conflict-free
+ * 128-bit LDS reads (one 1024-thread workgroup per CU, each wave reading
+ * 1 KB contiguous runs); returns the LDS read bytes per clock per CU, the
+ * shader clock in GHz measured under that load (shader-clock counter over
+ * the constant-rate counter), and the aggregate bytes per second.
+ * qcnn_probe_hbm: streams `bytes` (a multiple of 16 is used) of the device
+ * buffer src with 16-byte loads, then fills dst with 16-byte stores, then
+ * copies src to dst; returns the read rate, the write rate and the copy rate
+ * (bytes read + written per second).  src and dst: 16-byte aligned, `bytes`
+ * long each, not overlapping; dst is overwritten. */
+qcnn_status qcnn_probe_lds(double* bytes_per_clk_cu, double* clock_ghz, double* bytes_per_s, void* stream);
+qcnn_status qcnn_probe_hbm(const void* src, void* dst, size_t bytes, double* read_bytes_per_s,
+                           double* write_bytes_per_s, double* copy_bytes_per_s, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

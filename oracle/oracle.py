@@ -51,6 +51,7 @@ def _signatures():
         "qo_pq_update": [P, I, I, I, P, I, I, I, P, P, P],
         "qo_pq_kmeans": [P, I, I, I, I, I, I, I, P, P, P],
         "qo_threads": [],
+        "qo_set_threads": [I],
         "qo_code_bits": [I],
         "qo_pack_codes": [P, ctypes.c_longlong, I, P],
         "qo_unpack_codes": [P, ctypes.c_longlong, I, P],
@@ -114,6 +115,11 @@ def _opt_f32(a):
 
 def threads() -> int:
     return lib().qo_threads()
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the oracle's parallel loops (for timing it)."""
+    lib().qo_set_threads(int(n))
 
 
 def out_size(n: int, k: int, s: int, p: int) -> int:

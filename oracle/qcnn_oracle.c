@@ -626,9 +626,12 @@ int qo_unpack_codes(const uint8_t* in, long long n, int K, uint8_t* codes) {
   return 0;
 }
 
+/* Thread count of the parallel loops (timing of the oracle only). */
 #ifdef _OPENMP
 #include <omp.h>
 int qo_threads(void) { return omp_get_max_threads(); }
+void qo_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
 #else
 int qo_threads(void) { return 1; }
+void qo_set_threads(int n) { (void)n; }
 #endif

@@ -344,6 +344,40 @@ def timing_read() -> Tuple[float, int]:
     return ms.value, n.value
 
 
+def timing_read_each(capacity: int = 4096):
+    """Per-launch milliseconds of the main kernels timed since the last read
+    (launch order; at most ``capacity`` of them)."""
+    buf = (ctypes.c_double * max(1, capacity))()
+    n = ctypes.c_longlong(0)
+    check(lib().qcnn_timing_read_each(buf, capacity, ctypes.byref(n)), "qcnn_timing_read_each")
+    return [buf[i] for i in range(min(n.value, capacity))]
+
+
+def probe_lds(device=None) -> dict:
+    """Measured LDS read peak of the device (qcnn_probe_lds): bytes per clock
+    per CU, the shader clock under load (GHz) and bytes per second."""
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    vals = [ctypes.c_double(0.0) for _ in range(3)]
+    with torch.cuda.device(dev):
+        check(lib().qcnn_probe_lds(*[ctypes.byref(v) for v in vals], torch.cuda.current_stream(dev).cuda_stream),
+              "qcnn_probe_lds")
+    return {"bytes_per_clk_cu": vals[0].value, "clock_ghz": vals[1].value, "bytes_per_s": vals[2].value}
+
+
+def probe_hbm(nbytes: int = 2 << 30, device=None) -> dict:
+    """Measured HBM stream rates (qcnn_probe_hbm) over two buffers of
+    ``nbytes``: read, write and copy (read + written) bytes per second."""
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    rd, wr, cp = ctypes.c_double(0.0), ctypes.c_double(0.0), ctypes.c_double(0.0)
+    check(lib().qcnn_probe_hbm(src.data_ptr(), dst.data_ptr(), src.numel() * 4, ctypes.byref(rd), ctypes.byref(wr),
+                               ctypes.byref(cp), _stream(src)), "qcnn_probe_hbm")
+    del src, dst
+    return {"read_bytes_per_s": rd.value, "write_bytes_per_s": wr.value, "copy_bytes_per_s": cp.value,
+            "buffer_bytes": nbytes}
+
+
 # ------------------------------------------------------ parameter quantization
 
 def _quant_w(W: torch.Tensor):

@@ -22,7 +22,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libqcnn.so")
 ARCH = os.environ.get("QCNN_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["qcnn_api.cpp", "lut_build.hip", "conv_gather.hip", "conv_flat.hip", "conv_half.hip", "fc_gather.hip", "fc_tiled.hip", "glue.hip", "quantize.hip", "ec_fc.hip", "ec_conv.hip", "scratch.cpp", "noalloc.hip"]
+SOURCES = ["qcnn_api.cpp", "lut_build.hip", "conv_gather.hip", "conv_flat.hip", "conv_half.hip", "fc_gather.hip", "fc_tiled.hip", "glue.hip", "quantize.hip", "ec_fc.hip", "ec_conv.hip", "scratch.cpp", "noalloc.hip", "peaks.hip"]
 
 CXXFLAGS = [
     "-x", "hip", "--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17",

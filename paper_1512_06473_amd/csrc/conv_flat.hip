@@ -51,6 +51,7 @@
 // (and its L2) for the input reads of the table build.
 #include <stdio.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include "qcnn_internal.h"
 
@@ -187,7 +188,14 @@ __device__ __forceinline__ void gather_stream(float (&acc)[TW][4], const uint32_
 // GEN = false: one virtual subspace per subspace (stride 1, one row group),
 // so the input offsets of the table build are fixed per lane.  GEN = true:
 // stride phases and/or row groups; the offsets move with the virtual subspace.
-template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN, bool PRIO>
+//
+// VALU = true (comparison variant, stride 1 only): the table is built with
+// fused multiply-adds on the vector ALUs instead of MFMA, into the same
+// layout.  Lane l computes lut[16 kb + l % 16][16 pb + 4 (l / 16) + r],
+// r < 4: its C's codebook values come from the staged codebook in LDS and
+// its 4 x C's input values from the lanes that loaded them for the MFMA
+// operand layout, through ds_bpermute.
+template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN, bool PRIO, bool VALU = false>
 __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __restrict__ x,
                                                                  const float* __restrict__ D,
                                                                  const uint8_t* __restrict__ codes8,
@@ -364,14 +372,16 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     // reads and scalar loads share one wait counter, so a later wait for the
     // operands would also wait for the codes.
     float bv[kMaxKB][NC];
+    if constexpr (!VALU) {
 #pragma unroll
-    for (int kb = 0; kb < kMaxKB; ++kb)
+      for (int kb = 0; kb < kMaxKB; ++kb)
 #pragma unroll
-      for (int c = 0; c < NC; ++c) bv[kb][c] = dstage[(kb * NC + c) * 64 + lane];
+        for (int c = 0; c < NC; ++c) bv[kb][c] = dstage[(kb * NC + c) * 64 + lane];
 #pragma unroll
-    for (int kb = 0; kb < kMaxKB; ++kb)
+      for (int kb = 0; kb < kMaxKB; ++kb)
 #pragma unroll
-      for (int c = 0; c < NC; ++c) asm volatile("" ::"v"(bv[kb][c]));
+        for (int c = 0; c < NC; ++c) asm volatile("" ::"v"(bv[kb][c]));
+    }
     __builtin_amdgcn_sched_barrier(0);
     // The codes of v arrive during the build.  (A barrier waits for every
     // outstanding scalar load, so issuing them before one would expose their
@@ -379,11 +389,23 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
     load_codes(v, cw);
     // ---- table build: lut[k][pos] = sum_j D[m][k][j] x[pos][m C's + j]
     // d[r] = lut[k = kb*16 + lane%16][pos = 16 pb + 4 (lane/16) + r]
+    float xq[NC][4][4];  // VALU: x[16 pb + 4 (l / 16) + r][4 c + jj] in [c][jj][r]
     auto tile = [&](int i, int kb) -> f4v {
       f4v d = zero4;
+      if constexpr (VALU) {
 #pragma unroll
-      for (int c = 0; c < NC; ++c)
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], bv[kb][c], d, 0, 0, 0);
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const float dk = dstage[(kb * NC + c) * 64 + jj * 16 + arow];  // D[16 kb + l % 16][4 c + jj]
+#pragma unroll
+            for (int r = 0; r < 4; ++r) d[r] = fmaf(dk, xq[c][jj][r], d[r]);
+          }
+      } else {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][c], bv[kb][c], d, 0, 0, 0);
+      }
       return d;
     };
     auto put = [&](int i, int kb, const f4v& d) {
@@ -392,6 +414,17 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
 #pragma unroll
     for (int i = 0; i < kMaxPB; ++i) {
       if (wave + kWaves * i >= p.npb) continue;  // wave-uniform
+      if constexpr (VALU) {
+        // av[i][c] of lane q holds x[16 pb + q % 16][4 c + q / 16].
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              xq[c][jj][r] = __int_as_float(
+                  __builtin_amdgcn_ds_bpermute((4 * acol + r + 16 * jj) * 4, __float_as_int(av[i][c])));
+      }
       if (kblocks == kMaxKB) {
         // All blocks: straight-line code, each store one MFMA behind so
         // that the next MFMA is issued while the previous result drains.
@@ -555,6 +588,7 @@ struct FlatPlan {
   int TW;
   size_t lds;
   bool prio;  // one workgroup per CU: the plain-grid kernels step their waves' issue priority
+  bool valu = false;  // build the tables on the vector ALUs (comparison variant, stride 1 only)
 };
 
 // Estimated cost (arbitrary units ~ CU clocks) of a plan, for the choice of
@@ -673,7 +707,10 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
 template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN, bool PRIO>
 hipError_t launch_kernel(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8,
                          const float* bias, float* y, float* partial, hipStream_t stream) {
-  auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN, PRIO>;
+  auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN, PRIO, false>;
+  if constexpr (!GEN) {
+    if (pl.valu) k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN, PRIO, true>;
+  }
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes8, bias, y, partial, pl.p);
@@ -775,6 +812,10 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
   if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;
   pl.p.relu = relu;
   pl.prio = pl.lds > kLdsBytes / 2;  // no second workgroup fits beside this one
+  // QCNN_TABLE_BUILD=valu: the vector-ALU table build, for comparison with
+  // the MFMA build (read per call; the strided layouts keep MFMA).
+  const char* tb = getenv("QCNN_TABLE_BUILD");
+  pl.valu = !pl.gen && tb && strcmp(tb, "valu") == 0;
   static const bool trace = getenv("QCNN_TRACE_PLAN") && *getenv("QCNN_TRACE_PLAN") == '1';
   if (trace)
     fprintf(stderr, "qcnn conv_flat: taps %dx%d%s G=%d V=%d S=%d sw=%d Wg=%d Hg=%d tiles=%d TW=%d tc=%d tblocks=%d "

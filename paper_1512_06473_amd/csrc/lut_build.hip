@@ -13,7 +13,9 @@
 // positions times KY codewords, so that for every k the stores of a wave are
 // contiguous (PX >= 64) or, for tiny maps such as a fully-connected input
 // (H = W = 1, PX = 1), contiguous along k.  Each thread loads its C'_s input
-// values once and reuses them for all of its codewords.
+// values once and reuses them for all of its codewords; the block stages the
+// subspace's K x C'_s sub-codewords in LDS first, so every codeword is read
+// from HBM once per block and then served to the threads as LDS broadcasts.
 #include "qcnn_internal.h"
 
 namespace qcnn {
@@ -23,19 +25,22 @@ template <int CSP>
 __global__ __launch_bounds__(256) void lut_build_kernel(const float* __restrict__ x, const float* __restrict__ D,
                                                         float* __restrict__ lut, int Cs, int HW, int M, int K,
                                                         int csp_rt) {
+  extern __shared__ float cb[];  // K x C'_s sub-codewords of subspace m
   const int csp = CSP > 0 ? CSP : csp_rt;
   const int m = blockIdx.y, n = blockIdx.z;
+  const float* Dm = D + (size_t)m * K * csp;
+  for (int i = threadIdx.y * blockDim.x + threadIdx.x; i < K * csp; i += blockDim.x * blockDim.y) cb[i] = Dm[i];
+  __syncthreads();
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= HW) return;
   const float* xs = x + ((size_t)n * Cs + (size_t)m * csp) * HW + p;
-  const float* Dm = D + (size_t)m * K * csp;
   float* out = lut + ((size_t)n * M + m) * (size_t)K * HW + p;
   constexpr int XCAP = CSP > 0 ? CSP : 16;
   float xv[XCAP];
 #pragma unroll
   for (int j = 0; j < XCAP; ++j) xv[j] = (j < csp) ? xs[(size_t)j * HW] : 0.f;
   for (int k = threadIdx.y; k < K; k += blockDim.y) {
-    const float* d = Dm + (size_t)k * csp;
+    const float* d = cb + k * csp;
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < XCAP; ++j)
@@ -54,10 +59,11 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
   const int ky = 256 / px;
   dim3 block(px, ky);
   dim3 grid(ceil_div(HW, px), M, N);
+  const size_t lds = (size_t)K * Csp * sizeof(float);  // <= 256 x 16 x 4 = 16 KB
   KernelTimer timer(stream);
   switch (Csp) {
 #define QCNN_LUT_CASE(C) \
-  case C: hipLaunchKernelGGL(lut_build_kernel<C>, grid, block, 0, stream, x, D, lut, Cs, HW, M, K, Csp); break;
+  case C: hipLaunchKernelGGL(lut_build_kernel<C>, grid, block, lds, stream, x, D, lut, Cs, HW, M, K, Csp); break;
     QCNN_LUT_CASE(1)
     QCNN_LUT_CASE(2)
     QCNN_LUT_CASE(3)
@@ -66,7 +72,7 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
     QCNN_LUT_CASE(8)
 #undef QCNN_LUT_CASE
     default:
-      hipLaunchKernelGGL(lut_build_kernel<0>, grid, block, 0, stream, x, D, lut, Cs, HW, M, K, Csp);
+      hipLaunchKernelGGL(lut_build_kernel<0>, grid, block, lds, stream, x, D, lut, Cs, HW, M, K, Csp);
   }
   return hipGetLastError();
 }

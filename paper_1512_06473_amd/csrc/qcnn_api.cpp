@@ -153,25 +153,44 @@ qcnn_status qcnn_timing_enable(int enable) {
   return QCNN_OK;
 }
 
-qcnn_status qcnn_timing_read(double* total_ms, long long* launches) {
-  if (!total_ms || !launches) return QCNN_ERR_NULL;
+namespace {
+
+// Reads and destroys every recorded pair; per-launch milliseconds go to
+// `each` (the first `capacity` of them, when `each` is not null).
+qcnn_status drain_timing(double* total_ms, long long* launches, double* each, long long capacity) {
   TimingState& t = timing();
   std::lock_guard<std::mutex> lock(t.mu);
   double sum = 0.0;
   bool ok = !t.failed;
+  long long i = 0;
   for (auto& pr : t.pairs) {
     float ms = 0.f;
     if (hipEventSynchronize(pr.second) != hipSuccess || hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
       ok = false;
     sum += ms;
+    if (each && i < capacity) each[i] = ms;
+    ++i;
     (void)hipEventDestroy(pr.first);
     (void)hipEventDestroy(pr.second);
   }
-  *total_ms = sum;
+  if (total_ms) *total_ms = sum;
   *launches = (long long)t.pairs.size();
   t.pairs.clear();
   t.failed = false;
   return ok ? QCNN_OK : QCNN_ERR_HIP;
+}
+
+}  // namespace
+
+qcnn_status qcnn_timing_read(double* total_ms, long long* launches) {
+  if (!total_ms || !launches) return QCNN_ERR_NULL;
+  return drain_timing(total_ms, launches, nullptr, 0);
+}
+
+qcnn_status qcnn_timing_read_each(double* ms_each, long long capacity, long long* launches) {
+  if (!ms_each || !launches) return QCNN_ERR_NULL;
+  if (capacity < 0) return QCNN_ERR_SHAPE;
+  return drain_timing(nullptr, launches, ms_each, capacity);
 }
 
 int qcnn_version(void) { return 1; }
@@ -314,6 +333,21 @@ qcnn_status qcnn_fc_forward_packed(const float* x, int N, int C_s, const float* 
                                    void* stream) {
   if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
   return fc_forward(x, N, C_s, codebooks, M, K, Csp, packed_codes, qcnn::code_bits(K), C_t, bias, relu, y, stream);
+}
+
+qcnn_status qcnn_probe_lds(double* bytes_per_clk_cu, double* clock_ghz, double* bytes_per_s, void* stream) {
+  if (!bytes_per_clk_cu || !clock_ghz || !bytes_per_s) return QCNN_ERR_NULL;
+  return hip_status(qcnn::probe_lds((hipStream_t)stream, bytes_per_clk_cu, clock_ghz, bytes_per_s));
+}
+
+qcnn_status qcnn_probe_hbm(const void* src, void* dst, size_t bytes, double* read_bytes_per_s,
+                           double* write_bytes_per_s, double* copy_bytes_per_s, void* stream) {
+  if (!src || !dst || !read_bytes_per_s || !write_bytes_per_s || !copy_bytes_per_s) return QCNN_ERR_NULL;
+  if (bytes < 16 || bytes > kMaxElems) return QCNN_ERR_SHAPE;
+  if (((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return QCNN_ERR_UNSUPPORTED;
+  if (overlap(dst, bytes, src, bytes)) return QCNN_ERR_ALIAS;
+  return hip_status(
+      qcnn::probe_hbm(src, dst, bytes, (hipStream_t)stream, read_bytes_per_s, write_bytes_per_s, copy_bytes_per_s));
 }
 
 int qcnn_code_bits(int K) {

@@ -230,6 +230,12 @@ class Scratch {
 size_t noalloc_scratch_bytes();
 hipError_t noalloc_scratch(char** ptr);
 
+// Peak probes (peaks.hip): LDS read bytes per clock per CU with the shader
+// clock measured under that load, and HBM read / write / copy bytes per second.
+hipError_t probe_lds(hipStream_t stream, double* bytes_per_clk_cu, double* clock_ghz, double* bytes_per_s);
+hipError_t probe_hbm(const void* src, void* dst, size_t bytes, hipStream_t stream, double* read_bps,
+                     double* write_bps, double* copy_bps);
+
 // Lets `kernel` take up to kLdsBytes of dynamic LDS (once per device).
 hipError_t allow_max_lds(const void* kernel);
 

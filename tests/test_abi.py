@@ -158,6 +158,23 @@ def test_timing_calls_without_gpu(L):
     assert L.qcnn_timing_enable(0) == 0
     assert L.qcnn_timing_read(ctypes.byref(ms), ctypes.byref(n)) == 0
     assert ms.value == 0.0 and n.value == 0
+    buf = (ctypes.c_double * 4)()
+    assert L.qcnn_timing_read_each(None, 4, ctypes.byref(n)) == NULL
+    assert L.qcnn_timing_read_each(buf, 4, None) == NULL
+    assert L.qcnn_timing_read_each(buf, -1, ctypes.byref(n)) == SHAPE
+    assert L.qcnn_timing_read_each(buf, 4, ctypes.byref(n)) == 0 and n.value == 0
+
+
+def test_probes_reject_bad_arguments(L):
+    d = ctypes.c_double(0.0)
+    assert L.qcnn_probe_lds(None, ctypes.byref(d), ctypes.byref(d), None) == NULL
+    r = ctypes.byref(d)
+    assert L.qcnn_probe_hbm(None, FAKE2, 1024, r, r, r, None) == NULL
+    assert L.qcnn_probe_hbm(FAKE, FAKE2, 1024, None, r, r, None) == NULL
+    assert L.qcnn_probe_hbm(FAKE, FAKE2, 1024, r, None, r, None) == NULL
+    assert L.qcnn_probe_hbm(FAKE, FAKE2, 8, r, r, r, None) == SHAPE
+    assert L.qcnn_probe_hbm(FAKE + 4, FAKE2, 1024, r, r, r, None) == UNSUP
+    assert L.qcnn_probe_hbm(FAKE, FAKE + 512, 1024, r, r, r, None) == ALIAS
 
 
 def test_quantizer_rejects(L):

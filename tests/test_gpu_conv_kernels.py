@@ -3,8 +3,10 @@
 The library picks one kernel per layer (the flattened-grid kernel where it
 can tile the layer).  QCNN_CONV_KERNEL = half puts the two-table kernel
 (conv_half.hip: half-wave table rows, a builder wave, two tables in LDS)
-first, = generic forces the simple per-subspace kernel; both are checked
-here against the CPU oracle on the headline layer (full size, float within
+first, = generic forces the simple per-subspace kernel, and
+QCNN_TABLE_BUILD = valu makes the default kernel build its tables with
+vector fused multiply-adds instead of MFMA (the comparison variant); each is
+checked here against the CPU oracle on the headline layer (full size, float within
 the bound and integer data bit for bit) and on stride-1 edge shapes (ragged
 tiles and channel blocks, column strips, 1x1 kernels, every K block count).
 """
@@ -45,9 +47,13 @@ def dev():
     return torch.device("cuda:0")
 
 
-@pytest.fixture(params=["half", "generic"])
+@pytest.fixture(params=["half", "generic", "valu"])
 def kernel(request, monkeypatch):
-    monkeypatch.setenv("QCNN_CONV_KERNEL", request.param)
+    if request.param == "valu":  # the default kernel with its tables built on the vector ALUs
+        monkeypatch.delenv("QCNN_CONV_KERNEL", raising=False)
+        monkeypatch.setenv("QCNN_TABLE_BUILD", "valu")
+    else:
+        monkeypatch.setenv("QCNN_CONV_KERNEL", request.param)
     return request.param
 
 
@@ -101,9 +107,10 @@ def test_stride1_shapes(dev, oracle, kernel, shape):
 
 
 def test_default_kernel_unchanged_by_env_cleanup(dev, oracle):
-    # With the switch unset the default kernel serves the layer again (the
-    # switch is read per call).
+    # With the switches unset the default kernel serves the layer again (they
+    # are read per call).
     os.environ.pop("QCNN_CONV_KERNEL", None)
+    os.environ.pop("QCNN_TABLE_BUILD", None)
     d = wl.generate("small_conv_n1")
     L = d["layers"][0]
     y = run_conv(dev, d["x"], L["D"], L["codes"], L["stride"], L["pad"])
