@@ -56,24 +56,33 @@ def parse():
     return ap.parse_args()
 
 
-def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch of `kernel` on `workload` from the committed
-    rocprofv3 counter summary, or None when there is none or when the kernel's
-    source has changed since the counters were taken."""
+def measured_traffic(name: str, sources, field: str = "hbm_bytes_per_launch"):
+    """HBM bytes (per launch of the main kernel, or per step) from the
+    committed rocprofv3 counter summary profiles/<name>_traffic.txt, or None
+    when there is none or when a kernel source it was taken on has changed
+    since (its sha256 is recorded in the summary)."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "%s_%s_traffic.txt" % (kernel, workload))
-    src = os.path.join(ROOT, "paper_1512_06473_amd", "csrc", "%s.hip" % kernel)
-    if not (os.path.exists(path) and os.path.exists(src)):
+    path = os.path.join(ROOT, "profiles", "%s_traffic.txt" % name)
+    if not os.path.exists(path):
         return None
-    fields = {}
+    fields, shas = {}, {}
     for line in open(path):
-        if ":" in line and not line.startswith(" "):
-            k, v = line.split(":", 1)
-            fields[k.strip()] = v.strip()
-    if fields.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
-        return None
+        if ":" not in line or line.startswith(" "):
+            continue
+        k, v = line.split(":", 1)
+        k = k.strip()
+        if k == "source_sha256":
+            shas[sources[0]] = v.strip()
+        elif k.startswith("source_sha256 "):
+            shas[k.split(" ", 1)[1].strip()] = v.strip()
+        else:
+            fields[k] = v.strip()
+    for src in sources:
+        f = os.path.join(ROOT, "paper_1512_06473_amd", "csrc", src)
+        if not os.path.exists(f) or shas.get(src) != hashlib.sha256(open(f, "rb").read()).hexdigest():
+            return None
     try:
-        return float(fields["hbm_bytes_per_launch"])
+        return float(fields[field])
     except (KeyError, ValueError):
         return None
 
@@ -336,6 +345,10 @@ def main():
     # stream rates, reported beside the published figures.
     lds_peak = api.probe_lds(dev)
     hbm_peak = api.probe_hbm(2 << 30, dev)
+    valu = api.probe_valu(dev)
+    # The headline gather's VALU work per 1 KB table read (from its code: 300
+    # plain and 132 DPP adds and 108 address multiply-adds per 108 reads).
+    read_clk = (300 * valu["add_clk"] + 132 * valu["dpp_add_clk"] + 108 * valu["mad_clk"]) / 108 / 4
     peaks = {
         "lds": {"measured_bytes_per_clk_cu": lds_peak["bytes_per_clk_cu"],
                 "measured_shader_clock_ghz": lds_peak["clock_ghz"],
@@ -344,6 +357,10 @@ def main():
                 "spec_clock_ghz": workmodel.CLOCK_HZ / 1e9,
                 "spec_GB_s": workmodel.LDS_PEAK_BPS / 1e9,
                 "probe": "qcnn_probe_lds: one 1024-thread workgroup per CU, ds_read_b128 in 1 KB contiguous runs"},
+        "valu": {"clk_per_wave_instr_per_simd": valu,
+                 "headline_gather_cu_clk_per_read": read_clk,
+                 "headline_gather_valu_bound_bytes_per_clk_cu": 1024.0 / read_clk,
+                 "probe": "qcnn_probe_valu: 16 waves per CU, independent v_add_f32 / DPP v_add_f32 / v_mad_u32_u24"},
         "hbm": {"measured_read_GB_s": hbm_peak["read_bytes_per_s"] / 1e9,
                 "measured_write_GB_s": hbm_peak["write_bytes_per_s"] / 1e9,
                 "measured_copy_GB_s": hbm_peak["copy_bytes_per_s"] / 1e9,
@@ -362,7 +379,7 @@ def main():
     sec = ms * 1e-3
     images_s = wl.N / sec
     lds_achieved = w["lds"] / (kms * 1e-3)
-    traffic = measured_traffic("conv_flat", "alexnet_conv3_n32")
+    traffic = measured_traffic("conv_flat_alexnet_conv3_n32", ["conv_flat.hip"])
     frac = lds_achieved / workmodel.LDS_PEAK_BPS
     line = {
         "metric": "images/s (AlexNet-conv3-shaped PQ conv layer; also effective dense GFLOP/s and LDS roofline %)",
@@ -426,7 +443,7 @@ def main():
         if cfg in main_kernel:
             row["kernel_us_stats"] = stats(kl, 1e3)
             row["kernel_lds_frac"] = wc["lds"] / (float(np.mean(kl)) * 1e-3) / workmodel.LDS_PEAK_BPS
-            row["traffic"] = measured_traffic(main_kernel[cfg], cfg)
+            row["traffic"] = measured_traffic("%s_%s" % (main_kernel[cfg], cfg), [main_kernel[cfg] + ".hip"])
         if cfg == "alexnet_n64":
             # Table 1 per layer: the main kernel of every PQ layer (launch order
             # = layer order) and each layer's whole GPU time (its code
@@ -465,6 +482,8 @@ def main():
                     r_["layer_hbm_frac"] = lw.hbm_bytes / (layer_ms[i] * 1e-3) / workmodel.HBM_PEAK_BPS
                 rows.append(r_)
             row["per_layer"] = rows
+            row["traffic_per_step"] = measured_traffic("alexnet_n64", ["conv_flat.hip", "fc_tiled.hip", "glue.hip"],
+                                                       "hbm_bytes_per_step")
             row["step_lds_frac"] = row["lds_frac"]
             row["target_step_lds_frac"] = 0.35
             row["target_met"] = bool(row["lds_frac"] >= 0.35)

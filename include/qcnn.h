@@ -52,7 +52,8 @@
  *     are reentrant.  A conv or FC call that needs temporary device memory
  *     (re-laid-out codes, partial sums) uses a library-owned workspace, one
  *     per (device, stream): grown in stream order on `stream` (the old one
- *     released with hipFreeAsync, a larger one taken with hipMallocAsync),
+ *     released with hipFreeAsync, a larger one taken from a memory pool the
+ *     library creates per device; the device's default pool is not touched),
  *     locked for the enqueue of one call, and held until the process ends.
  *     Concurrent calls on different streams never share it; calls on one
  *     stream use it one after the other in stream order.
@@ -289,12 +290,16 @@ const char* qcnn_status_string(qcnn_status s);
 int qcnn_version(void);
 
 /* Kernel timing, for benchmarks and profiling.  While enabled, every
- * compute call above records a pair of HIP events on its stream around its
- * main kernel (the gather kernel of qcnn_conv_forward and qcnn_fc_forward,
- * the table kernel of qcnn_lut_build, the assignment or update kernels of
+ * compute call above times its main kernel (the gather kernel of
+ * qcnn_conv_forward and qcnn_fc_forward, the table kernel of
+ * qcnn_lut_build) with a pair of HIP events that the kernel's dispatch
+ * stamps at the start and the end of its execution (hipExtLaunchKernelGGL),
+ * so the pair measures the kernel alone; the quantizer calls record a pair
+ * on their stream around their kernels (the assignment or update kernels of
  * qcnn_pq_assign / qcnn_pq_update, the whole iteration loop of
- * qcnn_pq_kmeans); code re-layout and split-sum kernels are outside the pair.  Off by default; when off the calls create no events.
- * Enabling and disabling are process-wide and take effect for later calls. */
+ * qcnn_pq_kmeans).  Code re-layout and split-sum kernels are outside the
+ * pairs.  Off by default; when off the calls create no events.  Enabling
+ * and disabling are process-wide and take effect for later calls. */
 qcnn_status qcnn_timing_enable(int enable);
 
 /* Waits for every pair recorded since the last read, returns their summed
@@ -325,6 +330,13 @@ qcnn_status qcnn_timing_read_each(double* ms_each, long long capacity, long long
 qcnn_status qcnn_probe_lds(double* bytes_per_clk_cu, double* clock_ghz, double* bytes_per_s, void* stream);
 qcnn_status qcnn_probe_hbm(const void* src, void* dst, size_t bytes, double* read_bytes_per_s,
                            double* write_bytes_per_s, double* copy_bytes_per_s, void* stream);
+
+/* VALU issue probe: 16 waves per CU on every CU, each issuing independent
+ * streams of one instruction kind; returns the shader clocks per wave64
+ * instruction per SIMD of v_add_f32, of v_add_f32 with a DPP wave_shl:1
+ * operand, and of v_mad_u32_u24 (the instructions a table read of the conv
+ * gather issues). */
+qcnn_status qcnn_probe_valu(double* add_clk, double* dpp_add_clk, double* mad_clk, void* stream);
 
 #ifdef __cplusplus
 }

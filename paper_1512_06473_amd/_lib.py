@@ -37,6 +37,7 @@ SIGNATURES = {
     "qcnn_timing_enable": ([I], I),
     "qcnn_timing_read_each": ([ctypes.POINTER(ctypes.c_double), ctypes.c_longlong,
                                ctypes.POINTER(ctypes.c_longlong)], I),
+    "qcnn_probe_valu": ([ctypes.POINTER(ctypes.c_double)] * 3 + [P], I),
     "qcnn_probe_lds": ([ctypes.POINTER(ctypes.c_double)] * 3 + [P], I),
     "qcnn_probe_hbm": ([P, P, ctypes.c_size_t] + [ctypes.POINTER(ctypes.c_double)] * 3 + [P], I),
     "qcnn_timing_read": ([ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong)], I),

@@ -364,6 +364,17 @@ def probe_lds(device=None) -> dict:
     return {"bytes_per_clk_cu": vals[0].value, "clock_ghz": vals[1].value, "bytes_per_s": vals[2].value}
 
 
+def probe_valu(device=None) -> dict:
+    """Measured VALU issue costs (qcnn_probe_valu): shader clocks per wave64
+    instruction per SIMD of v_add_f32, DPP v_add_f32 and v_mad_u32_u24."""
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    vals = [ctypes.c_double(0.0) for _ in range(3)]
+    with torch.cuda.device(dev):
+        check(lib().qcnn_probe_valu(*[ctypes.byref(v) for v in vals], torch.cuda.current_stream(dev).cuda_stream),
+              "qcnn_probe_valu")
+    return {"add_clk": vals[0].value, "dpp_add_clk": vals[1].value, "mad_clk": vals[2].value}
+
+
 def probe_hbm(nbytes: int = 2 << 30, device=None) -> dict:
     """Measured HBM stream rates (qcnn_probe_hbm) over two buffers of
     ``nbytes``: read, write and copy (read + written) bytes per second."""

@@ -84,9 +84,12 @@ constexpr int kMaxKB = 8;   // 16-codeword blocks (K <= 128)
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-// acc += (value of v in lane l+1)
+// acc += (value of v in lane l+1): a wave_shl:1 DPP move the compiler folds
+// into the add (v_add_f32_dpp), with the wait states a DPP read needs after a
+// VALU write inserted by the compiler.  Lane 63 gets 0 (bound_ctrl off and
+// old value 0); its slots belong to the next tile and are never stored.
 __device__ __forceinline__ void add_from_next_lane(float& acc, float v) {
-  asm("v_add_f32_dpp %0, %1, %0 wave_shl:1 row_mask:0xf bank_mask:0xf" : "+v"(acc) : "v"(v));
+  acc += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x130, 0xf, 0xf, false));
 }
 
 template <int R>
@@ -515,22 +518,30 @@ __global__ __launch_bounds__(256) void flat_codes_kernel(CodeStream codes, CodeM
   const int taps = q.rows * q.cols;
   const int per_v = q.ct_pad * taps;
   const int nwords = (q.V * per_v + 3) / 4;  // the plan keeps V ct_pad taps below 2^31
+  const bool plain = q.G == 1 && q.stride == 1;  // v = m, tap = (ky, kx)
   for (int wi = blockIdx.x * blockDim.x + threadIdx.x; wi < nwords; wi += gridDim.x * blockDim.x) {
+    // (v, t, tap) of the word's first byte; the other three follow by
+    // stepping tap, then t, then v (no division per byte).
+    const int o = wi * 4;
+    int v = o / per_v;
+    const int r = o - v * per_v;
+    int t = r / taps, tap = r - t * taps;
     uint32_t word = 0;
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
-      const int o = wi * 4 + bb;
-      const int v = o / per_v;
-      const int r = o - v * per_v;
-      const int t = r / taps, tap = r - t * taps;
       uint32_t val = 0;
       if (v < q.V && t < q.Ct) {
-        const int g = v % q.G;
-        int rr = v / q.G;
-        const int pb = rr % q.stride;
-        rr /= q.stride;
-        const int pa = rr % q.stride, m = rr / q.stride;
-        const int ky = q.stride * (g * q.rows + tap / q.cols) + pa, kx = q.stride * (tap % q.cols) + pb;
+        int m = v, ky = tap / q.cols, kx = tap - ky * q.cols;
+        if (!plain) {
+          const int g = v % q.G;
+          int rr = v / q.G;
+          const int pb = rr % q.stride;
+          rr /= q.stride;
+          const int pa = rr % q.stride;
+          m = rr / q.stride;
+          ky = q.stride * (g * q.rows + ky) + pa;
+          kx = q.stride * kx + pb;
+        }
         if (ky < q.dk && kx < q.dk) {
           val = code_at(codes, (((size_t)t * q.dk + ky) * q.dk + kx) * q.M + m);
           val = val < (uint32_t)(q.K - 1) ? val : (uint32_t)(q.K - 1);
@@ -539,6 +550,13 @@ __global__ __launch_bounds__(256) void flat_codes_kernel(CodeStream codes, CodeM
         }
       }
       word |= val << (8 * bb);
+      if (++tap == taps) {
+        tap = 0;
+        if (++t == q.ct_pad) {
+          t = 0;
+          ++v;
+        }
+      }
     }
     codes8[wi] = word;
   }
@@ -706,24 +724,25 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
 
 template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN, bool PRIO>
 hipError_t launch_kernel(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8,
-                         const float* bias, float* y, float* partial, hipStream_t stream) {
+                         const float* bias, float* y, float* partial, hipStream_t stream, LaunchTimer* timer) {
   auto k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN, PRIO, false>;
   if constexpr (!GEN) {
     if (pl.valu) k = conv_flat_kernel<ROWS, COLS, WG4, NC, TW, GEN, PRIO, true>;
   }
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes8, bias, y, partial, pl.p);
-  return hipGetLastError();
+  return timed_launch(timer, k, dim3(8 * pl.p.per_xcd), dim3(kThreads), (uint32_t)pl.lds, stream, x, D, codes8, bias, y,
+                      partial, pl.p);
 }
 
 template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
 hipError_t launch_main(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
-                       float* y, float* partial, hipStream_t stream) {
+                       float* y, float* partial, hipStream_t stream, LaunchTimer* timer) {
   if constexpr (!GEN) {
-    if (pl.prio) return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, true>(pl, x, D, codes8, bias, y, partial, stream);
+    if (pl.prio)
+      return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, true>(pl, x, D, codes8, bias, y, partial, stream, timer);
   }
-  return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, false>(pl, x, D, codes8, bias, y, partial, stream);
+  return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, false>(pl, x, D, codes8, bias, y, partial, stream, timer);
 }
 
 struct LaunchArgs {
@@ -734,6 +753,7 @@ struct LaunchArgs {
   float* y;
   float* partial;
   hipStream_t stream;
+  LaunchTimer* timer;
 };
 
 template <int ROWS, int COLS, int WG4, bool GEN>
@@ -741,11 +761,11 @@ hipError_t launch_nc(const FlatPlan& pl, const LaunchArgs& a) {
   if (pl.p.Csp <= 4) {
     if constexpr (!GEN) {
       if (pl.TW == 12) return launch_main<ROWS, COLS, WG4, 1, 12, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial,
-                                                                       a.stream);
+                                                                       a.stream, a.timer);
     }
-    return launch_main<ROWS, COLS, WG4, 1, 8, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream);
+    return launch_main<ROWS, COLS, WG4, 1, 8, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream, a.timer);
   }
-  return launch_main<ROWS, COLS, WG4, 2, 8, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream);
+  return launch_main<ROWS, COLS, WG4, 2, 8, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream, a.timer);
 }
 
 template <int ROWS, int COLS, bool GEN>
@@ -837,8 +857,8 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
                      stream, codes, cm, reinterpret_cast<uint32_t*>(codes8));
   e = hipGetLastError();
   if (e == hipSuccess) {
-    KernelTimer timer(stream, ws == nullptr);
-    e = launch_plan(pl, LaunchArgs{x, D, codes8, bias, y, partial, stream});
+    LaunchTimer timer(ws == nullptr);
+    e = launch_plan(pl, LaunchArgs{x, D, codes8, bias, y, partial, stream, &timer});
   }
   if (e == hipSuccess && partial) {
     hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)ceil_div_z(partial_elems / p.splits, 256)), dim3(256), 0,

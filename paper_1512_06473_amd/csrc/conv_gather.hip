@@ -185,9 +185,8 @@ hipError_t launch_g(const ConvPtrs& a, const ConvParams& p, dim3 grid, size_t ld
   auto k = conv_pq_generic<CSP, G, kTW>;
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
-  KernelTimer timer(stream, a.timed);
-  hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, stream, a.x, a.D, a.codes, a.bias, a.y, p);
-  return hipGetLastError();
+  LaunchTimer timer(a.timed);
+  return timed_launch(&timer, k, grid, dim3(kThreads), (uint32_t)lds, stream, a.x, a.D, a.codes, a.bias, a.y, p);
 }
 
 template <int CSP>

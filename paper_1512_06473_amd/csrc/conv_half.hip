@@ -672,6 +672,7 @@ struct HalfArgs {
   float* y;
   float* partial;
   hipStream_t stream;
+  LaunchTimer* timer;
 };
 
 template <int ROWS, int COLS, int NC, int TWP, int KBL, bool BLD>
@@ -679,9 +680,8 @@ hipError_t launch_k(const HalfPlan& pl, const HalfArgs& a) {
   auto k = conv_half_kernel<ROWS, COLS, NC, TWP, KBL, BLD>;
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, a.stream, a.x, a.D, a.rowoff, a.bias, a.y,
-                     a.partial, pl.p);
-  return hipGetLastError();
+  return timed_launch(a.timer, k, dim3(8 * pl.p.per_xcd), dim3(kThreads), (uint32_t)pl.lds, a.stream, a.x, a.D,
+                      a.rowoff, a.bias, a.y, a.partial, pl.p);
 }
 
 template <int ROWS, int COLS, int NC, int TWP, bool BLD>
@@ -763,8 +763,8 @@ hipError_t launch_conv_half(const ConvShape& s, const float* x, const float* D, 
                      stream, codes, cm, (int)n_ro, rowoff);
   e = hipGetLastError();
   if (e == hipSuccess) {
-    KernelTimer timer(stream, ws == nullptr);
-    const HalfArgs a{x, D, rowoff, bias, y, partial, stream};
+    LaunchTimer timer(ws == nullptr);
+    const HalfArgs a{x, D, rowoff, bias, y, partial, stream, &timer};
     e = s.dk == 1 ? launch_taps<1, 1>(pl, a) : launch_taps<3, 3>(pl, a);
   }
   if (e == hipSuccess && partial) {

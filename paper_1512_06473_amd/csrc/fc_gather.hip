@@ -166,9 +166,8 @@ hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const
   }
   e = allow_max_lds((const void*)kern);
   if (e == hipSuccess) {
-    KernelTimer timer(stream);
-    hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, x, D, codes, bias, y, partial, p);
-    e = hipGetLastError();
+    LaunchTimer timer;
+    e = timed_launch(&timer, kern, grid, dim3(kThreads), (uint32_t)lds, stream, x, D, codes, bias, y, partial, p);
   }
   if (e == hipSuccess && splits > 1) {
     const size_t total = (size_t)N * Ct;

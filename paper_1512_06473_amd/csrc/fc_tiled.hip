@@ -453,25 +453,25 @@ bool make_fc_plan(int N, int Cs, int M, int K, int Csp, int Ct, FcPlan* out) {
 
 template <int LPC, int NC, int KB>
 hipError_t launch_t(const FcPlan& pl, const float* x, const float* D, const uint32_t* codes4, const float* bias,
-                    float* y, float* partial, hipStream_t stream) {
+                    float* y, float* partial, hipStream_t stream, LaunchTimer* timer) {
   auto k = fc_tiled_kernel<LPC, NC, KB, 4>;
   if constexpr (LPC == 16 && KB <= 2) {  // the only tables small enough for 8 subspaces per phase
     if (pl.p.MC == 8) k = fc_tiled_kernel<LPC, NC, KB, 8>;
   }
   hipError_t e = allow_max_lds((const void*)k);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, dim3(8 * pl.p.per_xcd), dim3(kThreads), pl.lds, stream, x, D, codes4, bias, y, partial, pl.p);
-  return hipGetLastError();
+  return timed_launch(timer, k, dim3(8 * pl.p.per_xcd), dim3(kThreads), (uint32_t)pl.lds, stream, x, D, codes4, bias, y,
+                      partial, pl.p);
 }
 
 template <int LPC, int NC>
 hipError_t launch_kb(const FcPlan& pl, const float* x, const float* D, const uint32_t* codes4, const float* bias,
-                     float* y, float* partial, hipStream_t stream) {
+                     float* y, float* partial, hipStream_t stream, LaunchTimer* timer) {
   switch (pl.KB) {
-    case 1: return launch_t<LPC, NC, 1>(pl, x, D, codes4, bias, y, partial, stream);
-    case 2: return launch_t<LPC, NC, 2>(pl, x, D, codes4, bias, y, partial, stream);
-    case 3: return launch_t<LPC, NC, 3>(pl, x, D, codes4, bias, y, partial, stream);
-    default: return launch_t<LPC, NC, 4>(pl, x, D, codes4, bias, y, partial, stream);
+    case 1: return launch_t<LPC, NC, 1>(pl, x, D, codes4, bias, y, partial, stream, timer);
+    case 2: return launch_t<LPC, NC, 2>(pl, x, D, codes4, bias, y, partial, stream, timer);
+    case 3: return launch_t<LPC, NC, 3>(pl, x, D, codes4, bias, y, partial, stream, timer);
+    default: return launch_t<LPC, NC, 4>(pl, x, D, codes4, bias, y, partial, stream, timer);
   }
 }
 
@@ -506,13 +506,13 @@ hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const f
                      dim3(256), 0, stream, codes, Ct, M, K, p.mgroups, p.ct_pad, codes4);
   e = hipGetLastError();
   if (e == hipSuccess) {
-    KernelTimer timer(stream);
+    LaunchTimer timer;
     if (pl.LPC == 16)
-      e = pl.NC == 1 ? launch_kb<16, 1>(pl, x, D, codes4, bias, y, partial, stream)
-                     : launch_kb<16, 2>(pl, x, D, codes4, bias, y, partial, stream);
+      e = pl.NC == 1 ? launch_kb<16, 1>(pl, x, D, codes4, bias, y, partial, stream, &timer)
+                     : launch_kb<16, 2>(pl, x, D, codes4, bias, y, partial, stream, &timer);
     else
-      e = pl.NC == 1 ? launch_kb<32, 1>(pl, x, D, codes4, bias, y, partial, stream)
-                     : launch_kb<32, 2>(pl, x, D, codes4, bias, y, partial, stream);
+      e = pl.NC == 1 ? launch_kb<32, 1>(pl, x, D, codes4, bias, y, partial, stream, &timer)
+                     : launch_kb<32, 2>(pl, x, D, codes4, bias, y, partial, stream, &timer);
   }
   if (e == hipSuccess && partial) {
     const int NT = p.nblocks * p.NS;

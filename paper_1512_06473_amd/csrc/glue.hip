@@ -93,15 +93,4 @@ hipError_t launch_code_check(CodeStream codes, size_t n, int K, int* bad, hipStr
   return hipGetLastError();
 }
 
-hipError_t retain_pool_memory() {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  hipMemPool_t pool;
-  e = hipDeviceGetDefaultMemPool(&pool, dev);
-  if (e != hipSuccess) return e;
-  uint64_t threshold = UINT64_MAX;
-  return hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
-}
-
 }  // namespace qcnn

@@ -60,10 +60,10 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
   dim3 block(px, ky);
   dim3 grid(ceil_div(HW, px), M, N);
   const size_t lds = (size_t)K * Csp * sizeof(float);  // <= 256 x 16 x 4 = 16 KB
-  KernelTimer timer(stream);
+  LaunchTimer timer;
   switch (Csp) {
 #define QCNN_LUT_CASE(C) \
-  case C: hipLaunchKernelGGL(lut_build_kernel<C>, grid, block, lds, stream, x, D, lut, Cs, HW, M, K, Csp); break;
+  case C: return timed_launch(&timer, lut_build_kernel<C>, grid, block, (uint32_t)lds, stream, x, D, lut, Cs, HW, M, K, Csp);
     QCNN_LUT_CASE(1)
     QCNN_LUT_CASE(2)
     QCNN_LUT_CASE(3)
@@ -72,9 +72,8 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
     QCNN_LUT_CASE(8)
 #undef QCNN_LUT_CASE
     default:
-      hipLaunchKernelGGL(lut_build_kernel<0>, grid, block, lds, stream, x, D, lut, Cs, HW, M, K, Csp);
+      return timed_launch(&timer, lut_build_kernel<0>, grid, block, (uint32_t)lds, stream, x, D, lut, Cs, HW, M, K, Csp);
   }
-  return hipGetLastError();
 }
 
 }  // namespace qcnn

@@ -10,8 +10,12 @@
 // against the constant-rate counter (s_memrealtime) over each workgroup's
 // loop.
 //
-// HBM: grid-stride streams of 16-byte loads over a caller buffer (read), of
-// 16-byte stores to a second buffer (write), and of both (copy).
+// VALU: clocks per wave64 instruction per SIMD for the three instructions a
+// gather read issues (plain add, DPP add, address multiply-add).
+//
+// HBM: streams of 16-byte loads over a caller buffer (read), of 16-byte
+// stores to a second buffer (write), and of both (copy), one 16 KB chunk per
+// 256-thread block over the whole buffer.
 #include <algorithm>
 #include <vector>
 
@@ -63,27 +67,90 @@ __global__ __launch_bounds__(kLdsProbeThreads, 1) void lds_probe_kernel(uint32_t
   }
 }
 
+// VALU issue probe: 16 waves per CU (4 per SIMD), each running kValuIters
+// iterations of 8 independent instructions of one kind (chains 8 apart, so
+// no dependency stalls), timed by wave 0 with s_memtime between two
+// barriers.  MODE 0: v_add_f32; 1: v_add_f32 with a DPP wave_shl:1 operand
+// (its source registers are not written in the loop); 2: v_mad_u32_u24.
+constexpr int kValuIters = 4096;
+
+template <int MODE>
+__global__ __launch_bounds__(1024, 1) void valu_probe_kernel(uint32_t* __restrict__ sink,
+                                                             unsigned long long* __restrict__ stamps) {
+  const int tid = threadIdx.x;
+  float f[8], g[8];
+  uint32_t u[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    f[k] = (float)(tid + k);
+    g[k] = 1.0f / (float)(k + 1 + (tid & 7));
+    u[k] = (uint32_t)(tid * 8 + k);
+  }
+  const uint32_t cm = (uint32_t)(tid & 255) | 1u, ca = (uint32_t)tid >> 3;
+  __syncthreads();
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  for (int it = 0; it < kValuIters; ++it) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if constexpr (MODE == 0) f[k] += g[k];
+      // The instruction itself, written out so that the compiler neither
+      // hoists the loop-invariant DPP move nor widens the 24-bit multiply;
+      // the DPP source g[k] is written only before the loop (no VALU-write /
+      // DPP-read hazard inside it).
+      if constexpr (MODE == 1)
+        asm volatile("v_add_f32_dpp %0, %1, %0 wave_shl:1 row_mask:0xf bank_mask:0xf" : "+v"(f[k]) : "v"(g[k]));
+      if constexpr (MODE == 2) asm volatile("v_mad_u32_u24 %0, %0, %1, %2" : "+v"(u[k]) : "v"(cm), "v"(ca));
+    }
+  }
+  __syncthreads();
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  uint32_t acc = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc ^= __float_as_uint(f[k]) ^ u[k];
+  sink[blockIdx.x * 1024 + tid] = acc;
+  if (tid == 0) stamps[blockIdx.x] = t1 - t0;
+}
+
+// Each thread handles 4 consecutive-by-256 uint4 of a 1024-element chunk per
+// block (coalesced 4 KB per wave), one chunk per block over the whole buffer.
 __global__ __launch_bounds__(256) void hbm_read_kernel(const uint4* __restrict__ src, size_t n16,
                                                        uint32_t* __restrict__ sink) {
+  const size_t base = (size_t)blockIdx.x * 1024 + threadIdx.x;
   uint32_t acc = 0;
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) {
-    const uint4 v = src[i];
-    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const size_t i = base + 256 * k;
+    if (i < n16) {
+      const uint4 v = src[i];
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
   }
-  sink[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = acc;
+  if (acc == 0x9e3779b9u) sink[threadIdx.x] = acc;  // practically never: keeps the loads live
 }
 
 __global__ __launch_bounds__(256) void hbm_write_kernel(uint4* __restrict__ dst, size_t n16) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
-    dst[i] = make_uint4((uint32_t)i, 1u, 2u, 3u);
+  const size_t base = (size_t)blockIdx.x * 1024 + threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const size_t i = base + 256 * k;
+    if (i < n16) dst[i] = make_uint4((uint32_t)i, 1u, 2u, 3u);
+  }
 }
 
 __global__ __launch_bounds__(256) void hbm_copy_kernel(const uint4* __restrict__ src, size_t n16,
                                                        uint4* __restrict__ dst) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
+  const size_t base = (size_t)blockIdx.x * 1024 + threadIdx.x;
+  uint4 v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const size_t i = base + 256 * k;
+    if (i < n16) v[k] = src[i];
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const size_t i = base + 256 * k;
+    if (i < n16) dst[i] = v[k];
+  }
 }
 
 // Elapsed milliseconds of `launch` enqueued `reps` times between two events.
@@ -146,16 +213,47 @@ hipError_t probe_lds(hipStream_t stream, double* bytes_per_clk_cu, double* clock
   return hipSuccess;
 }
 
-hipError_t probe_hbm(const void* src, void* dst, size_t bytes, hipStream_t stream, double* read_bps,
-                     double* write_bps, double* copy_bps) {
+hipError_t probe_valu(hipStream_t stream, double* add_clk, double* dpp_add_clk, double* mad_clk) {
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
-  const size_t n16 = bytes / 16;
-  const unsigned blocks = (unsigned)(cus * 16);
+  if (cus < 1) return hipErrorInvalidValue;
   uint32_t* sink = nullptr;
-  e = hipMalloc((void**)&sink, (size_t)blocks * 256 * sizeof(uint32_t));
+  unsigned long long* stamps = nullptr;
+  e = hipMalloc((void**)&sink, (size_t)cus * 1024 * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&stamps, (size_t)cus * sizeof(unsigned long long));
+  double* out[3] = {add_clk, dpp_add_clk, mad_clk};
+  std::vector<unsigned long long> host(cus);
+  for (int mode = 0; mode < 3 && e == hipSuccess; ++mode) {
+    for (int rep = 0; rep < 2 && e == hipSuccess; ++rep) {  // the first launch warms the clock up
+      if (mode == 0) hipLaunchKernelGGL(valu_probe_kernel<0>, dim3(cus), dim3(1024), 0, stream, sink, stamps);
+      if (mode == 1) hipLaunchKernelGGL(valu_probe_kernel<1>, dim3(cus), dim3(1024), 0, stream, sink, stamps);
+      if (mode == 2) hipLaunchKernelGGL(valu_probe_kernel<2>, dim3(cus), dim3(1024), 0, stream, sink, stamps);
+      e = hipGetLastError();
+      if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    }
+    if (e == hipSuccess) e = hipMemcpy(host.data(), stamps, host.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost);
+    if (e == hipSuccess) {
+      std::vector<unsigned long long> h(host);
+      std::sort(h.begin(), h.end());
+      // clocks per wave instruction on one SIMD: 4 waves per SIMD, 8 per iteration
+      *out[mode] = (double)h[h.size() / 2] / (4.0 * 8.0 * kValuIters);
+    }
+  }
+  if (sink) (void)hipFree(sink);
+  if (stamps) (void)hipFree(stamps);
+  return e;
+}
+
+hipError_t probe_hbm(const void* src, void* dst, size_t bytes, hipStream_t stream, double* read_bps,
+                     double* write_bps, double* copy_bps) {
+  const size_t n16 = bytes / 16;
+  const size_t nblk = (n16 + 1023) / 1024;
+  if (nblk > 0x7fffffffu) return hipErrorInvalidValue;
+  const unsigned blocks = (unsigned)nblk;
+  uint32_t* sink = nullptr;
+  hipError_t e = hipMalloc((void**)&sink, 256 * sizeof(uint32_t));
   float ms = 0.f;
   const int reps = 5;
   auto rd = [&]() {

@@ -56,20 +56,11 @@ qcnn_status check_pq(int N, int Cs, int M, int K, int Csp) {
 
 qcnn_status hip_status(hipError_t e) { return e == hipSuccess ? QCNN_OK : QCNN_ERR_HIP; }
 
-// Once per device: keep memory freed by hipFreeAsync in the default pool, so
-// the per-call workspaces are recycled instead of remapped.
+// Once per device: create the library's memory pool (the per-call
+// workspaces are recycled from it instead of remapped).
 bool prepare_device() {
-  static std::mutex mu;
-  static bool done[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return false;
-  if (dev >= 64) return true;
-  std::lock_guard<std::mutex> lock(mu);
-  if (!done[dev]) {
-    if (qcnn::retain_pool_memory() != hipSuccess) return false;
-    done[dev] = true;
-  }
-  return true;
+  hipMemPool_t pool = nullptr;
+  return qcnn::library_pool(&pool) == hipSuccess;
 }
 
 // Bytes of the stream of n codes of `bits` bits each as the library writes
@@ -86,7 +77,7 @@ qcnn_status check_codes(qcnn::CodeStream codes, size_t n, int K, hipStream_t st,
   int* bad = counter;
   int host = 0;
   hipError_t e = hipSuccess;
-  if (!bad) e = hipMallocAsync((void**)&bad, sizeof(int), st);
+  if (!bad) e = qcnn::pool_alloc((void**)&bad, sizeof(int), st);
   if (e != hipSuccess) return QCNN_ERR_HIP;
   e = qcnn::launch_code_check(codes, n, K, bad, st);
   if (e == hipSuccess) e = hipMemcpyAsync(&host, bad, sizeof(int), hipMemcpyDeviceToHost, st);
@@ -142,6 +133,28 @@ KernelTimer::~KernelTimer() {
   }
   std::lock_guard<std::mutex> lock(t.mu);
   t.pairs.emplace_back(start_, stop);
+}
+
+LaunchTimer::LaunchTimer(bool enabled) {
+  if (!enabled || !timing().on.load(std::memory_order_relaxed)) return;
+  if (hipEventCreate(&start_) != hipSuccess || hipEventCreate(&stop_) != hipSuccess) {
+    if (start_) (void)hipEventDestroy(start_);
+    if (stop_) (void)hipEventDestroy(stop_);
+    start_ = stop_ = nullptr;
+    std::lock_guard<std::mutex> lock(timing().mu);
+    timing().failed = true;
+  }
+}
+
+LaunchTimer::~LaunchTimer() {
+  if (!start_) return;
+  if (!launched_) {
+    (void)hipEventDestroy(start_);
+    (void)hipEventDestroy(stop_);
+    return;
+  }
+  std::lock_guard<std::mutex> lock(timing().mu);
+  timing().pairs.emplace_back(start_, stop_);
 }
 
 }  // namespace qcnn
@@ -338,6 +351,11 @@ qcnn_status qcnn_fc_forward_packed(const float* x, int N, int C_s, const float* 
 qcnn_status qcnn_probe_lds(double* bytes_per_clk_cu, double* clock_ghz, double* bytes_per_s, void* stream) {
   if (!bytes_per_clk_cu || !clock_ghz || !bytes_per_s) return QCNN_ERR_NULL;
   return hip_status(qcnn::probe_lds((hipStream_t)stream, bytes_per_clk_cu, clock_ghz, bytes_per_s));
+}
+
+qcnn_status qcnn_probe_valu(double* add_clk, double* dpp_add_clk, double* mad_clk, void* stream) {
+  if (!add_clk || !dpp_add_clk || !mad_clk) return QCNN_ERR_NULL;
+  return hip_status(qcnn::probe_valu((hipStream_t)stream, add_clk, dpp_add_clk, mad_clk));
 }
 
 qcnn_status qcnn_probe_hbm(const void* src, void* dst, size_t bytes, double* read_bytes_per_s,

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -125,6 +126,38 @@ class KernelTimer {
   hipEvent_t start_ = nullptr;
 };
 
+// Times one kernel launch exactly while kernel timing is on: its two events
+// go to hipExtLaunchKernelGGL, which stamps them at the dispatch's start and
+// end (an event recorded before the launch would also count the dispatch
+// latency).  The pair is handed to qcnn_timing_read by the destructor once
+// launched() was called; with timing off (or `enabled` false) both events are
+// null and the launch is a plain one.
+class LaunchTimer {
+ public:
+  explicit LaunchTimer(bool enabled = true);
+  ~LaunchTimer();
+  LaunchTimer(const LaunchTimer&) = delete;
+  LaunchTimer& operator=(const LaunchTimer&) = delete;
+  hipEvent_t start() const { return start_; }
+  hipEvent_t stop() const { return stop_; }
+  void launched() { launched_ = true; }
+
+ private:
+  hipEvent_t start_ = nullptr, stop_ = nullptr;
+  bool launched_ = false;
+};
+
+// hipExtLaunchKernelGGL with the events of `t` (may be null: no timing).
+template <typename... Args, typename F = void (*)(Args...)>
+hipError_t timed_launch(LaunchTimer* t, F kernel, const dim3& grid, const dim3& block, uint32_t lds,
+                        hipStream_t stream, Args... args) {
+  hipExtLaunchKernelGGL(kernel, grid, block, lds, stream, t ? t->start() : nullptr, t ? t->stop() : nullptr, 0,
+                        args...);
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess && t) t->launched();
+  return e;
+}
+
 // FC layer with tables of 4 subspaces per phase and 128-bit gathers over
 // images (fc_tiled.hip): K <= 64, C's <= 8.
 bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct);
@@ -196,9 +229,13 @@ hipError_t launch_ec_conv(int N, int Cs, int H, int W, int Ct, int dk, int strid
                           const float* S, const float* T, float* D, uint8_t* codes, int sweeps, int inner,
                           double* objective, hipStream_t stream);
 
-// Keep freed stream-ordered allocations in the device's default pool
-// (called once per device before the first hipMallocAsync).
-hipError_t retain_pool_memory();
+// The library's own stream-ordered memory pool on the current device
+// (scratch.cpp): created on first use, it keeps freed memory for reuse (its
+// release threshold is unlimited) and leaves the device's default pool, and
+// every other user of it, untouched.
+hipError_t library_pool(hipMemPool_t* pool);
+// hipMallocFromPoolAsync from the library pool; free with hipFreeAsync.
+hipError_t pool_alloc(void** ptr, size_t bytes, hipStream_t stream);
 
 // LDS per workgroup on gfx950.
 constexpr size_t kLdsBytes = 160 * 1024;
@@ -235,6 +272,7 @@ hipError_t noalloc_scratch(char** ptr);
 hipError_t probe_lds(hipStream_t stream, double* bytes_per_clk_cu, double* clock_ghz, double* bytes_per_s);
 hipError_t probe_hbm(const void* src, void* dst, size_t bytes, hipStream_t stream, double* read_bps,
                      double* write_bps, double* copy_bps);
+hipError_t probe_valu(hipStream_t stream, double* add_clk, double* dpp_add_clk, double* mad_clk);
 
 // Lets `kernel` take up to kLdsBytes of dynamic LDS (once per device).
 hipError_t allow_max_lds(const void* kernel);

@@ -7,8 +7,9 @@
 // keeps one buffer per (device, stream) instead:
 //   * grown in stream order: the old buffer is released with hipFreeAsync on
 //     the same stream (after the calls that used it) and a larger one is
-//     taken with hipMallocAsync;
-//   * held until the process ends (the default pool keeps it);
+//     taken from the library's own memory pool (hipMallocFromPoolAsync);
+//   * held until the process ends (the library pool keeps freed memory;
+//     the device's default pool is left as the application set it);
 //   * locked for the whole enqueue of a call, so that two host threads that
 //     share a stream cannot interleave their kernels over one buffer.
 // Calls on different streams use different buffers and never wait for each
@@ -66,7 +67,7 @@ hipError_t Scratch::acquire(hipStream_t stream, size_t bytes) {
     // Round up to 2 MiB and to 5/4 of the request, so that a few layers of
     // growing size do not each trigger a new allocation.
     const size_t want = ((bytes + bytes / 4) + ((size_t)2 << 20) - 1) & ~(((size_t)2 << 20) - 1);
-    e = hipMallocAsync(&s->ptr, want, stream);
+    e = pool_alloc(&s->ptr, want, stream);
     if (e != hipSuccess) {
       s->ptr = nullptr;
       return e;
@@ -75,6 +76,44 @@ hipError_t Scratch::acquire(hipStream_t stream, size_t bytes) {
   }
   ptr_ = s->ptr;
   return hipSuccess;
+}
+
+hipError_t library_pool(hipMemPool_t* pool) {
+  static std::mutex mu;
+  static auto* pools = new std::map<int, hipMemPool_t>();
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = pools->find(dev);
+  if (it != pools->end()) {
+    *pool = it->second;
+    return hipSuccess;
+  }
+  hipMemPoolProps props = {};
+  props.allocType = hipMemAllocationTypePinned;
+  props.handleTypes = hipMemHandleTypeNone;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = dev;
+  hipMemPool_t p = nullptr;
+  e = hipMemPoolCreate(&p, &props);
+  if (e != hipSuccess) return e;
+  uint64_t threshold = UINT64_MAX;  // keep freed memory for the next call
+  e = hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &threshold);
+  if (e != hipSuccess) {
+    (void)hipMemPoolDestroy(p);
+    return e;
+  }
+  (*pools)[dev] = p;  // kept until the process ends
+  *pool = p;
+  return hipSuccess;
+}
+
+hipError_t pool_alloc(void** ptr, size_t bytes, hipStream_t stream) {
+  hipMemPool_t pool = nullptr;
+  hipError_t e = library_pool(&pool);
+  if (e != hipSuccess) return e;
+  return hipMallocFromPoolAsync(ptr, bytes, pool, stream);
 }
 
 hipError_t Scratch::take(hipStream_t stream, size_t bytes, const Workspace* ws) {

@@ -168,6 +168,7 @@ def test_timing_calls_without_gpu(L):
 def test_probes_reject_bad_arguments(L):
     d = ctypes.c_double(0.0)
     assert L.qcnn_probe_lds(None, ctypes.byref(d), ctypes.byref(d), None) == NULL
+    assert L.qcnn_probe_valu(ctypes.byref(d), None, ctypes.byref(d), None) == NULL
     r = ctypes.byref(d)
     assert L.qcnn_probe_hbm(None, FAKE2, 1024, r, r, r, None) == NULL
     assert L.qcnn_probe_hbm(FAKE, FAKE2, 1024, None, r, r, None) == NULL
