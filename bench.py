@@ -142,7 +142,9 @@ def main():
         return e0.elapsed_time(e1) / steps, wall * 1e3 / steps
 
     def work_of(wl):
-        per_layer = workmodel.workload_work(wl)
+        # per library call: a conv and its max-pool are one call whose full
+        # output map never reaches HBM
+        per_layer = workmodel.call_work(wl)
         tot = dict(dense_flops=0, gathers=0, lut=0, lds=0, hbm=0)
         for _, w in per_layer:
             tot["dense_flops"] += w.dense_flops
@@ -468,9 +470,14 @@ def main():
             karr = np.asarray(kl[: per_step * nlc]).reshape(nlc, per_step)
             rows, ki = [], 0
             names = {"conv": 0, "fc": 5, "pool": 0}
-            for i, ((kind, lw), spec) in enumerate(zip(workmodel.workload_work(wlc), dc["layers"])):
-                names[kind] += 1
-                r_ = {"layer": "%s%d" % (kind, names[kind]), "kind": kind, "layer_ms": float(layer_ms[i]),
+            cw = workmodel.call_work(wlc)
+            assert [k for k, _ in cw] == [Lyr.name for Lyr in net.layers]
+            for i, (kind, lw) in enumerate(cw):
+                label = []
+                for part in kind.split("+"):
+                    names[part] += 1
+                    label.append("%s%d" % (part, names[part]))
+                r_ = {"layer": "+".join(label), "kind": kind, "layer_ms": float(layer_ms[i]),
                       "lds_bytes": lw.lds_bytes, "dense_flops": lw.dense_flops, "hbm_bytes": lw.hbm_bytes}
                 if kind != "pool":
                     kk = karr[:, ki]

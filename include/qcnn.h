@@ -112,6 +112,25 @@ qcnn_status qcnn_fc_forward(const float* x, int N, int C_s,
                             const uint8_t* codes, int C_t,
                             const float* bias, int relu, float* y, void* stream);
 
+/* qcnn_conv_forward followed by max pooling over pool_k x pool_k windows
+ * with stride pool_s and no padding (the pooling between the PQ conv layers
+ * of the AlexNet-shaped forward; Sec. 5.2 quantizes such networks layer by
+ * layer):
+ *   y[n][t][py][px] = max_{dy,dx < pool_k} z[n][t][py pool_s + dy][px pool_s + dx],
+ * z the output of qcnn_conv_forward with the same arguments (bias, ReLU),
+ * H_p = floor((H_o - pool_k) / pool_s) + 1 (likewise W_p).
+ * y (output): [N][C_t][H_p][W_p]; every other argument as in
+ * qcnn_conv_forward.  Equal, bit for bit, to qcnn_conv_forward then
+ * qcnn_maxpool2d.  A layer whose subspaces are split over workgroups takes
+ * the window maxima in the kernel that adds the splits' partial sums, so z
+ * never goes to memory; otherwise z lives in the library's workspace.
+ * QCNN_ERR_SHAPE for pool_k < 1, pool_s < 1 or an empty pooled map. */
+qcnn_status qcnn_conv_pool_forward(const float* x, int N, int C_s, int H, int W,
+                                   const float* codebooks, int M, int K, int Csp,
+                                   const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                                   const float* bias, int relu, int pool_k, int pool_s,
+                                   float* y, void* stream);
+
 /* qcnn_conv_forward for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): the same arguments, limits, kernels and results (bit for bit),

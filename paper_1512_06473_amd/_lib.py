@@ -26,6 +26,7 @@ SIGNATURES = {
     "qcnn_status_string": ([I], ctypes.c_char_p),
     "qcnn_version": ([], I),
     "qcnn_conv_forward_noalloc": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
+    "qcnn_conv_pool_forward": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, I, I, P, P], I),
     "qcnn_conv_forward_packed": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
     "qcnn_fc_forward_packed": ([P, I, I, P, I, I, I, P, I, P, I, P, P], I),
     "qcnn_code_bits": ([I], I),

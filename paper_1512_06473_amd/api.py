@@ -80,7 +80,17 @@ def conv_forward_noalloc(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.
     return _conv_call("qcnn_conv_forward_noalloc", x, codebooks, codes, stride, pad, bias, relu, out)
 
 
-def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out):
+def conv_pool_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor, stride: int, pad: int,
+                      pool_k: int, pool_s: int, bias: Optional[torch.Tensor] = None, relu: bool = False,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """conv_forward followed by pool_k x pool_k / stride pool_s max pooling
+    (qcnn_conv_pool_forward), equal bit for bit to conv_forward then
+    maxpool2d.  Returns y [N][C_t][H_p][W_p]."""
+    return _conv_call("qcnn_conv_pool_forward", x, codebooks, codes, stride, pad, bias, relu, out,
+                      pool=(int(pool_k), int(pool_s)))
+
+
+def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out, pool=None):
     _need(x, "x", torch.float32, 4)
     _need(codebooks, "codebooks", torch.float32, 3, x.device)
     _need(codes, "codes", torch.uint8, 4, x.device)
@@ -90,6 +100,8 @@ def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out):
     if dk != dk2 or M2 != M:
         raise ValueError("codes shape %s does not match [C_t][d_k][d_k][M=%d]" % (tuple(codes.shape), M))
     Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
+    if pool is not None:
+        Ho, Wo = out_size(Ho, pool[0], pool[1], 0), out_size(Wo, pool[0], pool[1], 0)
     bp = 0
     if bias is not None:
         _need(bias, "bias", torch.float32, 1, x.device)
@@ -101,9 +113,10 @@ def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out):
     _need(out, "out", torch.float32, 4, x.device)
     if tuple(out.shape) != (N, Ct, Ho, Wo):
         raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), (N, Ct, Ho, Wo)))
+    extra = () if pool is None else pool
     check(getattr(lib(), entry)(x.data_ptr(), N, Cs, H, W, codebooks.data_ptr(), M, K, Csp,
                                 codes.data_ptr(), Ct, dk, stride, pad, bp or None, int(bool(relu)),
-                                out.data_ptr(), _stream(x)), entry)
+                                *extra, out.data_ptr(), _stream(x)), entry)
     return out
 
 

@@ -597,6 +597,93 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   y[(((size_t)n * p.Ct + t) * p.Ho + yo) * p.Wo + xo] = s;
 }
 
+// split_reduce_kernel followed by max pooling, in one pass: one workgroup
+// per channel t and group of G consecutive images (G H_o W_o <=
+// kPoolMapMax).  The group's grid slots are one run of consecutive tiles;
+// for each tile the workgroup reads the channel's 1 KB block of partials of
+// every split (one float per thread, whole cache lines; two tiles' loads in
+// flight), adds the splits in order, adds the bias and rectifies exactly as
+// above, and puts each valid output of the group into LDS; the pooled
+// outputs are then window maxima over LDS, written as runs of H_p W_p
+// contiguous values.  The result equals the split sum followed by the
+// max-pool kernel bit for bit; the full map never goes to memory.  Groups
+// are mapped XCD-major with the image group fastest, so the tile two
+// neighbouring groups share is read from the same L2.
+constexpr int kPoolMapMax = 8192;
+constexpr int kPoolImages = 8;
+
+struct PoolGroups {
+  int G, groups;  // images per workgroup, image groups
+};
+
+__device__ __forceinline__ float split_sum(const float* __restrict__ partial, size_t per_split, size_t idx,
+                                           int splits) {
+  float s = 0.f;
+  int k = 0;
+  for (; k + 4 <= splits; k += 4) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = partial[(size_t)(k + u) * per_split + idx];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s += v[u];
+  }
+  for (; k < splits; ++k) s += partial[(size_t)k * per_split + idx];
+  return s;
+}
+
+__global__ __launch_bounds__(256) void split_reduce_pool_kernel(const float* __restrict__ partial, FlatParams p,
+                                                                PoolSpec q, PoolGroups pg,
+                                                                const float* __restrict__ bias,
+                                                                float* __restrict__ y) {
+  extern __shared__ float map[];  // [G][H_o][W_o] outputs of the group
+  const int units = p.Ct * pg.groups;
+  const int per_xcd = (units + 7) / 8;
+  const int w = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
+  if (w >= units) return;  // whole workgroup, before the barrier
+  const int grp = w % pg.groups, t = w / pg.groups;
+  const int n0 = grp * pg.G, nimg = min(pg.G, p.N - n0);
+  const int plane = p.S * p.Hg * p.Wg;  // grid slots of one image
+  const int start = n0 * plane, end = start + nimg * plane;
+  const size_t per_split = (size_t)p.tiles * p.ct_pad * 256;
+  const int lane = threadIdx.x & 63, j = threadIdx.x >> 6;
+  const float b = bias ? bias[t] : 0.f;
+  auto place = [&](int tile, float s) {
+    const int slot = tile * kTileSlots + 4 * lane + j;
+    if (lane == kWave - 1 || slot < start || slot >= end) return;
+    const int local = slot - start;
+    const int img = local / plane, rem = local - img * plane;
+    const int row = rem / p.Wg, xl = rem - row * p.Wg;
+    const int strip = row / p.Hg, yo = row - strip * p.Hg;
+    const int xo = strip * p.sw + xl;
+    if (yo >= p.Ho || xl >= p.sw || xo >= p.Wo) return;
+    if (bias) s += b;
+    if (p.relu) s = fmaxf(s, 0.f);
+    map[(img * p.Ho + yo) * p.Wo + xo] = s;
+  };
+  const int t_end = (end - 1) / kTileSlots;
+  int tile = start / kTileSlots;
+  for (; tile + 1 <= t_end; tile += 2) {
+    const size_t idx = ((size_t)tile * p.ct_pad + t) * 256 + threadIdx.x;
+    const float s0 = split_sum(partial, per_split, idx, p.splits);
+    const float s1 = split_sum(partial, per_split, idx + (size_t)p.ct_pad * 256, p.splits);
+    place(tile, s0);
+    place(tile + 1, s1);
+  }
+  if (tile <= t_end) place(tile, split_sum(partial, per_split, ((size_t)tile * p.ct_pad + t) * 256 + threadIdx.x,
+                                           p.splits));
+  __syncthreads();
+  const int per_img = q.Hp * q.Wp;
+  for (int i = threadIdx.x; i < nimg * per_img; i += blockDim.x) {
+    const int img = i / per_img, r = i - img * per_img;
+    const int py = r / q.Wp, px = r - py * q.Wp;
+    const float* win = map + (img * p.Ho + py * q.s) * p.Wo + px * q.s;
+    float best = win[0];
+    for (int dy = 0; dy < q.k; ++dy)
+      for (int dx = 0; dx < q.k; ++dx) best = fmaxf(best, win[dy * p.Wo + dx]);
+    y[((size_t)(n0 + img) * p.Ct + t) * per_img + r] = best;
+  }
+}
+
 
 
 struct FlatPlan {
@@ -826,10 +913,18 @@ size_t conv_flat_workspace(const ConvShape& s) {
   return make_plan(s, &pl) ? flat_ws(pl).total : 0;
 }
 
+bool conv_flat_pools(const ConvShape& s) {
+  FlatPlan pl;
+  return make_plan(s, &pl) && pl.p.splits > 1 && s.Ho * s.Wo <= kPoolMapMax &&
+         (long long)s.N * s.Ct <= 0x7ffffff0LL;
+}
+
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws) {
+                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws,
+                            const PoolSpec* pool) {
   FlatPlan pl;
   if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;
+  if (pool && (pl.p.splits < 2 || s.Ho * s.Wo > kPoolMapMax)) return hipErrorInvalidConfiguration;
   pl.p.relu = relu;
   pl.prio = pl.lds > kLdsBytes / 2;  // no second workgroup fits beside this one
   // QCNN_TABLE_BUILD=valu: the vector-ALU table build, for comparison with
@@ -857,10 +952,19 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
                      stream, codes, cm, reinterpret_cast<uint32_t*>(codes8));
   e = hipGetLastError();
   if (e == hipSuccess) {
-    LaunchTimer timer(ws == nullptr);
+    LaunchTimer timer(ws == nullptr || ws->timed);
     e = launch_plan(pl, LaunchArgs{x, D, codes8, bias, y, partial, stream, &timer});
   }
-  if (e == hipSuccess && partial) {
+  if (e == hipSuccess && partial && pool) {
+    PoolGroups pg;
+    pg.G = std::max(1, std::min(std::min(kPoolImages, p.N), kPoolMapMax / (s.Ho * s.Wo)));
+    pg.groups = ceil_div(p.N, pg.G);
+    const unsigned units = (unsigned)((size_t)p.Ct * pg.groups);
+    hipLaunchKernelGGL(split_reduce_pool_kernel, dim3((units + 7) / 8 * 8), dim3(256),
+                       (uint32_t)((size_t)pg.G * s.Ho * s.Wo * sizeof(float)), stream, partial, p, *pool, pg, bias,
+                       y);
+    e = hipGetLastError();
+  } else if (e == hipSuccess && partial) {
     hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)ceil_div_z(partial_elems / p.splits, 256)), dim3(256), 0,
                        stream, partial, p, bias, y);
     e = hipGetLastError();

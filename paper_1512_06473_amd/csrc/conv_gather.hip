@@ -247,7 +247,7 @@ hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* 
   if (kind == ConvKernel::kHalf) return launch_conv_half(s, x, D, codes, bias, relu, y, stream, ws);
   Tiling t;
   if (!choose_tiling(s, &t)) return hipErrorInvalidConfiguration;
-  const ConvPtrs a{x, D, codes, bias, y, ws == nullptr};
+  const ConvPtrs a{x, D, codes, bias, y, ws == nullptr || ws->timed};
   ConvParams p;
   p.N = s.N;
   p.Cs = s.Cs;
@@ -279,6 +279,25 @@ hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* 
     case 8: return launch_csp<8>(a, p, t.G, grid, t.lds, stream);
     default: return launch_csp<0>(a, p, t.G, grid, t.lds, stream);
   }
+}
+
+hipError_t launch_conv_pool_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
+                                    const float* bias, int relu, const PoolSpec& pool, float* y,
+                                    hipStream_t stream) {
+  if (pick_conv_kernel(s) == ConvKernel::kFlat && conv_flat_pools(s))
+    return launch_conv_flat(s, x, D, codes, bias, relu, y, stream, nullptr, &pool);
+  // One library buffer holds the layer's own temporaries and, after them,
+  // its full output map, which the max-pool kernel reads.
+  const size_t conv_ws = (conv_forward_workspace(s) + 255) & ~(size_t)255;
+  const size_t full = (size_t)s.N * s.Ct * s.Ho * s.Wo * sizeof(float);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, conv_ws + full);
+  if (e != hipSuccess) return e;
+  float* ymap = reinterpret_cast<float*>(scratch.get() + conv_ws);
+  const Workspace ws{scratch.get(), conv_ws, true};
+  e = launch_conv_forward(s, x, D, codes, bias, relu, ymap, stream, &ws);
+  if (e != hipSuccess) return e;
+  return launch_maxpool(ymap, s.N, s.Ct, s.Ho, s.Wo, pool.k, pool.s, pool.Hp, pool.Wp, y, stream);
 }
 
 }  // namespace qcnn

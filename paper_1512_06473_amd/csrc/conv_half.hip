@@ -763,7 +763,7 @@ hipError_t launch_conv_half(const ConvShape& s, const float* x, const float* D, 
                      stream, codes, cm, (int)n_ro, rowoff);
   e = hipGetLastError();
   if (e == hipSuccess) {
-    LaunchTimer timer(ws == nullptr);
+    LaunchTimer timer(ws == nullptr || ws->timed);
     const HalfArgs a{x, D, rowoff, bias, y, partial, stream, &timer};
     e = s.dk == 1 ? launch_taps<1, 1>(pl, a) : launch_taps<3, 3>(pl, a);
   }

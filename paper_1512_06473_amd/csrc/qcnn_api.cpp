@@ -247,19 +247,25 @@ qcnn_status qcnn_lut_build(const float* x, int N, int C_s, int H, int W, const f
 
 namespace {
 
-// Body of qcnn_conv_forward (bits = 8), qcnn_conv_forward_packed and (with
-// noalloc) qcnn_conv_forward_noalloc.
+// Body of qcnn_conv_forward (bits = 8), qcnn_conv_forward_packed, (with
+// noalloc) qcnn_conv_forward_noalloc and (with pool_k > 0)
+// qcnn_conv_pool_forward.
 qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M, int K,
                          int Csp, const uint8_t* codes, int bits, int C_t, int d_k, int stride, int pad,
-                         const float* bias, int relu, float* y, void* stream, bool noalloc = false) {
+                         const float* bias, int relu, float* y, void* stream, bool noalloc = false,
+                         int pool_k = 0, int pool_s = 0) {
   if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
   if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0) return QCNN_ERR_SHAPE;
   qcnn_status s = check_pq(N, C_s, M, K, Csp);
   if (s != QCNN_OK) return s;
   const int Ho = qcnn_out_size(H, d_k, stride, pad), Wo = qcnn_out_size(W, d_k, stride, pad);
   if (Ho < 1 || Wo < 1) return QCNN_ERR_SHAPE;
+  const bool pooled = pool_k != 0 || pool_s != 0;
+  const int Hp = pooled ? qcnn_out_size(Ho, pool_k, pool_s, 0) : Ho;
+  const int Wp = pooled ? qcnn_out_size(Wo, pool_k, pool_s, 0) : Wo;
+  if (pooled && (pool_k < 1 || pool_s < 1 || Hp < 1 || Wp < 1)) return QCNN_ERR_SHAPE;
   const size_t nx = elems({N, C_s, H, W}), nd = elems({M, K, Csp}), nc = elems({C_t, d_k, d_k, M});
-  const size_t ny = elems({N, C_t, Ho, Wo});
+  const size_t ny = elems({N, C_t, Hp, Wp});
   if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
   const size_t cb = code_stream_bytes(nc, bits);
   if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, cb) ||
@@ -286,6 +292,9 @@ qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const flo
   if (!prepare_device()) return QCNN_ERR_HIP;
   s = check_codes(cs, nc, K, st);
   if (s != QCNN_OK) return s;
+  if (pooled)
+    return hip_status(qcnn::launch_conv_pool_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0,
+                                                     qcnn::PoolSpec{pool_k, pool_s, Hp, Wp}, y, st));
   return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0, y, st));
 }
 
@@ -319,6 +328,15 @@ qcnn_status qcnn_conv_forward(const float* x, int N, int C_s, int H, int W, cons
                               int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
                               const float* bias, int relu, float* y, void* stream) {
   return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, codes, 8, C_t, d_k, stride, pad, bias, relu, y, stream);
+}
+
+qcnn_status qcnn_conv_pool_forward(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M,
+                                   int K, int Csp, const uint8_t* codes, int C_t, int d_k, int stride, int pad,
+                                   const float* bias, int relu, int pool_k, int pool_s, float* y, void* stream) {
+  if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
+  if (pool_k < 1 || pool_s < 1) return QCNN_ERR_SHAPE;
+  return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, codes, 8, C_t, d_k, stride, pad, bias, relu, y, stream,
+                      false, pool_k, pool_s);
 }
 
 qcnn_status qcnn_conv_forward_noalloc(const float* x, int N, int C_s, int H, int W, const float* codebooks, int M,

@@ -62,11 +62,21 @@ hipError_t launch_lut_build(const float* x, int N, int Cs, int H, int W, const f
 
 // Device memory a call brings for its temporaries in place of the
 // library's per-stream buffer (the allocation-free entry point's static
-// array): nothing is allocated, and a call that needs more than `bytes`
-// fails with hipErrorOutOfMemory before it launches anything.
+// array, or a region of a buffer the caller already holds): nothing is
+// allocated, and a call that needs more than `bytes` fails with
+// hipErrorOutOfMemory before it launches anything.  `timed`: the main kernel
+// is timed as on the allocating path (the allocation-free path records no
+// events).
 struct Workspace {
   char* ptr;
   size_t bytes;
+  bool timed = false;
+};
+
+// Max pooling of a conv layer's output, k x k windows with stride s and no
+// padding, to an H_p x W_p map.
+struct PoolSpec {
+  int k, s, Hp, Wp;
 };
 
 // Returns hipErrorInvalidConfiguration when no tiling fits the device.
@@ -78,6 +88,14 @@ hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* 
 // Bytes of temporaries launch_conv_forward needs for this layer with the
 // kernel it would pick now (host-side, no HIP call).
 size_t conv_forward_workspace(const ConvShape& s);
+
+// The conv layer followed by max pooling, y: [N][C_t][H_p][W_p].  A layer
+// whose subspaces the stride-1/strided flat kernel splits over workgroups
+// takes the window maxima in its split-sum kernel; any other layer writes
+// its full map to a temporary that the max-pool kernel reads.
+hipError_t launch_conv_pool_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
+                                    const float* bias, int relu, const PoolSpec& pool, float* y,
+                                    hipStream_t stream);
 
 hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
                              CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream);
@@ -100,8 +118,14 @@ bool conv_supported(const ConvShape& s);
 // Stride-1 kernel on the flattened padded grid (conv_flat.hip).
 bool conv_flat_supported(const ConvShape& s);
 size_t conv_flat_workspace(const ConvShape& s);
+// True when the flat kernel's plan for this layer splits the subspaces over
+// workgroups and an output map fits its pooled split-sum kernel (which then
+// takes the pooling maxima).
+bool conv_flat_pools(const ConvShape& s);
+// With `pool`, y is the pooled map; only for a layer with conv_flat_pools.
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws);
+                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws,
+                            const PoolSpec* pool = nullptr);
 
 // Stride-1 3x3 / 1x1 kernel with two tables in LDS and half-wave table rows
 // (conv_half.hip): C'_s <= 8, K <= 128.

@@ -1,8 +1,11 @@
 """A stack of PQ layers run through the C ABI on one stream (no host syncs).
 
 Used for the AlexNet-shaped forward: conv (ReLU fused in the gather's
-epilogue) -> max-pool -> ... -> FC.  Every layer is one library call; the
-activations between layers are torch tensors used as device memory only.
+epilogue) -> max-pool -> ... -> FC.  A conv layer followed by a max-pool is
+one library call (qcnn_conv_pool_forward: the pooling is taken where the
+conv's split partial sums are added); every other layer is one call of its
+own.  The activations between calls are torch tensors used as device memory
+only.
 """
 from __future__ import annotations
 
@@ -15,8 +18,13 @@ from . import api
 
 
 class DeviceLayer:
-    def __init__(self, spec: dict, device):
+    """One library call: a conv, FC or pool layer, or a conv and the max-pool
+    after it.  ``specs`` holds the layer specs it covers (one or two)."""
+
+    def __init__(self, spec: dict, device, pool: Optional[dict] = None):
         self.kind = spec["kind"]
+        self.specs = [spec] if pool is None else [spec, pool]
+        self.pool = None if pool is None else (pool["k"], pool["s"])
         if self.kind == "pool":
             self.k, self.s = spec["k"], spec["s"]
             return
@@ -29,19 +37,37 @@ class DeviceLayer:
         if self.kind == "conv":
             self.stride, self.pad = spec["stride"], spec["pad"]
 
+    @property
+    def name(self) -> str:
+        return "+".join(s["kind"] for s in self.specs)
+
     def __call__(self, h: torch.Tensor) -> torch.Tensor:
         if self.kind == "pool":
             return api.maxpool2d(h, self.k, self.s)
         if self.kind == "conv":
+            if self.pool is not None:
+                return api.conv_pool_forward(h, self.D, self.codes, self.stride, self.pad, self.pool[0],
+                                             self.pool[1], self.bias, self.relu)
             return api.conv_forward(h, self.D, self.codes, self.stride, self.pad, self.bias, self.relu)
         return api.fc_forward(h.reshape(h.shape[0], -1), self.D, self.codes, self.bias, self.relu)
 
 
 class Network:
-    """Layers from workloads.generate(...)['layers'], resident on ``device``."""
+    """Layers from workloads.generate(...)['layers'], resident on ``device``.
+    ``fuse_pools``: a conv followed by a max-pool becomes one call."""
 
-    def __init__(self, layer_specs: List[dict], device="cuda:0"):
-        self.layers = [DeviceLayer(s, device) for s in layer_specs]
+    def __init__(self, layer_specs: List[dict], device="cuda:0", fuse_pools: bool = True):
+        self.layers = []
+        i = 0
+        while i < len(layer_specs):
+            s = layer_specs[i]
+            nxt = layer_specs[i + 1] if i + 1 < len(layer_specs) else None
+            if fuse_pools and s["kind"] == "conv" and nxt is not None and nxt["kind"] == "pool":
+                self.layers.append(DeviceLayer(s, device, pool=nxt))
+                i += 2
+            else:
+                self.layers.append(DeviceLayer(s, device))
+                i += 1
 
     def forward(self, x: torch.Tensor, keep: Optional[list] = None) -> torch.Tensor:
         h = x

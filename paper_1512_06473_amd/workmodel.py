@@ -170,3 +170,41 @@ def workload_work(wl, N: Optional[int] = None):
             out.append(("fc", fc_work(n, Cs, L.Ct, L.Csp, L.K)))
             shape = (L.Ct,)
     return out
+
+
+def call_work(wl, N: Optional[int] = None, fuse_pools: bool = True):
+    """Per-library-call (name, LayerWork) list for a workloads.Workload, as
+    network.Network issues them: with ``fuse_pools`` a conv followed by a
+    max-pool is one call ("conv+pool"), whose HBM bytes are the conv's
+    without its full output map and with the pooled map instead."""
+    from .workloads import Conv, Pool  # shapes only
+    n = wl.N if N is None else N
+    layers = list(wl.layers)
+    per = workload_work(wl, N)
+    shape = tuple(wl.in_shape)
+    out = []
+    i = 0
+    while i < len(layers):
+        L = layers[i]
+        kind, lw = per[i]
+        if isinstance(L, Conv):
+            C, H, W = shape
+            shape = (L.Ct, out_size(H, L.dk, L.stride, L.pad), out_size(W, L.dk, L.stride, L.pad))
+            nxt = layers[i + 1] if i + 1 < len(layers) else None
+            if fuse_pools and isinstance(nxt, Pool):
+                Ct, Ho, Wo = shape
+                Hp, Wp = out_size(Ho, nxt.k, nxt.s, 0), out_size(Wo, nxt.k, nxt.s, 0)
+                hbm = lw.hbm_bytes - 4 * n * Ct * Ho * Wo + 4 * n * Ct * Hp * Wp
+                out.append(("conv+pool", LayerWork(dense_macs=lw.dense_macs, lut_entries=lw.lut_entries,
+                                                   gathers=lw.gathers, hbm_bytes=hbm, lds_bytes=lw.lds_bytes)))
+                shape = (Ct, Hp, Wp)
+                i += 2
+                continue
+        elif isinstance(L, Pool):
+            C, H, W = shape
+            shape = (C, out_size(H, L.k, L.s, 0), out_size(W, L.k, L.s, 0))
+        else:
+            shape = (L.Ct,)
+        out.append((kind, lw))
+        i += 1
+    return out

@@ -65,6 +65,15 @@ int main(void) {
   EXPECT(qcnn_pq_assign(FP(X), 4, 8, 3, FP(Dp), 3, 16, 4, (uint8_t*)C, NULL, NULL) == QCNN_ERR_SHAPE);
   EXPECT(qcnn_pq_kmeans(FP(X), 4, 8, 3, 2, 16, 4, -1, FW(Dp), (uint8_t*)C, NULL, NULL) == QCNN_ERR_SHAPE);
   EXPECT(qcnn_pq_update(FP(X), 4, 8, 3, CP(C), 2, 300, 4, FW(Dp), NULL, NULL) == QCNN_ERR_K_RANGE);
+  /* conv + max-pool: the conv's validation, then the pooling window */
+  EXPECT(qcnn_conv_pool_forward(FP(X), 2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 4, 3, 1, 1, NULL, 0, 3, 2, NULL, NULL) ==
+         QCNN_ERR_NULL);
+  EXPECT(qcnn_conv_pool_forward(FP(X), 2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 4, 3, 1, 1, NULL, 0, 0, 2, FW(Y), NULL) ==
+         QCNN_ERR_SHAPE);
+  EXPECT(qcnn_conv_pool_forward(FP(X), 2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 4, 3, 1, 1, NULL, 0, 6, 1, FW(Y), NULL) ==
+         QCNN_ERR_SHAPE);
+  EXPECT(qcnn_conv_pool_forward(FP(X), 2, 8, 5, 5, FP(Dp), 3, 16, 4, CP(C), 4, 3, 1, 1, NULL, 0, 3, 2, FW(Y), NULL) ==
+         QCNN_ERR_SHAPE);
   /* allocation-free conv: the same validation, then layers too large for its scratch */
   EXPECT(qcnn_conv_forward_noalloc(FP(X), 2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 4, 3, 1, 1, NULL, 0, NULL, NULL) ==
          QCNN_ERR_NULL);

@@ -100,6 +100,27 @@ def test_conv_rejects(L, kw, want):
     assert conv(L, "qcnn_conv_forward_noalloc", **kw) == want
 
 
+def conv_pool(L, pk=3, ps=2, **kw):
+    a = dict(x=FAKE, N=2, Cs=8, H=5, W=5, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, Ct=4, dk=3, s=1, p=1,
+             bias=None, relu=0, y=FAKE2, stream=None)
+    a.update(kw)
+    return L.qcnn_conv_pool_forward(a["x"], a["N"], a["Cs"], a["H"], a["W"], a["D"], a["M"], a["K"], a["Csp"],
+                                    a["codes"], a["Ct"], a["dk"], a["s"], a["p"], a["bias"], a["relu"], pk, ps,
+                                    a["y"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(x=None), NULL), (dict(codes=None), NULL), (dict(y=None), NULL),
+    (dict(N=0), SHAPE), (dict(Ct=0), SHAPE), (dict(M=3), SHAPE), (dict(K=0), KR),
+    (dict(codes=FAKE + 1), UNSUP), (dict(y=FAKE + 64), ALIAS), (dict(bias=FAKE2 + 16), ALIAS),
+    (dict(pk=0), SHAPE), (dict(ps=0), SHAPE), (dict(pk=-1, ps=-1), SHAPE),
+    (dict(pk=6), SHAPE),                          # window larger than the 5x5 conv output
+])
+def test_conv_pool_rejects(L, kw, want):
+    pk, ps = kw.pop("pk", 3), kw.pop("ps", 2)
+    assert conv_pool(L, pk, ps, **kw) == want
+
+
 def test_noalloc_rejects_layers_beyond_its_scratch(L):
     # AlexNet conv3 at N = 64 (256 -> 384, 13x13, 3x3 pad 1, C's = 4, K = 128)
     # needs more temporaries than the static scratch holds: refused on the

@@ -52,6 +52,18 @@ def assert_exact(gpu, ref, what):
     assert not diff.any(), "%s: %d of %d differ (integer data must be bit-exact)" % (what, int(diff.sum()), diff.size)
 
 
+def pool64(a, k, s):
+    """k x k / stride s window maxima of a float64 array [N][C][H][W] (no
+    padding), for references and bounds that must not be rounded."""
+    Hp, Wp = (a.shape[2] - k) // s + 1, (a.shape[3] - k) // s + 1
+    out = None
+    for dy in range(k):
+        for dx in range(k):
+            v = a[:, :, dy:dy + s * (Hp - 1) + 1:s, dx:dx + s * (Wp - 1) + 1:s]
+            out = v.copy() if out is None else np.maximum(out, v)
+    return out
+
+
 def run_conv(api, dev, x, D, codes, s, p, bias=None, relu=False):
     y = api.conv_forward(T(x, dev), T(D, dev), T(codes, dev), s, p,
                          None if bias is None else T(bias, dev), relu)
@@ -116,16 +128,24 @@ def test_alexnet_n64_every_layer_and_end_to_end(api, dev, oracle):
     out = net.forward(T(d["x"], dev), keep)
     torch.cuda.synchronize()
     acts = [d["x"]] + [k.cpu().numpy() for k in keep]
-    # Every layer, every output: the oracle gets the GPU's own fp32 input of
-    # that layer, so each layer is held to its own bound.
-    for i, spec in enumerate(d["layers"]):
+    assert sum(len(L.specs) for L in net.layers) == len(d["layers"])
+    assert [L.name for L in net.layers].count("conv+pool") == 3
+    # Every library call, every output: the oracle gets the GPU's own fp32
+    # input of that call, so each call is held to its own bound.  A conv
+    # with its max-pool: the pooled oracle output, bounded by the window
+    # maximum of the conv's bound (|max a - max b| <= max |a - b|).
+    for i, L in enumerate(net.layers):
+        spec = L.specs[0]
         hin, hout = acts[i], acts[i + 1]
-        what = "alexnet_n64 layer %d (%s)" % (i, spec["kind"])
+        what = "alexnet_n64 call %d (%s)" % (i, L.name)
         if spec["kind"] == "pool":
             assert_exact(hout, oracle.maxpool(hin, spec["k"], spec["s"]), what)
         elif spec["kind"] == "conv":
             ref, A = oracle.conv_lut(hin, spec["D"], spec["codes"], spec["stride"], spec["pad"],
                                      relu=spec["relu"], with_bound=True)
+            if len(L.specs) == 2:
+                k, s = L.specs[1]["k"], L.specs[1]["s"]
+                ref, A = pool64(ref, k, s), pool64(A, k, s)
             assert_bound(hout, ref, A, what)
         else:
             ref, A = oracle.fc_lut(hin.reshape(hin.shape[0], -1), spec["D"], spec["codes"], relu=spec["relu"],
