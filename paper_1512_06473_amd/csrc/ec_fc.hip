@@ -12,23 +12,32 @@
 // D_k^T G D_k - 2 D_k^T P_c, so only P touches the large arrays.
 //
 // State, all float64 but the codes: E = T - Y, the residual of the whole
-// quantized layer [N][C_t]; the sub-codebooks D64; the Gram blocks G[m]; the
-// codes transposed to [M][C_t] (one subspace's codes contiguous), written
-// back to [C_t][M] at the end.  ec_start_kernel forms the starting E in one
-// pass over the subspaces.  Per subspace m:
-//   ec_step_kernel   one pass over E: finishes the subspace m' fitted just
-//                    before (its assignment, Eq. (12), then
-//                    E -= S^(m') (W_new - W_old)), sums E^2 (the objective
-//                    after that step, Eq. (8)) and the partial products
-//                    S^(m)T E over chunks of images;
-//   ec_reduce_kernel P = sum of the partials (fixed order) + G W^(m), so that
-//                    P = S^(m)T R^(m) with R^(m) = E + S^(m) W^(m); then, per
-//                    block of channels, the sums of P_c over the channels
-//                    assigned to each sub-codeword;
-//   ec_fit_kernel    one workgroup: adds the blocks' sums and solves Eq. (11)
-//                    for every sub-codeword.
-// With `inner` > 1 the reduce kernel's second form (assignment from P, then
-// the sums) and the fit kernel repeat before the next step kernel.
+// quantized layer [N][C_t]; the sub-codebooks D64; the Gram blocks
+// Gc[m][d] = S^(m)T S^(m-d) for d < B (d = 0: G of Eq. (11)); the codes
+// transposed to [M][C_t] (one subspace's codes contiguous), written back to
+// [C_t][M] at the end.  ec_start_kernel forms the starting E in one pass
+// over the subspaces.
+//
+// Batches.  The subspaces are taken B = 32 / C'_s (at most 16) at a time.
+// One pass over E per batch (ec_pass_kernel) applies the updates of the
+// previous batch's steps in order, E -= S^(m) (W_new - W_old), summing E^2
+// after each (the objective after that step, Eq. (8)), and forms
+// X^(j) = S^(m_j)T E for every subspace m_j of the next batch.  The step of
+// m_j then needs P = S^(m_j)T R^(m_j) with R^(m_j) = E_j + S^(m_j) W^(m_j),
+// E_j the residual after the batch's earlier steps i < j, so
+//   P = X^(j) - sum_{i<j} Gc[m_j][j-i] (W_new - W_old)^(m_i) + G W^(m_j)
+// (the same quantity as a pass over E_j would give, up to rounding), which
+// ec_prep_kernel forms per channel without touching E.  Per subspace:
+//   ec_prep_kernel  the assignment (Eq. (12)) of the subspace fitted just
+//                   before (when it lies in the same batch), P as above,
+//                   then per block of channels the sums of P_c over the
+//                   channels assigned to each sub-codeword, in channel order
+//                   (a counting sort in LDS);
+//   ec_fit_kernel   one workgroup: adds the blocks' sums and solves Eq. (11)
+//                   for every sub-codeword.
+// With `inner` > 1 the prep kernel's second form (assignment from P, then
+// the sums) and the fit kernel repeat.  The last subspace of a batch is
+// assigned by the next pass.
 // Readings (shared with the oracle): the descent starts from the given
 // sub-codebooks and codes; a sweep visits m in order; a sub-codeword no
 // channel uses keeps its value; the normal equations are solved by
@@ -36,31 +45,38 @@
 // the largest diagonal entry of G dropping that coordinate (set to 0);
 // assignment ties go to the lowest index.
 //
-// Bound: HBM.  A subspace step reads and writes E once (16 N C_t bytes) and
-// reads S^(m) (4 N C'_s bytes); the fit kernel is latency-bound on one CU.
-// The starting residual is fp64 arithmetic, 2 N C_t C_s flops once.
+// Bound: HBM for the passes, latency for the per-subspace kernels.  A pass
+// reads and writes E once (16 N C_t bytes) per batch of B subspaces; the
+// prep and fit kernels move O(C'_s C_t) values each.  The starting residual
+// is fp64 arithmetic, 2 N C_t C_s flops once.
 #include "qcnn_internal.h"
 
 namespace qcnn {
 namespace {
 
-constexpr int kEcThreads = 256;      // pass / reduce kernels
-constexpr int kEcChunk = 16;         // images per pass workgroup
-constexpr int kUpdThreads = 256;     // update kernel (one workgroup; up to 512 registers per lane)
+constexpr int kEcThreads = 256;      // start / prep kernels
+constexpr int kEcChunk = 16;         // images per thread in the start and pass kernels
+constexpr int kPassCh = 16;          // channels per pass workgroup (16 image chunks each)
+constexpr int kUpdThreads = 256;     // fit / objective kernels (one workgroup)
+
+// Subspaces per batch: the pass keeps B x C'_s accumulators per thread.
+template <int CSP> constexpr int ec_batch() { return 32 / CSP < 1 ? 1 : (32 / CSP > 16 ? 16 : 32 / CSP); }
 
 struct EcParams {
   int N, Cs, Ct, M, K, Csp, inner;
-  int nchunks;
+  int nchunks;  // start kernel: image chunks
+  int B;        // subspaces per batch
 };
 
 // D64 = codebooks, ct[m][c] = codes[c][m] (codes >= K read as K - 1),
-// G[m][i][j] = sum_n S[n][m C's + i] S[n][m C's + j].
+// Gc[m][d][i][j] = sum_n S[n][m C's + i] S[n][(m - d) C's + j] (0 for m < d).
 __global__ __launch_bounds__(kEcThreads) void ec_init_kernel(const float* __restrict__ S, const float* __restrict__ D,
                                                            const uint8_t* __restrict__ codes, EcParams p,
                                                            double* __restrict__ D64, uint8_t* __restrict__ ct,
-                                                           double* __restrict__ G) {
+                                                           double* __restrict__ Gc) {
   const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (size_t)gridDim.x * blockDim.x;
-  const size_t nc = (size_t)p.M * p.Ct, nd = (size_t)p.M * p.K * p.Csp, ng = (size_t)p.M * p.Csp * p.Csp;
+  const size_t nc = (size_t)p.M * p.Ct, nd = (size_t)p.M * p.K * p.Csp;
+  const size_t cc = (size_t)p.Csp * p.Csp, ng = (size_t)p.M * p.B * cc;
   for (size_t i = tid; i < nc; i += stride) {
     const size_t m = i / p.Ct, c = i % p.Ct;
     const uint8_t k = codes[c * p.M + m];
@@ -68,25 +84,29 @@ __global__ __launch_bounds__(kEcThreads) void ec_init_kernel(const float* __rest
   }
   for (size_t i = tid; i < nd; i += stride) D64[i] = (double)D[i];
   for (size_t i = tid; i < ng; i += stride) {
-    const int m = (int)(i / ((size_t)p.Csp * p.Csp));
-    const int r = (int)(i % ((size_t)p.Csp * p.Csp));
-    const int a = m * p.Csp + r / p.Csp, b = m * p.Csp + r % p.Csp;
+    const int m = (int)(i / (p.B * cc));
+    const int d = (int)((i / cc) % p.B);
+    const int r = (int)(i % cc);
     double s = 0.0;
-    for (int n = 0; n < p.N; ++n) s += (double)S[(size_t)n * p.Cs + a] * (double)S[(size_t)n * p.Cs + b];
-    G[i] = s;
+    if (m >= d) {
+      const int a = m * p.Csp + r / p.Csp, b = (m - d) * p.Csp + r % p.Csp;
+      for (int n = 0; n < p.N; ++n) s += (double)S[(size_t)n * p.Cs + a] * (double)S[(size_t)n * p.Cs + b];
+    }
+    Gc[i] = s;
   }
 }
 
 // Fixed-order sum of one value per thread over the workgroup (wave
-// shuffles, then the waves in order) into opart[block].
-__device__ __forceinline__ void ec_block_sum(double v, double* red, double* __restrict__ opart) {
+// shuffles, then the waves in order) into *out.  Every thread must call it.
+__device__ __forceinline__ void ec_block_sum(double v, double* red, double* __restrict__ out) {
   for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+  __syncthreads();  // red may still be read by a previous call
   if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
   __syncthreads();
   if (threadIdx.x == 0) {
     double s = 0.0;
-    for (int w = 0; w < kEcThreads / kWave; ++w) s += red[w];
-    opart[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s;
+    for (int w = 0; w < (int)blockDim.x / kWave; ++w) s += red[w];
+    *out = s;
   }
 }
 
@@ -107,19 +127,51 @@ __global__ __launch_bounds__(kEcThreads) void ec_start_kernel(const float* __res
 #pragma unroll
   for (int i = 0; i < kEcChunk; ++i) e[i] = col && i < nn ? (double)T[(size_t)(n0 + i) * p.Ct + c] : 0.0;
   if (col) {
-    for (int m = 0; m < p.M; ++m) {
-      const double* w = D64 + ((size_t)m * p.K + ct[(size_t)m * p.Ct + c]) * CSP;
-      double dw[CSP];
+    // eight subspaces at a time: their codes, then their sub-codewords, are
+    // loaded together (each load waits on the one before it otherwise); the
+    // subtractions still go in subspace order
+    constexpr int U = 8;
+    for (int m0 = 0; m0 < p.M; m0 += U) {
+      int kc[U];
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) dw[j] = w[j];
+      for (int u = 0; u < U; ++u) kc[u] = ct[(size_t)min(m0 + u, p.M - 1) * p.Ct + c];
+      double dw[U][CSP];
 #pragma unroll
-      for (int i = 0; i < kEcChunk; ++i) {
-        if (i < nn) {
-          const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)m * CSP;
-          double d = 0.0;
+      for (int u = 0; u < U; ++u) {
+        const double* w = D64 + ((size_t)min(m0 + u, p.M - 1) * p.K + kc[u]) * CSP;
 #pragma unroll
-          for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[j];
-          e[i] -= d;
+        for (int j = 0; j < CSP; ++j) dw[u][j] = w[j];
+      }
+      // a full chunk takes the branch-free path (per-image branches would
+      // make each image's scalar loads wait on their own)
+      if (nn == kEcChunk && m0 + U <= p.M) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+          for (int i = 0; i < kEcChunk; ++i) {
+            const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)(m0 + u) * CSP;
+            double d = 0.0;
+#pragma unroll
+            for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[u][j];
+            e[i] -= d;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int m = m0 + u;
+          if (m < p.M) {
+#pragma unroll
+            for (int i = 0; i < kEcChunk; ++i) {
+              if (i < nn) {
+                const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)m * CSP;
+                double d = 0.0;
+#pragma unroll
+                for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[u][j];
+                e[i] -= d;
+              }
+            }
+          }
         }
       }
     }
@@ -130,7 +182,7 @@ __global__ __launch_bounds__(kEcThreads) void ec_start_kernel(const float* __res
     if (col && i < nn) E[(size_t)(n0 + i) * p.Ct + c] = e[i];
     sq += e[i] * e[i];
   }
-  ec_block_sum(sq, red, opart);
+  ec_block_sum(sq, red, opart + (size_t)blockIdx.y * gridDim.x + blockIdx.x);
 }
 
 // Eq. (12) for one output channel: the first k minimising
@@ -139,7 +191,8 @@ template <int CSP>
 __device__ __forceinline__ int ec_best(const double* sd, const double* q, int K, const double (&pc)[CSP]) {
   int best = 0;
   double bv = 0.0;
-  for (int k = 0; k < K; ++k) {
+#pragma unroll 8
+  for (int k = 0; k < K; ++k) {  // unrolled: the table reads of 8 sub-codewords in flight
     double d = 0.0;
 #pragma unroll
     for (int j = 0; j < CSP; ++j) d += sd[k * CSP + j] * pc[j];
@@ -152,254 +205,97 @@ __device__ __forceinline__ int ec_best(const double* sd, const double* q, int K,
   return best;
 }
 
-// One pass over E for a chunk of kEcChunk images and 256 columns, after the
-// fit of subspace ma (ma >= 0) and before that of mp (mp >= 0):
-//   assign:  knew(c) by Eq. (12) from P (still that of ma), D^(ma) and q;
-//            the chunk-0 workgroup stores it in ct[ma];
-//   apply:   E[n][c] -= sum_j S[n][ma C's + j] (D^(ma)[knew(c)][j] - Dold[kold(c)][j]);
-//   collect: part[chunk][j][c] = sum_n S[n][mp C's + j] E[n][c];
-//   obj:     opart[block] = sum of E[n][c]^2 over the block (after the apply).
-// The chunk's E is loaded into registers before any of it is written, so
-// the loads are all in flight together.
-template <int CSP>
-__global__ __launch_bounds__(kEcThreads) void ec_step_kernel(const float* __restrict__ S, EcParams p,
-                                                           double* __restrict__ E, int ma,
-                                                           const double* __restrict__ P,
-                                                           const double* __restrict__ D64,
-                                                           const double* __restrict__ qv, uint8_t* __restrict__ ct,
-                                                           const double* __restrict__ Dold,
-                                                           const uint8_t* __restrict__ codes_old, int mp,
-                                                           double* __restrict__ part, double* __restrict__ opart) {
-  extern __shared__ double sd[];  // D^(ma) [K][C's], q [K], block-sum scratch [4]
-  double* q = sd + (size_t)p.K * CSP;
-  double* red = q + p.K;
-  const int c = blockIdx.x * kEcThreads + threadIdx.x;
-  const int chunk = blockIdx.y;
-  const int n0 = chunk * kEcChunk, nn = min(p.N - n0, kEcChunk);
-  const bool col = c < p.Ct;
-  double e[kEcChunk];
-#pragma unroll
-  for (int i = 0; i < kEcChunk; ++i) e[i] = col && i < nn ? E[(size_t)(n0 + i) * p.Ct + c] : 0.0;
-  if (ma >= 0) {
-    // this channel's P_c and old sub-codeword are fetched before the LDS fill
-    double pc[CSP], dd[CSP];
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) pc[j] = col ? P[(size_t)j * p.Ct + c] : 0.0;
-    const double* ddp = Dold + (size_t)(col ? codes_old[c] : 0) * CSP;
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) dd[j] = ddp[j];
-    for (int i = threadIdx.x; i < p.K * CSP; i += kEcThreads) sd[i] = D64[(size_t)ma * p.K * CSP + i];
-    for (int i = threadIdx.x; i < p.K; i += kEcThreads) q[i] = qv[i];
-    __syncthreads();
-    if (col) {
-      const int kn = ec_best<CSP>(sd, q, p.K, pc);
-      if (chunk == 0) ct[(size_t)ma * p.Ct + c] = (uint8_t)kn;
-      double dw[CSP];
-#pragma unroll
-      for (int j = 0; j < CSP; ++j) dw[j] = sd[kn * CSP + j] - dd[j];
-#pragma unroll
-      for (int i = 0; i < kEcChunk; ++i) {
-        if (i < nn) {
-          const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)ma * CSP;
-          double d = 0.0;
-#pragma unroll
-          for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[j];
-          e[i] -= d;
-          E[(size_t)(n0 + i) * p.Ct + c] = e[i];
-        }
-      }
-    }
-  }
-  if (mp >= 0 && col) {
-    double acc[CSP];
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) acc[j] = 0.0;
-#pragma unroll
-    for (int i = 0; i < kEcChunk; ++i) {
-      if (i < nn) {
-        const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)mp * CSP;
-#pragma unroll
-        for (int j = 0; j < CSP; ++j) acc[j] += (double)srow[j] * e[i];
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) part[((size_t)chunk * CSP + j) * p.Ct + c] = acc[j];
-  }
-  double sq = 0.0;
-#pragma unroll
-  for (int i = 0; i < kEcChunk; ++i) sq += e[i] * e[i];
-  ec_block_sum(sq, red, opart);
-}
-
-// Doubles of the reduce kernel's LDS after its P block: D^(m) and q, later
-// reused for the quarter sums of one group of 64 sub-codewords.
-__host__ __device__ constexpr size_t red_area(int K, int Csp) {
-  return (size_t)K * (Csp + 1) > (size_t)(kEcThreads / kWave) * kWave * (Csp + 1)
-             ? (size_t)K * (Csp + 1)
-             : (size_t)(kEcThreads / kWave) * kWave * (Csp + 1);
-}
-
-// Per block of 256 output channels, for subspace m:
-//   assign == 0: P[j][c] = sum over chunks (in order) of part[chunk][j][c]
-//                + sum_i G[m][j][i] W^(m)[i][c], so that P = S^(m)T R^(m);
-//                codes_old[c] = ct[m][c];
-//   assign == 1: ct[m][c] by Eq. (12) from P, D^(m) and q (a later round);
-// then, in channel order, the block's sums over the channels assigned to
-// each sub-codeword: bins[block][k][j] = sum of P[j][c], nbin[block][k] the
-// number of those channels.
-template <int CSP>
-__global__ __launch_bounds__(kEcThreads) void ec_reduce_kernel(const double* __restrict__ part, EcParams p, int m,
-                                                             const double* __restrict__ G,
-                                                             const double* __restrict__ D64,
-                                                             const double* __restrict__ qv, int assign,
-                                                             uint8_t* __restrict__ ct, double* __restrict__ P,
-                                                             uint8_t* __restrict__ codes_old,
-                                                             double* __restrict__ bins, int* __restrict__ nbin) {
-  extern __shared__ double sr[];
-  double* Pl = sr;                             // [C's][256] this block's P
-  double* sd = Pl + CSP * kEcThreads;          // [K][C's] D^(m) (assign == 1)
-  double* q = sd + (size_t)p.K * CSP;          // [K]
-  // [256] codes, after the larger of that and the quarter sums below
-  uint8_t* ks = reinterpret_cast<uint8_t*>(sd + red_area(p.K, CSP));
-  const int tid = threadIdx.x, c = blockIdx.x * kEcThreads + tid;
-  const bool col = c < p.Ct;
-  double pc[CSP];
-  int k = 0;
-  if (assign) {
-    for (int i = tid; i < p.K * CSP; i += kEcThreads) sd[i] = D64[(size_t)m * p.K * CSP + i];
-    for (int i = tid; i < p.K; i += kEcThreads) q[i] = qv[i];
-    __syncthreads();
-    if (col) {
-#pragma unroll
-      for (int j = 0; j < CSP; ++j) pc[j] = P[(size_t)j * p.Ct + c];
-      k = ec_best<CSP>(sd, q, p.K, pc);
-      ct[(size_t)m * p.Ct + c] = (uint8_t)k;
-    }
-  } else if (col) {
-    k = ct[(size_t)m * p.Ct + c];
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) pc[j] = 0.0;
-    // the chunks in order, eight chunks' loads in flight at a time
-    for (int ch0 = 0; ch0 < p.nchunks; ch0 += 8) {
-      double v[8][CSP];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int j = 0; j < CSP; ++j)
-          v[u][j] = ch0 + u < p.nchunks ? part[((size_t)(ch0 + u) * CSP + j) * p.Ct + c] : 0.0;
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int j = 0; j < CSP; ++j)
-          if (ch0 + u < p.nchunks) pc[j] += v[u][j];
-    }
-    const double* g = G + (size_t)m * CSP * CSP;
-    const double* w = D64 + ((size_t)m * p.K + k) * CSP;
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) {
-#pragma unroll
-      for (int i = 0; i < CSP; ++i) pc[j] += g[j * CSP + i] * w[i];
-      P[(size_t)j * p.Ct + c] = pc[j];
-    }
-    codes_old[c] = (uint8_t)k;
-  }
-#pragma unroll
-  for (int j = 0; j < CSP; ++j) Pl[j * kEcThreads + tid] = col ? pc[j] : 0.0;
-  ks[tid] = (uint8_t)k;
-  __syncthreads();
-  // For k in groups of 64, wave w sums the channels of its quarter (in
-  // order) for k = group + lane: branch-free, every lane reads the same P_c
-  // (a broadcast).  The quarters' sums are then added in order.
-  constexpr int kQ = kEcThreads / kWave;
-  double* qs = sd;  // [4][64][C's] quarter sums (sd is free again)
-  int* qn = reinterpret_cast<int*>(qs + kQ * kWave * CSP);  // [4][64]
-  const int lane = tid & (kWave - 1), wave = tid / kWave;
-  const int i0 = wave * kWave;
-  const int i1 = min(i0 + kWave, p.Ct - (int)blockIdx.x * kEcThreads);
-  for (int k0 = 0; k0 < p.K; k0 += kWave) {
-    __syncthreads();  // sd / qs may still be read
-    const int kk = k0 + lane;
-    double b[CSP];
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) b[j] = 0.0;
-    int n = 0;
-#pragma unroll 4
-    for (int i = i0; i < i1; ++i) {
-      const bool hit = ks[i] == kk;
-      n += hit ? 1 : 0;
-#pragma unroll
-      for (int j = 0; j < CSP; ++j) b[j] += hit ? Pl[j * kEcThreads + i] : 0.0;
-    }
-#pragma unroll
-    for (int j = 0; j < CSP; ++j) qs[(wave * kWave + lane) * CSP + j] = b[j];
-    qn[wave * kWave + lane] = n;
-    __syncthreads();
-    const int nk = min(kWave, p.K - k0);
-    for (int i = tid; i < nk * CSP; i += kEcThreads) {
-      double v = 0.0;
-      for (int w = 0; w < kQ; ++w) v += qs[w * kWave * CSP + i];
-      bins[((size_t)blockIdx.x * p.K + k0) * CSP + i] = v;
-    }
-    for (int i = tid; i < nk; i += kEcThreads) {
-      int v = 0;
-      for (int w = 0; w < kQ; ++w) v += qn[w * kWave + i];
-      nbin[(size_t)blockIdx.x * p.K + k0 + i] = v;
-    }
-  }
-}
-
-// Threads of the fit kernel that solve at once, and the LDS each takes for
-// its elimination (registers up to C'_s = 8).
-template <int CSP> constexpr int fit_solvers() { return CSP <= 8 ? kUpdThreads : 16; }
-template <int CSP> constexpr int fit_solve_lds() {
+// Threads of a fit that solve at once, and the LDS each takes for its
+// elimination (registers up to C'_s = 8).
+template <int CSP> __host__ __device__ constexpr int fit_solvers() { return CSP <= 8 ? kUpdThreads : 16; }
+template <int CSP> __host__ __device__ constexpr int fit_solve_lds() {
   return CSP <= 8 ? 0 : fit_solvers<CSP>() * CSP * CSP * (int)sizeof(double);
 }
-template <int CSP> size_t fit_lds_bytes(int K) {
-  return (size_t)(CSP * CSP + 2 * K * CSP + kUpdThreads) * sizeof(double) + fit_solve_lds<CSP>() +
-         (size_t)K * sizeof(int);
+// LDS of one fit: G, D, b_k, q (doubles), the elimination storage, |L_k|.
+template <int CSP> __host__ __device__ size_t fit_lds_bytes(int K) {
+  return (size_t)(CSP * CSP + 2 * K * CSP + K) * sizeof(double) + fit_solve_lds<CSP>() + (size_t)K * sizeof(int);
 }
 
-// Eq. (11), one workgroup.  On the first round of a subspace (`first`) it
-// also records the objective after the previous step (from the step
-// kernel's block sums) and keeps the subspace's old sub-codebook for the
-// next step kernel.  b_k and |L_k| are the sums over the channel blocks (in
-// order) of the reduce kernel's bins; each sub-codeword used by some channel
-// becomes G^-1 b_k / |L_k|, and qv[k] = D_k^T G D_k for the assignment.
+struct FitLds {
+  double *Gs, *Ds, *bs, *qs, *Aw;
+  int* ns;
+};
+
 template <int CSP>
-__global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __restrict__ bins,
-                                                           const int* __restrict__ nbin, int nblk, EcParams p,
-                                                           int m, const double* __restrict__ G,
-                                                           double* __restrict__ D64, int first,
-                                                           double* __restrict__ Dold,
-                                                           const double* __restrict__ opart, int nopart,
-                                                           double* __restrict__ objective, double* __restrict__ qv) {
-  // All LDS is dynamic (the kernel may take up to the whole 160 KB, so it
-  // cannot also have static LDS).
-  extern __shared__ double sh[];
-  const int K = p.K;
-  double* Gs = sh;                               // [C's][C's]
-  double* Ds = Gs + CSP * CSP;                   // [K][C's]
-  double* bs = Ds + K * CSP;                     // [K][C's] b_k
-  double* red = bs + K * CSP;                    // [threads] objective tree
-  double* Aw = red + kUpdThreads;                // elimination storage (C'_s > 8)
-  int* ns = reinterpret_cast<int*>(Aw + fit_solve_lds<CSP>() / sizeof(double));  // [K] |L_k|
-  const int tid = threadIdx.x;
-  const bool obj = first && objective;
-  // the step kernel's block sums: thread strides, then a fixed tree (below)
-  double os = 0.0;
-  if (obj)
-    for (int i0 = tid; i0 < nopart; i0 += 4 * kUpdThreads) {
-      double v[4];
+__device__ __forceinline__ FitLds fit_lds(double* base, int K) {
+  FitLds f;
+  f.Gs = base;                        // [C's][C's]
+  f.Ds = f.Gs + CSP * CSP;            // [K][C's]
+  f.bs = f.Ds + K * CSP;              // [K][C's] b_k
+  f.qs = f.bs + K * CSP;              // [K] D_k^T G D_k
+  f.Aw = f.qs + K;                    // elimination storage (C'_s > 8)
+  f.ns = reinterpret_cast<int*>(f.Aw + fit_solve_lds<CSP>() / sizeof(double));  // [K] |L_k|
+  return f;
+}
+
+// Eq. (11) by one workgroup of kUpdThreads threads, for subspace mf: b_k and
+// |L_k| are the sums over the channel blocks (in order) of the prep
+// kernel's bins; each sub-codeword used by some channel becomes
+// G^-1 b_k / |L_k|, the others keep their value in Din.  Leaves D in f.Ds
+// and q_k = D_k^T G D_k in f.qs (LDS, after a barrier).  Every workgroup
+// that runs it on the same inputs gets the same values.
+// Inputs of a fit that one thread loads when K C'_s <= kUpdThreads and the
+// blocks number at most 16 (the usual case): issued together, straight-line,
+// so that a kernel can put them in flight with its own loads.
+struct FitRegs {
+  double b[16];
+  int n[16];
+  double din, g;
+  bool on;
+};
+
+template <int CSP>
+__device__ __forceinline__ void ec_fit_issue(const double* __restrict__ bins, const int* __restrict__ nbin, int nblk,
+                                             const EcParams& p, int mf, const double* __restrict__ Gc,
+                                             const double* __restrict__ Din, FitRegs& r) {
+  const int K = p.K, tid = threadIdx.x;
+  r.on = K * CSP <= kUpdThreads && nblk <= 16;
+  if (!r.on) return;  // uniform
+  const bool bi = tid < K * CSP, ki = tid < K;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kUpdThreads < nopart ? opart[i0 + u * kUpdThreads] : 0.0;
+  for (int u = 0; u < 16; ++u) {
+    const bool okb = bi && u < nblk, okn = ki && u < nblk;
+    const double vb = bins[okb ? (size_t)u * K * CSP + tid : 0];
+    const int vn = nbin[okn ? (size_t)u * K + tid : 0];
+    r.b[u] = okb ? vb : 0.0;
+    r.n[u] = okn ? vn : 0;
+  }
+  const double vd = Din[bi ? tid : 0];
+  const double vg = Gc[(size_t)mf * p.B * CSP * CSP + (tid < CSP * CSP ? tid : 0)];
+  r.din = vd;
+  r.g = vg;
+}
+
+template <int CSP>
+__device__ void ec_fit_wg(const double* __restrict__ bins, const int* __restrict__ nbin, int nblk,
+                          const EcParams& p, int mf, const double* __restrict__ Gc, const double* __restrict__ Din,
+                          const FitLds& f, const FitRegs* pre = nullptr) {
+  const int K = p.K, tid = threadIdx.x;
+  if (pre && pre->on) {  // the loads were issued by ec_fit_issue; the sums in block order
+    if (tid < CSP * CSP) f.Gs[tid] = pre->g;
+    if (tid < K * CSP) {
+      f.Ds[tid] = pre->din;
+      double s = 0.0;
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (i0 + u * kUpdThreads < nopart) os += v[u];
+      for (int u = 0; u < 16; ++u)
+        if (u < nblk) s += pre->b[u];
+      f.bs[tid] = s;
     }
-  for (int i = tid; i < CSP * CSP; i += kUpdThreads) Gs[i] = G[(size_t)m * CSP * CSP + i];
+    if (tid < K) {
+      int n = 0;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) n += pre->n[u];
+      f.ns[tid] = n;
+    }
+  } else {
+  for (int i = tid; i < CSP * CSP; i += kUpdThreads) f.Gs[i] = Gc[(size_t)mf * p.B * CSP * CSP + i];
+  for (int i = tid; i < K * CSP; i += kUpdThreads) f.Ds[i] = Din[i];
   for (int i = tid; i < K * CSP; i += kUpdThreads) {
-    Ds[i] = D64[(size_t)m * K * CSP + i];
-    if (first) Dold[i] = Ds[i];
     double s = 0.0;
     for (int b0 = 0; b0 < nblk; b0 += 8) {  // blocks in order, 8 loads in flight
       double v[8];
@@ -409,7 +305,7 @@ __global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __res
       for (int u = 0; u < 8; ++u)
         if (b0 + u < nblk) s += v[u];
     }
-    bs[i] = s;
+    f.bs[i] = s;
   }
   for (int k = tid; k < K; k += kUpdThreads) {
     int n = 0;
@@ -420,32 +316,25 @@ __global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __res
 #pragma unroll
       for (int u = 0; u < 8; ++u) n += v[u];
     }
-    ns[k] = n;
+    f.ns[k] = n;
   }
-  if (obj) red[tid] = os;
+  }
   __syncthreads();
-  if (obj) {
-    for (int h = kUpdThreads / 2; h > 0; h >>= 1) {
-      if (tid < h) red[tid] += red[tid + h];
-      __syncthreads();
-    }
-    if (tid == 0) *objective = red[0];
-  }
   constexpr int SOLVERS = fit_solvers<CSP>();
   for (int k0 = 0; k0 < K; k0 += SOLVERS) {
     const int k = k0 + tid;
-    if (tid < SOLVERS && k < K && ns[k] > 0) {
+    if (tid < SOLVERS && k < K && f.ns[k] > 0) {
       double bk[CSP], x[CSP];
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) bk[j] = bs[k * CSP + j];
+      for (int i = 0; i < CSP; ++i) bk[i] = f.bs[k * CSP + i];
       if constexpr (fit_solve_lds<CSP>() > 0) {
-        solve_normal<CSP>(Gs, bk, Aw + (size_t)tid * CSP * CSP, x);
+        solve_normal<CSP>(f.Gs, bk, f.Aw + (size_t)tid * CSP * CSP, x);
       } else {
         double A[CSP * CSP];
-        solve_normal<CSP>(Gs, bk, A, x);
+        solve_normal<CSP>(f.Gs, bk, A, x);
       }
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) Ds[k * CSP + j] = x[j] / ns[k];
+      for (int i = 0; i < CSP; ++i) f.Ds[k * CSP + i] = x[i] / f.ns[k];
     }
   }
   __syncthreads();
@@ -455,131 +344,577 @@ __global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __res
     for (int i = 0; i < CSP; ++i) {
       double g = 0.0;
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) g += Gs[i * CSP + j] * Ds[k * CSP + j];
-      s += Ds[k * CSP + i] * g;
+      for (int b = 0; b < CSP; ++b) g += f.Gs[i * CSP + b] * f.Ds[k * CSP + b];
+      s += f.Ds[k * CSP + i] * g;
     }
-    qv[k] = s;
+    f.qs[k] = s;
   }
-  for (int i = tid; i < K * CSP; i += kUpdThreads) D64[(size_t)m * K * CSP + i] = Ds[i];
+  __syncthreads();
 }
 
-// codebooks = fp32(D64), codes[c][m] = ct[m][c], and the final objective.
+// The fit of the last step of a batch on its own (one workgroup): Dout = D,
+// qv = q, for the pass kernel that assigns that subspace.
+template <int CSP>
+__global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __restrict__ bins,
+                                                           const int* __restrict__ nbin, int nblk, EcParams p,
+                                                           int mf, const double* __restrict__ Gc,
+                                                           const double* __restrict__ Din, double* __restrict__ Dout,
+                                                           double* __restrict__ qv) {
+  extern __shared__ double sh[];  // all LDS dynamic (up to the whole 160 KB)
+  const FitLds f = fit_lds<CSP>(sh, p.K);
+  ec_fit_wg<CSP>(bins, nbin, nblk, p, mf, Gc, Din, f);
+  for (int i = threadIdx.x; i < p.K * CSP; i += kUpdThreads) Dout[i] = f.Ds[i];
+  for (int k = threadIdx.x; k < p.K; k += kUpdThreads) qv[k] = f.qs[k];
+}
+
+// One pass over E for kPassCh channels and every image (16 chunks of
+// kEcChunk images per round of 256), between the batch of Lp subspaces
+// starting at mp0 (all fitted; Lp = 0: none) and the batch of Ln subspaces
+// starting at mn0 (Ln = 0: none):
+//   assign:  the last subspace of the previous batch, ml = mp0 + Lp - 1, by
+//            Eq. (12) from P (still that subspace's), its new D (Dlast) and
+//            q; the chunk-0 threads store the codes;
+//   apply:   for i < Lp in order, E[n][c] -= sum_j S[n][(mp0+i) C's + j]
+//            dW_i[j][c] (dW_i = D_new[k_new] - D_old[k_old] of step i: from
+//            the prep kernels, the last one here), with the block sum of E^2
+//            after each into opart[i][block];
+//   collect: X[j][a][c] = sum_n S[n][(mn0+j) C's + a] E[n][c] for j < Ln
+//            (per chunk, then the chunks in order).
+// Per round the images' S columns of both batches are staged in LDS; the
+// chunk's E is loaded into registers (all loads in flight) before any of it
+// is written.  dW, the per-thread sums of E^2 and the X partials live in
+// LDS, so the registers hold little more than the chunk of E.
+template <int CSP, int B>
+__global__ __launch_bounds__(kEcThreads) void ec_pass_kernel(const float* __restrict__ S, EcParams p,
+                                                           double* __restrict__ E, int mp0, int Lp,
+                                                           const double* __restrict__ P,
+                                                           const double* __restrict__ Dlast,
+                                                           const double* __restrict__ qv, uint8_t* __restrict__ ct,
+                                                           const double* __restrict__ D64,
+                                                           const uint8_t* __restrict__ codes_old,
+                                                           const double* __restrict__ dW, int mn0, int Ln,
+                                                           double* __restrict__ X, double* __restrict__ opart) {
+  // LDS: X partials [256][B C's], per-thread E^2 sums [B][256], dW [B][16][C's],
+  // block-sum scratch, then one area that holds D^(ml) [K][C's] and q [K]
+  // for the assignment and afterwards, per round of 256 images, the images'
+  // S columns: [image][B C's] of the previous batch, then of the next.
+  extern __shared__ double sh[];
+  constexpr int kRound = kEcChunk * (kEcThreads / kPassCh);  // images per round
+  constexpr int BC = B * CSP;
+  constexpr int kChunkF = kEcChunk * 2 * BC + 4;  // floats per chunk in the stage (padded: no bank conflicts)
+  constexpr int kStage = kRound * 2 * BC;
+  double* xr = sh;  // [B C's][256]: thread fastest
+  double* osq = xr + (size_t)kEcThreads * BC;
+  double* dws = osq + (size_t)B * kEcThreads;
+  double* red = dws + (size_t)B * kPassCh * CSP;  // [B][waves]
+  double* sd = red + B * (kEcThreads / kWave);
+  double* q = sd + (size_t)p.K * CSP;
+  float* ss = reinterpret_cast<float*>(sd);
+  const int tid = threadIdx.x, cl = tid % kPassCh, chunk = tid / kPassCh;
+  const int c = blockIdx.x * kPassCh + cl;
+  const bool col = c < p.Ct;
+  const int cc = col ? c : p.Ct - 1;  // a valid column for loads whose value is not used
+  for (int i = tid; i < kEcThreads * BC; i += kEcThreads) xr[i] = 0.0;
+  for (int i = tid; i < B * kEcThreads; i += kEcThreads) osq[i] = 0.0;
+  if (Lp > 0) {
+    const int ml = mp0 + Lp - 1;
+    // dW of the batch's earlier steps for the block's channels (zeros past the block)
+    for (int t = tid; t < (Lp - 1) * kPassCh * CSP; t += kEcThreads) {
+      const int i = t / (kPassCh * CSP), r = t % (kPassCh * CSP), ch = r / CSP, a = r % CSP;
+      const int c2 = blockIdx.x * kPassCh + ch;
+      dws[t] = c2 < p.Ct ? dW[((size_t)i * CSP + a) * p.Ct + c2] : 0.0;
+    }
+    for (int i = tid; i < p.K * CSP; i += kEcThreads) sd[i] = Dlast[i];
+    for (int i = tid; i < p.K; i += kEcThreads) q[i] = qv[i];
+    double pc[CSP];
+#pragma unroll
+    for (int j = 0; j < CSP; ++j) pc[j] = P[(size_t)j * p.Ct + cc];
+    const double* wo = D64 + ((size_t)ml * p.K + codes_old[(size_t)(Lp - 1) * p.Ct + cc]) * CSP;
+    double dwo[CSP];
+#pragma unroll
+    for (int j = 0; j < CSP; ++j) dwo[j] = wo[j];
+    __syncthreads();
+    const int knew = ec_best<CSP>(sd, q, p.K, pc);
+    if (col && chunk == 0) ct[(size_t)ml * p.Ct + c] = (uint8_t)knew;
+    if (chunk == 0)
+#pragma unroll
+      for (int j = 0; j < CSP; ++j)
+        dws[((size_t)(Lp - 1) * kPassCh + cl) * CSP + j] = col ? sd[knew * CSP + j] - dwo[j] : 0.0;
+  }
+  for (int r0 = 0; r0 < p.N; r0 += kRound) {
+    __syncthreads();  // the assignment table or the previous round's stage may still be read
+    constexpr int kPer = kStage / kEcThreads;  // stage values per thread, all loads in flight
+    static_assert(kStage % kEcThreads == 0 && kPer <= 64, "stage share per thread");
+    for (int t0 = 0; t0 < kStage; t0 += kPer * kEcThreads) {
+      float v[kPer];
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {  // straight-line: every load issued, unused values masked
+        const int t = t0 + u * kEcThreads + tid;
+        const int img = t / (2 * BC), col2 = t % (2 * BC);
+        const int half = col2 / BC, c3 = col2 % BC;
+        const int len = half == 0 ? Lp : Ln, m0 = half == 0 ? mp0 : mn0;
+        const bool ok = t < kStage && r0 + img < p.N && c3 < len * CSP;
+        const size_t at = ok ? (size_t)(r0 + img) * p.Cs + (size_t)m0 * CSP + c3 : 0;
+        const float x = S[at];
+        v[u] = ok ? x : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int t = t0 + u * kEcThreads + tid;
+        const int img = t / (2 * BC);
+        if (t < kStage) ss[(img / kEcChunk) * kChunkF + (img % kEcChunk) * 2 * BC + t % (2 * BC)] = v[u];
+      }
+    }
+    __syncthreads();
+    const int n0 = r0 + chunk * kEcChunk;
+    // images past N: E read at a valid row and zeroed (their S is 0 too)
+    double e[kEcChunk];
+#pragma unroll
+    for (int i = 0; i < kEcChunk; ++i) {
+      const double v = E[(size_t)min(n0 + i, p.N - 1) * p.Ct + cc];
+      e[i] = col && n0 + i < p.N ? v : 0.0;
+    }
+    const float* sr = ss + (size_t)chunk * kChunkF;  // [image][2 B C's] of this chunk
+    for (int s = 0; s < Lp; ++s) {
+      double dw[CSP];
+#pragma unroll
+      for (int j = 0; j < CSP; ++j) dw[j] = dws[((size_t)s * kPassCh + cl) * CSP + j];
+      double sq = 0.0;
+#pragma unroll
+      for (int i = 0; i < kEcChunk; ++i) {
+        const float* srow = sr + i * 2 * BC + s * CSP;
+        double d = 0.0;
+#pragma unroll
+        for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[j];
+        e[i] -= d;
+        sq += e[i] * e[i];
+      }
+      osq[(size_t)s * kEcThreads + tid] += sq;
+    }
+    if (Lp > 0 && col) {
+#pragma unroll
+      for (int i = 0; i < kEcChunk; ++i)
+        if (n0 + i < p.N) E[(size_t)(n0 + i) * p.Ct + c] = e[i];
+    }
+    for (int s = 0; s < Ln; ++s) {
+      double acc[CSP];
+#pragma unroll
+      for (int j = 0; j < CSP; ++j) acc[j] = 0.0;
+#pragma unroll
+      for (int i = 0; i < kEcChunk; ++i) {
+        const float* srow = sr + i * 2 * BC + BC + s * CSP;
+#pragma unroll
+        for (int j = 0; j < CSP; ++j) acc[j] += (double)srow[j] * e[i];
+      }
+#pragma unroll
+      for (int j = 0; j < CSP; ++j) xr[(size_t)(s * CSP + j) * kEcThreads + tid] += acc[j];
+    }
+  }
+  // the block sums of E^2 after each step, all at once: per wave in a fixed
+  // shuffle order, then the waves in order
+  if (Lp > 0) {
+    double* wred = red;  // [B][waves]
+    __syncthreads();
+    for (int s = 0; s < Lp; ++s) {
+      double v = osq[(size_t)s * kEcThreads + tid];
+      for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+      if ((tid & (kWave - 1)) == 0) wred[s * (kEcThreads / kWave) + tid / kWave] = v;
+    }
+    __syncthreads();
+    if (tid < Lp) {
+      double v = 0.0;
+      for (int w = 0; w < kEcThreads / kWave; ++w) v += wred[tid * (kEcThreads / kWave) + w];
+      opart[(size_t)tid * gridDim.x + blockIdx.x] = v;
+    }
+  }
+  if (Ln > 0) {
+    __syncthreads();
+    // (channel, subspace, coordinate) triples: the 16 chunks in order
+    for (int t = tid; t < kPassCh * Ln * CSP; t += kEcThreads) {
+      const int ch = t % kPassCh, sj = t / kPassCh;  // sj = s C's + j
+      const int c2 = blockIdx.x * kPassCh + ch;
+      double v = 0.0;
+      for (int k = 0; k < kEcThreads / kPassCh; ++k) v += xr[(size_t)sj * kEcThreads + k * kPassCh + ch];
+      if (c2 < p.Ct) X[(size_t)sj * p.Ct + c2] = v;
+    }
+  }
+}
+
+template <int CSP, int B> size_t pass_lds_bytes(int K) {
+  const size_t fixed = ((size_t)kEcThreads * B * CSP + (size_t)B * kEcThreads + (size_t)B * kPassCh * CSP +
+                        (size_t)B * (kEcThreads / kWave)) * sizeof(double);
+  const size_t table = (size_t)K * (CSP + 1) * sizeof(double);
+  const size_t stage = (size_t)(kEcThreads / kPassCh) * (kEcChunk * 2 * B * CSP + 4) * sizeof(float);
+  return fixed + std::max(table, stage);
+}
+
+// LDS of the prep kernel: a fit, then P of the block in sorted order and
+// the counting sort's counts and offsets.
+template <int CSP> size_t prep_lds_bytes(int K) {
+  return fit_lds_bytes<CSP>(K) + (size_t)kEcThreads * CSP * sizeof(double) +
+         ((size_t)(kEcThreads / kWave) * K + 2 * (size_t)K) * sizeof(int);
+}
+
+// Per block of 256 output channels, step j of the batch (subspace m = m0 + j),
+// round `it` of Eq. (11)-(12):
+//   first (fm >= 0), the fit this step depends on, as ec_fit_wg (every
+//   workgroup computes it; workgroup 0 stores it in Dout): that of the last
+//   round of m - 1 (it == 0) or of round it - 1 of m;
+//   it == 0: if j > 0, the assignment of m - 1 (Eq. (12)) with that fit,
+//            dW_{j-1}[a][c] = D_new[k_new][a] - D64[m-1][k_old][a] stored;
+//            then P_c = X^(j)_c - sum_{i<j} Gc[m][j-i] dW_i[.][c]
+//            + G W^(m)_c, stored, and codes_old[j] = the codes of m;
+//   it >= 1: the codes of m by Eq. (12) from P and the fit;
+// then the block's sums over the channels assigned to each sub-codeword,
+// in channel order: bins[block][k][j] = sum of P_c[j], nbin[block][k] the
+// count.  The sums come from a counting sort in LDS: per wave, the lanes
+// sharing a code find their rank with ballots; codes x waves give each
+// channel its place, and one thread per (k, j) adds its run in order.
+template <int CSP, int B>
+__global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0, int j, int it, int fm,
+                                                           const double* __restrict__ Din,
+                                                           const double* __restrict__ bins_in,
+                                                           const int* __restrict__ nbin_in, int nblk,
+                                                           double* __restrict__ Dout, const double* __restrict__ X,
+                                                           const double* __restrict__ Gc,
+                                                           const double* __restrict__ D64, uint8_t* __restrict__ ct,
+                                                           double* __restrict__ P, double* __restrict__ dW,
+                                                           uint8_t* __restrict__ codes_old,
+                                                           double* __restrict__ bins, int* __restrict__ nbin) {
+  extern __shared__ double sp[];
+  const FitLds f = fit_lds<CSP>(sp, p.K);
+  double* Ps = reinterpret_cast<double*>(reinterpret_cast<char*>(sp) + fit_lds_bytes<CSP>(p.K));  // [256][C's]
+  int* cnt = reinterpret_cast<int*>(Ps + (size_t)kEcThreads * CSP);  // [waves][K]
+  int* tot = cnt + (kEcThreads / kWave) * p.K;                       // [K]
+  int* base = tot + p.K;                                             // [K]
+  const int tid = threadIdx.x, c = blockIdx.x * kEcThreads + tid;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const bool col = c < p.Ct;
+  const int m = m0 + j;
+  const double* gm = Gc + (size_t)m * p.B * CSP * CSP;  // Gc[m][d] = gm + d C's^2
+  // the fit's loads and those that do not depend on it, issued first
+  FitRegs pre;
+  pre.on = false;
+  if (fm >= 0) ec_fit_issue<CSP>(bins_in, nbin_in, nblk, p, fm, Gc, Din, pre);
+  double pc[CSP], pp[CSP], dlast[CSP], wrow[CSP], worow[CSP];
+#pragma unroll
+  for (int a = 0; a < CSP; ++a) dlast[a] = 0.0;
+  int k = 0, kold_prev = 0;
+  double dwv[B][CSP];  // dW of the steps before the previous one
+  if (col) {
+    if (it == 0) {
+#pragma unroll
+      for (int a = 0; a < CSP; ++a) pc[a] = X[((size_t)j * CSP + a) * p.Ct + c];
+#pragma unroll
+      for (int i = 0; i < B; ++i)
+        if (i < j - 1)
+#pragma unroll
+          for (int a = 0; a < CSP; ++a) dwv[i][a] = dW[((size_t)i * CSP + a) * p.Ct + c];
+      k = ct[(size_t)m * p.Ct + c];
+      if (j > 0) kold_prev = codes_old[(size_t)(j - 1) * p.Ct + c];
+      const double* w = D64 + ((size_t)m * p.K + k) * CSP;
+      const double* wo = D64 + ((size_t)(j > 0 ? m - 1 : m) * p.K + kold_prev) * CSP;
+#pragma unroll
+      for (int a = 0; a < CSP; ++a) {
+        wrow[a] = w[a];
+        worow[a] = wo[a];
+      }
+    }
+    if (it > 0 || j > 0)
+#pragma unroll
+      for (int a = 0; a < CSP; ++a) pp[a] = P[(size_t)a * p.Ct + c];
+  }
+  if (fm >= 0) {
+    ec_fit_wg<CSP>(bins_in, nbin_in, nblk, p, fm, Gc, Din, f, &pre);
+    if (blockIdx.x == 0)
+      for (int i = tid; i < p.K * CSP; i += kEcThreads) Dout[i] = f.Ds[i];
+  }
+  if (col) {
+    if (it == 0) {
+      if (j > 0) {  // m - 1 with its last fit
+        const int knew = ec_best<CSP>(f.Ds, f.qs, p.K, pp);
+        ct[(size_t)(m - 1) * p.Ct + c] = (uint8_t)knew;
+#pragma unroll
+        for (int a = 0; a < CSP; ++a) {
+          dlast[a] = f.Ds[knew * CSP + a] - worow[a];
+          dW[((size_t)(j - 1) * CSP + a) * p.Ct + c] = dlast[a];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        if (i < j) {
+          const bool last = i == j - 1;
+          const double* g = gm + (size_t)(j - i) * CSP * CSP;
+#pragma unroll
+          for (int a = 0; a < CSP; ++a) {
+            double s = 0.0;
+#pragma unroll
+            for (int b = 0; b < CSP; ++b) s += g[a * CSP + b] * (last ? dlast[b] : dwv[i][b]);
+            pc[a] -= s;
+          }
+        }
+      }
+#pragma unroll
+      for (int a = 0; a < CSP; ++a) {
+        double s = 0.0;
+#pragma unroll
+        for (int b = 0; b < CSP; ++b) s += gm[a * CSP + b] * wrow[b];
+        pc[a] += s;
+        P[(size_t)a * p.Ct + c] = pc[a];
+      }
+      codes_old[(size_t)j * p.Ct + c] = (uint8_t)k;
+    } else {
+#pragma unroll
+      for (int a = 0; a < CSP; ++a) pc[a] = pp[a];
+      k = ec_best<CSP>(f.Ds, f.qs, p.K, pc);
+      ct[(size_t)m * p.Ct + c] = (uint8_t)k;
+    }
+  }
+  // ---- counting sort of the block's channels by code
+  for (int i = lane; i < p.K; i += kWave) cnt[wave * p.K + i] = 0;
+  // (each wave clears and fills only its own row of counts)
+  int rank = 0;
+  uint64_t todo = __ballot(col);
+  while (todo) {
+    const int leader = __ffsll((unsigned long long)todo) - 1;
+    const int kk = __builtin_amdgcn_readlane(k, leader);
+    const uint64_t same = __ballot(col && k == kk);
+    if (col && k == kk) rank = __popcll(same & ((1ull << lane) - 1ull));
+    if (lane == leader) cnt[wave * p.K + kk] = __popcll(same);
+    todo &= ~same;
+  }
+  __syncthreads();
+  for (int kk = tid; kk < p.K; kk += kEcThreads) {
+    int t = 0;
+    for (int w = 0; w < kEcThreads / kWave; ++w) t += cnt[w * p.K + kk];
+    tot[kk] = t;
+  }
+  __syncthreads();
+  if (p.K <= kWave) {  // exclusive prefix of tot by one wave's shuffles
+    if (wave == 0) {
+      const int t = lane < p.K ? tot[lane] : 0;
+      int v = t;
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int u = __shfl_up(v, off, kWave);
+        if (lane >= off) v += u;
+      }
+      if (lane < p.K) base[lane] = v - t;
+    }
+  } else {
+    for (int kk = tid; kk < p.K; kk += kEcThreads) {
+      int b0 = 0;
+      for (int i = 0; i < kk; ++i) b0 += tot[i];
+      base[kk] = b0;
+    }
+  }
+  __syncthreads();
+  if (col) {
+    int pos = base[k] + rank;
+    for (int w = 0; w < wave; ++w) pos += cnt[w * p.K + k];
+#pragma unroll
+    for (int a = 0; a < CSP; ++a) Ps[(size_t)pos * CSP + a] = pc[a];
+  }
+  __syncthreads();
+  for (int t = tid; t < p.K * CSP; t += kEcThreads) {
+    const int kk = t / CSP, a = t % CSP;
+    double s = 0.0;
+    for (int i = 0; i < tot[kk]; ++i) s += Ps[(size_t)(base[kk] + i) * CSP + a];
+    bins[((size_t)blockIdx.x * p.K + kk) * CSP + a] = s;
+  }
+  for (int kk = tid; kk < p.K; kk += kEcThreads) nbin[(size_t)blockIdx.x * p.K + kk] = tot[kk];
+}
+
+// After a batch's pass: D64[mp0 + i] = Dnew[i] for i < Lp (the batch's final
+// sub-codebooks), and objective[s] = the sum over the blocks of
+// opart[s][block] for s < rows <= 16, in a fixed order: 16 threads per row
+// each add a strided share of the blocks in order, then a fixed tree over
+// the 16.  One workgroup.
+__global__ __launch_bounds__(kUpdThreads) void ec_commit_kernel(const double* __restrict__ opart, int nblk,
+                                                              int rows, double* __restrict__ objective,
+                                                              const double* __restrict__ Dnew,
+                                                              double* __restrict__ D64, int mp0, int Lp, int kc) {
+  __shared__ double red[kUpdThreads];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < Lp * kc; i += kUpdThreads) D64[(size_t)mp0 * kc + i] = Dnew[i];
+  if (!objective) return;  // uniform
+  const int s = tid / 16, t = tid % 16;
+  double v = 0.0;
+  if (s < rows)
+    for (int b0 = t; b0 < nblk; b0 += 16 * 16) {  // 16 loads in flight, added in order
+      double x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = b0 + 16 * u < nblk ? opart[(size_t)s * nblk + b0 + 16 * u] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v += x[u];
+    }
+  red[tid] = v;
+  __syncthreads();
+  for (int h = 8; h > 0; h >>= 1) {
+    if (t < h) red[tid] += red[tid + h];
+    __syncthreads();
+  }
+  if (t == 0 && s < rows) objective[s] = red[tid];
+}
+
+// codebooks = fp32(D64), codes[c][m] = ct[m][c].
 __global__ __launch_bounds__(kEcThreads) void ec_finish_kernel(const double* __restrict__ D64, EcParams p,
                                                              const uint8_t* __restrict__ ct,
-                                                             float* __restrict__ D, uint8_t* __restrict__ codes,
-                                                             const double* __restrict__ opart, int nopart,
-                                                             double* __restrict__ objective) {
+                                                             float* __restrict__ D, uint8_t* __restrict__ codes) {
   const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (size_t)gridDim.x * blockDim.x;
   const size_t nd = (size_t)p.M * p.K * p.Csp, nc = (size_t)p.M * p.Ct;
   for (size_t i = tid; i < nd; i += stride) D[i] = (float)D64[i];
   for (size_t i = tid; i < nc; i += stride) codes[i] = ct[(i % p.M) * p.Ct + i / p.M];
-  if (tid == 0 && objective) {  // once per call: a serial sum is fine here
-    double s = 0.0;
-    for (int b = 0; b < nopart; ++b) s += opart[b];
-    *objective = s;
-  }
 }
 
 }  // namespace
-
-size_t ec_fc_workspace(int N, int Ct, int M, int K, int Csp) {
-  const int nchunks = ceil_div(N, kEcChunk);
-  const size_t cblocks = (size_t)ceil_div(Ct, kEcThreads);
-  size_t b = 0;
-  b += (size_t)N * Ct * 8;                       // E
-  b += (size_t)nchunks * Csp * Ct * 8;           // partial P
-  b += (size_t)Csp * Ct * 8;                     // P
-  b += (size_t)M * Csp * Csp * 8;                // G
-  b += (size_t)M * K * Csp * 8;                  // D64
-  b += (size_t)K * Csp * 8;                      // Dold
-  b += (size_t)K * 8;                            // q
-  b += cblocks * nchunks * 8;                    // objective partials
-  b += cblocks * K * Csp * 8;                    // bins
-  b += cblocks * K * 4;                          // nbin
-  b += (size_t)Ct;                               // codes_old
-  b += (size_t)M * Ct;                           // codes, [M][C_t]
-  return b + 16 * 256;                           // each slice is rounded up to 256 bytes
-}
 
 template <int CSP>
 hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, const float* T, float* D,
                          uint8_t* codes, int sweeps, int inner, double* objective, hipStream_t stream) {
   constexpr int Csp = CSP;
-  EcParams p{N, Cs, Ct, M, K, Csp, inner, ceil_div(N, kEcChunk)};
-  const int cblocks = ceil_div(Ct, kEcThreads);
-  const int nopart = cblocks * p.nchunks;
-  Scratch scratch;
-  hipError_t e = scratch.acquire(stream, ec_fc_workspace(N, Ct, M, K, Csp));
-  if (e != hipSuccess) return e;
-  auto step = ec_step_kernel<CSP>;
-  auto reduce = ec_reduce_kernel<CSP>;
+  constexpr int B = ec_batch<CSP>();
+  EcParams p{N, Cs, Ct, M, K, Csp, inner, ceil_div(N, kEcChunk), B};
+  const int cblocks = ceil_div(Ct, kEcThreads);     // start (columns) and prep (channel blocks)
+  const int pblocks = ceil_div(Ct, kPassCh);        // pass workgroups
+  const int nstart = cblocks * p.nchunks;           // start kernel's block sums
+  const int kc = K * Csp;
+  auto pass = ec_pass_kernel<CSP, B>;
+  auto prep = ec_prep_kernel<CSP, B>;
   auto fit = ec_fit_kernel<CSP>;
-  const size_t step_lds = ((size_t)K * (Csp + 1) + kEcThreads / kWave) * sizeof(double);
-  const size_t red_lds = ((size_t)Csp * kEcThreads + red_area(K, Csp)) * sizeof(double) + kEcThreads;
+  const size_t pass_lds = pass_lds_bytes<CSP, B>(K);
+  const size_t prep_lds = prep_lds_bytes<CSP>(K);
   const size_t fit_lds = fit_lds_bytes<CSP>(K);
-  if (step_lds > kLdsBytes || red_lds > kLdsBytes || fit_lds > kLdsBytes) return hipErrorInvalidValue;
-  if ((e = allow_max_lds((const void*)step)) != hipSuccess) return e;
-  if ((e = allow_max_lds((const void*)reduce)) != hipSuccess) return e;
+  if (pass_lds > kLdsBytes || prep_lds > kLdsBytes || fit_lds > kLdsBytes) return hipErrorInvalidValue;
+  hipError_t e;
+  if ((e = allow_max_lds((const void*)pass)) != hipSuccess) return e;
+  if ((e = allow_max_lds((const void*)prep)) != hipSuccess) return e;
   if ((e = allow_max_lds((const void*)fit)) != hipSuccess) return e;
+  // workspace slices, each rounded up to 256 bytes
+  const size_t sizes[] = {
+      (size_t)N * Ct * 8,                                  // E
+      (size_t)B * Csp * Ct * 8,                            // X
+      (size_t)Csp * Ct * 8,                                // P
+      (size_t)B * Csp * Ct * 8,                            // dW
+      (size_t)M * B * Csp * Csp * 8,                       // Gc
+      (size_t)M * kc * 8,                                  // D64
+      (size_t)B * kc * 8,                                  // Dnew
+      (size_t)2 * kc * 8,                                  // Dpp (fits of the inner rounds)
+      (size_t)K * 8,                                       // q
+      (size_t)std::max(nstart, B * pblocks) * 8,           // objective block sums
+      (size_t)2 * cblocks * kc * 8,                        // bins (two buffers)
+      (size_t)2 * cblocks * K * 4,                         // nbin (two buffers)
+      (size_t)B * Ct,                                      // codes_old
+      (size_t)M * Ct,                                      // codes, [M][C_t]
+  };
+  size_t total = 0;
+  for (size_t b : sizes) total += (b + 255) & ~(size_t)255;
+  Scratch scratch;
+  if ((e = scratch.acquire(stream, total)) != hipSuccess) return e;
   char* w = scratch.get();
-  auto take = [&](size_t bytes) {
+  int si = 0;
+  auto take = [&]() {
     char* r = w;
-    w += (bytes + 255) & ~(size_t)255;
+    w += (sizes[si++] + 255) & ~(size_t)255;
     return r;
   };
-  double* E = reinterpret_cast<double*>(take((size_t)N * Ct * 8));
-  double* part = reinterpret_cast<double*>(take((size_t)p.nchunks * Csp * Ct * 8));
-  double* P = reinterpret_cast<double*>(take((size_t)Csp * Ct * 8));
-  double* G = reinterpret_cast<double*>(take((size_t)M * Csp * Csp * 8));
-  double* D64 = reinterpret_cast<double*>(take((size_t)M * K * Csp * 8));
-  double* Dold = reinterpret_cast<double*>(take((size_t)K * Csp * 8));
-  double* qv = reinterpret_cast<double*>(take((size_t)K * 8));
-  double* opart = reinterpret_cast<double*>(take((size_t)nopart * 8));
-  double* bins = reinterpret_cast<double*>(take((size_t)cblocks * K * Csp * 8));
-  int* nbin = reinterpret_cast<int*>(take((size_t)cblocks * K * 4));
-  uint8_t* codes_old = reinterpret_cast<uint8_t*>(take((size_t)Ct));
-  uint8_t* ct = reinterpret_cast<uint8_t*>(take((size_t)M * Ct));
+  double* E = reinterpret_cast<double*>(take());
+  double* X = reinterpret_cast<double*>(take());
+  double* P = reinterpret_cast<double*>(take());
+  double* dW = reinterpret_cast<double*>(take());
+  double* Gc = reinterpret_cast<double*>(take());
+  double* D64 = reinterpret_cast<double*>(take());
+  double* Dnew = reinterpret_cast<double*>(take());
+  double* Dpp = reinterpret_cast<double*>(take());
+  double* qv = reinterpret_cast<double*>(take());
+  double* opart = reinterpret_cast<double*>(take());
+  double* bins = reinterpret_cast<double*>(take());
+  int* nbin = reinterpret_cast<int*>(take());
+  uint8_t* codes_old = reinterpret_cast<uint8_t*>(take());
+  uint8_t* ct = reinterpret_cast<uint8_t*>(take());
+  auto bins_at = [&](int sel) { return bins + (size_t)sel * cblocks * kc; };
+  auto nbin_at = [&](int sel) { return nbin + (size_t)sel * cblocks * K; };
 
-  const size_t ninit = std::max<size_t>({(size_t)M * Ct, (size_t)M * K * Csp, (size_t)M * Csp * Csp});
+  const size_t ninit = std::max<size_t>({(size_t)M * Ct, (size_t)M * kc, (size_t)M * B * Csp * Csp});
   const unsigned iblocks = (unsigned)std::min<size_t>(8192, ceil_div_z(ninit, kEcThreads));
   hipLaunchKernelGGL(ec_init_kernel, dim3(iblocks), dim3(kEcThreads), 0, stream, S, D, (const uint8_t*)codes, p,
-                     D64, ct, G);
+                     D64, ct, Gc);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const dim3 pgrid((unsigned)cblocks, (unsigned)p.nchunks);
-  hipLaunchKernelGGL(ec_start_kernel<CSP>, pgrid, dim3(kEcThreads), 0, stream, S, T, p, (const double*)D64,
-                     (const uint8_t*)ct, E, opart);
+  hipLaunchKernelGGL(ec_start_kernel<CSP>, dim3((unsigned)cblocks, (unsigned)p.nchunks), dim3(kEcThreads), 0,
+                     stream, S, T, p, (const double*)D64, (const uint8_t*)ct, E, opart);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  int nstep = 0;
-  int ma = -1;  // subspace fitted by the previous step, which the next step kernel finishes
-  for (int s = 0; s < sweeps; ++s) {
-    for (int m = 0; m < M; ++m, ++nstep) {
-      hipLaunchKernelGGL(step, pgrid, dim3(kEcThreads), step_lds, stream, S, p, E, ma, (const double*)P,
-                         (const double*)D64, (const double*)qv, ct, (const double*)Dold,
-                         (const uint8_t*)codes_old, m, part, opart);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-      for (int it = 0; it < inner; ++it) {
-        hipLaunchKernelGGL(reduce, dim3((unsigned)cblocks), dim3(kEcThreads), red_lds, stream, (const double*)part,
-                           p, m, (const double*)G, (const double*)D64, (const double*)qv, it == 0 ? 0 : 1, ct,
-                           P, codes_old, bins, nbin);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        // objective[nstep] is the value before this step (after the previous one)
-        hipLaunchKernelGGL(fit, dim3(1), dim3(kUpdThreads), fit_lds, stream, (const double*)bins,
-                           (const int*)nbin, cblocks, p, m, (const double*)G, D64, it == 0 ? 1 : 0, Dold,
-                           (const double*)opart, nopart, objective ? objective + nstep : nullptr, qv);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-      }
-      ma = m;
-    }
-  }
-  if (ma >= 0) {  // finish the last step and sum the final objective
-    hipLaunchKernelGGL(step, pgrid, dim3(kEcThreads), step_lds, stream, S, p, E, ma, (const double*)P,
-                       (const double*)D64, (const double*)qv, ct, (const double*)Dold, (const uint8_t*)codes_old,
-                       -1, part, opart);
+  if (objective) {
+    hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream, (const double*)opart, nstart, 1,
+                       objective, (const double*)Dnew, D64, 0, 0, kc);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  // Input of the fit of round r of subspace m: D64[m] for r = 0, else the
+  // previous round's fit (Dpp[(r - 1) % 2]); its output: Dpp[r % 2], or
+  // Dnew[j] for the last round.  No fit reads the buffer it writes.
+  auto fit_in = [&](int m, int r) -> const double* {
+    return r == 0 ? D64 + (size_t)m * kc : Dpp + (size_t)((r - 1) % 2) * kc;
+  };
+  auto fit_out = [&](int j, int r) -> double* {
+    return r == inner - 1 ? Dnew + (size_t)j * kc : Dpp + (size_t)(r % 2) * kc;
+  };
+  int sel = 0;            // bins buffer the last prep kernel wrote
+  int nstep = 0;          // subspace steps whose objective is recorded
+  int mp0 = -1, Lp = 0;   // the previous batch (fitted but for its last round, updates not yet in E)
+  auto close_and_pass = [&](int mn0, int Ln) -> hipError_t {
+    hipError_t r;
+    if (Lp > 0) {  // the last fit of the previous batch
+      const int ml = mp0 + Lp - 1;
+      hipLaunchKernelGGL(fit, dim3(1), dim3(kUpdThreads), fit_lds, stream, (const double*)bins_at(sel),
+                         (const int*)nbin_at(sel), cblocks, p, ml, (const double*)Gc, fit_in(ml, inner - 1),
+                         fit_out(Lp - 1, inner - 1), qv);
+      if ((r = hipGetLastError()) != hipSuccess) return r;
+    }
+    hipLaunchKernelGGL(pass, dim3((unsigned)pblocks), dim3(kEcThreads), pass_lds, stream, S, p, E, mp0, Lp,
+                       (const double*)P, (const double*)(Dnew + (size_t)(Lp > 0 ? Lp - 1 : 0) * kc),
+                       (const double*)qv, ct, (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0,
+                       Ln, X, opart);
+    if ((r = hipGetLastError()) != hipSuccess) return r;
+    if (Lp > 0) {
+      hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream, (const double*)opart, pblocks, Lp,
+                         objective ? objective + 1 + nstep : nullptr, (const double*)Dnew, D64, mp0, Lp, kc);
+      if ((r = hipGetLastError()) != hipSuccess) return r;
+    }
+    nstep += Lp;
+    return hipSuccess;
+  };
+  for (int s = 0; s < sweeps; ++s) {
+    for (int m0 = 0; m0 < M; m0 += B) {
+      const int L = std::min(B, M - m0);
+      if ((e = close_and_pass(m0, L)) != hipSuccess) return e;
+      for (int j = 0; j < L; ++j) {
+        for (int it = 0; it < inner; ++it) {
+          // the fit this step waits for: the last round of m - 1, or round it - 1 of m
+          int fm = -1, fj = 0, fr = 0;
+          if (it > 0) {
+            fm = m0 + j;
+            fj = j;
+            fr = it - 1;
+          } else if (j > 0) {
+            fm = m0 + j - 1;
+            fj = j - 1;
+            fr = inner - 1;
+          }
+          const double* din = fm >= 0 ? fit_in(fm, fr) : D64;
+          double* dout = fm >= 0 ? fit_out(fj, fr) : Dpp;
+          hipLaunchKernelGGL(prep, dim3((unsigned)cblocks), dim3(kEcThreads), prep_lds, stream, p, m0, j, it, fm, din,
+                             (const double*)bins_at(sel), (const int*)nbin_at(sel), cblocks, dout, (const double*)X,
+                             (const double*)Gc, (const double*)D64, ct, P, dW, codes_old, bins_at(sel ^ 1),
+                             nbin_at(sel ^ 1));
+          if ((e = hipGetLastError()) != hipSuccess) return e;
+          sel ^= 1;
+        }
+      }
+      mp0 = m0;
+      Lp = L;
+    }
+  }
+  if (Lp > 0 && (e = close_and_pass(-1, 0)) != hipSuccess) return e;  // finish the last batch
   hipLaunchKernelGGL(ec_finish_kernel, dim3(iblocks), dim3(kEcThreads), 0, stream, (const double*)D64, p,
-                     (const uint8_t*)ct, D, codes, (const double*)opart, nopart,
-                     objective ? objective + nstep : nullptr);
+                     (const uint8_t*)ct, D, codes);
   return hipGetLastError();
 }
 
