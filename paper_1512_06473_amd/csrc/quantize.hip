@@ -10,13 +10,14 @@
 //
 // * Assignment (pq_assign_kernel): one thread per sub-vector, the subspace's
 //   codebook in LDS (every thread reads the same sub-codeword at a time, a
-//   broadcast).  The distance is accumulated in fp32 as
+//   broadcast); for a fully-connected layer pq_assign_fc_kernel reads whole
+//   runs of weight rows instead (below), with the same arithmetic.  The distance is accumulated in fp32 as
 //   d = fma(w_j - c_j, w_j - c_j, d) over j in order and the first minimum
 //   wins, so the decision is reproducible bit for bit.  The minimum
 //   distances are summed in float64 in a fixed tree order per block, then
 //   per subspace (pq_objective_kernel).
-// * Update (pq_update_kernel): one workgroup per subspace and one thread per
-//   sub-codeword.  Chunks of the subspace's sub-vectors and their codes are
+// * Update (pq_update_kernel): one workgroup per subspace (XCD-major) and
+//   one thread per sub-codeword.  Chunks of the subspace's sub-vectors and their codes are
 //   staged in LDS with coalesced loads and sorted stably by code; thread k
 //   adds the sub-vectors coded k in float64 in sub-vector order, so each mean
 //   is summed in a fixed order and rounded once to fp32.  A sub-codeword that
@@ -48,32 +49,37 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* red) {
   return s;
 }
 
+// CSP > 0: C'_s fixed at compile time (the loops over a sub-vector are
+// exact); CSP = 0: any C'_s up to kMaxCsp, read at run time.
+template <int CSP>
 __global__ __launch_bounds__(kQThreads) void pq_assign_kernel(const float* __restrict__ W,
                                                               const float* __restrict__ D, QShape q,
                                                               uint8_t* __restrict__ codes,
                                                               double* __restrict__ part) {
+  constexpr int NJ = CSP > 0 ? CSP : kMaxCsp;
+  const int csp = CSP > 0 ? CSP : q.Csp;
   extern __shared__ float cb[];  // K x C'_s sub-codewords of subspace m
   __shared__ double red[kQThreads / kWave];
   const int m = blockIdx.y;
-  const float* Dm = D + (size_t)m * q.K * q.Csp;
-  for (int i = threadIdx.x; i < q.K * q.Csp; i += kQThreads) cb[i] = Dm[i];
+  const float* Dm = D + (size_t)m * q.K * csp;
+  for (int i = threadIdx.x; i < q.K * csp; i += kQThreads) cb[i] = Dm[i];
   __syncthreads();
   const int i = blockIdx.x * kQThreads + threadIdx.x;
   double mine = 0.0;
   if (i < q.n) {
     const int t = i / q.P, p = i - t * q.P;
-    const float* src = W + ((size_t)t * q.Cs + (size_t)m * q.Csp) * q.P + p;
-    float w[kMaxCsp];
+    const float* src = W + ((size_t)t * q.Cs + (size_t)m * csp) * q.P + p;
+    float w[NJ];
 #pragma unroll
-    for (int j = 0; j < kMaxCsp; ++j) w[j] = j < q.Csp ? src[(size_t)j * q.P] : 0.f;
+    for (int j = 0; j < NJ; ++j) w[j] = j < csp ? src[(size_t)j * q.P] : 0.f;
     int best = 0;
     float bd = 0.f;
     for (int k = 0; k < q.K; ++k) {
-      const float* c = cb + k * q.Csp;
+      const float* c = cb + k * csp;
       float d = 0.f;
 #pragma unroll
-      for (int j = 0; j < kMaxCsp; ++j) {
-        if (j < q.Csp) {
+      for (int j = 0; j < NJ; ++j) {
+        if (j < csp) {
           const float diff = w[j] - c[j];
           d = fmaf(diff, diff, d);
         }
@@ -88,6 +94,100 @@ __global__ __launch_bounds__(kQThreads) void pq_assign_kernel(const float* __res
   }
   const double s = block_sum_fixed(mine, red);
   if (threadIdx.x == 0) part[(size_t)m * gridDim.x + blockIdx.x] = s;
+}
+
+// Assignment of a fully-connected layer (one kernel position): a workgroup
+// takes kFcRows output channels x kFcSubs consecutive subspaces; thread
+// (r, s) decides rows r, r + 8, ... of subspace m0 + s.  Neighbouring lanes
+// read neighbouring subspaces of one weight row (kFcSubs C'_s contiguous
+// floats) and write neighbouring code bytes; the sub-codewords of the
+// workgroup's subspaces sit in LDS as [k][s][C'_s], so the lanes of one k
+// read consecutive addresses.  The distance and the first-minimum rule are
+// those of pq_assign_kernel; the minimum distances of each subspace are
+// summed per workgroup in a fixed order (each thread's rows in order, then
+// the 8 row groups in order) into part[m][row block].
+constexpr int kFcRows = 256;
+constexpr int kFcSubs = 32;
+
+template <int CSP>
+__global__ __launch_bounds__(kQThreads) void pq_assign_fc_kernel(const float* __restrict__ W,
+                                                                 const float* __restrict__ D, QShape q,
+                                                                 uint8_t* __restrict__ codes,
+                                                                 double* __restrict__ part) {
+  extern __shared__ float cbs[];  // [K][kFcSubs][C'_s]
+  __shared__ double red[kQThreads / kFcSubs][kFcSubs];
+  const int m0 = blockIdx.y * kFcSubs;
+  const int ns = min(kFcSubs, q.M - m0);
+  // staged with 16-byte loads: quad e covers (sub, k, 4 coordinates); the
+  // subspaces' codebooks are contiguous in D
+  static_assert(CSP % 4 == 0, "16-byte staging");
+  for (int e = threadIdx.x; e < q.K * kFcSubs * (CSP / 4); e += kQThreads) {
+    const int sub = e / (q.K * (CSP / 4)), r = e % (q.K * (CSP / 4)), k = r / (CSP / 4), j4 = r % (CSP / 4);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (sub < ns) v = *reinterpret_cast<const float4*>(D + ((size_t)(m0 + sub) * q.K + k) * CSP + 4 * j4);
+    *reinterpret_cast<float4*>(cbs + ((size_t)k * kFcSubs + sub) * CSP + 4 * j4) = v;
+  }
+  __syncthreads();
+  const int sub = threadIdx.x % kFcSubs, r0 = threadIdx.x / kFcSubs;
+  const int m = m0 + sub;
+  double mine = 0.0;
+  if (sub < ns) {
+    // four rows at a time: their loads in flight together (rows past C_t read
+    // row C_t - 1 and are dropped)
+    constexpr int RS = kQThreads / kFcSubs;  // row stride
+    for (int r = r0; r < kFcRows; r += 4 * RS) {
+      float w[4][CSP];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int t = min(blockIdx.x * kFcRows + r + u * RS, q.Ct - 1);
+        const float* src = W + (size_t)t * q.Cs + (size_t)m * CSP;
+#pragma unroll
+        for (int j4 = 0; j4 < CSP / 4; ++j4) {
+          const float4 v = *reinterpret_cast<const float4*>(src + 4 * j4);
+          w[u][4 * j4] = v.x;
+          w[u][4 * j4 + 1] = v.y;
+          w[u][4 * j4 + 2] = v.z;
+          w[u][4 * j4 + 3] = v.w;
+        }
+      }
+      int best[4] = {0, 0, 0, 0};
+      float bd[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < q.K; ++k) {
+        const float* c = cbs + ((size_t)k * kFcSubs + sub) * CSP;
+        float cv[CSP];
+#pragma unroll
+        for (int j = 0; j < CSP; ++j) cv[j] = c[j];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          float d = 0.f;
+#pragma unroll
+          for (int j = 0; j < CSP; ++j) {
+            const float diff = w[u][j] - cv[j];
+            d = fmaf(diff, diff, d);
+          }
+          if (k == 0 || d < bd[u]) {
+            bd[u] = d;
+            best[u] = k;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int t = blockIdx.x * kFcRows + r + u * RS;
+        if (t < q.Ct) {
+          codes[(size_t)t * q.M + m] = (uint8_t)best[u];
+          mine += (double)bd[u];
+        }
+      }
+    }
+  }
+  red[r0][sub] = mine;
+  __syncthreads();
+  if (r0 == 0 && sub < ns) {
+    double v = 0.0;
+    for (int g = 0; g < kQThreads / kFcSubs; ++g) v += red[g][sub];
+    part[(size_t)m * gridDim.x + blockIdx.x] = v;
+  }
 }
 
 // obj_m[m] = sum over the assignment blocks of subspace m, in block order.
@@ -118,39 +218,47 @@ __global__ __launch_bounds__(kQThreads) void pq_total_kernel(const double* __res
 // holding the same code are found bit by bit, a lane's rank is the number of
 // such lanes below it, earlier waves of the same round and earlier rounds
 // add their counts.
+// Subspaces are mapped XCD-major (blocks b, b+8, ... on one XCD take
+// consecutive subspaces), so the workgroups that share the cache lines of a
+// weight row (neighbouring subspaces of a fully-connected layer) share an L2.
+template <int CSP>
 __global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __restrict__ W,
                                                               const uint8_t* __restrict__ codes, QShape q,
                                                               float* __restrict__ D, int* __restrict__ counts) {
+  constexpr int NJ = CSP > 0 ? CSP : kMaxCsp;
   __shared__ float sv[kChunkFloats];        // staged sub-vectors, [il][C'_s]
   __shared__ uint8_t sc[kChunkFloats];      // their codes
   __shared__ uint16_t perm[kChunkFloats];   // chunk positions sorted by code, stable
   __shared__ int cnt[256], start[256], run[256];
   __shared__ int wcnt[kQThreads / kWave][256];
-  const int m = blockIdx.x;
+  const int per_xcd = (q.M + 7) / 8;
+  const int m = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
+  if (m >= q.M) return;  // whole workgroup, before any barrier
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int chunk = kChunkFloats / q.Csp;
-  double sum[kMaxCsp];
+  const int csp = CSP > 0 ? CSP : q.Csp;
+  const int chunk = kChunkFloats / csp;
+  double sum[NJ];
 #pragma unroll
-  for (int j = 0; j < kMaxCsp; ++j) sum[j] = 0.0;
+  for (int j = 0; j < NJ; ++j) sum[j] = 0.0;
   int total = 0;  // members of sub-codeword tid over all chunks (tid < K)
   for (int base = 0; base < q.n; base += chunk) {
     const int len = min(chunk, q.n - base);
     __syncthreads();  // the previous chunk is done
-    for (int e = tid; e < len * q.Csp; e += kQThreads) {
+    for (int e = tid; e < len * csp; e += kQThreads) {
       // Element (il, j).  Conv: j slowest, so that consecutive threads read
       // consecutive kernel positions of one input channel; FC (one position):
       // j fastest, so that they read the contiguous C'_s floats of a row.
       int j, il;
       if (q.P == 1) {
-        il = e / q.Csp;
-        j = e - il * q.Csp;
+        il = e / csp;
+        j = e - il * csp;
       } else {
         j = e / len;
         il = e - j * len;
       }
       const int i = base + il;
       const int t = i / q.P, p = i - t * q.P;
-      sv[il * q.Csp + j] = W[((size_t)t * q.Cs + (size_t)m * q.Csp + j) * q.P + p];
+      sv[il * csp + j] = W[((size_t)t * q.Cs + (size_t)m * csp + j) * q.P + p];
     }
     for (int il = tid; il < len; il += kQThreads) sc[il] = codes[(size_t)(base + il) * q.M + m];
     for (int k = tid; k < 256; k += kQThreads) {
@@ -211,20 +319,20 @@ __global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __res
     if (tid < q.K) {
       const int s0 = start[tid], n_k = cnt[tid];
       for (int r = 0; r < n_k; ++r) {
-        const float* v = sv + perm[s0 + r] * q.Csp;
+        const float* v = sv + perm[s0 + r] * csp;
 #pragma unroll
-        for (int j = 0; j < kMaxCsp; ++j)
-          if (j < q.Csp) sum[j] += (double)v[j];
+        for (int j = 0; j < NJ; ++j)
+          if (j < csp) sum[j] += (double)v[j];
       }
       total += n_k;
     }
   }
   if (tid < q.K) {
-    float* dst = D + ((size_t)m * q.K + tid) * q.Csp;
+    float* dst = D + ((size_t)m * q.K + tid) * csp;
     if (total) {
 #pragma unroll
-      for (int j = 0; j < kMaxCsp; ++j)
-        if (j < q.Csp) dst[j] = (float)(sum[j] / (double)total);
+      for (int j = 0; j < NJ; ++j)
+        if (j < csp) dst[j] = (float)(sum[j] / (double)total);
     }
     if (counts) counts[(size_t)m * q.K + tid] = total;
   }
@@ -236,11 +344,33 @@ QShape make_shape(int Ct, int Cs, int dk, int M, int K, int Csp) {
 
 // Assignment plus the objective reduction: obj_m ([M], may be null) and
 // total (may be null); obj_tmp is room for M doubles when obj_m is null.
+// True when the fully-connected assignment kernel serves this layer.
+bool fc_assign(const QShape& q, const float* W, const float* D) {
+  // 16-byte loads of the weight rows and codebooks: C_s and the base
+  // addresses must keep every sub-vector 16-byte aligned
+  return q.P == 1 && (q.Csp == 4 || q.Csp == 8) && q.Cs % 4 == 0 && ((uintptr_t)W & 15) == 0 &&
+         ((uintptr_t)D & 15) == 0 && (size_t)q.K * kFcSubs * q.Csp * sizeof(float) <= 64 * 1024;
+}
+
+// Blocks per subspace of the assignment (the objective partials per subspace).
+int assign_blocks(const QShape& q, bool fc) { return fc ? ceil_div(q.Ct, kFcRows) : ceil_div(q.n, kQThreads); }
+
 hipError_t assign(const QShape& q, const float* W, const float* D, uint8_t* codes, double* part, double* obj_m,
                   double* obj_tmp, double* total, hipStream_t stream) {
-  const int nblk = ceil_div(q.n, kQThreads);
-  hipLaunchKernelGGL(pq_assign_kernel, dim3((unsigned)nblk, (unsigned)q.M), dim3(kQThreads),
-                     (size_t)q.K * q.Csp * sizeof(float), stream, W, D, q, codes, part);
+  const bool fc = fc_assign(q, W, D);
+  const int nblk = assign_blocks(q, fc);
+  if (fc) {
+    auto k = q.Csp == 4 ? pq_assign_fc_kernel<4> : pq_assign_fc_kernel<8>;
+    hipLaunchKernelGGL(k, dim3((unsigned)nblk, (unsigned)ceil_div(q.M, kFcSubs)), dim3(kQThreads),
+                       (size_t)q.K * kFcSubs * q.Csp * sizeof(float), stream, W, D, q, codes, part);
+  } else {
+    auto k = pq_assign_kernel<0>;
+    if (q.Csp == 4) k = pq_assign_kernel<4>;
+    else if (q.Csp == 8) k = pq_assign_kernel<8>;
+    else if (q.Csp == 3) k = pq_assign_kernel<3>;
+    hipLaunchKernelGGL(k, dim3((unsigned)nblk, (unsigned)q.M), dim3(kQThreads),
+                       (size_t)q.K * q.Csp * sizeof(float), stream, W, D, q, codes, part);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || (!obj_m && !total)) return e;
   double* om = obj_m ? obj_m : obj_tmp;
@@ -254,12 +384,21 @@ hipError_t assign(const QShape& q, const float* W, const float* D, uint8_t* code
 
 hipError_t update(const QShape& q, const float* W, const uint8_t* codes, float* D, int* counts,
                   hipStream_t stream) {
-  hipLaunchKernelGGL(pq_update_kernel, dim3((unsigned)q.M), dim3(kQThreads), 0, stream, W, codes, q, D, counts);
+  auto k = pq_update_kernel<0>;
+  if (q.Csp == 4) k = pq_update_kernel<4>;
+  else if (q.Csp == 8) k = pq_update_kernel<8>;
+  else if (q.Csp == 3) k = pq_update_kernel<3>;
+  const unsigned blocks = (unsigned)(ceil_div(q.M, 8) * 8);
+  hipLaunchKernelGGL(k, dim3(blocks), dim3(kQThreads), 0, stream, W, codes, q, D, counts);
   return hipGetLastError();
 }
 
 // Workspace: the per-block objective partials, then M doubles.
-size_t part_bytes(const QShape& q) { return ((size_t)q.M * ceil_div(q.n, kQThreads) + q.M) * sizeof(double); }
+// (room for either assignment kernel's partials)
+size_t part_bytes(const QShape& q) {
+  const int nb = std::max(assign_blocks(q, true), assign_blocks(q, false));
+  return ((size_t)q.M * nb + q.M) * sizeof(double);
+}
 
 }  // namespace
 
@@ -290,7 +429,8 @@ hipError_t launch_pq_kmeans(int Ct, int Cs, int dk, const float* W, int M, int K
   double* part = reinterpret_cast<double*>(scratch.get());
   KernelTimer timer(stream);
   for (int it = 0; it <= iters && e == hipSuccess; ++it) {
-    e = assign(q, W, D, codes, part, nullptr, part + (size_t)q.M * ceil_div(q.n, kQThreads),
+    e = assign(q, W, D, codes, part, nullptr,
+               part + (size_t)q.M * std::max(assign_blocks(q, true), assign_blocks(q, false)),
                objective ? objective + it : nullptr, stream);
     if (e == hipSuccess && it < iters) e = update(q, W, codes, D, nullptr, stream);
   }
