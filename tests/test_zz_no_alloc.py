@@ -116,3 +116,37 @@ def test_noalloc_refuses_layers_beyond_its_scratch(dev):
     assert err.value.status == 8
     torch.cuda.synchronize()
     assert bool((y == 7.0).all())
+
+
+def test_noalloc_under_graph_capture(dev):
+    """The allocation-free forward recorded into a HIP graph (the callers it
+    is for): each replay, with eager work and a synchronization between
+    replays and a new input copied into the captured input buffer each time,
+    equals the eager qcnn_conv_forward on that input bit for bit.  The layer
+    is split over workgroups, so the captured work includes the code
+    re-layout, the gather kernel and the split-sum kernel."""
+    rng = np.random.Generator(np.random.PCG64(10))
+    c = layer(rng, dev, (4, 256, 13, 13, 384, 3, 1, 1, 4, 128))
+    y = torch.empty(c["shape"], device=dev)
+    # one eager call first: per-device set-up (the scratch address, kernel
+    # attributes) happens outside the capture
+    assert call("qcnn_conv_forward_noalloc", c["xd"], c["Dd"], c["cd"], 1, 1, c["bd"], True, y) == 0
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream(dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            st = call("qcnn_conv_forward_noalloc", c["xd"], c["Dd"], c["cd"], 1, 1, c["bd"], True, y)
+    assert st == 0, st
+    torch.cuda.synchronize()
+    for rep in range(4):
+        xn = np.abs(rng.standard_normal(c["x"].shape)).astype(np.float32)
+        c["xd"].copy_(T(xn, dev))
+        ref = torch.full(c["shape"], float("nan"), device=dev)
+        assert call("qcnn_conv_forward", c["xd"], c["Dd"], c["cd"], 1, 1, c["bd"], True, ref) == 0
+        torch.cuda.synchronize()
+        y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref), "replay %d differs from the eager forward" % rep
