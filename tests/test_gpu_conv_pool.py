@@ -33,6 +33,8 @@ CASES = [
     (1, 48, 10, 10, 24, 3, 1, 1, 4, 16, 1, 1, False, True),     # 1x1 windows: the conv itself
     (2, 16, 7, 7, 12, 3, 1, 1, 4, 8, 7, 1, True, True),         # one window over the whole map
     (2, 32, 16, 16, 20, 1, 1, 0, 4, 16, 2, 2, False, True),     # 1x1 conv
+    (9, 64, 13, 13, 64, 3, 1, 1, 4, 32, 3, 2, True, True),      # two image groups, the last of one image
+    (1, 16, 100, 100, 16, 3, 1, 1, 4, 16, 2, 2, False, True),   # 10000 outputs per map: pools a full map
 ]
 
 
