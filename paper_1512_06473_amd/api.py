@@ -120,6 +120,85 @@ def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out, pool=No
     return out
 
 
+class ConvPlan:
+    """A PQ conv layer prepared for repeated forwards on inputs of one shape
+    (qcnn_conv_plan_create / qcnn_conv_plan_forward / qcnn_conv_plan_destroy).
+
+    in_shape (N, C_s, H, W); codebooks [M][K][C'_s] fp32; codes uint8
+    [C_t][d_k][d_k][M], or with ``packed=(C_t, d_k)`` their packed stream
+    (pack_codes); bias [C_t] or None; pool None or (pool_k, pool_s).  The
+    plan keeps its own copies: the tensors given may change afterwards.
+    ``plan(x)`` equals conv_forward (or conv_pool_forward) with the same
+    arguments, bit for bit, without re-laying the codes on every call."""
+
+    def __init__(self, in_shape, codebooks: torch.Tensor, codes: torch.Tensor, stride: int = 1, pad: int = 0,
+                 bias: Optional[torch.Tensor] = None, relu: bool = False, pool=None, packed=None):
+        self._ptr = None
+        dev = codebooks.device
+        _need(codebooks, "codebooks", torch.float32, 3, dev)
+        N, Cs, H, W = (int(v) for v in in_shape)
+        M, K, Csp = codebooks.shape
+        keep = codes
+        if packed is None:
+            _need(codes, "codes", torch.uint8, 4, dev)
+            Ct, dk, dk2, M2 = codes.shape
+            if dk != dk2 or M2 != M:
+                raise ValueError("codes shape %s does not match [C_t][d_k][d_k][M=%d]" % (tuple(codes.shape), M))
+            cptr = codes.data_ptr()
+        else:
+            Ct, dk = (int(v) for v in packed)
+            cptr, keep = _packed_codes_arg(codes, Ct * dk * dk * M, K, dev)
+        bp = 0
+        if bias is not None:
+            _need(bias, "bias", torch.float32, 1, dev)
+            if bias.shape[0] != Ct:
+                raise ValueError("bias must have C_t=%d entries" % Ct)
+            bp = bias.data_ptr()
+        pk, ps = (0, 0) if pool is None else (int(pool[0]), int(pool[1]))
+        Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
+        if pool is not None:
+            Ho, Wo = out_size(Ho, pk, ps, 0), out_size(Wo, pk, ps, 0)
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(dev):
+            check(lib().qcnn_conv_plan_create(N, Cs, H, W, codebooks.data_ptr(), M, K, Csp, cptr,
+                                              int(packed is not None), Ct, dk, stride, pad, bp or None,
+                                              int(bool(relu)), pk, ps, ctypes.byref(handle),
+                                              _stream(codebooks)), "qcnn_conv_plan_create")
+        del keep
+        self._ptr = handle
+        self.device = dev
+        self.in_shape = (N, Cs, H, W)
+        self.out_shape = (N, Ct, Ho, Wo)
+
+    def __call__(self, x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if self._ptr is None:
+            raise ValueError("the plan is closed")
+        _need(x, "x", torch.float32, 4, self.device)
+        if tuple(x.shape) != self.in_shape:
+            raise ValueError("x has shape %s, the plan's is %s" % (tuple(x.shape), self.in_shape))
+        if out is None:
+            out = torch.empty(self.out_shape, dtype=torch.float32, device=self.device)
+        _need(out, "out", torch.float32, 4, self.device)
+        if tuple(out.shape) != self.out_shape:
+            raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), self.out_shape))
+        check(lib().qcnn_conv_plan_forward(self._ptr, x.data_ptr(), out.data_ptr(), _stream(x)),
+              "qcnn_conv_plan_forward")
+        return out
+
+    def close(self) -> None:
+        """Frees the plan (after its device has finished its work)."""
+        if self._ptr is not None:
+            ptr, self._ptr = self._ptr, None
+            with torch.cuda.device(self.device):
+                check(lib().qcnn_conv_plan_destroy(ptr), "qcnn_conv_plan_destroy")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def fc_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor,
                bias: Optional[torch.Tensor] = None, relu: bool = False,
                out: Optional[torch.Tensor] = None) -> torch.Tensor:

@@ -919,40 +919,44 @@ bool conv_flat_pools(const ConvShape& s) {
          (long long)s.N * s.Ct <= 0x7ffffff0LL;
 }
 
-hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws,
-                            const PoolSpec* pool) {
-  FlatPlan pl;
-  if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;
-  if (pool && (pl.p.splits < 2 || s.Ho * s.Wo > kPoolMapMax)) return hipErrorInvalidConfiguration;
-  pl.p.relu = relu;
-  pl.prio = pl.lds > kLdsBytes / 2;  // no second workgroup fits beside this one
+namespace {
+
+// The plan of a call: make_plan's choice and the per-call switches.
+bool flat_plan(const ConvShape& s, int relu, FlatPlan* pl) {
+  if (!make_plan(s, pl)) return false;
+  pl->p.relu = relu;
+  pl->prio = pl->lds > kLdsBytes / 2;  // no second workgroup fits beside this one
   // QCNN_TABLE_BUILD=valu: the vector-ALU table build, for comparison with
   // the MFMA build (read per call; the strided layouts keep MFMA).
   const char* tb = getenv("QCNN_TABLE_BUILD");
-  pl.valu = !pl.gen && tb && strcmp(tb, "valu") == 0;
+  pl->valu = !pl->gen && tb && strcmp(tb, "valu") == 0;
   static const bool trace = getenv("QCNN_TRACE_PLAN") && *getenv("QCNN_TRACE_PLAN") == '1';
   if (trace)
     fprintf(stderr, "qcnn conv_flat: taps %dx%d%s G=%d V=%d S=%d sw=%d Wg=%d Hg=%d tiles=%d TW=%d tc=%d tblocks=%d "
-            "splits=%d work=%d PR=%d npb=%d zrow=%d lds=%zu\n", pl.rows, pl.cols, pl.gen ? " gen" : "", pl.p.G,
-            pl.p.V, pl.p.S, pl.p.sw, pl.p.Wg, pl.p.Hg, pl.p.tiles, pl.TW, pl.p.tc, pl.p.tblocks, pl.p.splits,
-            pl.p.work, pl.p.PR, pl.p.npb, pl.p.zrow, pl.lds);
+            "splits=%d work=%d PR=%d npb=%d zrow=%d lds=%zu\n", pl->rows, pl->cols, pl->gen ? " gen" : "", pl->p.G,
+            pl->p.V, pl->p.S, pl->p.sw, pl->p.Wg, pl->p.Hg, pl->p.tiles, pl->TW, pl->p.tc, pl->p.tblocks, pl->p.splits,
+            pl->p.work, pl->p.PR, pl->p.npb, pl->p.zrow, pl->lds);
+  return true;
+}
+
+hipError_t launch_codes(const FlatPlan& pl, CodeStream codes, uint8_t* codes8, hipStream_t stream) {
   const FlatParams& p = pl.p;
-  const FlatWs w = flat_ws(pl);
-  const size_t n_codes = w.n_codes, partial_elems = w.partial_elems;
-  Scratch scratch;
-  hipError_t e = scratch.take(stream, w.total, ws);
-  if (e != hipSuccess) return e;
-  char* base = scratch.get();
-  uint8_t* codes8 = reinterpret_cast<uint8_t*>(base);
-  float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + w.code_bytes) : nullptr;
-  const size_t nwords = (n_codes + 3) / 4;
+  const size_t nwords = (flat_ws(pl).n_codes + 3) / 4;
   const CodeMap cm{p.Ct, p.dk, p.stride, p.M, p.G, pl.rows, pl.cols, p.K, p.ct_pad, p.zrow, p.V};
   hipLaunchKernelGGL(flat_codes_kernel, dim3((unsigned)std::min<size_t>(2048, ceil_div_z(nwords, 256))), dim3(256), 0,
                      stream, codes, cm, reinterpret_cast<uint32_t*>(codes8));
-  e = hipGetLastError();
-  if (e == hipSuccess) {
-    LaunchTimer timer(ws == nullptr || ws->timed);
+  return hipGetLastError();
+}
+
+// The kernels of a call after the code re-layout: the main kernel, then (split
+// plans) the split sum, which with `pool` takes the pooling maxima.
+hipError_t run_flat(const FlatPlan& pl, const ConvShape& s, const float* x, const float* D, const uint8_t* codes8,
+                    const float* bias, float* y, float* partial, hipStream_t stream, bool timed,
+                    const PoolSpec* pool) {
+  const FlatParams& p = pl.p;
+  hipError_t e;
+  {
+    LaunchTimer timer(timed);
     e = launch_plan(pl, LaunchArgs{x, D, codes8, bias, y, partial, stream, &timer});
   }
   if (e == hipSuccess && partial && pool) {
@@ -965,11 +969,62 @@ hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, 
                        y);
     e = hipGetLastError();
   } else if (e == hipSuccess && partial) {
-    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)ceil_div_z(partial_elems / p.splits, 256)), dim3(256), 0,
-                       stream, partial, p, bias, y);
+    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)ceil_div_z(flat_ws(pl).partial_elems / p.splits, 256)),
+                       dim3(256), 0, stream, partial, p, bias, y);
     e = hipGetLastError();
   }
   return e;
+}
+
+}  // namespace
+
+hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
+                            const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws,
+                            const PoolSpec* pool) {
+  FlatPlan pl;
+  if (!flat_plan(s, relu, &pl)) return hipErrorInvalidConfiguration;
+  if (pool && (pl.p.splits < 2 || s.Ho * s.Wo > kPoolMapMax)) return hipErrorInvalidConfiguration;
+  const FlatWs w = flat_ws(pl);
+  Scratch scratch;
+  hipError_t e = scratch.take(stream, w.total, ws);
+  if (e != hipSuccess) return e;
+  char* base = scratch.get();
+  uint8_t* codes8 = reinterpret_cast<uint8_t*>(base);
+  float* partial = pl.p.splits > 1 ? reinterpret_cast<float*>(base + w.code_bytes) : nullptr;
+  e = launch_codes(pl, codes, codes8, stream);
+  if (e != hipSuccess) return e;
+  return run_flat(pl, s, x, D, codes8, bias, y, partial, stream, ws == nullptr || ws->timed, pool);
+}
+
+size_t conv_flat_code_bytes(const ConvShape& s) {
+  FlatPlan pl;
+  return make_plan(s, &pl) ? flat_ws(pl).code_bytes : 0;
+}
+
+hipError_t launch_conv_flat_codes(const ConvShape& s, CodeStream codes, uint8_t* codes8, hipStream_t stream) {
+  FlatPlan pl;
+  if (!make_plan(s, &pl)) return hipErrorInvalidConfiguration;
+  return launch_codes(pl, codes, codes8, stream);
+}
+
+hipError_t launch_conv_flat_relaid(const ConvShape& s, const float* x, const float* D, const uint8_t* codes8,
+                                   const float* bias, int relu, float* y, hipStream_t stream, const PoolSpec* pool) {
+  FlatPlan pl;
+  if (!flat_plan(s, relu, &pl)) return hipErrorInvalidConfiguration;
+  const FlatWs w = flat_ws(pl);
+  // With a pooling that the split sum cannot take, the full map goes to the
+  // workspace after the partial sums and a max-pool kernel reads it.
+  const bool split_pools = pool && conv_flat_pools(s);
+  const size_t part = pl.p.splits > 1 ? (w.partial_elems * sizeof(float) + 255) & ~(size_t)255 : 0;
+  const size_t full = pool && !split_pools ? (size_t)s.N * s.Ct * s.Ho * s.Wo * sizeof(float) : 0;
+  Scratch scratch;
+  hipError_t e = scratch.take(stream, part + full, nullptr);
+  if (e != hipSuccess) return e;
+  float* partial = part ? reinterpret_cast<float*>(scratch.get()) : nullptr;
+  float* ymap = full ? reinterpret_cast<float*>(scratch.get() + part) : y;
+  e = run_flat(pl, s, x, D, codes8, bias, ymap, partial, stream, true, split_pools ? pool : nullptr);
+  if (e != hipSuccess || !full) return e;
+  return launch_maxpool(ymap, s.N, s.Ct, s.Ho, s.Wo, pool->k, pool->s, pool->Hp, pool->Wp, y, stream);
 }
 
 }  // namespace qcnn

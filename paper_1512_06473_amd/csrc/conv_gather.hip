@@ -232,6 +232,8 @@ ConvKernel pick_conv_kernel(const ConvShape& s) {
 
 }  // namespace
 
+bool conv_picks_flat(const ConvShape& s) { return pick_conv_kernel(s) == ConvKernel::kFlat; }
+
 size_t conv_forward_workspace(const ConvShape& s) {
   switch (pick_conv_kernel(s)) {
     case ConvKernel::kFlat: return conv_flat_workspace(s);

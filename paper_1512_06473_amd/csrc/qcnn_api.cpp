@@ -7,6 +7,7 @@
 #include <atomic>
 #include <initializer_list>
 #include <mutex>
+#include <new>
 #include <utility>
 #include <vector>
 
@@ -247,6 +248,40 @@ qcnn_status qcnn_lut_build(const float* x, int N, int C_s, int H, int W, const f
 
 namespace {
 
+// Shape of a conv call (with pool_k or pool_s non-zero, of the conv and the
+// max-pool after it) and the sizes of its arrays.
+struct ConvCall {
+  ConvShape sh;
+  bool pooled;
+  int Hp, Wp;
+  size_t nx, nd, nc, ny, cb;  // elements of x, codebooks, codes, y; bytes of the code stream
+};
+
+// The host-side checks of a conv call that do not involve x and y.
+qcnn_status check_conv(int N, int C_s, int H, int W, int M, int K, int Csp, const uint8_t* codes, int bits, int C_t,
+                       int d_k, int stride, int pad, int pool_k, int pool_s, ConvCall* c) {
+  if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0) return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(N, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  const int Ho = qcnn_out_size(H, d_k, stride, pad), Wo = qcnn_out_size(W, d_k, stride, pad);
+  if (Ho < 1 || Wo < 1) return QCNN_ERR_SHAPE;
+  c->pooled = pool_k != 0 || pool_s != 0;
+  c->Hp = c->pooled ? qcnn_out_size(Ho, pool_k, pool_s, 0) : Ho;
+  c->Wp = c->pooled ? qcnn_out_size(Wo, pool_k, pool_s, 0) : Wo;
+  if (c->pooled && (pool_k < 1 || pool_s < 1 || c->Hp < 1 || c->Wp < 1)) return QCNN_ERR_SHAPE;
+  c->nx = elems({N, C_s, H, W});
+  c->nd = elems({M, K, Csp});
+  c->nc = elems({C_t, d_k, d_k, M});
+  c->ny = elems({N, C_t, c->Hp, c->Wp});
+  if (!c->nx || !c->nd || !c->nc || !c->ny) return QCNN_ERR_SHAPE;
+  c->cb = code_stream_bytes(c->nc, bits);
+  if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
+  c->sh = ConvShape{N, C_s, H, W, M, K, Csp, C_t, d_k, stride, pad, Ho, Wo};
+  if (!qcnn::conv_supported(c->sh)) return QCNN_ERR_UNSUPPORTED;
+  if (qcnn::ceil_div(C_t, 32) > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
+  return QCNN_OK;
+}
+
 // Body of qcnn_conv_forward (bits = 8), qcnn_conv_forward_packed, (with
 // noalloc) qcnn_conv_forward_noalloc and (with pool_k > 0)
 // qcnn_conv_pool_forward.
@@ -255,26 +290,19 @@ qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const flo
                          const float* bias, int relu, float* y, void* stream, bool noalloc = false,
                          int pool_k = 0, int pool_s = 0) {
   if (!x || !codebooks || !codes || !y) return QCNN_ERR_NULL;
-  if (H < 1 || W < 1 || C_t < 1 || d_k < 1 || stride < 1 || pad < 0) return QCNN_ERR_SHAPE;
-  qcnn_status s = check_pq(N, C_s, M, K, Csp);
-  if (s != QCNN_OK) return s;
-  const int Ho = qcnn_out_size(H, d_k, stride, pad), Wo = qcnn_out_size(W, d_k, stride, pad);
-  if (Ho < 1 || Wo < 1) return QCNN_ERR_SHAPE;
-  const bool pooled = pool_k != 0 || pool_s != 0;
-  const int Hp = pooled ? qcnn_out_size(Ho, pool_k, pool_s, 0) : Ho;
-  const int Wp = pooled ? qcnn_out_size(Wo, pool_k, pool_s, 0) : Wo;
-  if (pooled && (pool_k < 1 || pool_s < 1 || Hp < 1 || Wp < 1)) return QCNN_ERR_SHAPE;
-  const size_t nx = elems({N, C_s, H, W}), nd = elems({M, K, Csp}), nc = elems({C_t, d_k, d_k, M});
-  const size_t ny = elems({N, C_t, Hp, Wp});
-  if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
-  const size_t cb = code_stream_bytes(nc, bits);
-  if (overlap(y, ny * 4, x, nx * 4) || overlap(y, ny * 4, codebooks, nd * 4) || overlap(y, ny * 4, codes, cb) ||
-      overlap(y, ny * 4, bias, (size_t)C_t * 4))
+  ConvCall c{};  // sizes 0 until check_conv has computed them
+  qcnn_status s = check_conv(N, C_s, H, W, M, K, Csp, codes, bits, C_t, d_k, stride, pad, pool_k, pool_s, &c);
+  // An overlap of y with an input is reported before the codes' alignment
+  // and the kernels' limits, as far as the sizes are known.
+  if (s != QCNN_OK && s != QCNN_ERR_UNSUPPORTED) return s;
+  if (c.ny && (overlap(y, c.ny * 4, x, c.nx * 4) || overlap(y, c.ny * 4, codebooks, c.nd * 4) ||
+               overlap(y, c.ny * 4, codes, c.cb) || overlap(y, c.ny * 4, bias, (size_t)C_t * 4)))
     return QCNN_ERR_ALIAS;
-  if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
-  ConvShape sh{N, C_s, H, W, M, K, Csp, C_t, d_k, stride, pad, Ho, Wo};
-  if (!qcnn::conv_supported(sh)) return QCNN_ERR_UNSUPPORTED;
-  if (qcnn::ceil_div(C_t, 32) > kMaxGridYZ) return QCNN_ERR_UNSUPPORTED;
+  if (s != QCNN_OK) return s;
+  const ConvShape& sh = c.sh;
+  const int Hp = c.Hp, Wp = c.Wp;
+  const bool pooled = c.pooled;
+  const size_t nc = c.nc;
   hipStream_t st = (hipStream_t)stream;
   const qcnn::CodeStream cs{codes, bits};
   if (noalloc) {
@@ -352,6 +380,115 @@ qcnn_status qcnn_conv_forward_packed(const float* x, int N, int C_s, int H, int 
   if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
   return conv_forward(x, N, C_s, H, W, codebooks, M, K, Csp, packed_codes, qcnn::code_bits(K), C_t, d_k, stride,
                       pad, bias, relu, y, stream);
+}
+
+}  // extern "C"
+
+// A conv layer prepared for repeated forwards on inputs of one shape: its own
+// copies of the codebooks and the bias, and the codes re-laid for the flat
+// kernel (or, for a layer another kernel runs, a copy of the caller's code
+// stream), in one device allocation.
+struct qcnn_conv_plan {
+  ConvShape sh;
+  int relu;
+  bool pooled;
+  qcnn::PoolSpec pool;
+  int device;
+  bool relaid;
+  int bits;  // of the code copy when !relaid
+  size_t nx, ny;
+  void* mem;
+  const float* D;
+  const float* bias;
+  const uint8_t* codes;
+};
+
+extern "C" {
+
+qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W, const float* codebooks, int M, int K, int Csp,
+                                  const uint8_t* codes, int packed, int C_t, int d_k, int stride, int pad,
+                                  const float* bias, int relu, int pool_k, int pool_s, qcnn_conv_plan** plan,
+                                  void* stream) {
+  if (!codebooks || !codes || !plan) return QCNN_ERR_NULL;
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  if (pool_k < 0 || pool_s < 0 || (pool_k == 0) != (pool_s == 0)) return QCNN_ERR_SHAPE;
+  const int bits = packed ? qcnn::code_bits(K) : 8;
+  ConvCall c{};
+  qcnn_status s = check_conv(N, C_s, H, W, M, K, Csp, codes, bits, C_t, d_k, stride, pad, pool_k, pool_s, &c);
+  if (s != QCNN_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return QCNN_ERR_HIP;
+  const bool relaid = qcnn::conv_picks_flat(c.sh);
+  const qcnn::CodeStream cs{codes, bits};
+  // [codebooks | bias | codes | code-check counter], 256-byte aligned parts.
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t d_bytes = up(c.nd * 4), b_bytes = bias ? up((size_t)C_t * 4) : 0;
+  const size_t c_bytes = up(relaid ? qcnn::conv_flat_code_bytes(c.sh) : (c.cb + 3) / 4 * 4);
+  char* mem = nullptr;
+  if (hipMalloc((void**)&mem, d_bytes + b_bytes + c_bytes + 256) != hipSuccess) return QCNN_ERR_HIP;
+  float* D = reinterpret_cast<float*>(mem);
+  float* bcopy = bias ? reinterpret_cast<float*>(mem + d_bytes) : nullptr;
+  uint8_t* ccopy = reinterpret_cast<uint8_t*>(mem + d_bytes + b_bytes);
+  int* bad = reinterpret_cast<int*>(mem + d_bytes + b_bytes + c_bytes);
+  int host_bad = 0;
+  hipError_t e = hipSuccess;
+  if ((1 << bits) > K) {  // the codes are verified once, here
+    e = qcnn::launch_code_check(cs, c.nc, K, bad, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(&host_bad, bad, sizeof(int), hipMemcpyDeviceToHost, st);
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(D, codebooks, c.nd * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && bias) e = hipMemcpyAsync(bcopy, bias, (size_t)C_t * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess)
+    e = relaid ? qcnn::launch_conv_flat_codes(c.sh, cs, ccopy, st)
+               : hipMemcpyAsync(ccopy, codes, c.cb, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess && host_bad) s = QCNN_ERR_CODE_RANGE;
+  qcnn_conv_plan* p = nullptr;
+  if (e == hipSuccess && s == QCNN_OK) {
+    p = new (std::nothrow) qcnn_conv_plan{c.sh, relu ? 1 : 0, c.pooled, qcnn::PoolSpec{pool_k, pool_s, c.Hp, c.Wp},
+                                          dev, relaid, bits, c.nx, c.ny, mem, D, bcopy, ccopy};
+    if (!p) s = QCNN_ERR_HIP;
+  }
+  if (e != hipSuccess || s != QCNN_OK) {
+    (void)hipStreamSynchronize(st);
+    (void)hipFree(mem);
+    return e != hipSuccess ? QCNN_ERR_HIP : s;
+  }
+  *plan = p;
+  return QCNN_OK;
+}
+
+qcnn_status qcnn_conv_plan_forward(const qcnn_conv_plan* plan, const float* x, float* y, void* stream) {
+  if (!plan || !x || !y) return QCNN_ERR_NULL;
+  if (overlap(y, plan->ny * 4, x, plan->nx * 4)) return QCNN_ERR_ALIAS;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return QCNN_ERR_HIP;
+  if (dev != plan->device) return QCNN_ERR_UNSUPPORTED;
+  if (!prepare_device()) return QCNN_ERR_HIP;
+  hipStream_t st = (hipStream_t)stream;
+  const qcnn::PoolSpec* pool = plan->pooled ? &plan->pool : nullptr;
+  if (plan->relaid)
+    return hip_status(
+        qcnn::launch_conv_flat_relaid(plan->sh, x, plan->D, plan->codes, plan->bias, plan->relu, y, st, pool));
+  const qcnn::CodeStream cs{plan->codes, plan->bits};
+  if (pool)
+    return hip_status(qcnn::launch_conv_pool_forward(plan->sh, x, plan->D, cs, plan->bias, plan->relu, *pool, y, st));
+  return hip_status(qcnn::launch_conv_forward(plan->sh, x, plan->D, cs, plan->bias, plan->relu, y, st));
+}
+
+qcnn_status qcnn_conv_plan_destroy(qcnn_conv_plan* plan) {
+  if (!plan) return QCNN_OK;
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipFree(plan->mem);
+  if (cur != plan->device) (void)hipSetDevice(cur);
+  if (e != hipSuccess) return QCNN_ERR_HIP;
+  delete plan;
+  return QCNN_OK;
 }
 
 qcnn_status qcnn_fc_forward(const float* x, int N, int C_s, const float* codebooks, int M, int K, int Csp,

@@ -89,6 +89,10 @@ hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* 
 // kernel it would pick now (host-side, no HIP call).
 size_t conv_forward_workspace(const ConvShape& s);
 
+// True when launch_conv_forward would run this layer on the flat kernel now
+// (QCNN_CONV_KERNEL is read per call; host-side, no HIP call).
+bool conv_picks_flat(const ConvShape& s);
+
 // The conv layer followed by max pooling, y: [N][C_t][H_p][W_p].  A layer
 // whose subspaces the stride-1/strided flat kernel splits over workgroups
 // takes the window maxima in its split-sum kernel; any other layer writes
@@ -126,6 +130,17 @@ bool conv_flat_pools(const ConvShape& s);
 hipError_t launch_conv_flat(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                             const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws,
                             const PoolSpec* pool = nullptr);
+// The same call in two parts, for a layer whose codes are re-laid once and
+// then serve many calls: the re-laid codes' size (0 when the flat kernel
+// cannot tile the layer), the re-layout into codes8, and the call on codes8
+// (which must come from launch_conv_flat_codes for the same shape).  With
+// `pool`, a plan the split sum cannot pool writes its full map to the
+// library's workspace and a max-pool kernel reads it.
+size_t conv_flat_code_bytes(const ConvShape& s);
+hipError_t launch_conv_flat_codes(const ConvShape& s, CodeStream codes, uint8_t* codes8, hipStream_t stream);
+hipError_t launch_conv_flat_relaid(const ConvShape& s, const float* x, const float* D, const uint8_t* codes8,
+                                   const float* bias, int relu, float* y, hipStream_t stream,
+                                   const PoolSpec* pool = nullptr);
 
 // Stride-1 3x3 / 1x1 kernel with two tables in LDS and half-wave table rows
 // (conv_half.hip): C'_s <= 8, K <= 128.

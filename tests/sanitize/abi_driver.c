@@ -83,6 +83,27 @@ int main(void) {
                                    NULL) == QCNN_ERR_WORKSPACE);
   EXPECT(qcnn_conv_forward_noalloc(FP(X), 2, 4096, 13, 13, FP(Dp), 1024, 128, 4, CP(C), 4096, 3, 1, 1, NULL, 0,
                                    FW(Y), NULL) == QCNN_ERR_WORKSPACE);
+  /* prepared conv layers: validation before any HIP call; *plan untouched on error */
+  {
+    qcnn_conv_plan* plan = (qcnn_conv_plan*)(uintptr_t)0xdead0;
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, NULL, 2, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 0, 0, &plan, NULL) ==
+           QCNN_ERR_NULL);
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 0, 0, NULL, NULL) ==
+           QCNN_ERR_NULL);
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 3, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 0, 0, &plan, NULL) ==
+           QCNN_ERR_SHAPE);
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 300, 4, CP(C), 1, 4, 3, 1, 1, NULL, 0, 0, 0, &plan, NULL) ==
+           QCNN_ERR_K_RANGE);
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 3, 0, &plan, NULL) ==
+           QCNN_ERR_SHAPE);
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 6, 1, &plan, NULL) ==
+           QCNN_ERR_SHAPE);
+    EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C + 1), 0, 4, 3, 1, 1, NULL, 0, 0, 0, &plan,
+                                 NULL) == QCNN_ERR_UNSUPPORTED);
+    EXPECT(plan == (qcnn_conv_plan*)(uintptr_t)0xdead0);
+    EXPECT(qcnn_conv_plan_forward(NULL, FP(X), FW(Y), NULL) == QCNN_ERR_NULL);
+    EXPECT(qcnn_conv_plan_destroy(NULL) == QCNN_OK);
+  }
   /* helpers */
   for (int s = 0; s <= 9; ++s) EXPECT(qcnn_status_string((qcnn_status)s) != NULL);
   EXPECT(qcnn_out_size(227, 11, 4, 0) == 55 && qcnn_out_size(2, 3, 1, 0) == 0);

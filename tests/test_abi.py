@@ -121,6 +121,39 @@ def test_conv_pool_rejects(L, kw, want):
     assert conv_pool(L, pk, ps, **kw) == want
 
 
+def plan_create(L, plan_out=True, **kw):
+    a = dict(N=2, Cs=8, H=5, W=5, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, packed=0, Ct=4, dk=3, s=1, p=1,
+             bias=None, relu=0, pk=0, ps=0, stream=None)
+    a.update(kw)
+    handle = ctypes.c_void_p(0xdead0)
+    st = L.qcnn_conv_plan_create(a["N"], a["Cs"], a["H"], a["W"], a["D"], a["M"], a["K"], a["Csp"], a["codes"],
+                                 a["packed"], a["Ct"], a["dk"], a["s"], a["p"], a["bias"], a["relu"], a["pk"],
+                                 a["ps"], ctypes.byref(handle) if plan_out else None, a["stream"])
+    return st, handle.value
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(D=None), NULL), (dict(codes=None), NULL), (dict(plan_out=False), NULL),
+    (dict(N=0), SHAPE), (dict(H=0), SHAPE), (dict(Ct=0), SHAPE), (dict(M=3), SHAPE), (dict(p=-1), SHAPE),
+    (dict(K=0), KR), (dict(K=257), KR), (dict(K=0, packed=1), KR),
+    (dict(H=1, W=1, p=0), SHAPE),                 # empty conv output
+    (dict(pk=3), SHAPE), (dict(ps=2), SHAPE),     # one of the pooling sizes 0
+    (dict(pk=-1, ps=-1), SHAPE), (dict(pk=6, ps=1), SHAPE),  # negative; window past the 5x5 map
+    (dict(Cs=34, M=2, Csp=17), UNSUP),           # C's > 16
+    (dict(codes=FAKE + 1), UNSUP), (dict(codes=FAKE + 2, packed=1), UNSUP),  # codes not 4-byte aligned
+    (dict(N=70000), UNSUP),                       # grid limit
+])
+def test_conv_plan_create_rejects(L, kw, want):
+    st, handle = plan_create(L, **kw)
+    assert st == want
+    assert handle == 0xdead0  # *plan is not written on an error
+
+
+def test_conv_plan_forward_and_destroy_without_gpu(L):
+    assert L.qcnn_conv_plan_forward(None, FAKE, FAKE2, None) == NULL
+    assert L.qcnn_conv_plan_destroy(None) == 0  # NULL is accepted, like free(NULL)
+
+
 def test_noalloc_rejects_layers_beyond_its_scratch(L):
     # AlexNet conv3 at N = 64 (256 -> 384, 13x13, 3x3 pad 1, C's = 4, K = 128)
     # needs more temporaries than the static scratch holds: refused on the
