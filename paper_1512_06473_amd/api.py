@@ -120,11 +120,61 @@ def _conv_call(entry, x, codebooks, codes, stride, pad, bias, relu, out, pool=No
     return out
 
 
-class ConvPlan:
-    """A PQ conv layer prepared for repeated forwards on inputs of one shape
-    (qcnn_conv_plan_create / qcnn_conv_plan_forward / qcnn_conv_plan_destroy).
+class _Plan:
+    """A layer prepared for repeated forwards on inputs of one shape
+    (qcnn_plan_forward / qcnn_plan_destroy); made by ConvPlan or FcPlan."""
 
-    in_shape (N, C_s, H, W); codebooks [M][K][C'_s] fp32; codes uint8
+    def _create(self, entry, dev, in_shape, out_shape, *args):
+        self._ptr = None
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(dev):
+            check(getattr(lib(), entry)(*args, ctypes.byref(handle), torch.cuda.current_stream(dev).cuda_stream),
+                  entry)
+        self._ptr = handle
+        self.device = dev
+        self.in_shape = tuple(in_shape)
+        self.out_shape = tuple(out_shape)
+
+    def __call__(self, x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if self._ptr is None:
+            raise ValueError("the plan is closed")
+        _need(x, "x", torch.float32, len(self.in_shape), self.device)
+        if tuple(x.shape) != self.in_shape:
+            raise ValueError("x has shape %s, the plan's is %s" % (tuple(x.shape), self.in_shape))
+        if out is None:
+            out = torch.empty(self.out_shape, dtype=torch.float32, device=self.device)
+        _need(out, "out", torch.float32, len(self.out_shape), self.device)
+        if tuple(out.shape) != self.out_shape:
+            raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), self.out_shape))
+        check(lib().qcnn_plan_forward(self._ptr, x.data_ptr(), out.data_ptr(), _stream(x)), "qcnn_plan_forward")
+        return out
+
+    def close(self) -> None:
+        """Frees the plan (after its device has finished its work)."""
+        if getattr(self, "_ptr", None) is not None:
+            ptr, self._ptr = self._ptr, None
+            with torch.cuda.device(self.device):
+                check(lib().qcnn_plan_destroy(ptr), "qcnn_plan_destroy")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _bias_arg(bias, Ct, dev) -> int:
+    if bias is None:
+        return 0
+    _need(bias, "bias", torch.float32, 1, dev)
+    if bias.shape[0] != Ct:
+        raise ValueError("bias must have C_t=%d entries" % Ct)
+    return bias.data_ptr()
+
+
+class ConvPlan(_Plan):
+    """A PQ conv layer prepared for inputs of shape in_shape (N, C_s, H, W)
+    (qcnn_conv_plan_create).  codebooks [M][K][C'_s] fp32; codes uint8
     [C_t][d_k][d_k][M], or with ``packed=(C_t, d_k)`` their packed stream
     (pack_codes); bias [C_t] or None; pool None or (pool_k, pool_s).  The
     plan keeps its own copies: the tensors given may change afterwards.
@@ -148,55 +198,44 @@ class ConvPlan:
         else:
             Ct, dk = (int(v) for v in packed)
             cptr, keep = _packed_codes_arg(codes, Ct * dk * dk * M, K, dev)
-        bp = 0
-        if bias is not None:
-            _need(bias, "bias", torch.float32, 1, dev)
-            if bias.shape[0] != Ct:
-                raise ValueError("bias must have C_t=%d entries" % Ct)
-            bp = bias.data_ptr()
+        bp = _bias_arg(bias, Ct, dev)
         pk, ps = (0, 0) if pool is None else (int(pool[0]), int(pool[1]))
         Ho, Wo = out_size(H, dk, stride, pad), out_size(W, dk, stride, pad)
         if pool is not None:
             Ho, Wo = out_size(Ho, pk, ps, 0), out_size(Wo, pk, ps, 0)
-        handle = ctypes.c_void_p()
-        with torch.cuda.device(dev):
-            check(lib().qcnn_conv_plan_create(N, Cs, H, W, codebooks.data_ptr(), M, K, Csp, cptr,
-                                              int(packed is not None), Ct, dk, stride, pad, bp or None,
-                                              int(bool(relu)), pk, ps, ctypes.byref(handle),
-                                              _stream(codebooks)), "qcnn_conv_plan_create")
+        self._create("qcnn_conv_plan_create", dev, (N, Cs, H, W), (N, Ct, Ho, Wo), N, Cs, H, W,
+                     codebooks.data_ptr(), M, K, Csp, cptr, int(packed is not None), Ct, dk, stride, pad,
+                     bp or None, int(bool(relu)), pk, ps)
         del keep
-        self._ptr = handle
-        self.device = dev
-        self.in_shape = (N, Cs, H, W)
-        self.out_shape = (N, Ct, Ho, Wo)
 
-    def __call__(self, x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-        if self._ptr is None:
-            raise ValueError("the plan is closed")
-        _need(x, "x", torch.float32, 4, self.device)
-        if tuple(x.shape) != self.in_shape:
-            raise ValueError("x has shape %s, the plan's is %s" % (tuple(x.shape), self.in_shape))
-        if out is None:
-            out = torch.empty(self.out_shape, dtype=torch.float32, device=self.device)
-        _need(out, "out", torch.float32, 4, self.device)
-        if tuple(out.shape) != self.out_shape:
-            raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), self.out_shape))
-        check(lib().qcnn_conv_plan_forward(self._ptr, x.data_ptr(), out.data_ptr(), _stream(x)),
-              "qcnn_conv_plan_forward")
-        return out
 
-    def close(self) -> None:
-        """Frees the plan (after its device has finished its work)."""
-        if self._ptr is not None:
-            ptr, self._ptr = self._ptr, None
-            with torch.cuda.device(self.device):
-                check(lib().qcnn_conv_plan_destroy(ptr), "qcnn_conv_plan_destroy")
+class FcPlan(_Plan):
+    """A PQ fully-connected layer prepared for inputs [N][C_s]
+    (qcnn_fc_plan_create).  codebooks [M][K][C'_s] fp32; codes uint8
+    [C_t][M], or with ``packed=C_t`` their packed stream; bias [C_t] or None.
+    ``plan(x)`` equals fc_forward with the same arguments, bit for bit."""
 
-    def __del__(self):
-        try:
-            self.close()
-        except Exception:
-            pass
+    def __init__(self, N: int, codebooks: torch.Tensor, codes: torch.Tensor,
+                 bias: Optional[torch.Tensor] = None, relu: bool = False, packed=None):
+        self._ptr = None
+        dev = codebooks.device
+        _need(codebooks, "codebooks", torch.float32, 3, dev)
+        M, K, Csp = codebooks.shape
+        keep = codes
+        if packed is None:
+            _need(codes, "codes", torch.uint8, 2, dev)
+            Ct, M2 = codes.shape
+            if M2 != M:
+                raise ValueError("codes shape %s does not match [C_t][M=%d]" % (tuple(codes.shape), M))
+            cptr = codes.data_ptr()
+        else:
+            Ct = int(packed)
+            cptr, keep = _packed_codes_arg(codes, Ct * M, K, dev)
+        bp = _bias_arg(bias, Ct, dev)
+        N, Cs = int(N), M * Csp
+        self._create("qcnn_fc_plan_create", dev, (N, Cs), (N, Ct), N, Cs, codebooks.data_ptr(), M, K, Csp, cptr,
+                     int(packed is not None), Ct, bp or None, int(bool(relu)))
+        del keep
 
 
 def fc_forward(x: torch.Tensor, codebooks: torch.Tensor, codes: torch.Tensor,

@@ -482,30 +482,35 @@ bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct) {
   return make_fc_plan(N, Cs, M, K, Csp, Ct, &pl);
 }
 
-hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
-                           CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream) {
-  FcPlan pl;
-  if (!make_fc_plan(N, Cs, M, K, Csp, Ct, &pl)) return hipErrorInvalidConfiguration;
-  pl.p.relu = relu;
+namespace {
+
+bool fc_plan(int N, int Cs, int M, int K, int Csp, int Ct, int relu, FcPlan* pl) {
+  if (!make_fc_plan(N, Cs, M, K, Csp, Ct, pl)) return false;
+  pl->p.relu = relu;
   static const bool trace = getenv("QCNN_TRACE_PLAN") && *getenv("QCNN_TRACE_PLAN") == '1';
   if (trace)
     fprintf(stderr, "qcnn fc_tiled: LPC=%d NC=%d KB=%d MC=%d NS=%d tc=%d tblocks=%d nblocks=%d splits=%d "
-            "phases/split=%d work=%d lds=%zu\n", pl.LPC, pl.NC, pl.KB, pl.p.MC, pl.p.NS, pl.p.tc, pl.p.tblocks,
-            pl.p.nblocks, pl.p.splits, pl.p.ph_per_split, pl.p.work, pl.lds);
-  const FcTParams& p = pl.p;
-  const size_t code_bytes = ((size_t)p.mgroups * p.ct_pad * 4 + 255) & ~(size_t)255;
-  const size_t partial_elems = (size_t)p.splits * p.ct_pad * p.nblocks * p.NS;
-  const size_t ws = code_bytes + (p.splits > 1 ? partial_elems * sizeof(float) : 0);
-  Scratch scratch;
-  hipError_t e = scratch.acquire(stream, ws);
-  if (e != hipSuccess) return e;
-  char* base = scratch.get();
-  uint32_t* codes4 = reinterpret_cast<uint32_t*>(base);
-  float* partial = p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
+            "phases/split=%d work=%d lds=%zu\n", pl->LPC, pl->NC, pl->KB, pl->p.MC, pl->p.NS, pl->p.tc,
+            pl->p.tblocks, pl->p.nblocks, pl->p.splits, pl->p.ph_per_split, pl->p.work, pl->lds);
+  return true;
+}
+
+size_t code_bytes_of(const FcTParams& p) { return ((size_t)p.mgroups * p.ct_pad * 4 + 255) & ~(size_t)255; }
+
+hipError_t launch_codes(const FcTParams& p, CodeStream codes, int Ct, int M, int K, uint32_t* codes4,
+                        hipStream_t stream) {
   hipLaunchKernelGGL(fc_codes_kernel, dim3((unsigned)ceil_div(p.mgroups, 64), (unsigned)ceil_div(p.ct_pad, 64)),
                      dim3(256), 0, stream, codes, Ct, M, K, p.mgroups, p.ct_pad, codes4);
-  e = hipGetLastError();
-  if (e == hipSuccess) {
+  return hipGetLastError();
+}
+
+// The kernels of a call after the code re-layout: the main kernel, then (split
+// plans) the split sum.
+hipError_t run_fc(const FcPlan& pl, const float* x, const float* D, const uint32_t* codes4, const float* bias,
+                  float* y, float* partial, hipStream_t stream) {
+  const FcTParams& p = pl.p;
+  hipError_t e;
+  {
     LaunchTimer timer;
     if (pl.LPC == 16)
       e = pl.NC == 1 ? launch_kb<16, 1>(pl, x, D, codes4, bias, y, partial, stream, &timer)
@@ -521,6 +526,52 @@ hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const f
     e = hipGetLastError();
   }
   return e;
+}
+
+size_t partial_bytes_of(const FcTParams& p) {
+  return p.splits > 1 ? (size_t)p.splits * p.ct_pad * p.nblocks * p.NS * sizeof(float) : 0;
+}
+
+}  // namespace
+
+hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
+                           CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream) {
+  FcPlan pl;
+  if (!fc_plan(N, Cs, M, K, Csp, Ct, relu, &pl)) return hipErrorInvalidConfiguration;
+  const size_t code_bytes = code_bytes_of(pl.p);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, code_bytes + partial_bytes_of(pl.p));
+  if (e != hipSuccess) return e;
+  char* base = scratch.get();
+  uint32_t* codes4 = reinterpret_cast<uint32_t*>(base);
+  float* partial = pl.p.splits > 1 ? reinterpret_cast<float*>(base + code_bytes) : nullptr;
+  e = launch_codes(pl.p, codes, Ct, M, K, codes4, stream);
+  if (e != hipSuccess) return e;
+  return run_fc(pl, x, D, codes4, bias, y, partial, stream);
+}
+
+size_t fc_tiled_code_bytes(int N, int Cs, int M, int K, int Csp, int Ct) {
+  FcPlan pl;
+  return make_fc_plan(N, Cs, M, K, Csp, Ct, &pl) ? code_bytes_of(pl.p) : 0;
+}
+
+hipError_t launch_fc_tiled_codes(int N, int Cs, int M, int K, int Csp, int Ct, CodeStream codes, uint32_t* codes4,
+                                 hipStream_t stream) {
+  FcPlan pl;
+  if (!make_fc_plan(N, Cs, M, K, Csp, Ct, &pl)) return hipErrorInvalidConfiguration;
+  return launch_codes(pl.p, codes, Ct, M, K, codes4, stream);
+}
+
+hipError_t launch_fc_tiled_relaid(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
+                                  const uint32_t* codes4, const float* bias, int relu, float* y,
+                                  hipStream_t stream) {
+  FcPlan pl;
+  if (!fc_plan(N, Cs, M, K, Csp, Ct, relu, &pl)) return hipErrorInvalidConfiguration;
+  const size_t part = partial_bytes_of(pl.p);
+  Scratch scratch;
+  hipError_t e = scratch.acquire(stream, part);
+  if (e != hipSuccess) return e;
+  return run_fc(pl, x, D, codes4, bias, y, part ? reinterpret_cast<float*>(scratch.get()) : nullptr, stream);
 }
 
 }  // namespace qcnn

@@ -384,12 +384,13 @@ qcnn_status qcnn_conv_forward_packed(const float* x, int N, int C_s, int H, int 
 
 }  // extern "C"
 
-// A conv layer prepared for repeated forwards on inputs of one shape: its own
-// copies of the codebooks and the bias, and the codes re-laid for the flat
-// kernel (or, for a layer another kernel runs, a copy of the caller's code
-// stream), in one device allocation.
-struct qcnn_conv_plan {
-  ConvShape sh;
+// A conv or FC layer prepared for repeated forwards on inputs of one shape:
+// its own copies of the codebooks and the bias, and the codes re-laid for the
+// kernel that runs the layer (or, for a layer whose kernel reads the caller's
+// layout, a copy of the code stream), in one device allocation.
+struct qcnn_plan {
+  bool fc;
+  ConvShape sh;  // FC: N, Cs, M, K, Csp, Ct
   int relu;
   bool pooled;
   qcnn::PoolSpec pool;
@@ -403,29 +404,23 @@ struct qcnn_conv_plan {
   const uint8_t* codes;
 };
 
-extern "C" {
+namespace {
 
-qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W, const float* codebooks, int M, int K, int Csp,
-                                  const uint8_t* codes, int packed, int C_t, int d_k, int stride, int pad,
-                                  const float* bias, int relu, int pool_k, int pool_s, qcnn_conv_plan** plan,
-                                  void* stream) {
-  if (!codebooks || !codes || !plan) return QCNN_ERR_NULL;
-  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
-  if (pool_k < 0 || pool_s < 0 || (pool_k == 0) != (pool_s == 0)) return QCNN_ERR_SHAPE;
-  const int bits = packed ? qcnn::code_bits(K) : 8;
-  ConvCall c{};
-  qcnn_status s = check_conv(N, C_s, H, W, M, K, Csp, codes, bits, C_t, d_k, stride, pad, pool_k, pool_s, &c);
-  if (s != QCNN_OK) return s;
-  hipStream_t st = (hipStream_t)stream;
+// Second half of a plan's creation, after validation: the allocation, the
+// copies, the code check and the re-layout (by `relayout`, or a copy of the
+// code stream when it is null), then a synchronisation of the stream.
+template <typename Relayout>
+qcnn_status make_plan(qcnn_plan proto, const float* codebooks, size_t nd, const uint8_t* codes, size_t nc,
+                      size_t code_stream, size_t relaid_bytes, const Relayout& relayout, const float* bias,
+                      qcnn_plan** plan, hipStream_t st) {
   if (!prepare_device()) return QCNN_ERR_HIP;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return QCNN_ERR_HIP;
-  const bool relaid = qcnn::conv_picks_flat(c.sh);
-  const qcnn::CodeStream cs{codes, bits};
+  if (hipGetDevice(&proto.device) != hipSuccess) return QCNN_ERR_HIP;
+  const int Ct = proto.sh.Ct, K = proto.sh.K;
+  const qcnn::CodeStream cs{codes, proto.bits};
   // [codebooks | bias | codes | code-check counter], 256-byte aligned parts.
   auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
-  const size_t d_bytes = up(c.nd * 4), b_bytes = bias ? up((size_t)C_t * 4) : 0;
-  const size_t c_bytes = up(relaid ? qcnn::conv_flat_code_bytes(c.sh) : (c.cb + 3) / 4 * 4);
+  const size_t d_bytes = up(nd * 4), b_bytes = bias ? up((size_t)Ct * 4) : 0;
+  const size_t c_bytes = up(proto.relaid ? relaid_bytes : (code_stream + 3) / 4 * 4);
   char* mem = nullptr;
   if (hipMalloc((void**)&mem, d_bytes + b_bytes + c_bytes + 256) != hipSuccess) return QCNN_ERR_HIP;
   float* D = reinterpret_cast<float*>(mem);
@@ -434,21 +429,24 @@ qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W, const float* cod
   int* bad = reinterpret_cast<int*>(mem + d_bytes + b_bytes + c_bytes);
   int host_bad = 0;
   hipError_t e = hipSuccess;
-  if ((1 << bits) > K) {  // the codes are verified once, here
-    e = qcnn::launch_code_check(cs, c.nc, K, bad, st);
+  if ((1 << proto.bits) > K) {  // the codes are verified once, here
+    e = qcnn::launch_code_check(cs, nc, K, bad, st);
     if (e == hipSuccess) e = hipMemcpyAsync(&host_bad, bad, sizeof(int), hipMemcpyDeviceToHost, st);
   }
-  if (e == hipSuccess) e = hipMemcpyAsync(D, codebooks, c.nd * 4, hipMemcpyDeviceToDevice, st);
-  if (e == hipSuccess && bias) e = hipMemcpyAsync(bcopy, bias, (size_t)C_t * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(D, codebooks, nd * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && bias) e = hipMemcpyAsync(bcopy, bias, (size_t)Ct * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess)
-    e = relaid ? qcnn::launch_conv_flat_codes(c.sh, cs, ccopy, st)
-               : hipMemcpyAsync(ccopy, codes, c.cb, hipMemcpyDeviceToDevice, st);
+    e = proto.relaid ? relayout(cs, ccopy) : hipMemcpyAsync(ccopy, codes, code_stream, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
+  qcnn_status s = QCNN_OK;
   if (e == hipSuccess && host_bad) s = QCNN_ERR_CODE_RANGE;
-  qcnn_conv_plan* p = nullptr;
+  qcnn_plan* p = nullptr;
   if (e == hipSuccess && s == QCNN_OK) {
-    p = new (std::nothrow) qcnn_conv_plan{c.sh, relu ? 1 : 0, c.pooled, qcnn::PoolSpec{pool_k, pool_s, c.Hp, c.Wp},
-                                          dev, relaid, bits, c.nx, c.ny, mem, D, bcopy, ccopy};
+    proto.mem = mem;
+    proto.D = D;
+    proto.bias = bcopy;
+    proto.codes = ccopy;
+    p = new (std::nothrow) qcnn_plan(proto);
     if (!p) s = QCNN_ERR_HIP;
   }
   if (e != hipSuccess || s != QCNN_OK) {
@@ -460,7 +458,68 @@ qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W, const float* cod
   return QCNN_OK;
 }
 
-qcnn_status qcnn_conv_plan_forward(const qcnn_conv_plan* plan, const float* x, float* y, void* stream) {
+}  // namespace
+
+extern "C" {
+
+qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W, const float* codebooks, int M, int K, int Csp,
+                                  const uint8_t* codes, int packed, int C_t, int d_k, int stride, int pad,
+                                  const float* bias, int relu, int pool_k, int pool_s, qcnn_plan** plan,
+                                  void* stream) {
+  if (!codebooks || !codes || !plan) return QCNN_ERR_NULL;
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  if (pool_k < 0 || pool_s < 0 || (pool_k == 0) != (pool_s == 0)) return QCNN_ERR_SHAPE;
+  const int bits = packed ? qcnn::code_bits(K) : 8;
+  ConvCall c{};
+  qcnn_status s = check_conv(N, C_s, H, W, M, K, Csp, codes, bits, C_t, d_k, stride, pad, pool_k, pool_s, &c);
+  if (s != QCNN_OK) return s;
+  hipStream_t st = (hipStream_t)stream;
+  qcnn_plan proto{};
+  proto.sh = c.sh;
+  proto.relu = relu ? 1 : 0;
+  proto.pooled = c.pooled;
+  proto.pool = qcnn::PoolSpec{pool_k, pool_s, c.Hp, c.Wp};
+  proto.relaid = qcnn::conv_picks_flat(c.sh);
+  proto.bits = bits;
+  proto.nx = c.nx;
+  proto.ny = c.ny;
+  const ConvShape sh = c.sh;
+  return make_plan(
+      proto, codebooks, c.nd, codes, c.nc, c.cb, proto.relaid ? qcnn::conv_flat_code_bytes(sh) : 0,
+      [&](const qcnn::CodeStream& cs, uint8_t* out) { return qcnn::launch_conv_flat_codes(sh, cs, out, st); }, bias,
+      plan, st);
+}
+
+qcnn_status qcnn_fc_plan_create(int N, int C_s, const float* codebooks, int M, int K, int Csp, const uint8_t* codes,
+                                int packed, int C_t, const float* bias, int relu, qcnn_plan** plan, void* stream) {
+  if (!codebooks || !codes || !plan) return QCNN_ERR_NULL;
+  if (K < 1 || K > 256) return QCNN_ERR_K_RANGE;
+  if (C_t < 1) return QCNN_ERR_SHAPE;
+  qcnn_status s = check_pq(N, C_s, M, K, Csp);
+  if (s != QCNN_OK) return s;
+  const size_t nx = elems({N, C_s}), nd = elems({M, K, Csp}), nc = elems({C_t, M}), ny = elems({N, C_t});
+  if (!nx || !nd || !nc || !ny) return QCNN_ERR_SHAPE;
+  if ((uintptr_t)codes & 3) return QCNN_ERR_UNSUPPORTED;
+  const int bits = packed ? qcnn::code_bits(K) : 8;
+  hipStream_t st = (hipStream_t)stream;
+  qcnn_plan proto{};
+  proto.fc = true;
+  proto.sh = ConvShape{N, C_s, 1, 1, M, K, Csp, C_t, 1, 1, 0, 1, 1};
+  proto.relu = relu ? 1 : 0;
+  proto.relaid = qcnn::fc_tiled_supported(N, C_s, M, K, Csp, C_t);
+  proto.bits = bits;
+  proto.nx = nx;
+  proto.ny = ny;
+  return make_plan(
+      proto, codebooks, nd, codes, nc, code_stream_bytes(nc, bits),
+      proto.relaid ? qcnn::fc_tiled_code_bytes(N, C_s, M, K, Csp, C_t) : 0,
+      [&](const qcnn::CodeStream& cs, uint8_t* out) {
+        return qcnn::launch_fc_tiled_codes(N, C_s, M, K, Csp, C_t, cs, reinterpret_cast<uint32_t*>(out), st);
+      },
+      bias, plan, st);
+}
+
+qcnn_status qcnn_plan_forward(const qcnn_plan* plan, const float* x, float* y, void* stream) {
   if (!plan || !x || !y) return QCNN_ERR_NULL;
   if (overlap(y, plan->ny * 4, x, plan->nx * 4)) return QCNN_ERR_ALIAS;
   int dev = 0;
@@ -468,17 +527,24 @@ qcnn_status qcnn_conv_plan_forward(const qcnn_conv_plan* plan, const float* x, f
   if (dev != plan->device) return QCNN_ERR_UNSUPPORTED;
   if (!prepare_device()) return QCNN_ERR_HIP;
   hipStream_t st = (hipStream_t)stream;
+  const ConvShape& sh = plan->sh;
+  const qcnn::CodeStream cs{plan->codes, plan->bits};
+  if (plan->fc) {
+    if (plan->relaid)
+      return hip_status(qcnn::launch_fc_tiled_relaid(sh.N, sh.Cs, sh.M, sh.K, sh.Csp, sh.Ct, x, plan->D,
+                                                     reinterpret_cast<const uint32_t*>(plan->codes), plan->bias,
+                                                     plan->relu, y, st));
+    return hip_status(
+        qcnn::launch_fc_forward(sh.N, sh.Cs, sh.M, sh.K, sh.Csp, sh.Ct, x, plan->D, cs, plan->bias, plan->relu, y, st));
+  }
   const qcnn::PoolSpec* pool = plan->pooled ? &plan->pool : nullptr;
   if (plan->relaid)
-    return hip_status(
-        qcnn::launch_conv_flat_relaid(plan->sh, x, plan->D, plan->codes, plan->bias, plan->relu, y, st, pool));
-  const qcnn::CodeStream cs{plan->codes, plan->bits};
-  if (pool)
-    return hip_status(qcnn::launch_conv_pool_forward(plan->sh, x, plan->D, cs, plan->bias, plan->relu, *pool, y, st));
-  return hip_status(qcnn::launch_conv_forward(plan->sh, x, plan->D, cs, plan->bias, plan->relu, y, st));
+    return hip_status(qcnn::launch_conv_flat_relaid(sh, x, plan->D, plan->codes, plan->bias, plan->relu, y, st, pool));
+  if (pool) return hip_status(qcnn::launch_conv_pool_forward(sh, x, plan->D, cs, plan->bias, plan->relu, *pool, y, st));
+  return hip_status(qcnn::launch_conv_forward(sh, x, plan->D, cs, plan->bias, plan->relu, y, st));
 }
 
-qcnn_status qcnn_conv_plan_destroy(qcnn_conv_plan* plan) {
+qcnn_status qcnn_plan_destroy(qcnn_plan* plan) {
   if (!plan) return QCNN_OK;
   int cur = 0;
   hipError_t e = hipGetDevice(&cur);

@@ -202,6 +202,15 @@ hipError_t timed_launch(LaunchTimer* t, F kernel, const dim3& grid, const dim3& 
 bool fc_tiled_supported(int N, int Cs, int M, int K, int Csp, int Ct);
 hipError_t launch_fc_tiled(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
                            CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream);
+// The same call in two parts (as for the flat conv kernel): the re-laid
+// codes' size (0 when the kernel cannot tile the layer), the re-layout, and
+// the call on codes re-laid for the same shape.
+size_t fc_tiled_code_bytes(int N, int Cs, int M, int K, int Csp, int Ct);
+hipError_t launch_fc_tiled_codes(int N, int Cs, int M, int K, int Csp, int Ct, CodeStream codes, uint32_t* codes4,
+                                 hipStream_t stream);
+hipError_t launch_fc_tiled_relaid(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
+                                  const uint32_t* codes4, const float* bias, int relu, float* y,
+                                  hipStream_t stream);
 
 // Parameter quantization (quantize.hip); objective arrays are device float64.
 hipError_t launch_pq_assign(int Ct, int Cs, int dk, const float* W, const float* D, int M, int K, int Csp,

@@ -83,9 +83,9 @@ int main(void) {
                                    NULL) == QCNN_ERR_WORKSPACE);
   EXPECT(qcnn_conv_forward_noalloc(FP(X), 2, 4096, 13, 13, FP(Dp), 1024, 128, 4, CP(C), 4096, 3, 1, 1, NULL, 0,
                                    FW(Y), NULL) == QCNN_ERR_WORKSPACE);
-  /* prepared conv layers: validation before any HIP call; *plan untouched on error */
+  /* prepared layers: validation before any HIP call; *plan untouched on error */
   {
-    qcnn_conv_plan* plan = (qcnn_conv_plan*)(uintptr_t)0xdead0;
+    qcnn_plan* plan = (qcnn_plan*)(uintptr_t)0xdead0;
     EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, NULL, 2, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 0, 0, &plan, NULL) ==
            QCNN_ERR_NULL);
     EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C), 0, 4, 3, 1, 1, NULL, 0, 0, 0, NULL, NULL) ==
@@ -100,9 +100,14 @@ int main(void) {
            QCNN_ERR_SHAPE);
     EXPECT(qcnn_conv_plan_create(2, 8, 5, 5, FP(Dp), 2, 16, 4, CP(C + 1), 0, 4, 3, 1, 1, NULL, 0, 0, 0, &plan,
                                  NULL) == QCNN_ERR_UNSUPPORTED);
-    EXPECT(plan == (qcnn_conv_plan*)(uintptr_t)0xdead0);
-    EXPECT(qcnn_conv_plan_forward(NULL, FP(X), FW(Y), NULL) == QCNN_ERR_NULL);
-    EXPECT(qcnn_conv_plan_destroy(NULL) == QCNN_OK);
+    EXPECT(qcnn_fc_plan_create(2, 8, FP(Dp), 2, 16, 4, CP(C), 0, 4, NULL, 0, NULL, NULL) == QCNN_ERR_NULL);
+    EXPECT(qcnn_fc_plan_create(2, 8, FP(Dp), 3, 16, 4, CP(C), 0, 4, NULL, 0, &plan, NULL) == QCNN_ERR_SHAPE);
+    EXPECT(qcnn_fc_plan_create(2, 8, FP(Dp), 2, 0, 4, CP(C), 0, 4, NULL, 0, &plan, NULL) == QCNN_ERR_K_RANGE);
+    EXPECT(qcnn_fc_plan_create(2, 8, FP(Dp), 2, 16, 4, CP(C + 1), 0, 4, NULL, 0, &plan, NULL) ==
+           QCNN_ERR_UNSUPPORTED);
+    EXPECT(plan == (qcnn_plan*)(uintptr_t)0xdead0);
+    EXPECT(qcnn_plan_forward(NULL, FP(X), FW(Y), NULL) == QCNN_ERR_NULL);
+    EXPECT(qcnn_plan_destroy(NULL) == QCNN_OK);
   }
   /* helpers */
   for (int s = 0; s <= 9; ++s) EXPECT(qcnn_status_string((qcnn_status)s) != NULL);

@@ -149,9 +149,30 @@ def test_conv_plan_create_rejects(L, kw, want):
     assert handle == 0xdead0  # *plan is not written on an error
 
 
-def test_conv_plan_forward_and_destroy_without_gpu(L):
-    assert L.qcnn_conv_plan_forward(None, FAKE, FAKE2, None) == NULL
-    assert L.qcnn_conv_plan_destroy(None) == 0  # NULL is accepted, like free(NULL)
+def fc_plan_create(L, plan_out=True, **kw):
+    a = dict(N=2, Cs=8, D=FAKE, M=2, K=16, Csp=4, codes=FAKE, packed=0, Ct=4, bias=None, relu=0, stream=None)
+    a.update(kw)
+    handle = ctypes.c_void_p(0xdead0)
+    st = L.qcnn_fc_plan_create(a["N"], a["Cs"], a["D"], a["M"], a["K"], a["Csp"], a["codes"], a["packed"], a["Ct"],
+                               a["bias"], a["relu"], ctypes.byref(handle) if plan_out else None, a["stream"])
+    return st, handle.value
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(D=None), NULL), (dict(codes=None), NULL), (dict(plan_out=False), NULL),
+    (dict(N=0), SHAPE), (dict(Ct=0), SHAPE), (dict(M=3), SHAPE), (dict(Cs=0), SHAPE),
+    (dict(K=0), KR), (dict(K=257, packed=1), KR),
+    (dict(Cs=34, M=2, Csp=17), UNSUP), (dict(codes=FAKE + 1), UNSUP), (dict(N=70000), UNSUP),
+])
+def test_fc_plan_create_rejects(L, kw, want):
+    st, handle = fc_plan_create(L, **kw)
+    assert st == want
+    assert handle == 0xdead0
+
+
+def test_plan_forward_and_destroy_without_gpu(L):
+    assert L.qcnn_plan_forward(None, FAKE, FAKE2, None) == NULL
+    assert L.qcnn_plan_destroy(None) == 0  # NULL is accepted, like free(NULL)
 
 
 def test_noalloc_rejects_layers_beyond_its_scratch(L):

@@ -1,5 +1,5 @@
-"""GPU checks of the prepared conv layer (qcnn_conv_plan_create / _forward /
-_destroy).
+"""GPU checks of the prepared conv layer (qcnn_conv_plan_create,
+qcnn_plan_forward, qcnn_plan_destroy).
 
 A plan's forward must equal the per-call entry point with the same
 arguments bit for bit: qcnn_conv_forward without pooling, and
@@ -168,8 +168,8 @@ def test_plan_rejects_overlapping_output(api, dev):
     xd = T(x, dev)
     plan = api.ConvPlan((N, Cs, H, W), T(D, dev), T(codes, dev), st, pad)
     y = xd.reshape(-1)[:N * Ct * H * W].view(N, Ct, H, W)
-    st_ = _lib.lib().qcnn_conv_plan_forward(plan._ptr, xd.data_ptr(), y.data_ptr(),
-                                            torch.cuda.current_stream(dev).cuda_stream)
+    st_ = _lib.lib().qcnn_plan_forward(plan._ptr, xd.data_ptr(), y.data_ptr(),
+                                       torch.cuda.current_stream(dev).cuda_stream)
     assert st_ == 7  # QCNN_ERR_ALIAS; nothing launched
     assert torch.equal(xd, T(x, dev))
 
