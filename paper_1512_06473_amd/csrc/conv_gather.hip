@@ -232,10 +232,18 @@ ConvKernel pick_conv_kernel(const ConvShape& s) {
 
 }  // namespace
 
-bool conv_picks_flat(const ConvShape& s) { return pick_conv_kernel(s) == ConvKernel::kFlat; }
+int conv_kernel_pick(const ConvShape& s) { return static_cast<int>(pick_conv_kernel(s)); }
 
-size_t conv_forward_workspace(const ConvShape& s) {
-  switch (pick_conv_kernel(s)) {
+namespace {
+
+ConvKernel kind_or_pick(const ConvShape& s, int kind) {
+  return kind < 0 ? pick_conv_kernel(s) : static_cast<ConvKernel>(kind);
+}
+
+}  // namespace
+
+size_t conv_forward_workspace(const ConvShape& s, int kind) {
+  switch (kind_or_pick(s, kind)) {
     case ConvKernel::kFlat: return conv_flat_workspace(s);
     case ConvKernel::kHalf: return conv_half_workspace(s);
     default: return 0;  // the generic kernel reads the caller's codes directly
@@ -243,10 +251,11 @@ size_t conv_forward_workspace(const ConvShape& s) {
 }
 
 hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
-                               const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws) {
-  const ConvKernel kind = pick_conv_kernel(s);
-  if (kind == ConvKernel::kFlat) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream, ws);
-  if (kind == ConvKernel::kHalf) return launch_conv_half(s, x, D, codes, bias, relu, y, stream, ws);
+                               const float* bias, int relu, float* y, hipStream_t stream, const Workspace* ws,
+                               int kind) {
+  const ConvKernel k = kind_or_pick(s, kind);
+  if (k == ConvKernel::kFlat) return launch_conv_flat(s, x, D, codes, bias, relu, y, stream, ws);
+  if (k == ConvKernel::kHalf) return launch_conv_half(s, x, D, codes, bias, relu, y, stream, ws);
   Tiling t;
   if (!choose_tiling(s, &t)) return hipErrorInvalidConfiguration;
   const ConvPtrs a{x, D, codes, bias, y, ws == nullptr || ws->timed};
@@ -285,19 +294,20 @@ hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* 
 
 hipError_t launch_conv_pool_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                                     const float* bias, int relu, const PoolSpec& pool, float* y,
-                                    hipStream_t stream) {
-  if (pick_conv_kernel(s) == ConvKernel::kFlat && conv_flat_pools(s))
+                                    hipStream_t stream, int kind) {
+  const ConvKernel k = kind_or_pick(s, kind);
+  if (k == ConvKernel::kFlat && conv_flat_pools(s))
     return launch_conv_flat(s, x, D, codes, bias, relu, y, stream, nullptr, &pool);
   // One library buffer holds the layer's own temporaries and, after them,
   // its full output map, which the max-pool kernel reads.
-  const size_t conv_ws = (conv_forward_workspace(s) + 255) & ~(size_t)255;
+  const size_t conv_ws = (conv_forward_workspace(s, static_cast<int>(k)) + 255) & ~(size_t)255;
   const size_t full = (size_t)s.N * s.Ct * s.Ho * s.Wo * sizeof(float);
   Scratch scratch;
   hipError_t e = scratch.acquire(stream, conv_ws + full);
   if (e != hipSuccess) return e;
   float* ymap = reinterpret_cast<float*>(scratch.get() + conv_ws);
   const Workspace ws{scratch.get(), conv_ws, true};
-  e = launch_conv_forward(s, x, D, codes, bias, relu, ymap, stream, &ws);
+  e = launch_conv_forward(s, x, D, codes, bias, relu, ymap, stream, &ws, static_cast<int>(k));
   if (e != hipSuccess) return e;
   return launch_maxpool(ymap, s.N, s.Ct, s.Ho, s.Wo, pool.k, pool.s, pool.Hp, pool.Wp, y, stream);
 }

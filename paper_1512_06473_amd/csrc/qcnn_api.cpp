@@ -309,13 +309,14 @@ qcnn_status conv_forward(const float* x, int N, int C_s, int H, int W, const flo
     // The static scratch: the layer's temporaries, then 256 bytes for the
     // code-check counter.  Checked before any HIP call.
     const size_t room = qcnn::noalloc_scratch_bytes() - 256;
-    if (qcnn::conv_forward_workspace(sh) > room) return QCNN_ERR_WORKSPACE;
+    const int kind = qcnn::conv_kernel_pick(sh);  // one choice for the size check and the launch
+    if (qcnn::conv_forward_workspace(sh, kind) > room) return QCNN_ERR_WORKSPACE;
     char* base = nullptr;
     if (qcnn::noalloc_scratch(&base) != hipSuccess) return QCNN_ERR_HIP;
     s = check_codes(cs, nc, K, st, reinterpret_cast<int*>(base + room));
     if (s != QCNN_OK) return s;
     const qcnn::Workspace ws{base, room};
-    return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0, y, st, &ws));
+    return hip_status(qcnn::launch_conv_forward(sh, x, codebooks, cs, bias, relu ? 1 : 0, y, st, &ws, kind));
   }
   if (!prepare_device()) return QCNN_ERR_HIP;
   s = check_codes(cs, nc, K, st);
@@ -396,6 +397,7 @@ struct qcnn_plan {
   qcnn::PoolSpec pool;
   int device;
   bool relaid;
+  int kind;  // conv kernel family, fixed at creation
   int bits;  // of the code copy when !relaid
   size_t nx, ny;
   void* mem;
@@ -479,7 +481,8 @@ qcnn_status qcnn_conv_plan_create(int N, int C_s, int H, int W, const float* cod
   proto.relu = relu ? 1 : 0;
   proto.pooled = c.pooled;
   proto.pool = qcnn::PoolSpec{pool_k, pool_s, c.Hp, c.Wp};
-  proto.relaid = qcnn::conv_picks_flat(c.sh);
+  proto.kind = qcnn::conv_kernel_pick(c.sh);
+  proto.relaid = proto.kind == 0;
   proto.bits = bits;
   proto.nx = c.nx;
   proto.ny = c.ny;
@@ -540,8 +543,10 @@ qcnn_status qcnn_plan_forward(const qcnn_plan* plan, const float* x, float* y, v
   const qcnn::PoolSpec* pool = plan->pooled ? &plan->pool : nullptr;
   if (plan->relaid)
     return hip_status(qcnn::launch_conv_flat_relaid(sh, x, plan->D, plan->codes, plan->bias, plan->relu, y, st, pool));
-  if (pool) return hip_status(qcnn::launch_conv_pool_forward(sh, x, plan->D, cs, plan->bias, plan->relu, *pool, y, st));
-  return hip_status(qcnn::launch_conv_forward(sh, x, plan->D, cs, plan->bias, plan->relu, y, st));
+  if (pool)
+    return hip_status(
+        qcnn::launch_conv_pool_forward(sh, x, plan->D, cs, plan->bias, plan->relu, *pool, y, st, plan->kind));
+  return hip_status(qcnn::launch_conv_forward(sh, x, plan->D, cs, plan->bias, plan->relu, y, st, nullptr, plan->kind));
 }
 
 qcnn_status qcnn_plan_destroy(qcnn_plan* plan) {

@@ -79,19 +79,21 @@ struct PoolSpec {
   int k, s, Hp, Wp;
 };
 
+// The conv kernel family for a layer: 0 the flat kernel, 1 the two-table
+// kernel, 2 the generic one; conv_kernel_pick gives the one the launchers
+// pick now (QCNN_CONV_KERNEL is read per call; host-side, no HIP call).  The
+// launchers below take a `kind` from it, or -1 to pick at the call.
+int conv_kernel_pick(const ConvShape& s);
+
 // Returns hipErrorInvalidConfiguration when no tiling fits the device.
 // With `ws` the temporaries live there (nothing allocated, no timing events).
 hipError_t launch_conv_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                                const float* bias, int relu, float* y, hipStream_t stream,
-                               const Workspace* ws = nullptr);
+                               const Workspace* ws = nullptr, int kind = -1);
 
-// Bytes of temporaries launch_conv_forward needs for this layer with the
-// kernel it would pick now (host-side, no HIP call).
-size_t conv_forward_workspace(const ConvShape& s);
-
-// True when launch_conv_forward would run this layer on the flat kernel now
-// (QCNN_CONV_KERNEL is read per call; host-side, no HIP call).
-bool conv_picks_flat(const ConvShape& s);
+// Bytes of temporaries launch_conv_forward needs for this layer with kernel
+// `kind` (-1: the one it would pick now; host-side, no HIP call).
+size_t conv_forward_workspace(const ConvShape& s, int kind = -1);
 
 // The conv layer followed by max pooling, y: [N][C_t][H_p][W_p].  A layer
 // whose subspaces the stride-1/strided flat kernel splits over workgroups
@@ -99,7 +101,7 @@ bool conv_picks_flat(const ConvShape& s);
 // its full map to a temporary that the max-pool kernel reads.
 hipError_t launch_conv_pool_forward(const ConvShape& s, const float* x, const float* D, CodeStream codes,
                                     const float* bias, int relu, const PoolSpec& pool, float* y,
-                                    hipStream_t stream);
+                                    hipStream_t stream, int kind = -1);
 
 hipError_t launch_fc_forward(int N, int Cs, int M, int K, int Csp, int Ct, const float* x, const float* D,
                              CodeStream codes, const float* bias, int relu, float* y, hipStream_t stream);

@@ -220,3 +220,22 @@ def test_plan_closed_and_shape_checks(api, dev):
     plan.close()  # a second close does nothing
     with pytest.raises(ValueError):
         plan(T(x, dev))
+
+
+def test_plan_keeps_the_kernel_chosen_at_creation(api, dev, monkeypatch):
+    """A plan made under QCNN_CONV_KERNEL=generic keeps the generic kernel
+    after the variable is unset (float data: the kernels sum in different
+    orders, so the bits tell them apart)."""
+    case = CASES[7]
+    N, Cs, H, W, Ct, dk, st, pad, Csp, K, pool, has_bias, relu = case
+    x, D, codes, bias = draw(case, False)
+    xd, Dd, cd = T(x, dev), T(D, dev), T(codes, dev)
+    monkeypatch.setenv("QCNN_CONV_KERNEL", "generic")
+    plan = api.ConvPlan((N, Cs, H, W), Dd, cd, st, pad, None, relu, pool)
+    ref_generic = per_call(api, case, xd, Dd, cd, None)
+    monkeypatch.delenv("QCNN_CONV_KERNEL")
+    ref_default = per_call(api, case, xd, Dd, cd, None)
+    y = plan(xd)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(y), bits(ref_generic))
+    assert not np.array_equal(bits(ref_default), bits(ref_generic))  # the case does tell them apart
