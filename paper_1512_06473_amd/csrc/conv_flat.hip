@@ -119,13 +119,16 @@ __device__ __forceinline__ int s_rows_in_kernel(const FlatParams& p, int a) {
 // taps would read the zero row); only the PD reads already in flight are
 // spent on it.  The stream is unrolled by template recursion (a counted loop
 // this long exceeds the compiler's unroll limit).  PRIO: a
-// wave issues the first three quarters of its stream at raised priority and
-// the rest at the base level (a drop at 1/3 or 5/6 was slower, at 1/2 or 2/3
-// up to 1 % slower), so that waves ahead of the others yield the SIMD to the
-// ones behind and the waves of a workgroup finish their gathers closer
-// together (the last ones alone do not keep the LDS busy).  Only for a
-// workgroup that has its CU to itself: beside a second workgroup, the
-// priority starves that one's table build.
+// wave steps its issue priority down along its stream, 3 for the first 5/8
+// of its reads, 2 until 13/16, 1 until 15/16, then the base level, so that
+// waves ahead of the others yield the SIMD to the ones behind and the waves
+// of a workgroup finish their gathers closer together (the last ones alone
+// do not keep the LDS busy).  Measured on the AlexNet conv3 layer against
+// other schedules: one drop from 1 to 0 at 3/4 gave a 2 % longer kernel,
+// a single drop at 7/8 4 % longer, steps that start at 3/4 2 % longer, and
+// steps that start at 1/4 or 1/2 up to 3 % longer.  Only for a workgroup that
+// has its CU to itself: beside a second workgroup, the priority starves that
+// one's table build.
 template <int ROWS, int COLS, int TW, int CW, bool LAST_ROW_AT_END, bool PRIO>
 struct GatherStream {
   static constexpr int TAPS = ROWS * COLS;
@@ -155,8 +158,10 @@ struct GatherStream {
   template <int K, int WG4, int PD>
   __device__ __forceinline__ void step(float (&acc)[TW][4], f4v (&qb)[PD]) const {
     if constexpr (K < NS) {
-      if constexpr (PRIO && K == 0) __builtin_amdgcn_s_setprio(1);
-      if constexpr (PRIO && K == (3 * NS) / 4) __builtin_amdgcn_s_setprio(0);
+      if constexpr (PRIO && K == 0) __builtin_amdgcn_s_setprio(3);
+      if constexpr (PRIO && K == (5 * NS) / 8) __builtin_amdgcn_s_setprio(2);
+      if constexpr (PRIO && K == (13 * NS) / 16) __builtin_amdgcn_s_setprio(1);
+      if constexpr (PRIO && K == (15 * NS) / 16) __builtin_amdgcn_s_setprio(0);
       if constexpr (K == B) {
         if (!last_row) return;  // wave-uniform
       }
