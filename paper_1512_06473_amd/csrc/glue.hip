@@ -16,6 +16,11 @@
 namespace qcnn {
 namespace {
 
+// One thread per output.  KW > 0: a KW x KW window, unrolled, so that all
+// of a thread's loads are in flight together (with a run-time window size
+// each load waited for the previous max: 36 us for AlexNet's pool1 at N = 64,
+// 2.6 TB/s); KW = 0: any window size.
+template <int KW>
 __global__ __launch_bounds__(256) void maxpool_kernel(const float* __restrict__ x, int H, int W, int k, int s,
                                                       int Ho, int Wo, size_t total, float* __restrict__ y) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -25,8 +30,18 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const float* __restrict__ 
   const size_t plane = i / ((size_t)Wo * Ho);
   const float* src = x + plane * H * W + (size_t)(yo * s) * W + xo * s;
   float best = src[0];
-  for (int dy = 0; dy < k; ++dy)
-    for (int dx = 0; dx < k; ++dx) best = fmaxf(best, src[dy * W + dx]);
+  if constexpr (KW > 0) {
+    float v[KW * KW];
+#pragma unroll
+    for (int dy = 0; dy < KW; ++dy)
+#pragma unroll
+      for (int dx = 0; dx < KW; ++dx) v[dy * KW + dx] = src[dy * W + dx];
+#pragma unroll
+    for (int q = 0; q < KW * KW; ++q) best = fmaxf(best, v[q]);
+  } else {
+    for (int dy = 0; dy < k; ++dy)
+      for (int dx = 0; dx < k; ++dx) best = fmaxf(best, src[dy * W + dx]);
+  }
   y[i] = best;
 }
 
@@ -66,8 +81,9 @@ __global__ __launch_bounds__(256) void unpack_codes_kernel(CodeStream packed, si
 hipError_t launch_maxpool(const float* x, int N, int C, int H, int W, int k, int s, int Ho, int Wo, float* y,
                           hipStream_t stream) {
   const size_t total = (size_t)N * C * Ho * Wo;
-  hipLaunchKernelGGL(maxpool_kernel, dim3((unsigned)ceil_div_z(total, 256)), dim3(256), 0, stream, x, H, W, k, s,
-                     Ho, Wo, total, y);
+  auto kern = k == 3 ? maxpool_kernel<3> : k == 2 ? maxpool_kernel<2> : maxpool_kernel<0>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)ceil_div_z(total, 256)), dim3(256), 0, stream, x, H, W, k, s, Ho, Wo,
+                     total, y);
   return hipGetLastError();
 }
 
