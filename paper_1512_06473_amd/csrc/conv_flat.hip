@@ -41,10 +41,12 @@
 // multiply-add and four fp32 adds per lane, all reads are aligned and
 // bank-conflict free.
 //
-// Codes are re-laid out once per call to codes8[v][t][tap] (clamped to K-1,
-// the zero row for grid taps past the kernel), so that one wave's codes for
-// a virtual subspace are a few contiguous dwords that scalar loads bring into
-// SGPRs during the table build.  The virtual subspaces may be split over
+// Codes are re-laid out (once per call, or once per prepared plan) to
+// codes8[v][t][tap] (clamped to K-1, the zero row for grid taps past the
+// kernel; each channel's taps padded to a stride that keeps every wave's run
+// dword aligned), so that one wave's codes for a virtual subspace are a few
+// contiguous dwords that scalar loads bring into SGPRs during the table
+// build.  The virtual subspaces may be split over
 // workgroups: each then stores its partial sums tile by tile (whole cache
 // lines per store instruction) and a second kernel adds them in a fixed
 // order.  Blocks are mapped so that the workgroups of one tile share an XCD
@@ -83,6 +85,16 @@ constexpr int kMaxPB = 2;   // 16-position table blocks per wave
 constexpr int kMaxKB = 8;   // 16-codeword blocks (K <= 128)
 
 typedef float f4v __attribute__((ext_vector_type(4)));
+
+// Bytes per channel of the re-laid codes: the tap count, padded so that a
+// wave's run of TW channels is a whole number of dwords (a wave reads its
+// codes with scalar dword loads, whose addresses must be 4-byte aligned;
+// every run starts at a multiple of TW channels).
+__host__ __device__ constexpr int code_stride(int TW, int taps) {
+  int c = taps;
+  while ((TW * c) % 4 != 0) ++c;
+  return c;
+}
 
 // acc += (value of v in lane l+1): a wave_shl:1 DPP move the compiler folds
 // into the add (v_add_f32_dpp), with the wait states a DPP read needs after a
@@ -149,9 +161,12 @@ struct GatherStream {
   const char* lbase;
   bool last_row;  // read the last row's taps
 
+  static constexpr int CS = code_stride(TW, TAPS);
+
   template <int KF>
   __device__ __forceinline__ f4v read() const {
-    const uint32_t code = (cw[KF >> 2] >> (8 * (KF & 3))) & 0xffu;
+    constexpr int cb = (KF / TAPS) * CS + KF % TAPS;  // byte of the code in the wave's run
+    const uint32_t code = (cw[cb >> 2] >> (8 * (cb & 3))) & 0xffu;
     return *reinterpret_cast<const f4v*>(lbase + __umul24(code, row_bytes) + tapbase[KF % TAPS]);
   }
 
@@ -214,7 +229,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   float* lut = reinterpret_cast<float*>(lut4);
   constexpr int TAPS = ROWS * COLS;
   constexpr int NQ = TW * TAPS;        // table reads per wave and virtual subspace
-  constexpr int CW = (NQ + 3) / 4;     // code dwords per wave and virtual subspace
+  constexpr int CS = code_stride(TW, TAPS);  // code bytes per channel
+  constexpr int CW = (TW * CS + 3) / 4;      // code dwords per wave and virtual subspace
   constexpr int PD = 6;                // table reads kept in flight (4 to 6 equal, 8 ~1 % slower)
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -366,7 +382,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   dstage[wave * 64 + lane] = dnext;  // published by the loop's first barrier
   // This wave's codes for virtual subspace v: TW x TAPS consecutive bytes, in SGPRs.
   auto load_codes = [&](int vv, uint32_t (&cwv)[CW]) {
-    const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)vv * p.ct_pad + t0) * TAPS);
+    const uint32_t* ow = reinterpret_cast<const uint32_t*>(codes8 + ((size_t)vv * p.ct_pad + t0) * CS);
 #pragma unroll
     for (int k = 0; k < CW; ++k) cwv[k] = ow[k];
   };
@@ -511,17 +527,19 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
 // codes8[v][t][tap]: the code of kernel tap (ky, kx) = (s (g ROWS + u') + a,
 // s v' + b) of subspace m for virtual subspace v = ((m s + a) s + b) G + g
 // and grid tap (u', v') = (tap / COLS, tap % COLS), clamped to K-1; grid taps
-// past the kernel get the zero row; channels past C_t get 0.  One thread
+// past the kernel get the zero row; channels past C_t and the padding bytes
+// of a channel (tap >= ROWS COLS, up to the code stride) get 0.  One thread
 // writes one dword (4 consecutive bytes); the bytes it reads are scattered,
 // but the whole code array is small and L2-resident.
 struct CodeMap {
   int Ct, dk, stride, M, G, rows, cols, K, ct_pad, zrow, V;
+  int cstride;  // bytes per channel (>= rows cols; the bytes past the taps are 0 and never read)
 };
 
 __global__ __launch_bounds__(256) void flat_codes_kernel(CodeStream codes, CodeMap q,
                                                          uint32_t* __restrict__ codes8) {
   const int taps = q.rows * q.cols;
-  const int per_v = q.ct_pad * taps;
+  const int per_v = q.ct_pad * q.cstride;
   const int nwords = (q.V * per_v + 3) / 4;  // the plan keeps V ct_pad taps below 2^31
   const bool plain = q.G == 1 && q.stride == 1;  // v = m, tap = (ky, kx)
   for (int wi = blockIdx.x * blockDim.x + threadIdx.x; wi < nwords; wi += gridDim.x * blockDim.x) {
@@ -530,12 +548,12 @@ __global__ __launch_bounds__(256) void flat_codes_kernel(CodeStream codes, CodeM
     const int o = wi * 4;
     int v = o / per_v;
     const int r = o - v * per_v;
-    int t = r / taps, tap = r - t * taps;
+    int t = r / q.cstride, tap = r - t * q.cstride;
     uint32_t word = 0;
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
       uint32_t val = 0;
-      if (v < q.V && t < q.Ct) {
+      if (v < q.V && t < q.Ct && tap < taps) {
         int m = v, ky = tap / q.cols, kx = tap - ky * q.cols;
         if (!plain) {
           const int g = v % q.G;
@@ -555,7 +573,7 @@ __global__ __launch_bounds__(256) void flat_codes_kernel(CodeStream codes, CodeM
         }
       }
       word |= val << (8 * bb);
-      if (++tap == taps) {
+      if (++tap == q.cstride) {
         tap = 0;
         if (++t == q.ct_pad) {
           t = 0;
@@ -782,10 +800,15 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
     for (int S = 1; S <= 16 && S <= s.Wo; ++S) {
       size_t lds = 0;
       if (!set_geometry(s, L, S, &p, &lds)) continue;
-      for (int TW : {8, 12}) {
+      for (int TW : {6, 8, 12}) {
         // two channel groups, ten taps or moving offsets with 12 channels per
-        // wave do not fit the registers
+        // wave do not fit the registers.  6 channels per wave only for the
+        // stride-phase layouts (they take no 12): a layer of 96 channels
+        // (AlexNet conv1) then keeps all 16 waves gathering, where 8 per wave
+        // left 4 of them idle (the cost below counts the reads of idle
+        // channel slots, so it is not asked to weigh 6 against 8 elsewhere).
         if (TW == 12 && (s.Csp > 4 || L.gen)) continue;
+        if (TW == 6 && (s.Csp > 4 || !L.gen || s.stride == 1)) continue;
         const int tc = kWaves * TW;
         const int tblocks = ceil_div(s.Ct, tc);
         for (int splits = 1; splits <= 16 && splits <= p.V; ++splits) {
@@ -800,7 +823,7 @@ bool make_plan(const ConvShape& s, FlatPlan* out) {
           q.work = (int)work;
           q.per_xcd = ceil_div(q.work, 8);
           q.ct_pad = tblocks * tc;
-          if ((long long)p.V * q.ct_pad * taps + 4 > (1LL << 31)) continue;
+          if ((long long)p.V * q.ct_pad * code_stride(TW, taps) + 4 > (1LL << 31)) continue;
           const double c = plan_cost(q, taps, TW);
           if (!found || c < best) {
             found = true;
@@ -850,6 +873,10 @@ struct LaunchArgs {
 
 template <int ROWS, int COLS, int WG4, bool GEN>
 hipError_t launch_nc(const FlatPlan& pl, const LaunchArgs& a) {
+  if constexpr (GEN) {
+    if (pl.TW == 6)  // the planner gives 6 channels per wave only with C's <= 4
+      return launch_main<ROWS, COLS, WG4, 1, 6, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial, a.stream, a.timer);
+  }
   if (pl.p.Csp <= 4) {
     if constexpr (!GEN) {
       if (pl.TW == 12) return launch_main<ROWS, COLS, WG4, 1, 12, GEN>(pl, a.x, a.D, a.codes8, a.bias, a.y, a.partial,
@@ -904,7 +931,7 @@ struct FlatWs {
 FlatWs flat_ws(const FlatPlan& pl) {
   const FlatParams& p = pl.p;
   FlatWs w;
-  w.n_codes = (size_t)p.V * p.ct_pad * pl.rows * pl.cols;
+  w.n_codes = (size_t)p.V * p.ct_pad * code_stride(pl.TW, pl.rows * pl.cols);
   w.code_bytes = (w.n_codes + 4 + 255) & ~(size_t)255;  // + the tail of the last dword load
   w.partial_elems = (size_t)p.splits * p.tiles * p.ct_pad * 256;
   w.total = w.code_bytes + (p.splits > 1 ? w.partial_elems * sizeof(float) : 0);
@@ -947,7 +974,8 @@ bool flat_plan(const ConvShape& s, int relu, FlatPlan* pl) {
 hipError_t launch_codes(const FlatPlan& pl, CodeStream codes, uint8_t* codes8, hipStream_t stream) {
   const FlatParams& p = pl.p;
   const size_t nwords = (flat_ws(pl).n_codes + 3) / 4;
-  const CodeMap cm{p.Ct, p.dk, p.stride, p.M, p.G, pl.rows, pl.cols, p.K, p.ct_pad, p.zrow, p.V};
+  const CodeMap cm{p.Ct, p.dk, p.stride, p.M, p.G, pl.rows, pl.cols, p.K, p.ct_pad, p.zrow, p.V,
+                   code_stride(pl.TW, pl.rows * pl.cols)};
   hipLaunchKernelGGL(flat_codes_kernel, dim3((unsigned)std::min<size_t>(2048, ceil_div_z(nwords, 256))), dim3(256), 0,
                      stream, codes, cm, reinterpret_cast<uint32_t*>(codes8));
   return hipGetLastError();
