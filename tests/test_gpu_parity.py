@@ -212,6 +212,9 @@ CONV_EDGE = [
     (3, 20, 9, 40, 70, 5, 1, 2, 5, 128),     # 5x5 pad 2, row groups, C's = 5
     (2, 8, 11, 11, 9, 5, 1, 0, 8, 100),      # 5x5 pad 0
     (1, 6, 12, 12, 5, 4, 2, 1, 2, 16),       # even kernel, stride 2
+    # stride phases with 6 channels per wave: ragged channel blocks of 96, split subspaces
+    (2, 12, 25, 25, 200, 3, 2, 1, 4, 32),    # 3x3 stride 2: three channel blocks, 12 splits
+    (1, 64, 23, 23, 100, 5, 2, 2, 4, 64),    # 5x5 stride 2: 3x3 phase grids with a zero row, 16 splits
 ]
 
 
