@@ -228,7 +228,6 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
   extern __shared__ float4 lut4[];
   float* lut = reinterpret_cast<float*>(lut4);
   constexpr int TAPS = ROWS * COLS;
-  constexpr int NQ = TW * TAPS;        // table reads per wave and virtual subspace
   constexpr int CS = code_stride(TW, TAPS);  // code bytes per channel
   constexpr int CW = (TW * CS + 3) / 4;      // code dwords per wave and virtual subspace
   constexpr int PD = 6;                // table reads kept in flight (4 to 6 equal, 8 ~1 % slower)
