@@ -138,9 +138,11 @@ __device__ __forceinline__ int s_rows_in_kernel(const FlatParams& p, int a) {
 // do not keep the LDS busy).  Measured on the AlexNet conv3 layer against
 // other schedules: one drop from 1 to 0 at 3/4 gave a 2 % longer kernel,
 // a single drop at 7/8 4 % longer, steps that start at 3/4 2 % longer, and
-// steps that start at 1/4 or 1/2 up to 3 % longer.  Only for a workgroup that
-// has its CU to itself: beside a second workgroup, the priority starves that
-// one's table build.
+// steps that start at 1/4 or 1/2 up to 3 % longer.  With LAST_ROW_AT_END the
+// steps span the reads before the last row (AlexNet conv2: 593 -> 587 us
+// with the pooled split sum).  Only for a workgroup that has its CU to
+// itself: beside a second workgroup, the priority starves that one's table
+// build.
 template <int ROWS, int COLS, int TW, int CW, bool LAST_ROW_AT_END, bool PRIO>
 struct GatherStream {
   static constexpr int TAPS = ROWS * COLS;
@@ -173,10 +175,13 @@ struct GatherStream {
   template <int K, int WG4, int PD>
   __device__ __forceinline__ void step(float (&acc)[TW][4], f4v (&qb)[PD]) const {
     if constexpr (K < NS) {
+      // With an early stop the steps run over the reads before it (steps
+      // placed after it made the compiler spill 66-160 registers).
+      constexpr int PN = LAST_ROW_AT_END ? B : NS;
       if constexpr (PRIO && K == 0) __builtin_amdgcn_s_setprio(3);
-      if constexpr (PRIO && K == (5 * NS) / 8) __builtin_amdgcn_s_setprio(2);
-      if constexpr (PRIO && K == (13 * NS) / 16) __builtin_amdgcn_s_setprio(1);
-      if constexpr (PRIO && K == (15 * NS) / 16) __builtin_amdgcn_s_setprio(0);
+      if constexpr (PRIO && K == (5 * PN) / 8) __builtin_amdgcn_s_setprio(2);
+      if constexpr (PRIO && K == (13 * PN) / 16) __builtin_amdgcn_s_setprio(1);
+      if constexpr (PRIO && K == (15 * PN) / 16) __builtin_amdgcn_s_setprio(0);
       if constexpr (K == B) {
         if (!last_row) return;  // wave-uniform
       }
@@ -479,8 +484,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_flat_kernel(const float* __r
         // Grid row u' is kernel row s (g ROWS + u') + a.
         const int g = v % p.G, a = (v / p.G / p.stride) % p.stride;
         const bool last_row = s_rows_in_kernel(p, a) - g * ROWS >= ROWS;
-        // (no priority steps here: with the early stop they made the compiler spill)
-        gather_stream<ROWS, COLS, WG4, TW, PD, (ROWS > 1), false>(acc, cw, tapbase, row_bytes, lbase, last_row);
+        gather_stream<ROWS, COLS, WG4, TW, PD, (ROWS > 1), PRIO>(acc, cw, tapbase, row_bytes, lbase, last_row);
       } else {
         gather_stream<ROWS, COLS, WG4, TW, PD, false, PRIO>(acc, cw, tapbase, row_bytes, lbase, true);
       }
@@ -852,10 +856,8 @@ hipError_t launch_kernel(const FlatPlan& pl, const float* x, const float* D, con
 template <int ROWS, int COLS, int WG4, int NC, int TW, bool GEN>
 hipError_t launch_main(const FlatPlan& pl, const float* x, const float* D, const uint8_t* codes8, const float* bias,
                        float* y, float* partial, hipStream_t stream, LaunchTimer* timer) {
-  if constexpr (!GEN) {
-    if (pl.prio)
-      return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, true>(pl, x, D, codes8, bias, y, partial, stream, timer);
-  }
+  if (pl.prio)
+    return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, true>(pl, x, D, codes8, bias, y, partial, stream, timer);
   return launch_kernel<ROWS, COLS, WG4, NC, TW, GEN, false>(pl, x, D, codes8, bias, y, partial, stream, timer);
 }
 
@@ -956,7 +958,10 @@ namespace {
 bool flat_plan(const ConvShape& s, int relu, FlatPlan* pl) {
   if (!make_plan(s, pl)) return false;
   pl->p.relu = relu;
-  pl->prio = pl->lds > kLdsBytes / 2;  // no second workgroup fits beside this one
+  // The priority steps only where no second workgroup can share the CU: by
+  // LDS, or for the layouts with moving offsets by registers (their kernels
+  // use 103-111 VGPRs per lane, so one 16-wave workgroup fills a CU's waves).
+  pl->prio = pl->lds > kLdsBytes / 2 || pl->gen;
   // QCNN_TABLE_BUILD=valu: the vector-ALU table build, for comparison with
   // the MFMA build (read per call; the strided layouts keep MFMA).
   const char* tb = getenv("QCNN_TABLE_BUILD");
