@@ -49,13 +49,16 @@
 // reads and writes E once (16 N C_t bytes) per batch of B subspaces; the
 // prep and fit kernels move O(C'_s C_t) values each.  The starting residual
 // is fp64 arithmetic, 2 N C_t C_s flops once.
+#include <stdlib.h>
+#include <string.h>
+
 #include "qcnn_internal.h"
 
 namespace qcnn {
 namespace {
 
 constexpr int kEcThreads = 256;      // start / prep kernels
-constexpr int kEcChunk = 16;         // images per thread in the start and pass kernels
+constexpr int kEcChunk = 16;         // images per thread in the pass kernel
 constexpr int kPassCh = 16;          // channels per pass workgroup (16 image chunks each)
 constexpr int kUpdThreads = 256;     // fit / objective kernels (one workgroup)
 
@@ -64,17 +67,18 @@ template <int CSP> constexpr int ec_batch() { return 32 / CSP < 1 ? 1 : (32 / CS
 
 struct EcParams {
   int N, Cs, Ct, M, K, Csp, inner;
-  int nchunks;  // start kernel: image chunks
   int B;        // subspaces per batch
 };
 
 // D64 = codebooks, ct[m][c] = codes[c][m] (codes >= K read as K - 1),
-// Gc[m][d][i][j] = sum_n S[n][m C's + i] S[n][(m - d) C's + j] (0 for m < d).
+// Gc[m][d][i][j] = sum_n S[n][m C's + i] S[n][(m - d) C's + j] (0 for m < d),
+// and the grid barriers' failure flag cleared.
 __global__ __launch_bounds__(kEcThreads) void ec_init_kernel(const float* __restrict__ S, const float* __restrict__ D,
                                                            const uint8_t* __restrict__ codes, EcParams p,
                                                            double* __restrict__ D64, uint8_t* __restrict__ ct,
-                                                           double* __restrict__ Gc) {
+                                                           double* __restrict__ Gc, int* __restrict__ fail) {
   const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (size_t)gridDim.x * blockDim.x;
+  if (tid == 0) *fail = 0;
   const size_t nc = (size_t)p.M * p.Ct, nd = (size_t)p.M * p.K * p.Csp;
   const size_t cc = (size_t)p.Csp * p.Csp, ng = (size_t)p.M * p.B * cc;
   for (size_t i = tid; i < nc; i += stride) {
@@ -110,77 +114,104 @@ __device__ __forceinline__ void ec_block_sum(double v, double* red, double* __re
   }
 }
 
-// The starting residual E = T - sum_m S^(m) W^(m) for a chunk of kEcChunk
-// images and 256 columns (one column per thread, the chunk's E in
-// registers, the subspaces in order), and its block sums of E^2.
+// The starting residual E = T - S W^T, W[c][m C's + a] = D^(m)[k_m(c)][a]
+// (the quantized layer's weights, decoded from the codes), as a float64 GEMM
+// on MFMA (v_mfma_f64_16x16x4_f64), and its block sums of E^2.  A workgroup
+// of 4 waves owns 64 images x 64 channels; wave w the images 16 w .. 16 w +
+// 15 as four 16 x 16 tiles.  The input dimensions go in stages of kStartKB:
+// each thread loads its share of the stage's S values (fp32, widened) and
+// decoded weights (code, then sub-codeword entry) one stage ahead into
+// registers, stores them into one of two LDS buffers, and every wave runs
+// the stage's MFMAs from LDS.  Rows and columns past N, C_t or C_s are 0.
+constexpr int kStartTile = 64;  // images and channels per workgroup
+constexpr int kStartKB = 32;    // input dimensions per stage
+constexpr int kStartLd = kStartKB + 1;  // LDS row stride in doubles (odd: spreads the rows over the banks)
+typedef double d4v __attribute__((ext_vector_type(4)));
+
 template <int CSP>
 __global__ __launch_bounds__(kEcThreads) void ec_start_kernel(const float* __restrict__ S,
                                                             const float* __restrict__ T, EcParams p,
                                                             const double* __restrict__ D64,
                                                             const uint8_t* __restrict__ ct,
                                                             double* __restrict__ E, double* __restrict__ opart) {
+  __shared__ double As[2][kStartTile * kStartLd];  // [image][dim]
+  __shared__ double Bs[2][kStartTile * kStartLd];  // [channel][dim]
   __shared__ double red[kEcThreads / kWave];
-  const int c = blockIdx.x * kEcThreads + threadIdx.x;
-  const int n0 = blockIdx.y * kEcChunk, nn = min(p.N - n0, kEcChunk);
-  const bool col = c < p.Ct;
-  double e[kEcChunk];
+  constexpr int PER = kStartTile * kStartKB / kEcThreads;  // values of each operand per thread and stage (8)
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int c0 = blockIdx.x * kStartTile, n0 = blockIdx.y * kStartTile;
+  // this thread's share of a stage: row r (an image of A, a channel of B),
+  // dimensions q0 .. q0 + PER - 1 of the stage
+  const int r = tid / (kStartKB / PER), q0 = (tid % (kStartKB / PER)) * PER;
+  const int na = n0 + r, cb = c0 + r;
+  const bool rowa = na < p.N, rowb = cb < p.Ct;
+  const int nst = (p.Cs + kStartKB - 1) / kStartKB;
+  float sv[PER];
+  double wv[PER];
+  auto load_stage = [&](int st) {
+    int code[PER];
 #pragma unroll
-  for (int i = 0; i < kEcChunk; ++i) e[i] = col && i < nn ? (double)T[(size_t)(n0 + i) * p.Ct + c] : 0.0;
-  if (col) {
-    // eight subspaces at a time: their codes, then their sub-codewords, are
-    // loaded together (each load waits on the one before it otherwise); the
-    // subtractions still go in subspace order
-    constexpr int U = 8;
-    for (int m0 = 0; m0 < p.M; m0 += U) {
-      int kc[U];
+    for (int i = 0; i < PER; ++i) {
+      const int k = st * kStartKB + q0 + i;
+      const bool okk = k < p.Cs;
+      const float x = S[rowa && okk ? (size_t)na * p.Cs + k : 0];
+      sv[i] = rowa && okk ? x : 0.f;
+      const int m = okk ? k / CSP : 0;
+      const int cd = ct[rowb && okk ? (size_t)m * p.Ct + cb : 0];
+      code[i] = cd;
+    }
 #pragma unroll
-      for (int u = 0; u < U; ++u) kc[u] = ct[(size_t)min(m0 + u, p.M - 1) * p.Ct + c];
-      double dw[U][CSP];
+    for (int i = 0; i < PER; ++i) {
+      const int k = st * kStartKB + q0 + i;
+      const bool ok = rowb && k < p.Cs;
+      const int m = ok ? k / CSP : 0, a = ok ? k % CSP : 0;
+      const double w = D64[((size_t)m * p.K + code[i]) * CSP + a];
+      wv[i] = ok ? w : 0.0;
+    }
+  };
+  auto store_stage = [&](int buf) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const double* w = D64 + ((size_t)min(m0 + u, p.M - 1) * p.K + kc[u]) * CSP;
+    for (int i = 0; i < PER; ++i) {
+      As[buf][r * kStartLd + q0 + i] = (double)sv[i];
+      Bs[buf][r * kStartLd + q0 + i] = wv[i];
+    }
+  };
+  d4v acc[4];
 #pragma unroll
-        for (int j = 0; j < CSP; ++j) dw[u][j] = w[j];
-      }
-      // a full chunk takes the branch-free path (per-image branches would
-      // make each image's scalar loads wait on their own)
-      if (nn == kEcChunk && m0 + U <= p.M) {
+  for (int t = 0; t < 4; ++t) acc[t] = d4v{0.0, 0.0, 0.0, 0.0};
+  const int arow = 16 * wave + (lane & 15), kq = lane >> 4;
+  load_stage(0);
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    store_stage(buf);
+    __syncthreads();  // the stage is in LDS; the other buffer's readers (stage st - 1) are done
+    if (st + 1 < nst) load_stage(st + 1);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+    for (int kk = 0; kk < kStartKB / 4; ++kk) {
+      const double av = As[buf][arow * kStartLd + 4 * kk + kq];
 #pragma unroll
-          for (int i = 0; i < kEcChunk; ++i) {
-            const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)(m0 + u) * CSP;
-            double d = 0.0;
-#pragma unroll
-            for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[u][j];
-            e[i] -= d;
-          }
-        }
-      } else {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int m = m0 + u;
-          if (m < p.M) {
-#pragma unroll
-            for (int i = 0; i < kEcChunk; ++i) {
-              if (i < nn) {
-                const float* srow = S + (size_t)(n0 + i) * p.Cs + (size_t)m * CSP;
-                double d = 0.0;
-#pragma unroll
-                for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[u][j];
-                e[i] -= d;
-              }
-            }
-          }
-        }
+      for (int t = 0; t < 4; ++t) {
+        const double bv = Bs[buf][(16 * t + (lane & 15)) * kStartLd + 4 * kk + kq];
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[t], 0, 0, 0);
       }
     }
   }
+  // acc[t][i]: image n0 + 16 wave + 4 i + lane / 16, channel c0 + 16 t + lane % 16
+  // (the f64 instruction's output layout: register i of lane l holds row
+  // 4 i + l / 16, column l % 16)
   double sq = 0.0;
 #pragma unroll
-  for (int i = 0; i < kEcChunk; ++i) {
-    if (col && i < nn) E[(size_t)(n0 + i) * p.Ct + c] = e[i];
-    sq += e[i] * e[i];
+  for (int t = 0; t < 4; ++t) {
+    const int c = c0 + 16 * t + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int n = n0 + 16 * wave + 4 * i + kq;
+      if (n < p.N && c < p.Ct) {
+        const double e = (double)T[(size_t)n * p.Ct + c] - acc[t][i];
+        E[(size_t)n * p.Ct + c] = e;
+        sq += e * e;
+      }
+    }
   }
   ec_block_sum(sq, red, opart + (size_t)blockIdx.y * gridDim.x + blockIdx.x);
 }
@@ -393,7 +424,8 @@ __global__ __launch_bounds__(kEcThreads) void ec_pass_kernel(const float* __rest
                                                            const double* __restrict__ D64,
                                                            const uint8_t* __restrict__ codes_old,
                                                            const double* __restrict__ dW, int mn0, int Ln,
-                                                           double* __restrict__ X, double* __restrict__ opart) {
+                                                           double* __restrict__ X, double* __restrict__ opart,
+                                                           unsigned* __restrict__ bar) {
   // LDS: X partials [256][B C's], per-thread E^2 sums [B][256], dW [B][16][C's],
   // block-sum scratch, then one area that holds D^(ml) [K][C's] and q [K]
   // for the assignment and afterwards, per round of 256 images, the images'
@@ -414,6 +446,7 @@ __global__ __launch_bounds__(kEcThreads) void ec_pass_kernel(const float* __rest
   const int c = blockIdx.x * kPassCh + cl;
   const bool col = c < p.Ct;
   const int cc = col ? c : p.Ct - 1;  // a valid column for loads whose value is not used
+  if (blockIdx.x == 0 && tid == 0) *bar = 0;  // for the steps kernel that follows
   for (int i = tid; i < kEcThreads * BC; i += kEcThreads) xr[i] = 0.0;
   for (int i = tid; i < B * kEcThreads; i += kEcThreads) osq[i] = 0.0;
   if (Lp > 0) {
@@ -571,17 +604,14 @@ template <int CSP> size_t prep_lds_bytes(int K) {
 // sharing a code find their rank with ballots; codes x waves give each
 // channel its place, and one thread per (k, j) adds its run in order.
 template <int CSP, int B>
-__global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0, int j, int it, int fm,
-                                                           const double* __restrict__ Din,
-                                                           const double* __restrict__ bins_in,
-                                                           const int* __restrict__ nbin_in, int nblk,
-                                                           double* __restrict__ Dout, const double* __restrict__ X,
-                                                           const double* __restrict__ Gc,
-                                                           const double* __restrict__ D64, uint8_t* __restrict__ ct,
-                                                           double* __restrict__ P, double* __restrict__ dW,
-                                                           uint8_t* __restrict__ codes_old,
-                                                           double* __restrict__ bins, int* __restrict__ nbin) {
-  extern __shared__ double sp[];
+__device__ __forceinline__ void ec_prep_step(const EcParams& p, int m0, int j, int it, int fm,
+                                             const double* __restrict__ Din, const double* __restrict__ bins_in,
+                                             const int* __restrict__ nbin_in, int nblk, double* __restrict__ Dout,
+                                             const double* __restrict__ X, const double* __restrict__ Gc,
+                                             const double* __restrict__ D64, uint8_t* __restrict__ ct,
+                                             double* __restrict__ P, double* __restrict__ dW,
+                                             uint8_t* __restrict__ codes_old, double* __restrict__ bins,
+                                             int* __restrict__ nbin, double* sp) {
   const FitLds f = fit_lds<CSP>(sp, p.K);
   double* Ps = reinterpret_cast<double*>(reinterpret_cast<char*>(sp) + fit_lds_bytes<CSP>(p.K));  // [256][C's]
   int* cnt = reinterpret_cast<int*>(Ps + (size_t)kEcThreads * CSP);  // [waves][K]
@@ -724,6 +754,124 @@ __global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0,
   for (int kk = tid; kk < p.K; kk += kEcThreads) nbin[(size_t)blockIdx.x * p.K + kk] = tot[kk];
 }
 
+template <int CSP, int B>
+__global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0, int j, int it, int fm,
+                                                           const double* __restrict__ Din,
+                                                           const double* __restrict__ bins_in,
+                                                           const int* __restrict__ nbin_in, int nblk,
+                                                           double* __restrict__ Dout, const double* __restrict__ X,
+                                                           const double* __restrict__ Gc,
+                                                           const double* __restrict__ D64, uint8_t* __restrict__ ct,
+                                                           double* __restrict__ P, double* __restrict__ dW,
+                                                           uint8_t* __restrict__ codes_old,
+                                                           double* __restrict__ bins, int* __restrict__ nbin) {
+  extern __shared__ double sp[];
+  ec_prep_step<CSP, B>(p, m0, j, it, fm, Din, bins_in, nbin_in, nblk, Dout, X, Gc, D64, ct, P, dW, codes_old, bins,
+                       nbin, sp);
+}
+
+// Buffers of a batch's steps (the workspace slices of launch_ec_csp).
+struct EcSteps {
+  const double* X;
+  const double* Gc;
+  double* D64;
+  uint8_t* ct;
+  double* P;
+  double* dW;
+  uint8_t* codes_old;
+  double* bins;       // [2][blocks][K][C's]
+  int* nbin;          // [2][blocks][K]
+  double* Dnew;       // [B][K][C's]: each step's last fit
+  double* Dpp;        // [2][K][C's]: the fits of the inner rounds before the last
+  double* qv;         // [K]: q of the batch's last fit
+  unsigned* bar;      // arrival count of the grid barriers (0 at launch)
+  int* fail;          // set when a barrier gives up waiting
+};
+
+// Polls of a grid barrier before it gives up (each a memory round trip and
+// ~64 clocks of sleep: about a second, against microseconds when every
+// workgroup is resident).
+constexpr int kBarrierPolls = 1 << 20;
+
+// Every workgroup of the grid arrives here before any leaves: the writes
+// before it (global memory, every thread) are visible after it to every
+// workgroup.  Arrivals count up on *bar; `target` is the count once every
+// workgroup has arrived at this barrier.  Requires every workgroup of the
+// grid to be resident (a cooperative launch).  The wait is bounded: after
+// kBarrierPolls polls the workgroup sets *fail and goes on, and once *fail
+// is set a barrier gives up within 256 polls.
+__device__ __forceinline__ void grid_barrier(unsigned* bar, unsigned target, int* fail) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int polls = 0; __hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target; ++polls) {
+      if (polls >= kBarrierPolls) {
+        __hip_atomic_store(fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      if ((polls & 255) == 255 && __hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Every step of a batch (subspaces m0 .. m0 + L - 1, `inner` rounds each) in
+// one launch, one workgroup per block of 256 channels as ec_prep_kernel,
+// the steps separated by grid barriers instead of kernel boundaries; then
+// workgroup 0 makes the batch's last fit (Dnew[L - 1] and q, as
+// ec_fit_kernel).  The step sequence, its inputs and outputs and every sum's
+// order are those of the per-step kernels, so the results are the same bit
+// for bit.  sel0: the bins buffer the step before the batch wrote.
+template <int CSP, int B>
+__global__ __launch_bounds__(kEcThreads) void ec_steps_kernel(EcParams p, int m0, int L, int sel0, EcSteps b) {
+  extern __shared__ double sp[];
+  const int kc = p.K * CSP, nblk = gridDim.x;
+  auto bins_at = [&](int sel) { return b.bins + (size_t)sel * nblk * kc; };
+  auto nbin_at = [&](int sel) { return b.nbin + (size_t)sel * nblk * p.K; };
+  auto fit_in = [&](int m, int r) -> const double* {
+    return r == 0 ? b.D64 + (size_t)m * kc : b.Dpp + (size_t)((r - 1) % 2) * kc;
+  };
+  auto fit_out = [&](int jj, int r) -> double* {
+    return r == p.inner - 1 ? b.Dnew + (size_t)jj * kc : b.Dpp + (size_t)(r % 2) * kc;
+  };
+  int sel = sel0;
+  unsigned target = 0;
+  for (int j = 0; j < L; ++j) {
+    for (int it = 0; it < p.inner; ++it) {
+      int fm = -1, fj = 0, fr = 0;  // the fit this step waits for, as in the per-step launches
+      if (it > 0) {
+        fm = m0 + j;
+        fj = j;
+        fr = it - 1;
+      } else if (j > 0) {
+        fm = m0 + j - 1;
+        fj = j - 1;
+        fr = p.inner - 1;
+      }
+      if (fm >= 0) {  // the previous step's bins (and fit) from every workgroup
+        target += (unsigned)nblk;
+        grid_barrier(b.bar, target, b.fail);
+      }
+      ec_prep_step<CSP, B>(p, m0, j, it, fm, fm >= 0 ? fit_in(fm, fr) : b.D64, bins_at(sel), nbin_at(sel), nblk,
+                           fm >= 0 ? fit_out(fj, fr) : b.Dpp, b.X, b.Gc, b.D64, b.ct, b.P, b.dW, b.codes_old,
+                           bins_at(sel ^ 1), nbin_at(sel ^ 1), sp);
+      sel ^= 1;
+    }
+  }
+  target += (unsigned)nblk;
+  grid_barrier(b.bar, target, b.fail);
+  if (blockIdx.x != 0) return;
+  const int ml = m0 + L - 1;
+  const FitLds f = fit_lds<CSP>(sp, p.K);
+  ec_fit_wg<CSP>(bins_at(sel), nbin_at(sel), nblk, p, ml, b.Gc, fit_in(ml, p.inner - 1), f);
+  double* dout = fit_out(L - 1, p.inner - 1);
+  for (int i = threadIdx.x; i < kc; i += kEcThreads) dout[i] = f.Ds[i];
+  for (int k = threadIdx.x; k < p.K; k += kEcThreads) b.qv[k] = f.qs[k];
+}
+
 // After a batch's pass: D64[mp0 + i] = Dnew[i] for i < Lp (the batch's final
 // sub-codebooks), and objective[s] = the sum over the blocks of
 // opart[s][block] for s < rows <= 16, in a fixed order: 16 threads per row
@@ -756,13 +904,16 @@ __global__ __launch_bounds__(kUpdThreads) void ec_commit_kernel(const double* __
   if (t == 0 && s < rows) objective[s] = red[tid];
 }
 
-// codebooks = fp32(D64), codes[c][m] = ct[m][c].
+// codebooks = fp32(D64) (all NaN if a grid barrier of the call gave up
+// waiting), codes[c][m] = ct[m][c].
 __global__ __launch_bounds__(kEcThreads) void ec_finish_kernel(const double* __restrict__ D64, EcParams p,
                                                              const uint8_t* __restrict__ ct,
+                                                             const int* __restrict__ fail,
                                                              float* __restrict__ D, uint8_t* __restrict__ codes) {
   const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (size_t)gridDim.x * blockDim.x;
   const size_t nd = (size_t)p.M * p.K * p.Csp, nc = (size_t)p.M * p.Ct;
-  for (size_t i = tid; i < nd; i += stride) D[i] = (float)D64[i];
+  const bool bad = *fail != 0;  // a grid barrier gave up: the results are not the method's
+  for (size_t i = tid; i < nd; i += stride) D[i] = bad ? __builtin_nanf("") : (float)D64[i];
   for (size_t i = tid; i < nc; i += stride) codes[i] = ct[(i % p.M) * p.Ct + i / p.M];
 }
 
@@ -773,14 +924,16 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
                          uint8_t* codes, int sweeps, int inner, double* objective, hipStream_t stream) {
   constexpr int Csp = CSP;
   constexpr int B = ec_batch<CSP>();
-  EcParams p{N, Cs, Ct, M, K, Csp, inner, ceil_div(N, kEcChunk), B};
-  const int cblocks = ceil_div(Ct, kEcThreads);     // start (columns) and prep (channel blocks)
+  EcParams p{N, Cs, Ct, M, K, Csp, inner, B};
+  const int cblocks = ceil_div(Ct, kEcThreads);     // prep workgroups (channel blocks)
   const int pblocks = ceil_div(Ct, kPassCh);        // pass workgroups
-  const int nstart = cblocks * p.nchunks;           // start kernel's block sums
+  const int sblocks_c = ceil_div(Ct, kStartTile), sblocks_n = ceil_div(N, kStartTile);
+  const int nstart = sblocks_c * sblocks_n;         // start kernel's block sums
   const int kc = K * Csp;
   auto pass = ec_pass_kernel<CSP, B>;
   auto prep = ec_prep_kernel<CSP, B>;
   auto fit = ec_fit_kernel<CSP>;
+  auto steps = ec_steps_kernel<CSP, B>;
   const size_t pass_lds = pass_lds_bytes<CSP, B>(K);
   const size_t prep_lds = prep_lds_bytes<CSP>(K);
   const size_t fit_lds = fit_lds_bytes<CSP>(K);
@@ -789,6 +942,24 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   if ((e = allow_max_lds((const void*)pass)) != hipSuccess) return e;
   if ((e = allow_max_lds((const void*)prep)) != hipSuccess) return e;
   if ((e = allow_max_lds((const void*)fit)) != hipSuccess) return e;
+  if ((e = allow_max_lds((const void*)steps)) != hipSuccess) return e;
+  // QCNN_EC_STEPS=batch (read per call): a batch's steps in one cooperative
+  // launch with grid barriers between them, where the device supports it and
+  // every channel block's workgroup can be resident at once.  Not the
+  // default: on the fc6 shape a step then takes ~16 us of the kernel against
+  // 12.7 us for a prep kernel of its own (a barrier's fences and memory-side
+  // atomics across the XCDs cost more than a kernel boundary).
+  bool coop = false;
+  {
+    const char* env = getenv("QCNN_EC_STEPS");
+    int dev = 0, attr = 0, cus = 0, per_cu = 0;
+    if (env && strcmp(env, "batch") == 0 && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&attr, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess && attr &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)steps, kEcThreads, prep_lds) ==
+            hipSuccess)
+      coop = (long long)per_cu * cus >= cblocks;
+  }
   // workspace slices, each rounded up to 256 bytes
   const size_t sizes[] = {
       (size_t)N * Ct * 8,                                  // E
@@ -805,6 +976,8 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
       (size_t)2 * cblocks * K * 4,                         // nbin (two buffers)
       (size_t)B * Ct,                                      // codes_old
       (size_t)M * Ct,                                      // codes, [M][C_t]
+      sizeof(unsigned),                                    // grid barrier arrivals
+      sizeof(int),                                         // grid barrier failure flag
   };
   size_t total = 0;
   for (size_t b : sizes) total += (b + 255) & ~(size_t)255;
@@ -831,15 +1004,17 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   int* nbin = reinterpret_cast<int*>(take());
   uint8_t* codes_old = reinterpret_cast<uint8_t*>(take());
   uint8_t* ct = reinterpret_cast<uint8_t*>(take());
+  unsigned* bar = reinterpret_cast<unsigned*>(take());
+  int* fail = reinterpret_cast<int*>(take());
   auto bins_at = [&](int sel) { return bins + (size_t)sel * cblocks * kc; };
   auto nbin_at = [&](int sel) { return nbin + (size_t)sel * cblocks * K; };
 
   const size_t ninit = std::max<size_t>({(size_t)M * Ct, (size_t)M * kc, (size_t)M * B * Csp * Csp});
   const unsigned iblocks = (unsigned)std::min<size_t>(8192, ceil_div_z(ninit, kEcThreads));
   hipLaunchKernelGGL(ec_init_kernel, dim3(iblocks), dim3(kEcThreads), 0, stream, S, D, (const uint8_t*)codes, p,
-                     D64, ct, Gc);
+                     D64, ct, Gc, fail);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(ec_start_kernel<CSP>, dim3((unsigned)cblocks, (unsigned)p.nchunks), dim3(kEcThreads), 0,
+  hipLaunchKernelGGL(ec_start_kernel<CSP>, dim3((unsigned)sblocks_c, (unsigned)sblocks_n), dim3(kEcThreads), 0,
                      stream, S, T, p, (const double*)D64, (const uint8_t*)ct, E, opart);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (objective) {
@@ -861,7 +1036,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   int mp0 = -1, Lp = 0;   // the previous batch (fitted but for its last round, updates not yet in E)
   auto close_and_pass = [&](int mn0, int Ln) -> hipError_t {
     hipError_t r;
-    if (Lp > 0) {  // the last fit of the previous batch
+    if (Lp > 0 && !coop) {  // the last fit of the previous batch (the steps kernel made it)
       const int ml = mp0 + Lp - 1;
       hipLaunchKernelGGL(fit, dim3(1), dim3(kUpdThreads), fit_lds, stream, (const double*)bins_at(sel),
                          (const int*)nbin_at(sel), cblocks, p, ml, (const double*)Gc, fit_in(ml, inner - 1),
@@ -871,7 +1046,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
     hipLaunchKernelGGL(pass, dim3((unsigned)pblocks), dim3(kEcThreads), pass_lds, stream, S, p, E, mp0, Lp,
                        (const double*)P, (const double*)(Dnew + (size_t)(Lp > 0 ? Lp - 1 : 0) * kc),
                        (const double*)qv, ct, (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0,
-                       Ln, X, opart);
+                       Ln, X, opart, bar);
     if ((r = hipGetLastError()) != hipSuccess) return r;
     if (Lp > 0) {
       hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream, (const double*)opart, pblocks, Lp,
@@ -885,6 +1060,18 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
     for (int m0 = 0; m0 < M; m0 += B) {
       const int L = std::min(B, M - m0);
       if ((e = close_and_pass(m0, L)) != hipSuccess) return e;
+      if (coop) {
+        EcSteps sb{X, Gc, D64, ct, P, dW, codes_old, bins, nbin, Dnew, Dpp, qv, bar, fail};
+        int a_m0 = m0, a_L = L, a_sel = sel;
+        void* args[] = {&p, &a_m0, &a_L, &a_sel, &sb};
+        if ((e = hipLaunchCooperativeKernel((const void*)steps, dim3((unsigned)cblocks), dim3(kEcThreads), args,
+                                            (unsigned)prep_lds, stream)) != hipSuccess)
+          return e;
+        sel ^= (L * inner) & 1;
+        mp0 = m0;
+        Lp = L;
+        continue;
+      }
       for (int j = 0; j < L; ++j) {
         for (int it = 0; it < inner; ++it) {
           // the fit this step waits for: the last round of m - 1, or round it - 1 of m
@@ -914,7 +1101,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   }
   if (Lp > 0 && (e = close_and_pass(-1, 0)) != hipSuccess) return e;  // finish the last batch
   hipLaunchKernelGGL(ec_finish_kernel, dim3(iblocks), dim3(kEcThreads), 0, stream, (const double*)D64, p,
-                     (const uint8_t*)ct, D, codes);
+                     (const uint8_t*)ct, (const int*)fail, D, codes);
   return hipGetLastError();
 }
 

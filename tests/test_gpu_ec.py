@@ -165,3 +165,35 @@ def test_ec_full_size_first_steps(api, dev):
         assert np.array_equal(c[:, m], cr[:, m]), m
         assert np.allclose(D[m], Dr[m], rtol=1e-6, atol=1e-7 * float(np.abs(Dr[m]).max())), m
     assert np.allclose(obj[:4], hist, rtol=1e-9), (obj[:4], hist)
+
+
+# (N, C_s, C_t, C'_s, K, sweeps, inner): inner rounds, several channel blocks
+# (grid barriers over 1 to 16 workgroups), batches of 16 down to 2, a ragged
+# last batch, and the fc6 shape at full size
+STEP_CASES = [
+    (64, 48, 40, 4, 8, 2, 2),
+    (37, 30, 50, 3, 5, 1, 3),
+    (40, 48, 600, 12, 32, 2, 2),
+    (120, 200, 1000, 8, 16, 1, 1),
+    (50, 26, 300, 1, 2, 1, 2),
+    (256, 9216, 4096, 4, 32, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", STEP_CASES, ids=[str(c) for c in STEP_CASES])
+def test_ec_batch_launch_equals_step_launches(api, dev, case, monkeypatch):
+    """A batch's steps in one cooperative launch (grid barriers between the
+    steps, QCNN_EC_STEPS=batch) against one launch per step (the default):
+    the same steps in the same order with every sum in the same order, so
+    codebooks, codes and the objective history are equal bit for bit."""
+    N, Cs, Ct, Csp, K, sweeps, inner = case
+    rng = np.random.Generator(np.random.PCG64(sum(case)))
+    S, T, D0, c0 = problem(rng, N, Cs, Ct, Csp, K)
+    print("ec batch launch", case, flush=True)
+    D2, c2, o2 = run_gpu(api, dev, S, T, D0, c0, sweeps, inner)
+    monkeypatch.setenv("QCNN_EC_STEPS", "batch")
+    D1, c1, o1 = run_gpu(api, dev, S, T, D0, c0, sweeps, inner)
+    assert not np.isnan(D1).any()
+    assert np.array_equal(c1, c2), int((c1 != c2).sum())
+    assert np.array_equal(D1.view(np.uint32), D2.view(np.uint32))
+    assert np.array_equal(o1.view(np.uint64), o2.view(np.uint64))
