@@ -212,9 +212,10 @@ __global__ __launch_bounds__(kQThreads) void pq_total_kernel(const double* __res
 
 // Update of one subspace per workgroup.  Sub-vectors are taken in chunks:
 // the chunk's sub-vectors and codes are staged in LDS, a stable counting sort
-// by code lists every sub-codeword's members in sub-vector order, and thread
-// k then adds its members in that order (float64), continuing its sums from
-// the previous chunk.  The stable order comes from wave ballots: the lanes
+// by code lists every sub-codeword's members in sub-vector order, and one
+// thread per (sub-codeword k, coordinate j) then adds coordinate j of k's
+// members in that order (float64, eight members' reads in flight),
+// continuing its sum from the previous chunk.  The stable order comes from wave ballots: the lanes
 // holding the same code are found bit by bit, a lane's rank is the number of
 // such lanes below it, earlier waves of the same round and earlier rounds
 // add their counts.
@@ -237,10 +238,16 @@ __global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __res
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int csp = CSP > 0 ? CSP : q.Csp;
   const int chunk = kChunkFloats / csp;
+  // Thread tid owns the pairs (k, j) = pair tid + kQThreads u, pair = k C'_s + j
+  // (at most NJ of them: K <= 256).
   double sum[NJ];
+  int total[NJ];  // members of the pair's sub-codeword over all chunks
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) sum[j] = 0.0;
-  int total = 0;  // members of sub-codeword tid over all chunks (tid < K)
+  for (int u = 0; u < NJ; ++u) {
+    sum[u] = 0.0;
+    total[u] = 0;
+  }
+  const int npairs = q.K * csp;
   for (int base = 0; base < q.n; base += chunk) {
     const int len = min(chunk, q.n - base);
     __syncthreads();  // the previous chunk is done
@@ -316,25 +323,38 @@ __global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __res
       }
       __syncthreads();
     }
-    if (tid < q.K) {
-      const int s0 = start[tid], n_k = cnt[tid];
-      for (int r = 0; r < n_k; ++r) {
-        const float* v = sv + perm[s0 + r] * csp;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j)
-          if (j < csp) sum[j] += (double)v[j];
+    for (int u = 0; u < NJ; ++u) {
+      const int pr = tid + u * kQThreads;
+      if (pr < npairs) {
+        const int k = pr / csp, j = pr - k * csp;
+        const int s0 = start[k], n_k = cnt[k];
+        double acc = sum[u];
+        int r = 0;
+        for (; r + 8 <= n_k; r += 8) {  // the members' reads first, then the adds in order
+          int pi[8];
+          float v[8];
+#pragma unroll
+          for (int x = 0; x < 8; ++x) pi[x] = perm[s0 + r + x];
+#pragma unroll
+          for (int x = 0; x < 8; ++x) v[x] = sv[pi[x] * csp + j];
+#pragma unroll
+          for (int x = 0; x < 8; ++x) acc += (double)v[x];
+        }
+        for (; r < n_k; ++r) acc += (double)sv[perm[s0 + r] * csp + j];
+        sum[u] = acc;
+        total[u] += n_k;
       }
-      total += n_k;
     }
   }
-  if (tid < q.K) {
-    float* dst = D + ((size_t)m * q.K + tid) * csp;
-    if (total) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        if (j < csp) dst[j] = (float)(sum[j] / (double)total);
+  for (int u = 0; u < NJ; ++u) {
+    const int pr = tid + u * kQThreads;
+    if (pr < npairs) {
+      const int k = pr / csp, j = pr - k * csp;
+      if (total[u]) D[((size_t)m * q.K + k) * csp + j] = (float)(sum[u] / (double)total[u]);
+      if (counts && j == 0) counts[(size_t)m * q.K + k] = total[u];
     }
-    if (counts) counts[(size_t)m * q.K + tid] = total;
   }
 }
 
