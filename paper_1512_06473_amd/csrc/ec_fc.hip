@@ -581,6 +581,49 @@ template <int CSP, int B> size_t pass_lds_bytes(int K) {
   return fixed + std::max(table, stage);
 }
 
+// After a batch's pass: D64[mp0 + i] = Dnew[i] for i < Lp (the batch's final
+// sub-codebooks), and objective[s] = the sum over the blocks of
+// opart[s][block] for s < rows <= 16, in a fixed order: 16 threads per row
+// each add a strided share of the blocks in order, then a fixed tree over
+// the 16.  One workgroup of kUpdThreads threads; red: kUpdThreads doubles of
+// LDS.
+struct EcCommit {
+  const double* opart;
+  int nblk, rows;
+  double* objective;  // null: the sub-codebooks only
+  const double* Dnew;
+  double* D64;
+  int mp0, Lp, kc;
+};
+
+__device__ void ec_commit_wg(const EcCommit& c, double* red) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < c.Lp * c.kc; i += kUpdThreads) c.D64[(size_t)c.mp0 * c.kc + i] = c.Dnew[i];
+  if (!c.objective) return;  // uniform
+  const int s = tid / 16, t = tid % 16;
+  double v = 0.0;
+  if (s < c.rows)
+    for (int b0 = t; b0 < c.nblk; b0 += 16 * 16) {  // 16 loads in flight, added in order
+      double x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = b0 + 16 * u < c.nblk ? c.opart[(size_t)s * c.nblk + b0 + 16 * u] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v += x[u];
+    }
+  red[tid] = v;
+  __syncthreads();
+  for (int h = 8; h > 0; h >>= 1) {
+    if (t < h) red[tid] += red[tid + h];
+    __syncthreads();
+  }
+  if (t == 0 && s < c.rows) c.objective[s] = red[tid];
+}
+
+__global__ __launch_bounds__(kUpdThreads) void ec_commit_kernel(EcCommit c) {
+  __shared__ double red[kUpdThreads];
+  ec_commit_wg(c, red);
+}
+
 // LDS of the prep kernel: a fit, then P of the block in sorted order and
 // the counting sort's counts and offsets.
 template <int CSP> size_t prep_lds_bytes(int K) {
@@ -703,15 +746,20 @@ __device__ __forceinline__ void ec_prep_step(const EcParams& p, int m0, int j, i
   // ---- counting sort of the block's channels by code
   for (int i = lane; i < p.K; i += kWave) cnt[wave * p.K + i] = 0;
   // (each wave clears and fills only its own row of counts)
+  // the lanes holding this lane's code: matched bit by bit over the code's
+  // bits, one ballot per bit
   int rank = 0;
-  uint64_t todo = __ballot(col);
-  while (todo) {
-    const int leader = __ffsll((unsigned long long)todo) - 1;
-    const int kk = __builtin_amdgcn_readlane(k, leader);
-    const uint64_t same = __ballot(col && k == kk);
-    if (col && k == kk) rank = __popcll(same & ((1ull << lane) - 1ull));
-    if (lane == leader) cnt[wave * p.K + kk] = __popcll(same);
-    todo &= ~same;
+  {
+    uint64_t same = __ballot(col);
+    for (int bit = 0; (1 << bit) < p.K; ++bit) {
+      const bool one = ((k >> bit) & 1) != 0;
+      const uint64_t ones = __ballot(col && one);
+      same &= one ? ones : ~ones;
+    }
+    if (col) {
+      rank = __popcll(same & ((1ull << lane) - 1ull));
+      if (rank == 0) cnt[wave * p.K + k] = __popcll(same);  // the code's lowest lane
+    }
   }
   __syncthreads();
   for (int kk = tid; kk < p.K; kk += kEcThreads) {
@@ -747,8 +795,18 @@ __device__ __forceinline__ void ec_prep_step(const EcParams& p, int m0, int j, i
   __syncthreads();
   for (int t = tid; t < p.K * CSP; t += kEcThreads) {
     const int kk = t / CSP, a = t % CSP;
+    const int n = tot[kk];
+    const double* run = Ps + (size_t)base[kk] * CSP + a;
     double s = 0.0;
-    for (int i = 0; i < tot[kk]; ++i) s += Ps[(size_t)(base[kk] + i) * CSP + a];
+    int i = 0;
+    for (; i + 8 <= n; i += 8) {  // eight reads in flight, added in order
+      double v[8];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) v[x] = run[(size_t)(i + x) * CSP];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) s += v[x];
+    }
+    for (; i < n; ++i) s += run[(size_t)i * CSP];
     bins[((size_t)blockIdx.x * p.K + kk) * CSP + a] = s;
   }
   for (int kk = tid; kk < p.K; kk += kEcThreads) nbin[(size_t)blockIdx.x * p.K + kk] = tot[kk];
@@ -764,8 +822,13 @@ __global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0,
                                                            const double* __restrict__ D64, uint8_t* __restrict__ ct,
                                                            double* __restrict__ P, double* __restrict__ dW,
                                                            uint8_t* __restrict__ codes_old,
-                                                           double* __restrict__ bins, int* __restrict__ nbin) {
+                                                           double* __restrict__ bins, int* __restrict__ nbin,
+                                                           EcCommit cm) {
   extern __shared__ double sp[];
+  if ((int)blockIdx.x >= nblk) {  // the workgroup past the channel blocks: the previous batch's commit
+    ec_commit_wg(cm, sp);
+    return;
+  }
   ec_prep_step<CSP, B>(p, m0, j, it, fm, Din, bins_in, nbin_in, nblk, Dout, X, Gc, D64, ct, P, dW, codes_old, bins,
                        nbin, sp);
 }
@@ -870,38 +933,6 @@ __global__ __launch_bounds__(kEcThreads) void ec_steps_kernel(EcParams p, int m0
   double* dout = fit_out(L - 1, p.inner - 1);
   for (int i = threadIdx.x; i < kc; i += kEcThreads) dout[i] = f.Ds[i];
   for (int k = threadIdx.x; k < p.K; k += kEcThreads) b.qv[k] = f.qs[k];
-}
-
-// After a batch's pass: D64[mp0 + i] = Dnew[i] for i < Lp (the batch's final
-// sub-codebooks), and objective[s] = the sum over the blocks of
-// opart[s][block] for s < rows <= 16, in a fixed order: 16 threads per row
-// each add a strided share of the blocks in order, then a fixed tree over
-// the 16.  One workgroup.
-__global__ __launch_bounds__(kUpdThreads) void ec_commit_kernel(const double* __restrict__ opart, int nblk,
-                                                              int rows, double* __restrict__ objective,
-                                                              const double* __restrict__ Dnew,
-                                                              double* __restrict__ D64, int mp0, int Lp, int kc) {
-  __shared__ double red[kUpdThreads];
-  const int tid = threadIdx.x;
-  for (int i = tid; i < Lp * kc; i += kUpdThreads) D64[(size_t)mp0 * kc + i] = Dnew[i];
-  if (!objective) return;  // uniform
-  const int s = tid / 16, t = tid % 16;
-  double v = 0.0;
-  if (s < rows)
-    for (int b0 = t; b0 < nblk; b0 += 16 * 16) {  // 16 loads in flight, added in order
-      double x[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) x[u] = b0 + 16 * u < nblk ? opart[(size_t)s * nblk + b0 + 16 * u] : 0.0;
-#pragma unroll
-      for (int u = 0; u < 16; ++u) v += x[u];
-    }
-  red[tid] = v;
-  __syncthreads();
-  for (int h = 8; h > 0; h >>= 1) {
-    if (t < h) red[tid] += red[tid + h];
-    __syncthreads();
-  }
-  if (t == 0 && s < rows) objective[s] = red[tid];
 }
 
 // codebooks = fp32(D64) (all NaN if a grid barrier of the call gave up
@@ -1018,8 +1049,8 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
                      stream, S, T, p, (const double*)D64, (const uint8_t*)ct, E, opart);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (objective) {
-    hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream, (const double*)opart, nstart, 1,
-                       objective, (const double*)Dnew, D64, 0, 0, kc);
+    hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream,
+                       EcCommit{opart, nstart, 1, objective, Dnew, D64, 0, 0, kc});
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   // Input of the fit of round r of subspace m: D64[m] for r = 0, else the
@@ -1034,6 +1065,18 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   int sel = 0;            // bins buffer the last prep kernel wrote
   int nstep = 0;          // subspace steps whose objective is recorded
   int mp0 = -1, Lp = 0;   // the previous batch (fitted but for its last round, updates not yet in E)
+  // The previous batch's commit after its pass: run by an extra workgroup of
+  // the next batch's first prep kernel (it touches only that batch's rows of
+  // D64 and the pass's block sums, which no prep kernel reads), else by a
+  // kernel of its own (after the last pass, and with the batch launches).
+  EcCommit pending{};
+  bool has_pending = false;
+  auto launch_pending = [&]() -> hipError_t {
+    if (!has_pending) return hipSuccess;
+    has_pending = false;
+    hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream, pending);
+    return hipGetLastError();
+  };
   auto close_and_pass = [&](int mn0, int Ln) -> hipError_t {
     hipError_t r;
     if (Lp > 0 && !coop) {  // the last fit of the previous batch (the steps kernel made it)
@@ -1049,9 +1092,9 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
                        Ln, X, opart, bar);
     if ((r = hipGetLastError()) != hipSuccess) return r;
     if (Lp > 0) {
-      hipLaunchKernelGGL(ec_commit_kernel, dim3(1), dim3(kUpdThreads), 0, stream, (const double*)opart, pblocks, Lp,
-                         objective ? objective + 1 + nstep : nullptr, (const double*)Dnew, D64, mp0, Lp, kc);
-      if ((r = hipGetLastError()) != hipSuccess) return r;
+      pending = EcCommit{opart, pblocks, Lp, objective ? objective + 1 + nstep : nullptr, Dnew, D64, mp0, Lp, kc};
+      has_pending = true;
+      if ((coop || Ln == 0) && (r = launch_pending()) != hipSuccess) return r;
     }
     nstep += Lp;
     return hipSuccess;
@@ -1087,11 +1130,13 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
           }
           const double* din = fm >= 0 ? fit_in(fm, fr) : D64;
           double* dout = fm >= 0 ? fit_out(fj, fr) : Dpp;
-          hipLaunchKernelGGL(prep, dim3((unsigned)cblocks), dim3(kEcThreads), prep_lds, stream, p, m0, j, it, fm, din,
-                             (const double*)bins_at(sel), (const int*)nbin_at(sel), cblocks, dout, (const double*)X,
-                             (const double*)Gc, (const double*)D64, ct, P, dW, codes_old, bins_at(sel ^ 1),
-                             nbin_at(sel ^ 1));
+          const bool with_commit = has_pending;  // the batch's first step
+          hipLaunchKernelGGL(prep, dim3((unsigned)(cblocks + (with_commit ? 1 : 0))), dim3(kEcThreads), prep_lds,
+                             stream, p, m0, j, it, fm, din, (const double*)bins_at(sel), (const int*)nbin_at(sel),
+                             cblocks, dout, (const double*)X, (const double*)Gc, (const double*)D64, ct, P, dW,
+                             codes_old, bins_at(sel ^ 1), nbin_at(sel ^ 1), pending);
           if ((e = hipGetLastError()) != hipSuccess) return e;
+          has_pending = false;
           sel ^= 1;
         }
       }
