@@ -58,8 +58,9 @@ namespace qcnn {
 namespace {
 
 constexpr int kEcThreads = 256;      // start / prep kernels
-constexpr int kEcChunk = 16;         // images per thread in the pass kernel
-constexpr int kPassCh = 16;          // channels per pass workgroup (16 image chunks each)
+constexpr int kPassThreads = 512;    // pass kernel
+constexpr int kPassChunk = 8;        // images per thread in the pass kernel
+constexpr int kPassCh = 16;          // channels per pass workgroup (32 image chunks each)
 constexpr int kUpdThreads = 256;     // fit / objective kernels (one workgroup)
 
 // Subspaces per batch: the pass keeps B x C'_s accumulators per thread.
@@ -398,10 +399,10 @@ __global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __res
   for (int k = threadIdx.x; k < p.K; k += kUpdThreads) qv[k] = f.qs[k];
 }
 
-// One pass over E for kPassCh channels and every image (16 chunks of
-// kEcChunk images per round of 256), between the batch of Lp subspaces
-// starting at mp0 (all fitted; Lp = 0: none) and the batch of Ln subspaces
-// starting at mn0 (Ln = 0: none):
+// One pass over E for kPassCh channels and every image (kPassThreads /
+// kPassCh chunks of kPassChunk images per round of 256), between the batch of
+// Lp subspaces starting at mp0 (all fitted; Lp = 0: none) and the batch of
+// Ln subspaces starting at mn0 (Ln = 0: none):
 //   assign:  the last subspace of the previous batch, ml = mp0 + Lp - 1, by
 //            Eq. (12) from P (still that subspace's), its new D (Dlast) and
 //            q; the chunk-0 threads store the codes;
@@ -409,56 +410,65 @@ __global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __res
 //            dW_i[j][c] (dW_i = D_new[k_new] - D_old[k_old] of step i: from
 //            the prep kernels, the last one here), with the block sum of E^2
 //            after each into opart[i][block];
-//   collect: X[j][a][c] = sum_n S[n][(mn0+j) C's + a] E[n][c] for j < Ln
-//            (per chunk, then the chunks in order).
+//   collect: X[j][a][c] = sum_n S[n][(mn0+j) C's + a] E[n][c] for j < Ln.
 // Per round the images' S columns of both batches are staged in LDS; the
 // chunk's E is loaded into registers (all loads in flight) before any of it
-// is written.  dW, the per-thread sums of E^2 and the X partials live in
-// LDS, so the registers hold little more than the chunk of E.
+// is written.  Each thread keeps its sums of E^2 (one per step) and its X
+// partials (B C's of them) in registers; at the end the four chunks of a
+// wave are added by shuffles, then the waves in order through LDS (a fixed
+// order throughout).  Eight waves per workgroup and ~71 KB of LDS, so that
+// two waves share each SIMD.
 template <int CSP, int B>
-__global__ __launch_bounds__(kEcThreads) void ec_pass_kernel(const float* __restrict__ S, EcParams p,
-                                                           double* __restrict__ E, int mp0, int Lp,
-                                                           const double* __restrict__ P,
-                                                           const double* __restrict__ Dlast,
-                                                           const double* __restrict__ qv, uint8_t* __restrict__ ct,
-                                                           const double* __restrict__ D64,
-                                                           const uint8_t* __restrict__ codes_old,
-                                                           const double* __restrict__ dW, int mn0, int Ln,
-                                                           double* __restrict__ X, double* __restrict__ opart,
-                                                           unsigned* __restrict__ bar) {
-  // LDS: X partials [256][B C's], per-thread E^2 sums [B][256], dW [B][16][C's],
-  // block-sum scratch, then one area that holds D^(ml) [K][C's] and q [K]
-  // for the assignment and afterwards, per round of 256 images, the images'
-  // S columns: [image][B C's] of the previous batch, then of the next.
+__global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __restrict__ S, EcParams p,
+                                                             double* __restrict__ E, int mp0, int Lp,
+                                                             const double* __restrict__ P,
+                                                             const double* __restrict__ Dlast,
+                                                             const double* __restrict__ qv, uint8_t* __restrict__ ct,
+                                                             const double* __restrict__ D64,
+                                                             const uint8_t* __restrict__ codes_old,
+                                                             const double* __restrict__ dW, int mn0, int Ln,
+                                                             double* __restrict__ X, double* __restrict__ opart,
+                                                             unsigned* __restrict__ bar) {
+  // LDS: dW [B][16][C's], the per-wave sums of E^2 [B][waves], then one area
+  // that holds D^(ml) [K][C's] and q [K] for the assignment, then per round
+  // the images' S columns ([chunk][image][2 B C's]: the previous batch's,
+  // then the next one's), and at the end the waves' X partials [wave][B C's][16].
   extern __shared__ double sh[];
-  constexpr int kRound = kEcChunk * (kEcThreads / kPassCh);  // images per round
+  constexpr int NCH = kPassThreads / kPassCh;             // image chunks
+  constexpr int NW = kPassThreads / kWave;                // waves
+  constexpr int kRound = kPassChunk * NCH;                // images per round
   constexpr int BC = B * CSP;
-  constexpr int kChunkF = kEcChunk * 2 * BC + 4;  // floats per chunk in the stage (padded: no bank conflicts)
+  constexpr int kChunkF = kPassChunk * 2 * BC + 4;        // floats per chunk in the stage (padded: no bank conflicts)
   constexpr int kStage = kRound * 2 * BC;
-  double* xr = sh;  // [B C's][256]: thread fastest
-  double* osq = xr + (size_t)kEcThreads * BC;
-  double* dws = osq + (size_t)B * kEcThreads;
+  static_assert(kWave % kPassCh == 0, "a wave holds whole chunks");
+  double* dws = sh;
   double* red = dws + (size_t)B * kPassCh * CSP;  // [B][waves]
-  double* sd = red + B * (kEcThreads / kWave);
+  double* area = red + B * NW;
+  double* sd = area;
   double* q = sd + (size_t)p.K * CSP;
-  float* ss = reinterpret_cast<float*>(sd);
+  float* ss = reinterpret_cast<float*>(area);
+  double* xw = area;
   const int tid = threadIdx.x, cl = tid % kPassCh, chunk = tid / kPassCh;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
   const int c = blockIdx.x * kPassCh + cl;
   const bool col = c < p.Ct;
   const int cc = col ? c : p.Ct - 1;  // a valid column for loads whose value is not used
   if (blockIdx.x == 0 && tid == 0) *bar = 0;  // for the steps kernel that follows
-  for (int i = tid; i < kEcThreads * BC; i += kEcThreads) xr[i] = 0.0;
-  for (int i = tid; i < B * kEcThreads; i += kEcThreads) osq[i] = 0.0;
+  double xacc[BC], sq[B];
+#pragma unroll
+  for (int i = 0; i < BC; ++i) xacc[i] = 0.0;
+#pragma unroll
+  for (int i = 0; i < B; ++i) sq[i] = 0.0;
   if (Lp > 0) {
     const int ml = mp0 + Lp - 1;
     // dW of the batch's earlier steps for the block's channels (zeros past the block)
-    for (int t = tid; t < (Lp - 1) * kPassCh * CSP; t += kEcThreads) {
+    for (int t = tid; t < (Lp - 1) * kPassCh * CSP; t += kPassThreads) {
       const int i = t / (kPassCh * CSP), r = t % (kPassCh * CSP), ch = r / CSP, a = r % CSP;
       const int c2 = blockIdx.x * kPassCh + ch;
       dws[t] = c2 < p.Ct ? dW[((size_t)i * CSP + a) * p.Ct + c2] : 0.0;
     }
-    for (int i = tid; i < p.K * CSP; i += kEcThreads) sd[i] = Dlast[i];
-    for (int i = tid; i < p.K; i += kEcThreads) q[i] = qv[i];
+    for (int i = tid; i < p.K * CSP; i += kPassThreads) sd[i] = Dlast[i];
+    for (int i = tid; i < p.K; i += kPassThreads) q[i] = qv[i];
     double pc[CSP];
 #pragma unroll
     for (int j = 0; j < CSP; ++j) pc[j] = P[(size_t)j * p.Ct + cc];
@@ -467,118 +477,132 @@ __global__ __launch_bounds__(kEcThreads) void ec_pass_kernel(const float* __rest
 #pragma unroll
     for (int j = 0; j < CSP; ++j) dwo[j] = wo[j];
     __syncthreads();
-    const int knew = ec_best<CSP>(sd, q, p.K, pc);
-    if (col && chunk == 0) ct[(size_t)ml * p.Ct + c] = (uint8_t)knew;
-    if (chunk == 0)
+    if (chunk == 0) {
+      const int knew = ec_best<CSP>(sd, q, p.K, pc);
+      if (col) ct[(size_t)ml * p.Ct + c] = (uint8_t)knew;
 #pragma unroll
       for (int j = 0; j < CSP; ++j)
         dws[((size_t)(Lp - 1) * kPassCh + cl) * CSP + j] = col ? sd[knew * CSP + j] - dwo[j] : 0.0;
+    }
   }
   for (int r0 = 0; r0 < p.N; r0 += kRound) {
     __syncthreads();  // the assignment table or the previous round's stage may still be read
-    constexpr int kPer = kStage / kEcThreads;  // stage values per thread, all loads in flight
-    static_assert(kStage % kEcThreads == 0 && kPer <= 64, "stage share per thread");
-    for (int t0 = 0; t0 < kStage; t0 += kPer * kEcThreads) {
+    constexpr int kPer = kStage / kPassThreads;  // stage values per thread, all loads in flight
+    static_assert(kStage % kPassThreads == 0 && kPer <= 64, "stage share per thread");
+    {
       float v[kPer];
 #pragma unroll
       for (int u = 0; u < kPer; ++u) {  // straight-line: every load issued, unused values masked
-        const int t = t0 + u * kEcThreads + tid;
+        const int t = u * kPassThreads + tid;
         const int img = t / (2 * BC), col2 = t % (2 * BC);
         const int half = col2 / BC, c3 = col2 % BC;
         const int len = half == 0 ? Lp : Ln, m0 = half == 0 ? mp0 : mn0;
-        const bool ok = t < kStage && r0 + img < p.N && c3 < len * CSP;
+        const bool ok = r0 + img < p.N && c3 < len * CSP;
         const size_t at = ok ? (size_t)(r0 + img) * p.Cs + (size_t)m0 * CSP + c3 : 0;
         const float x = S[at];
         v[u] = ok ? x : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < kPer; ++u) {
-        const int t = t0 + u * kEcThreads + tid;
+        const int t = u * kPassThreads + tid;
         const int img = t / (2 * BC);
-        if (t < kStage) ss[(img / kEcChunk) * kChunkF + (img % kEcChunk) * 2 * BC + t % (2 * BC)] = v[u];
+        ss[(img / kPassChunk) * kChunkF + (img % kPassChunk) * 2 * BC + t % (2 * BC)] = v[u];
       }
     }
     __syncthreads();
-    const int n0 = r0 + chunk * kEcChunk;
+    const int n0 = r0 + chunk * kPassChunk;
     // images past N: E read at a valid row and zeroed (their S is 0 too)
-    double e[kEcChunk];
+    double e[kPassChunk];
 #pragma unroll
-    for (int i = 0; i < kEcChunk; ++i) {
+    for (int i = 0; i < kPassChunk; ++i) {
       const double v = E[(size_t)min(n0 + i, p.N - 1) * p.Ct + cc];
       e[i] = col && n0 + i < p.N ? v : 0.0;
     }
     const float* sr = ss + (size_t)chunk * kChunkF;  // [image][2 B C's] of this chunk
-    for (int s = 0; s < Lp; ++s) {
-      double dw[CSP];
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) dw[j] = dws[((size_t)s * kPassCh + cl) * CSP + j];
-      double sq = 0.0;
+    for (int s = 0; s < B; ++s) {
+      if (s < Lp) {
+        double dw[CSP];
 #pragma unroll
-      for (int i = 0; i < kEcChunk; ++i) {
-        const float* srow = sr + i * 2 * BC + s * CSP;
-        double d = 0.0;
+        for (int j = 0; j < CSP; ++j) dw[j] = dws[((size_t)s * kPassCh + cl) * CSP + j];
+        double sqs = 0.0;
 #pragma unroll
-        for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[j];
-        e[i] -= d;
-        sq += e[i] * e[i];
+        for (int i = 0; i < kPassChunk; ++i) {
+          const float* srow = sr + i * 2 * BC + s * CSP;
+          double d = 0.0;
+#pragma unroll
+          for (int j = 0; j < CSP; ++j) d += (double)srow[j] * dw[j];
+          e[i] -= d;
+          sqs += e[i] * e[i];
+        }
+        sq[s] += sqs;
       }
-      osq[(size_t)s * kEcThreads + tid] += sq;
     }
     if (Lp > 0 && col) {
 #pragma unroll
-      for (int i = 0; i < kEcChunk; ++i)
+      for (int i = 0; i < kPassChunk; ++i)
         if (n0 + i < p.N) E[(size_t)(n0 + i) * p.Ct + c] = e[i];
     }
-    for (int s = 0; s < Ln; ++s) {
-      double acc[CSP];
 #pragma unroll
-      for (int j = 0; j < CSP; ++j) acc[j] = 0.0;
+    for (int s = 0; s < B; ++s) {
+      if (s < Ln) {
 #pragma unroll
-      for (int i = 0; i < kEcChunk; ++i) {
-        const float* srow = sr + i * 2 * BC + BC + s * CSP;
+        for (int i = 0; i < kPassChunk; ++i) {
+          const float* srow = sr + i * 2 * BC + BC + s * CSP;
 #pragma unroll
-        for (int j = 0; j < CSP; ++j) acc[j] += (double)srow[j] * e[i];
+          for (int j = 0; j < CSP; ++j) xacc[s * CSP + j] += (double)srow[j] * e[i];
+        }
       }
-#pragma unroll
-      for (int j = 0; j < CSP; ++j) xr[(size_t)(s * CSP + j) * kEcThreads + tid] += acc[j];
     }
   }
-  // the block sums of E^2 after each step, all at once: per wave in a fixed
-  // shuffle order, then the waves in order
+  // the block sums of E^2 after each step: per wave in a fixed shuffle
+  // order, then the waves in order
   if (Lp > 0) {
-    double* wred = red;  // [B][waves]
-    __syncthreads();
-    for (int s = 0; s < Lp; ++s) {
-      double v = osq[(size_t)s * kEcThreads + tid];
-      for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
-      if ((tid & (kWave - 1)) == 0) wred[s * (kEcThreads / kWave) + tid / kWave] = v;
+#pragma unroll
+    for (int s = 0; s < B; ++s) {
+      if (s < Lp) {
+        double v = sq[s];
+        for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+        if (lane == 0) red[s * NW + wave] = v;
+      }
     }
     __syncthreads();
     if (tid < Lp) {
       double v = 0.0;
-      for (int w = 0; w < kEcThreads / kWave; ++w) v += wred[tid * (kEcThreads / kWave) + w];
+      for (int w = 0; w < NW; ++w) v += red[tid * NW + w];
       opart[(size_t)tid * gridDim.x + blockIdx.x] = v;
     }
   }
   if (Ln > 0) {
+    // X partials: the wave's four chunks of each channel by shuffles, then
+    // the waves in order
+    __syncthreads();  // the last round's stage is no longer read
+#pragma unroll
+    for (int sj = 0; sj < BC; ++sj) {
+      if (sj < Ln * CSP) {
+        double v = xacc[sj];
+        for (int off = kWave / 2; off >= kPassCh; off >>= 1) v += __shfl_down(v, off, kWave);
+        if (lane < kPassCh) xw[((size_t)wave * BC + sj) * kPassCh + lane] = v;
+      }
+    }
     __syncthreads();
-    // (channel, subspace, coordinate) triples: the 16 chunks in order
-    for (int t = tid; t < kPassCh * Ln * CSP; t += kEcThreads) {
+    for (int t = tid; t < kPassCh * Ln * CSP; t += kPassThreads) {
       const int ch = t % kPassCh, sj = t / kPassCh;  // sj = s C's + j
       const int c2 = blockIdx.x * kPassCh + ch;
       double v = 0.0;
-      for (int k = 0; k < kEcThreads / kPassCh; ++k) v += xr[(size_t)sj * kEcThreads + k * kPassCh + ch];
+      for (int w = 0; w < NW; ++w) v += xw[((size_t)w * BC + sj) * kPassCh + ch];
       if (c2 < p.Ct) X[(size_t)sj * p.Ct + c2] = v;
     }
   }
 }
 
 template <int CSP, int B> size_t pass_lds_bytes(int K) {
-  const size_t fixed = ((size_t)kEcThreads * B * CSP + (size_t)B * kEcThreads + (size_t)B * kPassCh * CSP +
-                        (size_t)B * (kEcThreads / kWave)) * sizeof(double);
+  constexpr int NCH = kPassThreads / kPassCh, NW = kPassThreads / kWave;
+  const size_t fixed = ((size_t)B * kPassCh * CSP + (size_t)B * NW) * sizeof(double);
   const size_t table = (size_t)K * (CSP + 1) * sizeof(double);
-  const size_t stage = (size_t)(kEcThreads / kPassCh) * (kEcChunk * 2 * B * CSP + 4) * sizeof(float);
-  return fixed + std::max(table, stage);
+  const size_t stage = (size_t)NCH * (kPassChunk * 2 * B * CSP + 4) * sizeof(float);
+  const size_t xpart = (size_t)NW * B * CSP * kPassCh * sizeof(double);
+  return fixed + std::max({table, stage, xpart});
 }
 
 // After a batch's pass: D64[mp0 + i] = Dnew[i] for i < Lp (the batch's final
@@ -1086,7 +1110,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
                          fit_out(Lp - 1, inner - 1), qv);
       if ((r = hipGetLastError()) != hipSuccess) return r;
     }
-    hipLaunchKernelGGL(pass, dim3((unsigned)pblocks), dim3(kEcThreads), pass_lds, stream, S, p, E, mp0, Lp,
+    hipLaunchKernelGGL(pass, dim3((unsigned)pblocks), dim3(kPassThreads), pass_lds, stream, S, p, E, mp0, Lp,
                        (const double*)P, (const double*)(Dnew + (size_t)(Lp > 0 ? Lp - 1 : 0) * kc),
                        (const double*)qv, ct, (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0,
                        Ln, X, opart, bar);
