@@ -251,23 +251,59 @@ __global__ __launch_bounds__(kQThreads) void pq_update_kernel(const float* __res
   for (int base = 0; base < q.n; base += chunk) {
     const int len = min(chunk, q.n - base);
     __syncthreads();  // the previous chunk is done
-    for (int e = tid; e < len * csp; e += kQThreads) {
+    {
       // Element (il, j).  Conv: j slowest, so that consecutive threads read
       // consecutive kernel positions of one input channel; FC (one position):
       // j fastest, so that they read the contiguous C'_s floats of a row.
-      int j, il;
-      if (q.P == 1) {
-        il = e / csp;
-        j = e - il * csp;
-      } else {
-        j = e / len;
-        il = e - j * len;
+      // Every load of the chunk is issued before any is stored.
+      constexpr int EPT = kChunkFloats / kQThreads;  // elements per thread
+      constexpr int CPT = (kChunkFloats + kQThreads - 1) / kQThreads;  // codes per thread (>= len / kQThreads)
+      float v[EPT];
+      uint8_t cv[CPT];
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + u * kQThreads;
+        const bool ok = e < len * csp;
+        int j, il;
+        if (q.P == 1) {
+          il = e / csp;
+          j = e - il * csp;
+        } else {
+          j = e / len;
+          il = e - j * len;
+        }
+        const int i = base + il;
+        const int t = i / q.P, p = i - t * q.P;
+        const float x = W[ok ? ((size_t)t * q.Cs + (size_t)m * csp + j) * q.P + p : 0];
+        v[u] = x;
       }
-      const int i = base + il;
-      const int t = i / q.P, p = i - t * q.P;
-      sv[il * csp + j] = W[((size_t)t * q.Cs + (size_t)m * csp + j) * q.P + p];
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int il = tid + u * kQThreads;
+        const uint8_t c = codes[il < len ? (size_t)(base + il) * q.M + m : 0];
+        cv[u] = c;
+      }
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + u * kQThreads;
+        if (e < len * csp) {
+          int j, il;
+          if (q.P == 1) {
+            il = e / csp;
+            j = e - il * csp;
+          } else {
+            j = e / len;
+            il = e - j * len;
+          }
+          sv[il * csp + j] = v[u];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int il = tid + u * kQThreads;
+        if (il < len) sc[il] = cv[u];
+      }
     }
-    for (int il = tid; il < len; il += kQThreads) sc[il] = codes[(size_t)(base + il) * q.M + m];
     for (int k = tid; k < 256; k += kQThreads) {
       cnt[k] = 0;
       run[k] = 0;
