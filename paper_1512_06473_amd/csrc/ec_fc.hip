@@ -28,15 +28,15 @@
 //   P = X^(j) - sum_{i<j} Gc[m_j][j-i] (W_new - W_old)^(m_i) + G W^(m_j)
 // (the same quantity as a pass over E_j would give, up to rounding), which
 // ec_prep_kernel forms per channel without touching E.  Per subspace:
-//   ec_prep_kernel  the assignment (Eq. (12)) of the subspace fitted just
-//                   before (when it lies in the same batch), P as above,
-//                   then per block of channels the sums of P_c over the
-//                   channels assigned to each sub-codeword, in channel order
-//                   (a counting sort in LDS);
-//   ec_fit_kernel   one workgroup: adds the blocks' sums and solves Eq. (11)
-//                   for every sub-codeword.
-// With `inner` > 1 the prep kernel's second form (assignment from P, then
-// the sums) and the fit kernel repeat.  The last subspace of a batch is
+//   ec_prep_kernel  the fit (Eq. (11)) the step waits for, which every
+//                   workgroup solves from the blocks' sums of the step
+//                   before; the assignment (Eq. (12)) of the subspace fitted
+//                   just before (when it lies in the same batch), P as
+//                   above, then per block of channels the sums of P_c over
+//                   the channels assigned to each sub-codeword, in channel
+//                   order (a counting sort in LDS).
+// With `inner` > 1 the prep kernel's second form (fit, assignment from P,
+// then the sums) repeats.  The last subspace of a batch is fitted and
 // assigned by the next pass.
 // Readings (shared with the oracle): the descent starts from the given
 // sub-codebooks and codes; a sweep visits m in order; a sub-codeword no
@@ -265,7 +265,10 @@ __device__ __forceinline__ FitLds fit_lds(double* base, int K) {
   return f;
 }
 
-// Eq. (11) by one workgroup of kUpdThreads threads, for subspace mf: b_k and
+// Eq. (11) by one workgroup of kUpdThreads threads (vt: the thread's index
+// in that role, threadIdx.x if negative; threads of a larger workgroup take
+// part with an index >= kUpdThreads and only pass its barriers), for
+// subspace mf: b_k and
 // |L_k| are the sums over the channel blocks (in order) of the prep
 // kernel's bins; each sub-codeword used by some channel becomes
 // G^-1 b_k / |L_k|, the others keep their value in Din.  Leaves D in f.Ds
@@ -284,8 +287,8 @@ struct FitRegs {
 template <int CSP>
 __device__ __forceinline__ void ec_fit_issue(const double* __restrict__ bins, const int* __restrict__ nbin, int nblk,
                                              const EcParams& p, int mf, const double* __restrict__ Gc,
-                                             const double* __restrict__ Din, FitRegs& r) {
-  const int K = p.K, tid = threadIdx.x;
+                                             const double* __restrict__ Din, FitRegs& r, int vt = -1) {
+  const int K = p.K, tid = vt >= 0 ? vt : (int)threadIdx.x;
   r.on = K * CSP <= kUpdThreads && nblk <= 16;
   if (!r.on) return;  // uniform
   const bool bi = tid < K * CSP, ki = tid < K;
@@ -306,8 +309,8 @@ __device__ __forceinline__ void ec_fit_issue(const double* __restrict__ bins, co
 template <int CSP>
 __device__ void ec_fit_wg(const double* __restrict__ bins, const int* __restrict__ nbin, int nblk,
                           const EcParams& p, int mf, const double* __restrict__ Gc, const double* __restrict__ Din,
-                          const FitLds& f, const FitRegs* pre = nullptr) {
-  const int K = p.K, tid = threadIdx.x;
+                          const FitLds& f, const FitRegs* pre = nullptr, int vt = -1) {
+  const int K = p.K, tid = vt >= 0 ? vt : (int)threadIdx.x;
   if (pre && pre->on) {  // the loads were issued by ec_fit_issue; the sums in block order
     if (tid < CSP * CSP) f.Gs[tid] = pre->g;
     if (tid < K * CSP) {
@@ -384,28 +387,15 @@ __device__ void ec_fit_wg(const double* __restrict__ bins, const int* __restrict
   __syncthreads();
 }
 
-// The fit of the last step of a batch on its own (one workgroup): Dout = D,
-// qv = q, for the pass kernel that assigns that subspace.
-template <int CSP>
-__global__ __launch_bounds__(kUpdThreads) void ec_fit_kernel(const double* __restrict__ bins,
-                                                           const int* __restrict__ nbin, int nblk, EcParams p,
-                                                           int mf, const double* __restrict__ Gc,
-                                                           const double* __restrict__ Din, double* __restrict__ Dout,
-                                                           double* __restrict__ qv) {
-  extern __shared__ double sh[];  // all LDS dynamic (up to the whole 160 KB)
-  const FitLds f = fit_lds<CSP>(sh, p.K);
-  ec_fit_wg<CSP>(bins, nbin, nblk, p, mf, Gc, Din, f);
-  for (int i = threadIdx.x; i < p.K * CSP; i += kUpdThreads) Dout[i] = f.Ds[i];
-  for (int k = threadIdx.x; k < p.K; k += kUpdThreads) qv[k] = f.qs[k];
-}
-
 // One pass over E for kPassCh channels and every image (kPassThreads /
 // kPassCh chunks of kPassChunk images per round of 256), between the batch of
 // Lp subspaces starting at mp0 (all fitted; Lp = 0: none) and the batch of
 // Ln subspaces starting at mn0 (Ln = 0: none):
 //   assign:  the last subspace of the previous batch, ml = mp0 + Lp - 1, by
-//            Eq. (12) from P (still that subspace's), its new D (Dlast) and
-//            q; the chunk-0 threads store the codes;
+//            Eq. (12) from P (still that subspace's) and its last fit, which
+//            every workgroup makes from the last prep kernel's bins (Din in,
+//            Dout out, stored by workgroup 0); the chunk-0
+//            threads store the codes;
 //   apply:   for i < Lp in order, E[n][c] -= sum_j S[n][(mp0+i) C's + j]
 //            dW_i[j][c] (dW_i = D_new[k_new] - D_old[k_old] of step i: from
 //            the prep kernels, the last one here), with the block sum of E^2
@@ -422,15 +412,18 @@ template <int CSP, int B>
 __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __restrict__ S, EcParams p,
                                                              double* __restrict__ E, int mp0, int Lp,
                                                              const double* __restrict__ P,
-                                                             const double* __restrict__ Dlast,
-                                                             const double* __restrict__ qv, uint8_t* __restrict__ ct,
+                                                             const double* __restrict__ bins,
+                                                             const int* __restrict__ nbin, int nblk,
+                                                             const double* __restrict__ Gc,
+                                                             const double* __restrict__ Din,
+                                                             double* __restrict__ Dout, uint8_t* __restrict__ ct,
                                                              const double* __restrict__ D64,
                                                              const uint8_t* __restrict__ codes_old,
                                                              const double* __restrict__ dW, int mn0, int Ln,
                                                              double* __restrict__ X, double* __restrict__ opart,
                                                              unsigned* __restrict__ bar) {
   // LDS: dW [B][16][C's], the per-wave sums of E^2 [B][waves], then one area
-  // that holds D^(ml) [K][C's] and q [K] for the assignment, then per round
+  // that holds the fit of ml (its D and q) for the assignment, then per round
   // the images' S columns ([chunk][image][2 B C's]: the previous batch's,
   // then the next one's), and at the end the waves' X partials [wave][B C's][16].
   extern __shared__ double sh[];
@@ -444,8 +437,6 @@ __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __re
   double* dws = sh;
   double* red = dws + (size_t)B * kPassCh * CSP;  // [B][waves]
   double* area = red + B * NW;
-  double* sd = area;
-  double* q = sd + (size_t)p.K * CSP;
   float* ss = reinterpret_cast<float*>(area);
   double* xw = area;
   const int tid = threadIdx.x, cl = tid % kPassCh, chunk = tid / kPassCh;
@@ -467,8 +458,9 @@ __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __re
       const int c2 = blockIdx.x * kPassCh + ch;
       dws[t] = c2 < p.Ct ? dW[((size_t)i * CSP + a) * p.Ct + c2] : 0.0;
     }
-    for (int i = tid; i < p.K * CSP; i += kPassThreads) sd[i] = Dlast[i];
-    for (int i = tid; i < p.K; i += kPassThreads) q[i] = qv[i];
+    const int vt = tid < kUpdThreads ? tid : kUpdThreads + tid;  // the fit's first kUpdThreads threads
+    FitRegs pre;
+    ec_fit_issue<CSP>(bins, nbin, nblk, p, ml, Gc, Din, pre, vt);
     double pc[CSP];
 #pragma unroll
     for (int j = 0; j < CSP; ++j) pc[j] = P[(size_t)j * p.Ct + cc];
@@ -476,9 +468,13 @@ __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __re
     double dwo[CSP];
 #pragma unroll
     for (int j = 0; j < CSP; ++j) dwo[j] = wo[j];
-    __syncthreads();
+    const FitLds f = fit_lds<CSP>(area, p.K);
+    ec_fit_wg<CSP>(bins, nbin, nblk, p, ml, Gc, Din, f, &pre, vt);  // ends with a barrier
+    if (blockIdx.x == 0)
+      for (int i = tid; i < p.K * CSP; i += kPassThreads) Dout[i] = f.Ds[i];
+    const double* sd = f.Ds;
     if (chunk == 0) {
-      const int knew = ec_best<CSP>(sd, q, p.K, pc);
+      const int knew = ec_best<CSP>(sd, f.qs, p.K, pc);
       if (col) ct[(size_t)ml * p.Ct + c] = (uint8_t)knew;
 #pragma unroll
       for (int j = 0; j < CSP; ++j)
@@ -599,10 +595,10 @@ __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __re
 template <int CSP, int B> size_t pass_lds_bytes(int K) {
   constexpr int NCH = kPassThreads / kPassCh, NW = kPassThreads / kWave;
   const size_t fixed = ((size_t)B * kPassCh * CSP + (size_t)B * NW) * sizeof(double);
-  const size_t table = (size_t)K * (CSP + 1) * sizeof(double);
+  const size_t fit = fit_lds_bytes<CSP>(K);
   const size_t stage = (size_t)NCH * (kPassChunk * 2 * B * CSP + 4) * sizeof(float);
   const size_t xpart = (size_t)NW * B * CSP * kPassCh * sizeof(double);
-  return fixed + std::max({table, stage, xpart});
+  return fixed + std::max({fit, stage, xpart});
 }
 
 // After a batch's pass: D64[mp0 + i] = Dnew[i] for i < Lp (the batch's final
@@ -870,7 +866,6 @@ struct EcSteps {
   int* nbin;          // [2][blocks][K]
   double* Dnew;       // [B][K][C's]: each step's last fit
   double* Dpp;        // [2][K][C's]: the fits of the inner rounds before the last
-  double* qv;         // [K]: q of the batch's last fit
   unsigned* bar;      // arrival count of the grid barriers (0 at launch)
   int* fail;          // set when a barrier gives up waiting
 };
@@ -907,9 +902,8 @@ __device__ __forceinline__ void grid_barrier(unsigned* bar, unsigned target, int
 
 // Every step of a batch (subspaces m0 .. m0 + L - 1, `inner` rounds each) in
 // one launch, one workgroup per block of 256 channels as ec_prep_kernel,
-// the steps separated by grid barriers instead of kernel boundaries; then
-// workgroup 0 makes the batch's last fit (Dnew[L - 1] and q, as
-// ec_fit_kernel).  The step sequence, its inputs and outputs and every sum's
+// the steps separated by grid barriers instead of kernel boundaries (the
+// batch's last fit is made by the pass that follows).  The step sequence, its inputs and outputs and every sum's
 // order are those of the per-step kernels, so the results are the same bit
 // for bit.  sel0: the bins buffer the step before the batch wrote.
 template <int CSP, int B>
@@ -948,15 +942,6 @@ __global__ __launch_bounds__(kEcThreads) void ec_steps_kernel(EcParams p, int m0
       sel ^= 1;
     }
   }
-  target += (unsigned)nblk;
-  grid_barrier(b.bar, target, b.fail);
-  if (blockIdx.x != 0) return;
-  const int ml = m0 + L - 1;
-  const FitLds f = fit_lds<CSP>(sp, p.K);
-  ec_fit_wg<CSP>(bins_at(sel), nbin_at(sel), nblk, p, ml, b.Gc, fit_in(ml, p.inner - 1), f);
-  double* dout = fit_out(L - 1, p.inner - 1);
-  for (int i = threadIdx.x; i < kc; i += kEcThreads) dout[i] = f.Ds[i];
-  for (int k = threadIdx.x; k < p.K; k += kEcThreads) b.qv[k] = f.qs[k];
 }
 
 // codebooks = fp32(D64) (all NaN if a grid barrier of the call gave up
@@ -987,16 +972,13 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   const int kc = K * Csp;
   auto pass = ec_pass_kernel<CSP, B>;
   auto prep = ec_prep_kernel<CSP, B>;
-  auto fit = ec_fit_kernel<CSP>;
   auto steps = ec_steps_kernel<CSP, B>;
   const size_t pass_lds = pass_lds_bytes<CSP, B>(K);
   const size_t prep_lds = prep_lds_bytes<CSP>(K);
-  const size_t fit_lds = fit_lds_bytes<CSP>(K);
-  if (pass_lds > kLdsBytes || prep_lds > kLdsBytes || fit_lds > kLdsBytes) return hipErrorInvalidValue;
+  if (pass_lds > kLdsBytes || prep_lds > kLdsBytes) return hipErrorInvalidValue;
   hipError_t e;
   if ((e = allow_max_lds((const void*)pass)) != hipSuccess) return e;
   if ((e = allow_max_lds((const void*)prep)) != hipSuccess) return e;
-  if ((e = allow_max_lds((const void*)fit)) != hipSuccess) return e;
   if ((e = allow_max_lds((const void*)steps)) != hipSuccess) return e;
   // QCNN_EC_STEPS=batch (read per call): a batch's steps in one cooperative
   // launch with grid barriers between them, where the device supports it and
@@ -1025,7 +1007,6 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
       (size_t)M * kc * 8,                                  // D64
       (size_t)B * kc * 8,                                  // Dnew
       (size_t)2 * kc * 8,                                  // Dpp (fits of the inner rounds)
-      (size_t)K * 8,                                       // q
       (size_t)std::max(nstart, B * pblocks) * 8,           // objective block sums
       (size_t)2 * cblocks * kc * 8,                        // bins (two buffers)
       (size_t)2 * cblocks * K * 4,                         // nbin (two buffers)
@@ -1053,7 +1034,6 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   double* D64 = reinterpret_cast<double*>(take());
   double* Dnew = reinterpret_cast<double*>(take());
   double* Dpp = reinterpret_cast<double*>(take());
-  double* qv = reinterpret_cast<double*>(take());
   double* opart = reinterpret_cast<double*>(take());
   double* bins = reinterpret_cast<double*>(take());
   int* nbin = reinterpret_cast<int*>(take());
@@ -1103,17 +1083,12 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   };
   auto close_and_pass = [&](int mn0, int Ln) -> hipError_t {
     hipError_t r;
-    if (Lp > 0 && !coop) {  // the last fit of the previous batch (the steps kernel made it)
-      const int ml = mp0 + Lp - 1;
-      hipLaunchKernelGGL(fit, dim3(1), dim3(kUpdThreads), fit_lds, stream, (const double*)bins_at(sel),
-                         (const int*)nbin_at(sel), cblocks, p, ml, (const double*)Gc, fit_in(ml, inner - 1),
-                         fit_out(Lp - 1, inner - 1), qv);
-      if ((r = hipGetLastError()) != hipSuccess) return r;
-    }
+    // the last fit of the previous batch is made inside the pass
+    const int ml = Lp > 0 ? mp0 + Lp - 1 : 0;
     hipLaunchKernelGGL(pass, dim3((unsigned)pblocks), dim3(kPassThreads), pass_lds, stream, S, p, E, mp0, Lp,
-                       (const double*)P, (const double*)(Dnew + (size_t)(Lp > 0 ? Lp - 1 : 0) * kc),
-                       (const double*)qv, ct, (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0,
-                       Ln, X, opart, bar);
+                       (const double*)P, (const double*)bins_at(sel), (const int*)nbin_at(sel), cblocks,
+                       (const double*)Gc, fit_in(ml, inner - 1), fit_out(Lp > 0 ? Lp - 1 : 0, inner - 1), ct,
+                       (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0, Ln, X, opart, bar);
     if ((r = hipGetLastError()) != hipSuccess) return r;
     if (Lp > 0) {
       pending = EcCommit{opart, pblocks, Lp, objective ? objective + 1 + nstep : nullptr, Dnew, D64, mp0, Lp, kc};
@@ -1128,7 +1103,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
       const int L = std::min(B, M - m0);
       if ((e = close_and_pass(m0, L)) != hipSuccess) return e;
       if (coop) {
-        EcSteps sb{X, Gc, D64, ct, P, dW, codes_old, bins, nbin, Dnew, Dpp, qv, bar, fail};
+        EcSteps sb{X, Gc, D64, ct, P, dW, codes_old, bins, nbin, Dnew, Dpp, bar, fail};
         int a_m0 = m0, a_L = L, a_sel = sel;
         void* args[] = {&p, &a_m0, &a_L, &a_sel, &sb};
         if ((e = hipLaunchCooperativeKernel((const void*)steps, dim3((unsigned)cblocks), dim3(kEcThreads), args,
