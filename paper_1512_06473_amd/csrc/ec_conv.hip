@@ -102,55 +102,152 @@ __global__ __launch_bounds__(kCThreads) void ecc_gram_kernel(const float* __rest
     for (int yo = 0; yo < q.Ho; ++yo) {
       const int y = yo * q.stride - q.pad + ky, y2 = yo * q.stride - q.pad + ky2;
       if ((unsigned)y >= (unsigned)q.H || (unsigned)y2 >= (unsigned)q.H) continue;
-      for (int xo = 0; xo < q.Wo; ++xo) {
-        const int x = xo * q.stride - q.pad + kx, x2 = xo * q.stride - q.pad + kx2;
-        if ((unsigned)x >= (unsigned)q.W || (unsigned)x2 >= (unsigned)q.W) continue;
-        s += (double)si[y * q.W + x] * (double)sj[y2 * q.W + x2];
+      for (int xo0 = 0; xo0 < q.Wo; xo0 += 8) {  // eight positions' loads in flight, added in order
+        float a[8], b[8];
+        bool ok[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int xo = xo0 + u;
+          const int x = xo * q.stride - q.pad + kx, x2 = xo * q.stride - q.pad + kx2;
+          ok[u] = xo < q.Wo && (unsigned)x < (unsigned)q.W && (unsigned)x2 < (unsigned)q.W;
+          const float va = si[ok[u] ? y * q.W + x : 0], vb = sj[ok[u] ? y2 * q.W + x2 : 0];
+          a[u] = va;
+          b[u] = vb;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (ok[u]) s += (double)a[u] * (double)b[u];
       }
     }
   }
   G[i0] = s;
 }
 
-// E = T - sum_m sum_p D^(m)[k(c, p)]^T s_p, one element per thread (o
-// fastest), subspaces and positions in order; block sums of E^2.
+// E = T - sum_m sum_p D^(m)[k(c, p)]^T s_p as a float64 implicit GEMM on
+// MFMA (v_mfma_f64_16x16x4_f64): rows are the output channels, columns the
+// output positions of all images (g = n O + o), and the reduction runs over
+// (kernel position p, input channel cs), p outer, so that a stage of
+// kStartKB reduction indices mostly shares one p.  A workgroup of 4 waves
+// owns 64 channels x 64 columns, wave w the channels 16 w .. 16 w + 15 as
+// four 16 x 16 tiles.  Each thread loads its share of a stage (the decoded
+// weights D^(m)[k(c, p)][a], cs = m C's + a: code, then sub-codeword entry;
+// the input values, 0 outside the map) one stage ahead into registers,
+// stores them into one of two LDS buffers, and every wave runs the stage's
+// MFMAs from LDS.  Register i of lane l of a 16 x 16 f64 result holds row
+// 4 i + l / 16, column l % 16.  Block sums of E^2 into
+// opart[blockIdx.y gridDim.x + blockIdx.x].
+constexpr int kStartTile = 64;          // channels and columns per workgroup
+constexpr int kStartKB = 32;            // reduction indices per stage
+constexpr int kStartLd = kStartKB + 1;  // LDS row stride in doubles (odd: spreads the rows over the banks)
+typedef double d4v __attribute__((ext_vector_type(4)));
+
 template <int CSP>
 __global__ __launch_bounds__(kCThreads) void ecc_start_kernel(const float* __restrict__ S,
                                                             const float* __restrict__ T, EccParams q,
                                                             const double* __restrict__ D64,
                                                             const uint8_t* __restrict__ ct, double* __restrict__ E,
                                                             double* __restrict__ opart) {
+  static_assert(kCThreads == 256, "four waves, 8 values per thread and operand");
+  __shared__ double As[2][kStartTile * kStartLd];  // [channel][index]
+  __shared__ double Bs[2][kStartTile * kStartLd];  // [column][index]
   __shared__ double red[kCThreads / kWave];
-  const size_t i = (size_t)blockIdx.x * kCThreads + threadIdx.x;
-  const size_t total = (size_t)q.N * q.Ct * q.O;
-  double e = 0.0;
-  if (i < total) {
-    const int o = (int)(i % q.O);
-    const int c = (int)((i / q.O) % q.Ct);
-    const int n = (int)(i / ((size_t)q.O * q.Ct));
-    e = (double)T[i];
-    const int yo = o / q.Wo, xo = o - yo * q.Wo;
-    const size_t HW = (size_t)q.H * q.W;
-    for (int m = 0; m < q.M; ++m) {
-      const uint8_t* km = ct + ((size_t)m * q.Ct + c) * q.P;
-      const float* sn = S + ((size_t)n * q.Cs + (size_t)m * CSP) * HW;
-      double d = 0.0;  // positions outside the input add exact zeros: skipped
-      for (int ky = 0; ky < q.dk; ++ky) {
-        const int y = yo * q.stride - q.pad + ky;
-        if ((unsigned)y >= (unsigned)q.H) continue;
-        for (int kx = 0; kx < q.dk; ++kx) {
-          const int x = xo * q.stride - q.pad + kx;
-          if ((unsigned)x >= (unsigned)q.W) continue;
-          const double* w = D64 + ((size_t)m * q.K + km[ky * q.dk + kx]) * CSP;
+  constexpr int PER = kStartTile * kStartKB / kCThreads;  // 8
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int c0 = blockIdx.x * kStartTile, g0 = blockIdx.y * kStartTile;
+  const int ncol = q.N * q.O, KD = q.Cs * q.P;
+  // this thread's share of a stage: row r (channel c0 + r of the weights,
+  // column g0 + r of the inputs), reduction indices q0 .. q0 + PER - 1
+  const int r = tid / (kStartKB / PER), q0 = (tid % (kStartKB / PER)) * PER;
+  const int cw = c0 + r, gb = g0 + r;
+  const bool rowa = cw < q.Ct, rowb = gb < ncol;
+  const int nb = rowb ? gb / q.O : 0, ob = rowb ? gb - (gb / q.O) * q.O : 0;
+  const int yb = (ob / q.Wo) * q.stride - q.pad, xb = (ob - (ob / q.Wo) * q.Wo) * q.stride - q.pad;
+  const size_t HW = (size_t)q.H * q.W;
+  const float* sb = S + (size_t)nb * q.Cs * HW;
+  const int nst = (KD + kStartKB - 1) / kStartKB;
+  float sv[PER];
+  double wv[PER];
+  auto load_stage = [&](int st) {
+    const int k0 = st * kStartKB + q0;
+    int p = k0 / q.Cs, cs = k0 - p * q.Cs;
+    int code[PER], ma[PER];
 #pragma unroll
-          for (int j = 0; j < CSP; ++j) d += (double)sn[j * HW + (size_t)y * q.W + x] * w[j];
-        }
+    for (int i = 0; i < PER; ++i) {
+      const bool okk = p < q.P;
+      const int pp = okk ? p : 0, cc = okk ? cs : 0;
+      const int ky = pp / q.dk, kx = pp - ky * q.dk;
+      const int y = yb + ky, x = xb + kx;
+      const bool oks = rowb && okk && (unsigned)y < (unsigned)q.H && (unsigned)x < (unsigned)q.W;
+      const float v = sb[oks ? cc * HW + (size_t)y * q.W + x : 0];
+      sv[i] = oks ? v : 0.f;
+      const int m = cc / CSP;
+      const bool okw = rowa && okk;
+      const int cd = ct[okw ? ((size_t)m * q.Ct + cw) * q.P + pp : 0];
+      code[i] = cd;
+      ma[i] = okw ? (m * q.K) * CSP + (cc - m * CSP) : -1;
+      if (++cs == q.Cs) {
+        cs = 0;
+        ++p;
       }
-      e -= d;
     }
-    E[i] = e;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const double w = D64[ma[i] >= 0 ? ma[i] + (size_t)code[i] * CSP : 0];
+      wv[i] = ma[i] >= 0 ? w : 0.0;
+    }
+  };
+  auto store_stage = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      As[buf][r * kStartLd + q0 + i] = wv[i];
+      Bs[buf][r * kStartLd + q0 + i] = (double)sv[i];
+    }
+  };
+  d4v acc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) acc[t] = d4v{0.0, 0.0, 0.0, 0.0};
+  const int arow = 16 * wave + (lane & 15), kq = lane >> 4;
+  load_stage(0);
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    store_stage(buf);
+    __syncthreads();  // the stage is in LDS; the other buffer's readers (stage st - 1) are done
+    if (st + 1 < nst) load_stage(st + 1);
+#pragma unroll
+    for (int kk = 0; kk < kStartKB / 4; ++kk) {
+      const double av = As[buf][arow * kStartLd + 4 * kk + kq];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const double bv = Bs[buf][(16 * t + (lane & 15)) * kStartLd + 4 * kk + kq];
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[t], 0, 0, 0);
+      }
+    }
   }
-  ecc_block_sum(e * e, red, opart);
+  // acc[t][i]: channel c0 + 16 wave + 4 i + lane / 16, column g0 + 16 t + lane % 16
+  double sq = 0.0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int g = g0 + 16 * t + (lane & 15);
+    const int n = g / q.O, o = g - (g / q.O) * q.O;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = c0 + 16 * wave + 4 * i + kq;
+      if (g < ncol && c < q.Ct) {
+        const size_t at = ((size_t)n * q.Ct + c) * q.O + o;
+        const double e = (double)T[at] - acc[t][i];
+        E[at] = e;
+        sq += e * e;
+      }
+    }
+  }
+  for (int off = kWave / 2; off > 0; off >>= 1) sq += __shfl_down(sq, off, kWave);
+  if (lane == 0) red[wave] = sq;
+  __syncthreads();
+  if (tid == 0) {
+    double s2 = 0.0;
+    for (int w = 0; w < kCThreads / kWave; ++w) s2 += red[w];
+    opart[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = s2;
+  }
 }
 
 // E -= sum_p delta[c][p]^T s_p for subspace ma; block sums of E^2.
@@ -676,10 +773,17 @@ __global__ __launch_bounds__(kCThreads) void ecc_finish_kernel(const double* __r
     const size_t m = i % q.M, cp = i / q.M;
     codes[i] = ct[m * q.Ct * q.P + cp];
   }
-  if (tid == 0 && objective) {  // once per call: a serial sum is fine here
+  if (objective && blockIdx.x == 0) {  // the block sums in a fixed order: strided per thread, then a tree
+    __shared__ double red[kCThreads];
     double s = 0.0;
-    for (int b = 0; b < nopart; ++b) s += opart[b];
-    *objective = s;
+    for (int b = threadIdx.x; b < nopart; b += kCThreads) s += opart[b];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = kCThreads / 2; h > 0; h >>= 1) {
+      if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) *objective = red[0];
   }
 }
 
@@ -705,6 +809,8 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
   const size_t total = (size_t)q.N * q.Ct * q.O;
   const int npairs = q.Ct * q.P;
   const int eblocks = (int)ceil_div_z(total, kCThreads);
+  const unsigned sbx = (unsigned)ceil_div(q.Ct, kStartTile), sby = (unsigned)ceil_div_z((size_t)q.N * q.O, kStartTile);
+  const int sblocks = (int)(sbx * sby);  // the starting residual's block sums
   const int pblocks = ceil_div(npairs, kCThreads);
   // the Gram blocks go to LDS when they fit beside the rest
   const bool gl = solve_lds_bytes<CSP>(q.K, npairs, q.P, true) <= kLdsBytes;
@@ -721,7 +827,7 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
   size_t bytes = 0;
   const size_t szE = total * 8, szPart = (size_t)q.nchunks * npairs * CSP * 8, szH = (size_t)npairs * CSP * 8;
   const size_t szG = (size_t)q.M * q.P * q.P * CSP * CSP * 8, szD = (size_t)q.M * q.K * CSP * 8;
-  const size_t szDelta = (size_t)npairs * CSP * 8, szOp = (size_t)eblocks * 8, szCt = (size_t)q.M * npairs;
+  const size_t szDelta = (size_t)npairs * CSP * 8, szOp = (size_t)std::max(eblocks, sblocks) * 8, szCt = (size_t)q.M * npairs;
   const size_t szDold = (size_t)q.K * CSP * 8, szCold = (size_t)npairs, szQk = (size_t)q.P * q.K * 8;
   for (size_t b : {szE, szPart, szH, szG, szD, szDelta, szOp, szCt, szDold, szCold, szQk})
     bytes += (b + 255) & ~(size_t)255;
@@ -753,7 +859,7 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
   hipLaunchKernelGGL(ecc_gram_kernel, dim3((unsigned)ceil_div_z(ng, kCThreads)), dim3(kCThreads), 0, stream, S, q,
                      G);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(ecc_start_kernel<CSP>, dim3((unsigned)eblocks), dim3(kCThreads), 0, stream, S, T, q,
+  hipLaunchKernelGGL(ecc_start_kernel<CSP>, dim3(sbx, sby), dim3(kCThreads), 0, stream, S, T, q,
                      (const double*)D64, (const uint8_t*)ct, E, opart);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   int nstep = 0;
@@ -774,7 +880,8 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
       for (int it = 0; it < inner; ++it) {
         hipLaunchKernelGGL(dupdate, dim3(1), dim3(kCThreads), slds, stream, (const double*)Hs, q, m,
                            (const double*)G, D64, (const uint8_t*)ct, it == 0 ? 1 : 0, Dold, cold, qkg,
-                           (const double*)opart, eblocks, objective ? objective + nstep : nullptr);
+                           (const double*)opart, nstep == 0 ? sblocks : eblocks,
+                           objective ? objective + nstep : nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(bupdate, dim3((unsigned)ceil_div(q.Ct, NW)), dim3(kCThreads), blds, stream,
                            (const double*)Hs, q, m, (const double*)G, (const double*)D64, (const double*)qkg, ct,
@@ -790,7 +897,7 @@ hipError_t launch_ecc_csp(const EccParams& q, const float* S, const float* T, fl
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   hipLaunchKernelGGL(ecc_finish_kernel, dim3(iblocks), dim3(kCThreads), 0, stream, (const double*)D64, q,
-                     (const uint8_t*)ct, D, codes, (const double*)opart, eblocks,
+                     (const uint8_t*)ct, D, codes, (const double*)opart, ma >= 0 ? eblocks : sblocks,
                      objective ? objective + nstep : nullptr);
   return hipGetLastError();
 }
