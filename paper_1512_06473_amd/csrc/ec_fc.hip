@@ -400,7 +400,10 @@ __device__ void ec_fit_wg(const double* __restrict__ bins, const int* __restrict
 //            dW_i[j][c] (dW_i = D_new[k_new] - D_old[k_old] of step i: from
 //            the prep kernels, the last one here), with the block sum of E^2
 //            after each into opart[i][block];
-//   collect: X[j][a][c] = sum_n S[n][(mn0+j) C's + a] E[n][c] for j < Ln.
+//   collect: X[j][a][c] = sum_n S[n][(mn0+j) C's + a] E[n][c] for j < Ln;
+//   rows:    Wb[j][a][c] = D^(mn0+j)[k(c)][a] for j < Lw (read before this
+//            pass's assignment and before the previous batch's commit, so
+//            only for batches that share no subspace with the previous one).
 // Per round the images' S columns of both batches are staged in LDS; the
 // chunk's E is loaded into registers (all loads in flight) before any of it
 // is written.  Each thread keeps its sums of E^2 (one per step) and its X
@@ -421,6 +424,7 @@ __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __re
                                                              const uint8_t* __restrict__ codes_old,
                                                              const double* __restrict__ dW, int mn0, int Ln,
                                                              double* __restrict__ X, double* __restrict__ opart,
+                                                             double* __restrict__ Wb, int Lw,
                                                              unsigned* __restrict__ bar) {
   // LDS: dW [B][16][C's], the per-wave sums of E^2 [B][waves], then one area
   // that holds the fit of ml (its D and q) for the assignment, then per round
@@ -445,6 +449,17 @@ __global__ __launch_bounds__(kPassThreads) void ec_pass_kernel(const float* __re
   const bool col = c < p.Ct;
   const int cc = col ? c : p.Ct - 1;  // a valid column for loads whose value is not used
   if (blockIdx.x == 0 && tid == 0) *bar = 0;  // for the steps kernel that follows
+  // the next batch's weight rows W^(mn0+s)_c = D^(mn0+s)[k(c)], s < Lw, for its
+  // prep kernels (Lw = 0 when the two batches share subspaces: ec_rows_kernel
+  // gathers them after the commit)
+  for (int t = tid; t < Lw * CSP * kPassCh; t += kPassThreads) {
+    const int ch = t % kPassCh, sa = t / kPassCh, s = sa / CSP, a = sa - s * CSP;
+    const int c2 = blockIdx.x * kPassCh + ch;
+    if (c2 < p.Ct) {
+      const int kk = ct[(size_t)(mn0 + s) * p.Ct + c2];
+      Wb[(size_t)sa * p.Ct + c2] = D64[((size_t)(mn0 + s) * p.K + kk) * CSP + a];
+    }
+  }
   double xacc[BC], sq[B];
 #pragma unroll
   for (int i = 0; i < BC; ++i) xacc[i] = 0.0;
@@ -644,6 +659,20 @@ __global__ __launch_bounds__(kUpdThreads) void ec_commit_kernel(EcCommit c) {
   ec_commit_wg(c, red);
 }
 
+// Wb[s][a][c] = D64[m0 + s][ct[m0 + s][c]][a] for s < L: a batch's weight
+// rows at its start, when the pass cannot gather them (the batch shares
+// subspaces with the previous one, whose assignment and commit come first).
+__global__ __launch_bounds__(kEcThreads) void ec_rows_kernel(EcParams p, const double* __restrict__ D64,
+                                                           const uint8_t* __restrict__ ct, int m0, int L,
+                                                           double* __restrict__ Wb) {
+  const size_t t = (size_t)blockIdx.x * kEcThreads + threadIdx.x;
+  if (t >= (size_t)L * p.Csp * p.Ct) return;
+  const int c = (int)(t % p.Ct);
+  const int sa = (int)(t / p.Ct), s = sa / p.Csp, a = sa - s * p.Csp;
+  const int kk = ct[(size_t)(m0 + s) * p.Ct + c];
+  Wb[t] = D64[((size_t)(m0 + s) * p.K + kk) * p.Csp + a];
+}
+
 // LDS of the prep kernel: a fit, then P of the block in sorted order and
 // the counting sort's counts and offsets.
 template <int CSP> size_t prep_lds_bytes(int K) {
@@ -671,7 +700,7 @@ __device__ __forceinline__ void ec_prep_step(const EcParams& p, int m0, int j, i
                                              const double* __restrict__ Din, const double* __restrict__ bins_in,
                                              const int* __restrict__ nbin_in, int nblk, double* __restrict__ Dout,
                                              const double* __restrict__ X, const double* __restrict__ Gc,
-                                             const double* __restrict__ D64, uint8_t* __restrict__ ct,
+                                             const double* __restrict__ Wb, uint8_t* __restrict__ ct,
                                              double* __restrict__ P, double* __restrict__ dW,
                                              uint8_t* __restrict__ codes_old, double* __restrict__ bins,
                                              int* __restrict__ nbin, double* sp) {
@@ -692,7 +721,7 @@ __device__ __forceinline__ void ec_prep_step(const EcParams& p, int m0, int j, i
   double pc[CSP], pp[CSP], dlast[CSP], wrow[CSP], worow[CSP];
 #pragma unroll
   for (int a = 0; a < CSP; ++a) dlast[a] = 0.0;
-  int k = 0, kold_prev = 0;
+  int k = 0;
   double dwv[B][CSP];  // dW of the steps before the previous one
   if (col) {
     if (it == 0) {
@@ -704,13 +733,11 @@ __device__ __forceinline__ void ec_prep_step(const EcParams& p, int m0, int j, i
 #pragma unroll
           for (int a = 0; a < CSP; ++a) dwv[i][a] = dW[((size_t)i * CSP + a) * p.Ct + c];
       k = ct[(size_t)m * p.Ct + c];
-      if (j > 0) kold_prev = codes_old[(size_t)(j - 1) * p.Ct + c];
-      const double* w = D64 + ((size_t)m * p.K + k) * CSP;
-      const double* wo = D64 + ((size_t)(j > 0 ? m - 1 : m) * p.K + kold_prev) * CSP;
+      // W^(m)_c and W^(m-1)_c as they were when the batch began (gathered by the pass)
 #pragma unroll
       for (int a = 0; a < CSP; ++a) {
-        wrow[a] = w[a];
-        worow[a] = wo[a];
+        wrow[a] = Wb[((size_t)j * CSP + a) * p.Ct + c];
+        worow[a] = Wb[((size_t)(j > 0 ? j - 1 : j) * CSP + a) * p.Ct + c];
       }
     }
     if (it > 0 || j > 0)
@@ -839,7 +866,7 @@ __global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0,
                                                            const int* __restrict__ nbin_in, int nblk,
                                                            double* __restrict__ Dout, const double* __restrict__ X,
                                                            const double* __restrict__ Gc,
-                                                           const double* __restrict__ D64, uint8_t* __restrict__ ct,
+                                                           const double* __restrict__ Wb, uint8_t* __restrict__ ct,
                                                            double* __restrict__ P, double* __restrict__ dW,
                                                            uint8_t* __restrict__ codes_old,
                                                            double* __restrict__ bins, int* __restrict__ nbin,
@@ -849,13 +876,14 @@ __global__ __launch_bounds__(kEcThreads) void ec_prep_kernel(EcParams p, int m0,
     ec_commit_wg(cm, sp);
     return;
   }
-  ec_prep_step<CSP, B>(p, m0, j, it, fm, Din, bins_in, nbin_in, nblk, Dout, X, Gc, D64, ct, P, dW, codes_old, bins,
+  ec_prep_step<CSP, B>(p, m0, j, it, fm, Din, bins_in, nbin_in, nblk, Dout, X, Gc, Wb, ct, P, dW, codes_old, bins,
                        nbin, sp);
 }
 
 // Buffers of a batch's steps (the workspace slices of launch_ec_csp).
 struct EcSteps {
   const double* X;
+  const double* Wb;   // [B][C's][C_t]: the batch's weight rows at its start
   const double* Gc;
   double* D64;
   uint8_t* ct;
@@ -937,7 +965,7 @@ __global__ __launch_bounds__(kEcThreads) void ec_steps_kernel(EcParams p, int m0
         grid_barrier(b.bar, target, b.fail);
       }
       ec_prep_step<CSP, B>(p, m0, j, it, fm, fm >= 0 ? fit_in(fm, fr) : b.D64, bins_at(sel), nbin_at(sel), nblk,
-                           fm >= 0 ? fit_out(fj, fr) : b.Dpp, b.X, b.Gc, b.D64, b.ct, b.P, b.dW, b.codes_old,
+                           fm >= 0 ? fit_out(fj, fr) : b.Dpp, b.X, b.Gc, b.Wb, b.ct, b.P, b.dW, b.codes_old,
                            bins_at(sel ^ 1), nbin_at(sel ^ 1), sp);
       sel ^= 1;
     }
@@ -1001,6 +1029,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   const size_t sizes[] = {
       (size_t)N * Ct * 8,                                  // E
       (size_t)B * Csp * Ct * 8,                            // X
+      (size_t)B * Csp * Ct * 8,                            // Wb
       (size_t)Csp * Ct * 8,                                // P
       (size_t)B * Csp * Ct * 8,                            // dW
       (size_t)M * B * Csp * Csp * 8,                       // Gc
@@ -1028,6 +1057,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   };
   double* E = reinterpret_cast<double*>(take());
   double* X = reinterpret_cast<double*>(take());
+  double* Wb = reinterpret_cast<double*>(take());
   double* P = reinterpret_cast<double*>(take());
   double* dW = reinterpret_cast<double*>(take());
   double* Gc = reinterpret_cast<double*>(take());
@@ -1072,7 +1102,8 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   // The previous batch's commit after its pass: run by an extra workgroup of
   // the next batch's first prep kernel (it touches only that batch's rows of
   // D64 and the pass's block sums, which no prep kernel reads), else by a
-  // kernel of its own (after the last pass, and with the batch launches).
+  // kernel of its own (after the last pass, with the batch launches, and when
+  // the next batch shares subspaces with the previous one).
   EcCommit pending{};
   bool has_pending = false;
   auto launch_pending = [&]() -> hipError_t {
@@ -1083,17 +1114,26 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
   };
   auto close_and_pass = [&](int mn0, int Ln) -> hipError_t {
     hipError_t r;
+    // one batch per sweep (M <= B): the next batch is the previous one again
+    const bool shared = Lp > 0 && Ln > 0 && mp0 < mn0 + Ln && mn0 < mp0 + Lp;
     // the last fit of the previous batch is made inside the pass
     const int ml = Lp > 0 ? mp0 + Lp - 1 : 0;
     hipLaunchKernelGGL(pass, dim3((unsigned)pblocks), dim3(kPassThreads), pass_lds, stream, S, p, E, mp0, Lp,
                        (const double*)P, (const double*)bins_at(sel), (const int*)nbin_at(sel), cblocks,
                        (const double*)Gc, fit_in(ml, inner - 1), fit_out(Lp > 0 ? Lp - 1 : 0, inner - 1), ct,
-                       (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0, Ln, X, opart, bar);
+                       (const double*)D64, (const uint8_t*)codes_old, (const double*)dW, mn0, Ln, X, opart, Wb,
+                       shared ? 0 : Ln, bar);
     if ((r = hipGetLastError()) != hipSuccess) return r;
     if (Lp > 0) {
       pending = EcCommit{opart, pblocks, Lp, objective ? objective + 1 + nstep : nullptr, Dnew, D64, mp0, Lp, kc};
       has_pending = true;
-      if ((coop || Ln == 0) && (r = launch_pending()) != hipSuccess) return r;
+      if ((coop || Ln == 0 || shared) && (r = launch_pending()) != hipSuccess) return r;
+    }
+    if (shared) {
+      const size_t nrows = (size_t)Ln * Csp * Ct;
+      hipLaunchKernelGGL(ec_rows_kernel, dim3((unsigned)ceil_div_z(nrows, kEcThreads)), dim3(kEcThreads), 0, stream, p,
+                         (const double*)D64, (const uint8_t*)ct, mn0, Ln, Wb);
+      if ((r = hipGetLastError()) != hipSuccess) return r;
     }
     nstep += Lp;
     return hipSuccess;
@@ -1103,7 +1143,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
       const int L = std::min(B, M - m0);
       if ((e = close_and_pass(m0, L)) != hipSuccess) return e;
       if (coop) {
-        EcSteps sb{X, Gc, D64, ct, P, dW, codes_old, bins, nbin, Dnew, Dpp, bar, fail};
+        EcSteps sb{X, Wb, Gc, D64, ct, P, dW, codes_old, bins, nbin, Dnew, Dpp, bar, fail};
         int a_m0 = m0, a_L = L, a_sel = sel;
         void* args[] = {&p, &a_m0, &a_L, &a_sel, &sb};
         if ((e = hipLaunchCooperativeKernel((const void*)steps, dim3((unsigned)cblocks), dim3(kEcThreads), args,
@@ -1132,7 +1172,7 @@ hipError_t launch_ec_csp(int N, int Cs, int Ct, int M, int K, const float* S, co
           const bool with_commit = has_pending;  // the batch's first step
           hipLaunchKernelGGL(prep, dim3((unsigned)(cblocks + (with_commit ? 1 : 0))), dim3(kEcThreads), prep_lds,
                              stream, p, m0, j, it, fm, din, (const double*)bins_at(sel), (const int*)nbin_at(sel),
-                             cblocks, dout, (const double*)X, (const double*)Gc, (const double*)D64, ct, P, dW,
+                             cblocks, dout, (const double*)X, (const double*)Gc, (const double*)Wb, ct, P, dW,
                              codes_old, bins_at(sel ^ 1), nbin_at(sel ^ 1), pending);
           if ((e = hipGetLastError()) != hipSuccess) return e;
           has_pending = false;

@@ -63,6 +63,8 @@ CASES = [
     (300, 128, 70, 4, 32, 1, 1, None),    # more images than one pass chunk
     (40, 48, 600, 12, 32, 2, 2, None),    # three channel blocks, C'_s > 8
     (30, 16, 20, 4, 8, 0, 1, None),       # no sweep: the starting objective only
+    (30, 16, 300, 4, 8, 3, 1, None),      # M = 4 <= B: one batch per sweep, sweeps follow each other
+    (25, 12, 40, 2, 5, 2, 2, None),       # M = 6 <= B = 16, inner rounds
 ]
 
 
@@ -176,6 +178,7 @@ STEP_CASES = [
     (40, 48, 600, 12, 32, 2, 2),
     (120, 200, 1000, 8, 16, 1, 1),
     (50, 26, 300, 1, 2, 1, 2),
+    (30, 16, 300, 4, 8, 3, 1),     # one batch per sweep
     (256, 9216, 4096, 4, 32, 1, 1),
 ]
 
